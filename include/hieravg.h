@@ -1,0 +1,172 @@
+/*
+ * hieravg.h -- C ABI of the Hier-AVG data-parallel hot path on one MI355X.
+ *
+ * Hier-AVG (Zhou & Cong, "A Distributed Hierarchical Averaging SGD
+ * Algorithm: Trading Local Reductions for Global Reductions", arXiv
+ * 1903.05133), Algorithm 1 in Sec. 3.1: P learners each run K1 local SGD
+ * steps on their own minibatch of size B, then every local cluster of S
+ * learners replaces its parameters by their mean; after K2 such blocks all P
+ * learners replace their parameters by the global mean.  Sec. 2 fixes
+ * S | P and S >= 1.
+ *
+ * Units.  K2 here counts local-averaging blocks per round (the paper's beta,
+ * Sec. 3.1), so one round is K1*K2 SGD steps per learner and the paper's
+ * global averaging interval is K1*K2 steps.
+ *
+ * All P learners are rows of one replica array on one GPU; a round is a
+ * sequence of kernels enqueued on the handle's HIP stream.  The handle owns
+ * every device buffer it allocates; callers own the buffers they pass in.
+ * A handle is not thread-safe; distinct handles are independent.
+ *
+ * Errors.  Functions returning int return HIERAVG_OK (0) or a negative code;
+ * hieravg_last_error() then describes the failure (thread-local string,
+ * valid until the next failing call on the same thread).  Constructors return
+ * NULL on failure.  Asynchronous GPU faults surface as HIERAVG_EHIP at the
+ * next call that synchronises.
+ */
+#ifndef HIERAVG_H
+#define HIERAVG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct hieravg* hieravg_t;
+
+/* Return codes. */
+#define HIERAVG_OK 0
+#define HIERAVG_EINVAL (-1) /* bad argument or handle                      */
+#define HIERAVG_EHIP (-2)   /* HIP runtime or kernel error                 */
+#define HIERAVG_ESIZE (-3)  /* destination/source size too small / too big */
+
+/* Model kinds (what one learner's SGD step computes). */
+#define HIERAVG_KIND_SOFTMAX 0   /* softmax regression, IN -> C             */
+#define HIERAVG_KIND_MLP 1       /* IN -> H (ReLU) -> C, softmax CE         */
+#define HIERAVG_KIND_AVERAGING 2 /* momentum SGD on given gradients, no model */
+
+/* Named workloads accepted by hieravg_create (the `model` argument). */
+#define HIERAVG_MODEL_SOFTMAX_3072_10 0      /* N=2048, class means z, noise std 1 */
+#define HIERAVG_MODEL_MLP_3072_512_10 1      /* N=50000, noise std 0.5             */
+#define HIERAVG_MODEL_MLP_150528_1024_1000 2 /* N=100000, noise std 1              */
+#define HIERAVG_MODEL_AVERAGING_11_7M 3      /* D=11.7e6, momentum 0.9, stds 0.01  */
+
+/*
+ * Full description of a workload.  Synthetic data, minibatch draws, initial
+ * parameters and (averaging kind) the given gradients are all generated on
+ * the GPU from `seed` with the SplitMix64 counter generator (Steele, Lea &
+ * Flood, OOPSLA 2014), H(key, c) = mix64(key + (c + 1) * 0x9E3779B97F4A7C15):
+ *   sample s of learner j at global step t: H(k_index, t<<32 | j<<16 | s) mod N
+ *   label of row i:                         H(k_label, i) mod C
+ *   X[i][d] = fp32(mu[y_i][d] + noise_std * z(k_noise, i*IN + d)),
+ *   mu[c][d] = z(k_mean, c*IN + d),  z = exact Irwin-Hall(12) normal surrogate,
+ *   weights (2u - 1) * fp32(1/sqrt(fan_in)), u = (H(k_init, layer<<48 | e) >> 40) / 2^24,
+ *   biases 0; averaging kind: w0[d] = fp32(init_std * z(k_init, d)) and
+ *   gradient of learner j at step-in-round k: fp32(grad_std * z(k_grad, (k*2^16 + j)*D + d)).
+ * Stream keys are k_x = H(seed, tag_x) for fixed 64-bit tags.
+ */
+typedef struct hieravg_config {
+  int32_t P;        /* learners, 1 <= P < 65536                            */
+  int32_t S;        /* learners per local cluster, S | P                    */
+  int32_t K1;       /* local SGD steps per block, >= 1                      */
+  int32_t K2;       /* blocks per round (the paper's beta), >= 1            */
+  int32_t B;        /* minibatch size, 1 <= B < 65536 (ignored: averaging)  */
+  int32_t kind;     /* HIERAVG_KIND_*                                        */
+  int64_t in_dim;   /* softmax/MLP: input features; averaging: D            */
+  int64_t hidden;   /* MLP hidden width; 0 otherwise                        */
+  int64_t classes;  /* softmax/MLP classes; 0 for averaging                 */
+  int64_t n_samples;/* dataset rows N (softmax/MLP), N < 2^32               */
+  float noise_std;  /* data noise std                                       */
+  float lr;         /* step size gamma, finite and >= 0                     */
+  float momentum;   /* averaging kind: heavy-ball coefficient mu in [0, 1)  */
+  float init_std;   /* averaging kind: std of the initial replica           */
+  float grad_std;   /* averaging kind: std of the given gradients           */
+  uint64_t seed;
+} hieravg_config;
+
+/*
+ * Create a handle for one of the named workloads (HIERAVG_MODEL_*), as
+ * Algorithm 1's first line: builds the dataset, draws the initial global
+ * parameter w~_1 and copies it into all P replica rows.  Blocks until the
+ * set-up kernels have finished.  Returns NULL (and sets the last error) on
+ * invalid arguments (P<1, S<1, S not dividing P, K1<1, K2<1, B<1, P or B >=
+ * 65536, lr not finite or negative, unknown model) or allocation failure.
+ */
+hieravg_t hieravg_create(int32_t P, int32_t S, int32_t K1, int32_t K2, int32_t model, float lr,
+                         int32_t B, uint64_t seed);
+
+/* Same, for an explicit workload description (any dimensions). */
+hieravg_t hieravg_create_config(const hieravg_config* cfg);
+
+/*
+ * Enqueue one round (one outer iteration n of Algorithm 1): K2 blocks of K1
+ * local SGD steps, a local mean over each cluster after every block but the
+ * last, and the global mean at the end (the local mean right before the
+ * global mean does not change the exact result and is skipped).
+ * Asynchronous with respect to the host.  Returns HIERAVG_OK or an error.
+ */
+int hieravg_round(hieravg_t h);
+
+/*
+ * Synchronise the handle's stream and copy all replicas to `dst` as a dense
+ * row-major [P][D] float32 array (D = hieravg_dim(h)), each row packed as
+ * softmax [W (C x IN row-major) | b (C)], MLP [W1 (H x IN) | b1 (H) |
+ * W2 (C x H) | b2 (C)], averaging [w (D)].  `dst` may be host or device
+ * memory; `n_floats` is its capacity and must be >= P*D (else HIERAVG_ESIZE).
+ */
+int hieravg_params(hieravg_t h, float* dst, size_t n_floats);
+
+/* Overwrite all replicas from a dense [P][D] array laid out as above (host
+ * or device memory, n_floats >= P*D).  Momentum buffers are left as they are.
+ * Synchronous. */
+int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats);
+
+/* Release every resource of the handle.  NULL-safe. */
+void hieravg_destroy(hieravg_t h);
+
+/* Thread-local description of the last failure ("" if none). */
+const char* hieravg_last_error(void);
+
+/* Parameters per replica D, or a negative code for a NULL handle. */
+int64_t hieravg_dim(hieravg_t h);
+
+/* Global SGD steps taken since creation (K1*K2 per round). */
+int64_t hieravg_step_count(hieravg_t h);
+
+/*
+ * Copy the minibatch indices the last round drew, as int32 [K2][K1][P][B],
+ * to `dst` (host or device, n >= K2*K1*P*B).  Synchronises.  HIERAVG_EINVAL
+ * for the averaging kind (it draws no samples).
+ */
+int hieravg_last_indices(hieravg_t h, int32_t* dst, size_t n);
+
+/*
+ * Make the handle enqueue on `hip_stream` (a hipStream_t, e.g. a torch
+ * stream's handle; NULL selects the handle's own stream).  The caller keeps
+ * ownership of the stream and must keep it alive while the handle uses it.
+ * Synchronises the previous stream first.
+ */
+int hieravg_set_stream(hieravg_t h, void* hip_stream);
+
+/* Block until all work enqueued by the handle has finished. */
+int hieravg_sync(hieravg_t h);
+
+/*
+ * Per-kernel timing with HIP events recorded on the handle's stream around
+ * every launch.  enable != 0 starts recording (clearing earlier records);
+ * enable == 0 stops.  hieravg_profile_read synchronises and writes, for every
+ * kernel class c < min(n, hieravg_kernel_classes()), the number of launches
+ * and their summed duration in milliseconds.
+ */
+int hieravg_profile(hieravg_t h, int enable);
+int hieravg_profile_read(hieravg_t h, int64_t* launches, double* total_ms, int n);
+int hieravg_kernel_classes(void);
+const char* hieravg_kernel_class_name(int c);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HIERAVG_H */

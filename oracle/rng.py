@@ -151,17 +151,21 @@ def init_uniform(seed: int, layer: int, rows: int, cols: int):
     return w.reshape(rows, cols)
 
 
-def init_vector(seed: int, D: int, std: float):
-    """Initial replica of the averaging-only workload: fp32(std * z)."""
+def init_vector(seed: int, D: int, std: float, cols=None):
+    """Initial replica of the averaging-only workload: fp32(std * z); only the
+    coordinates `cols` when given (coordinates never interact)."""
     key = stream_key(seed, TAG_INIT)
-    z = normal_surrogate(key, np.arange(D, dtype=np.uint64))
+    d = np.arange(D, dtype=np.uint64) if cols is None else np.asarray(cols, dtype=np.uint64)
+    z = normal_surrogate(key, d)
     return (float(np.float32(std)) * z).astype(np.float32).astype(np.float64)
 
 
-def given_gradients(seed: int, k: int, learner: int, D: int, std: float):
+def given_gradients(seed: int, k: int, learner: int, D: int, std: float, cols=None):
     """Gradient handed to learner `learner` at step-in-round k in the
-    averaging-only workload: fp32(std * z) at counters (k*2^16 + j)*D + d."""
+    averaging-only workload: fp32(std * z) at counters (k*2^16 + j)*D + d
+    (only the coordinates `cols` when given)."""
     key = stream_key(seed, TAG_GRAD)
     base = (np.uint64(k) * np.uint64(65536) + np.uint64(learner)) * np.uint64(D)
-    z = normal_surrogate(key, base + np.arange(D, dtype=np.uint64))
+    d = np.arange(D, dtype=np.uint64) if cols is None else np.asarray(cols, dtype=np.uint64)
+    z = normal_surrogate(key, base + d)
     return (float(np.float32(std)) * z).astype(np.float32).astype(np.float64)

@@ -1,0 +1,561 @@
+// C ABI, handle and round scheduler of the Hier-AVG hot path (Algorithm 1,
+// Sec. 3.1).  A round is enqueued on one HIP stream with no host
+// synchronisation inside it:
+//
+//   draw the round's minibatch indices
+//   for b in 0..K2-1, k in 0..K1-1:    one local SGD step of all P learners
+//     (after the last step of block b < K2-1: local mean over each cluster)
+//   global mean over all P learners
+//
+// The local mean right before the global mean is left out: means of
+// equal-size cluster means equal the global mean, so it changes nothing but
+// rounding.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace hav;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+void set_error(const std::string& s) { g_last_error = s; }
+
+const char* kClassNames[KC_COUNT] = {
+    "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",  "softmax_grad",     "bwd_hidden",
+    "update2_gemm", "update1_gemm", "group_mean",   "global_mean", "momentum",        "momentum_group_mean",
+    "momentum_global_mean"};
+
+struct ProfRec {
+  hipEvent_t a, b;
+  int kc;
+};
+
+#define HAV_CHECK(expr)                                                                 \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) {                                                             \
+      set_error(std::string(#expr) + " failed: " + hipGetErrorString(e_));             \
+      return HIERAVG_EHIP;                                                              \
+    }                                                                                   \
+  } while (0)
+
+}  // namespace
+
+struct hieravg {
+  hieravg_config cfg{};
+  int64_t IN = 0, H = 0, C = 0, N = 0;
+  int64_t INp = 0, Hp = 0, Cp = 0;
+  int64_t D = 0, Dp = 0;
+  int Bp = 0;
+  int64_t off_W1 = 0, off_b1 = 0, off_W2 = 0, off_b2 = 0;
+
+  float* W = nullptr;    // [P][Dp] replicas
+  float* V = nullptr;    // [P][Dp] momentum buffers (averaging kind)
+  float* Gr = nullptr;   // [K1*K2][P][Dp] given gradients (averaging kind)
+  float* X = nullptr;    // [N][INp] dataset
+  int32_t* y = nullptr;  // [N] labels
+  int32_t* idx = nullptr;  // [K2][K1][P][B] indices of the current round
+  float* part = nullptr;   // split-K partial sums
+  float* Z1 = nullptr;     // [P][Bp][Hp] hidden pre-activations
+  float* G2 = nullptr;     // [P][Bp][Cp] output error
+  float* G1 = nullptr;     // [P][Bp][Hp] hidden error
+  uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
+
+  uint64_t key_index = 0;
+  int KS1 = 1, cps1 = 1, KS2 = 1, cps2 = 1;
+  hipStream_t own_stream = nullptr, stream = nullptr;
+  int64_t steps = 0;
+
+  bool profiling = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+template <class F>
+void run(hieravg* h, int kc, F&& launch) {
+  if (!h->profiling) {
+    launch();
+    return;
+  }
+  hipEvent_t ev[2];
+  for (int i = 0; i < 2; ++i) {
+    if (!h->pool.empty()) {
+      ev[i] = h->pool.back();
+      h->pool.pop_back();
+    } else if (hipEventCreate(&ev[i]) != hipSuccess) {
+      launch();
+      return;
+    }
+  }
+  hipEventRecord(ev[0], h->stream);
+  launch();
+  hipEventRecord(ev[1], h->stream);
+  h->recs.push_back({ev[0], ev[1], kc});
+}
+
+void release(hieravg* h) {
+  if (!h) return;
+  if (h->stream) hipStreamSynchronize(h->stream);
+  void* bufs[] = {h->W, h->V, h->Gr, h->X, h->y, h->idx, h->part, h->Z1, h->G2, h->G1, h->ctr};
+  for (void* b : bufs)
+    if (b) hipFree(b);
+  for (auto& r : h->recs) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  for (auto e : h->pool) hipEventDestroy(e);
+  if (h->own_stream) hipStreamDestroy(h->own_stream);
+  delete h;
+}
+
+int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    set_error(std::string("hipMalloc of ") + what + " (" + std::to_string(bytes) + " bytes) failed: " +
+              hipGetErrorString(e));
+    return HIERAVG_EHIP;
+  }
+  e = hipMemsetAsync(*p, 0, bytes, h->stream);
+  if (e != hipSuccess) {
+    set_error(std::string("hipMemsetAsync failed: ") + hipGetErrorString(e));
+    return HIERAVG_EHIP;
+  }
+  return HIERAVG_OK;
+}
+
+int validate(const hieravg_config& c) {
+  auto bad = [](const char* m) {
+    set_error(m);
+    return HIERAVG_EINVAL;
+  };
+  if (c.P < 1 || c.P > 65535) return bad("P must be in [1, 65535]");
+  if (c.S < 1) return bad("S must be >= 1");
+  if (c.P % c.S != 0) return bad("S must divide P (Sec. 2: S | P)");
+  if (c.K1 < 1) return bad("K1 must be >= 1");
+  if (c.K2 < 1) return bad("K2 must be >= 1");
+  if ((int64_t)c.K1 * c.K2 > (1 << 20)) return bad("K1*K2 must be <= 2^20");
+  if (!std::isfinite(c.lr) || c.lr < 0.0f) return bad("lr must be finite and >= 0");
+  if (c.kind == HIERAVG_KIND_AVERAGING) {
+    if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
+    if (!std::isfinite(c.momentum) || c.momentum < 0.0f || c.momentum >= 1.0f)
+      return bad("averaging: momentum must be in [0, 1)");
+    if (!std::isfinite(c.init_std) || !std::isfinite(c.grad_std)) return bad("averaging: stds must be finite");
+    if ((int64_t)c.K1 * c.K2 * c.P > 65535) return bad("averaging: K1*K2*P must be <= 65535");
+    return HIERAVG_OK;
+  }
+  if (c.kind != HIERAVG_KIND_SOFTMAX && c.kind != HIERAVG_KIND_MLP) return bad("unknown model kind");
+  if (c.B < 1 || c.B > 65535) return bad("B must be in [1, 65535]");
+  if (c.in_dim < 1 || c.in_dim > (1 << 24)) return bad("in_dim must be in [1, 2^24]");
+  if (c.classes < 1 || c.classes > (1 << 20)) return bad("classes must be in [1, 2^20]");
+  if (c.kind == HIERAVG_KIND_MLP && (c.hidden < 1 || c.hidden > (1 << 20))) return bad("hidden must be in [1, 2^20]");
+  if (c.n_samples < 1 || c.n_samples > 0x7fffffffLL) return bad("n_samples must be in [1, 2^31 - 1]");
+  if (!std::isfinite(c.noise_std)) return bad("noise_std must be finite");
+  if ((int64_t)c.K1 * c.K2 * c.P * c.B > 0x7fffffffLL) return bad("K1*K2*P*B must be < 2^31");
+  return HIERAVG_OK;
+}
+
+float fan_in_scale(int64_t fan_in) { return (float)(1.0 / std::sqrt((double)fan_in)); }
+
+int build(hieravg* h) {
+  const hieravg_config& c = h->cfg;
+  HAV_CHECK(hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
+  h->stream = h->own_stream;
+  const int P = c.P;
+  const uint64_t seed = c.seed;
+
+  if (c.kind == HIERAVG_KIND_AVERAGING) {
+    h->D = c.in_dim;
+    h->Dp = round_up(h->D, 64);
+    const int T = c.K1 * c.K2;
+    int rc;
+    if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->V, sizeof(float) * P * h->Dp, "momentum buffers"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->Gr, sizeof(float) * (size_t)T * P * h->Dp, "given gradients"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
+    launch_init_vector(h->stream, h->W, h->D, hash64(seed, kTagInit), c.init_std);
+    launch_gen_grads(h->stream, h->Gr, h->D, h->Dp, P, T, hash64(seed, kTagGrad), c.grad_std);
+  } else {
+    const bool mlp = c.kind == HIERAVG_KIND_MLP;
+    h->IN = c.in_dim;
+    h->C = c.classes;
+    h->H = mlp ? c.hidden : 0;
+    h->N = c.n_samples;
+    h->INp = round_up(h->IN, 64);
+    h->Cp = round_up(h->C, 16);
+    h->Hp = mlp ? round_up(h->H, 64) : 0;
+    h->Bp = (int)round_up(c.B, 16);
+    if (mlp) {
+      h->off_W1 = 0;
+      h->off_b1 = h->Hp * h->INp;
+      h->off_W2 = h->off_b1 + h->Hp;
+      h->off_b2 = h->off_W2 + h->Cp * h->Hp;
+      h->Dp = round_up(h->off_b2 + h->Cp, 64);
+      h->D = h->H * h->IN + h->H + h->C * h->H + h->C;
+      plan_split(P, (int)h->Hp, (int)h->INp, &h->KS1, &h->cps1);
+      plan_split(P, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
+    } else {
+      h->off_W1 = 0;
+      h->off_b1 = h->Cp * h->INp;
+      h->Dp = round_up(h->off_b1 + h->Cp, 64);
+      h->D = h->C * h->IN + h->C;
+      plan_split(P, (int)h->Cp, (int)h->INp, &h->KS1, &h->cps1);
+    }
+    const int T = c.K1 * c.K2;
+    const int64_t n1 = mlp ? h->Hp : h->Cp;
+    const int64_t part_floats =
+        std::max<int64_t>((int64_t)h->KS1 * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
+    int rc;
+    if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->X, sizeof(float) * h->N * h->INp, "dataset"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->y, sizeof(int32_t) * h->N, "labels"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->idx, sizeof(int32_t) * (size_t)T * P * c.B, "indices"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->part, sizeof(float) * part_floats, "split-K partials"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->G2, sizeof(float) * P * h->Bp * h->Cp, "output error"))) return rc;
+    if (mlp) {
+      if ((rc = alloc_zero(h, (void**)&h->Z1, sizeof(float) * P * h->Bp * h->Hp, "hidden activations"))) return rc;
+      if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
+    }
+    if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
+    h->key_index = hash64(seed, kTagIndex);
+    launch_gen_labels(h->stream, h->y, h->N, hash64(seed, kTagLabel), (uint64_t)h->C);
+    launch_gen_data(h->stream, h->X, h->y, h->N, h->IN, h->INp, hash64(seed, kTagMean), hash64(seed, kTagNoise),
+                    c.noise_std);
+    const uint64_t kinit = hash64(seed, kTagInit);
+    if (mlp) {
+      launch_init_matrix(h->stream, h->W + h->off_W1, h->H, h->IN, h->INp, kinit, 0, fan_in_scale(h->IN));
+      launch_init_matrix(h->stream, h->W + h->off_W2, h->C, h->H, h->Hp, kinit, 1, fan_in_scale(h->H));
+    } else {
+      launch_init_matrix(h->stream, h->W + h->off_W1, h->C, h->IN, h->INp, kinit, 0, fan_in_scale(h->IN));
+    }
+  }
+  HAV_CHECK(hipGetLastError());
+  // Synchronize every learner with w~_1 (Algorithm 1, first lines).
+  for (int p = 1; p < P; ++p)
+    HAV_CHECK(hipMemcpyAsync(h->W + (int64_t)p * h->Dp, h->W, sizeof(float) * h->Dp, hipMemcpyDeviceToDevice,
+                             h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  return HIERAVG_OK;
+}
+
+// One local SGD step of all P learners at step tt of the round (Algorithm 1:
+// w <- w - lr/B * sum_s grad f(w; xi_s) for every learner concurrently).
+void enqueue_step(hieravg* h, int tt) {
+  const hieravg_config& c = h->cfg;
+  const int P = c.P, B = c.B;
+  const int32_t* ix = h->idx + (int64_t)tt * P * B;
+  hipStream_t s = h->stream;
+  if (c.kind == HIERAVG_KIND_SOFTMAX) {
+    FwdArgs f{h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->part, P, B, h->Bp, (int)h->Cp, (int)h->INp,
+              h->KS1, h->cps1};
+    run(h, KC_FWD1, [&] { launch_fwd(s, f, A_GATHER); });
+    run(h, KC_SOFTMAX, [&] {
+      launch_softmax_grad(s, h->part, h->KS1, h->W + h->off_b1, h->Dp, h->y, ix, h->G2, P, B, h->Bp, (int)h->C,
+                          (int)h->Cp);
+    });
+    UpdArgs u{h->G2, h->Cp, h->Bp, h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->W + h->off_b1,
+              P, B, (int)h->Cp, (int)h->INp, c.lr};
+    run(h, KC_UPDATE1, [&] { launch_update(s, u, A_GATHER); });
+    return;
+  }
+  FwdArgs f1{h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->part, P, B, h->Bp, (int)h->Hp, (int)h->INp,
+             h->KS1, h->cps1};
+  run(h, KC_FWD1, [&] { launch_fwd(s, f1, A_GATHER); });
+  run(h, KC_REDUCE1, [&] {
+    launch_reduce_bias(s, h->part, h->KS1, h->W + h->off_b1, h->Dp, h->Z1, P, B, h->Bp, (int)h->Hp);
+  });
+  FwdArgs f2{h->Z1, nullptr, h->Hp, h->W + h->off_W2, h->Dp, h->Hp, h->part, P, B, h->Bp, (int)h->Cp, (int)h->Hp,
+             h->KS2, h->cps2};
+  run(h, KC_FWD2, [&] { launch_fwd(s, f2, A_RELU); });
+  run(h, KC_SOFTMAX, [&] {
+    launch_softmax_grad(s, h->part, h->KS2, h->W + h->off_b2, h->Dp, h->y, ix, h->G2, P, B, h->Bp, (int)h->C,
+                        (int)h->Cp);
+  });
+  run(h, KC_BWD_HIDDEN, [&] {
+    launch_bwd_hidden(s, h->G2, h->W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, h->Bp, (int)h->C, (int)h->Cp,
+                      (int)h->Hp);
+  });
+  UpdArgs u2{h->G2, h->Cp, h->Bp, h->Z1, nullptr, h->Hp, h->W + h->off_W2, h->Dp, h->Hp, h->W + h->off_b2,
+             P, B, (int)h->Cp, (int)h->Hp, c.lr};
+  run(h, KC_UPDATE2, [&] { launch_update(s, u2, A_RELU); });
+  UpdArgs u1{h->G1, h->Hp, h->Bp, h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->W + h->off_b1,
+             P, B, (int)h->Hp, (int)h->INp, c.lr};
+  run(h, KC_UPDATE1, [&] { launch_update(s, u1, A_GATHER); });
+}
+
+struct Segment {
+  int64_t rows, cols, src_ld, src_off, dst_off;
+};
+
+std::vector<Segment> segments(const hieravg* h) {
+  if (h->cfg.kind == HIERAVG_KIND_AVERAGING) return {{1, h->D, h->D, 0, 0}};
+  if (h->cfg.kind == HIERAVG_KIND_SOFTMAX)
+    return {{h->C, h->IN, h->INp, h->off_W1, 0}, {1, h->C, h->C, h->off_b1, h->C * h->IN}};
+  const int64_t o1 = h->H * h->IN, o2 = o1 + h->H, o3 = o2 + h->C * h->H;
+  return {{h->H, h->IN, h->INp, h->off_W1, 0},
+          {1, h->H, h->H, h->off_b1, o1},
+          {h->C, h->H, h->Hp, h->off_W2, o2},
+          {1, h->C, h->C, h->off_b2, o3}};
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hieravg_last_error(void) { return g_last_error.c_str(); }
+
+hieravg_t hieravg_create_config(const hieravg_config* cfg) {
+  if (!cfg) {
+    set_error("cfg is NULL");
+    return nullptr;
+  }
+  if (validate(*cfg) != HIERAVG_OK) return nullptr;
+  hieravg* h = new (std::nothrow) hieravg;
+  if (!h) {
+    set_error("out of host memory");
+    return nullptr;
+  }
+  h->cfg = *cfg;
+  if (build(h) != HIERAVG_OK) {
+    std::string msg = g_last_error;
+    release(h);
+    set_error(msg);
+    return nullptr;
+  }
+  g_last_error.clear();
+  return h;
+}
+
+hieravg_t hieravg_create(int32_t P, int32_t S, int32_t K1, int32_t K2, int32_t model, float lr, int32_t B,
+                         uint64_t seed) {
+  hieravg_config c{};
+  c.P = P;
+  c.S = S;
+  c.K1 = K1;
+  c.K2 = K2;
+  c.B = B;
+  c.lr = lr;
+  c.seed = seed;
+  switch (model) {
+    case HIERAVG_MODEL_SOFTMAX_3072_10:
+      c.kind = HIERAVG_KIND_SOFTMAX;
+      c.in_dim = 3072;
+      c.classes = 10;
+      c.n_samples = 2048;
+      c.noise_std = 1.0f;
+      break;
+    case HIERAVG_MODEL_MLP_3072_512_10:
+      c.kind = HIERAVG_KIND_MLP;
+      c.in_dim = 3072;
+      c.hidden = 512;
+      c.classes = 10;
+      c.n_samples = 50000;
+      c.noise_std = 0.5f;
+      break;
+    case HIERAVG_MODEL_MLP_150528_1024_1000:
+      c.kind = HIERAVG_KIND_MLP;
+      c.in_dim = 150528;
+      c.hidden = 1024;
+      c.classes = 1000;
+      c.n_samples = 100000;
+      c.noise_std = 1.0f;
+      break;
+    case HIERAVG_MODEL_AVERAGING_11_7M:
+      c.kind = HIERAVG_KIND_AVERAGING;
+      c.in_dim = 11700000;
+      c.momentum = 0.9f;
+      c.init_std = 0.01f;
+      c.grad_std = 0.01f;
+      break;
+    default:
+      set_error("unknown model id " + std::to_string(model));
+      return nullptr;
+  }
+  return hieravg_create_config(&c);
+}
+
+int hieravg_round(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  const hieravg_config& c = h->cfg;
+  const int T = c.K1 * c.K2;
+  const int P = c.P, S = c.S;
+  hipStream_t s = h->stream;
+  if (c.kind == HIERAVG_KIND_AVERAGING) {
+    for (int b = 0; b < c.K2; ++b) {
+      for (int k = 0; k < c.K1; ++k) {
+        const int tt = b * c.K1 + k;
+        const float* g = h->Gr + (int64_t)tt * P * h->Dp;
+        const bool end_block = k == c.K1 - 1, end_round = end_block && b == c.K2 - 1;
+        if (end_round && P > 1)
+          run(h, KC_MOMENTUM_GLOBAL, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, P, true, c.lr, c.momentum); });
+        else if (end_block && !end_round && S > 1)
+          run(h, KC_MOMENTUM_GROUP, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, S, true, c.lr, c.momentum); });
+        else
+          run(h, KC_MOMENTUM, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, 1, false, c.lr, c.momentum); });
+      }
+    }
+  } else {
+    run(h, KC_DRAW, [&] {
+      launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, c.B, T, (uint64_t)h->N, h->key_index);
+    });
+    for (int b = 0; b < c.K2; ++b) {
+      for (int k = 0; k < c.K1; ++k) enqueue_step(h, b * c.K1 + k);
+      if (b < c.K2 - 1 && S > 1) run(h, KC_GROUP_MEAN, [&] { launch_group_mean(s, h->W, h->Dp, P, S); });
+    }
+    if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_group_mean(s, h->W, h->Dp, P, P); });
+  }
+  HAV_CHECK(hipGetLastError());
+  h->steps += T;
+  return HIERAVG_OK;
+}
+
+int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {
+  if (!h || !dst) {
+    set_error("NULL handle or destination");
+    return HIERAVG_EINVAL;
+  }
+  const int P = h->cfg.P;
+  if (n_floats < (size_t)P * (size_t)h->D) {
+    set_error("destination holds " + std::to_string(n_floats) + " floats, need P*D = " +
+              std::to_string((int64_t)P * h->D));
+    return HIERAVG_ESIZE;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (int p = 0; p < P; ++p)
+    for (const Segment& g : segments(h))
+      HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
+                                 h->W + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
+                                 sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  return HIERAVG_OK;
+}
+
+int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
+  if (!h || !src) {
+    set_error("NULL handle or source");
+    return HIERAVG_EINVAL;
+  }
+  const int P = h->cfg.P;
+  if (n_floats < (size_t)P * (size_t)h->D) {
+    set_error("source holds fewer than P*D floats");
+    return HIERAVG_ESIZE;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (int p = 0; p < P; ++p)
+    for (const Segment& g : segments(h))
+      HAV_CHECK(hipMemcpy2DAsync(h->W + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
+                                 src + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
+                                 sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  return HIERAVG_OK;
+}
+
+void hieravg_destroy(hieravg_t h) { release(h); }
+
+int64_t hieravg_dim(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  return h->D;
+}
+
+int64_t hieravg_step_count(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  return h->steps;
+}
+
+int hieravg_last_indices(hieravg_t h, int32_t* dst, size_t n) {
+  if (!h || !dst) {
+    set_error("NULL handle or destination");
+    return HIERAVG_EINVAL;
+  }
+  if (h->cfg.kind == HIERAVG_KIND_AVERAGING) {
+    set_error("the averaging-only workload draws no samples");
+    return HIERAVG_EINVAL;
+  }
+  const size_t need = (size_t)h->cfg.K1 * h->cfg.K2 * h->cfg.P * h->cfg.B;
+  if (n < need) {
+    set_error("destination holds fewer than K2*K1*P*B indices");
+    return HIERAVG_ESIZE;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  HAV_CHECK(hipMemcpy(dst, h->idx, need * sizeof(int32_t), hipMemcpyDefault));
+  return HIERAVG_OK;
+}
+
+int hieravg_set_stream(hieravg_t h, void* hip_stream) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  h->stream = hip_stream ? (hipStream_t)hip_stream : h->own_stream;
+  return HIERAVG_OK;
+}
+
+int hieravg_sync(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  return HIERAVG_OK;
+}
+
+int hieravg_profile(hieravg_t h, int enable) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (auto& r : h->recs) {
+    h->pool.push_back(r.a);
+    h->pool.push_back(r.b);
+  }
+  h->recs.clear();
+  h->profiling = enable != 0;
+  return HIERAVG_OK;
+}
+
+int hieravg_profile_read(hieravg_t h, int64_t* launches, double* total_ms, int n) {
+  if (!h || !launches || !total_ms || n < 0) {
+    set_error("bad arguments");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (int i = 0; i < n; ++i) {
+    launches[i] = 0;
+    total_ms[i] = 0.0;
+  }
+  for (auto& r : h->recs) {
+    float ms = 0.0f;
+    HAV_CHECK(hipEventElapsedTime(&ms, r.a, r.b));
+    if (r.kc < n) {
+      launches[r.kc] += 1;
+      total_ms[r.kc] += ms;
+    }
+  }
+  return HIERAVG_OK;
+}
+
+int hieravg_kernel_classes(void) { return KC_COUNT; }
+
+const char* hieravg_kernel_class_name(int c) { return (c >= 0 && c < KC_COUNT) ? kClassNames[c] : ""; }
+
+}  // extern "C"

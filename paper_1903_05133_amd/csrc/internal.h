@@ -1,0 +1,143 @@
+// Internal declarations of the Hier-AVG HIP library (gfx950).
+//
+// Replica layout in HBM.  Every learner j owns row j of one [P][Dp] float32
+// array.  A row holds the model's parameter blocks at offsets that are
+// multiples of 16 floats, each block stored with padded dimensions
+// (INp = roundup(IN, 64), Hp = roundup(H, 64), Cp = roundup(C, 16)) so that the
+// GEMM kernels need no ragged-edge handling along K.  Padding entries are
+// zero when the handle is created and stay zero: a zero input column, a zero
+// hidden unit (ReLU(0) has derivative 0) and a zero class (masked out of the
+// softmax) all receive zero gradient, and means of zeros are zero.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "hieravg.h"
+
+namespace hav {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// ------------------------------------------------------------ SplitMix64
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
+
+__host__ __device__ inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// H(key, c): SplitMix64 output at counter c of the stream `key`.
+__host__ __device__ inline uint64_t hash64(uint64_t key, uint64_t c) { return mix64(key + (c + 1) * kGolden); }
+
+// Exact Irwin-Hall(12) normal surrogate: the twelve 16-bit fields of three
+// hashes, summed, centred and scaled by 2^-16 (exactly representable).
+__device__ inline float irwin_hall(uint64_t key, uint64_t e) {
+  int64_t acc = 0;
+#pragma unroll
+  for (int r = 0; r < 3; ++r) {
+    uint64_t v = hash64(key, e * 3 + r);
+    acc += (int64_t)(v & 0xFFFF) + (int64_t)((v >> 16) & 0xFFFF) + (int64_t)((v >> 32) & 0xFFFF) +
+           (int64_t)(v >> 48);
+  }
+  return (float)(acc - 393210) * (1.0f / 65536.0f);
+}
+
+// Stream tags (ASCII names, big-endian).
+constexpr uint64_t kTagIndex = 0x68762e696e646578ull;  // "hv.index"
+constexpr uint64_t kTagLabel = 0x68762e6c6162656cull;  // "hv.label"
+constexpr uint64_t kTagMean = 0x68762e636d65616eull;   // "hv.cmean"
+constexpr uint64_t kTagNoise = 0x68762e6e6f697365ull;  // "hv.noise"
+constexpr uint64_t kTagInit = 0x68762e77696e6974ull;   // "hv.winit"
+constexpr uint64_t kTagGrad = 0x68762e6772616473ull;   // "hv.grads"
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Workgroup index -> logical tile index such that consecutive logical tiles
+// run on the same XCD (the hardware deals workgroups to the 8 XCDs round
+// robin).  Tiles that share operands then share an L2.
+__device__ inline int xcd_remap(int bid, int nblocks) {
+  constexpr int kXcd = 8;
+  int q = nblocks / kXcd, r = nblocks % kXcd;
+  int x = bid % kXcd, i = bid / kXcd;
+  return x * q + (x < r ? x : r) + i;
+}
+
+// ------------------------------------------------------------ kernel classes
+enum KernelClass {
+  KC_DRAW = 0,       // minibatch index draw (once per round)
+  KC_FWD1,           // layer-1 forward GEMM (split-K partials)
+  KC_REDUCE1,        // split-K reduction + bias of layer 1
+  KC_FWD2,           // layer-2 forward GEMM (split-K partials)
+  KC_SOFTMAX,        // logits reduction, softmax, loss gradient
+  KC_BWD_HIDDEN,     // hidden-layer error: (G2 W2) masked by ReLU'
+  KC_UPDATE2,        // layer-2 weight gradient fused with the SGD update
+  KC_UPDATE1,        // layer-1 weight gradient fused with the SGD update
+  KC_GROUP_MEAN,     // local mean over each cluster of S replicas
+  KC_GLOBAL_MEAN,    // global mean over all P replicas
+  KC_MOMENTUM,       // averaging kind: momentum update (no mean)
+  KC_MOMENTUM_GROUP, // averaging kind: momentum update fused with the local mean
+  KC_MOMENTUM_GLOBAL,// averaging kind: momentum update fused with the global mean
+  KC_COUNT
+};
+
+// ------------------------------------------------------------ launchers
+// Data and initial state (k_data.hip).
+void launch_gen_labels(hipStream_t s, int32_t* y, int64_t N, uint64_t key, uint64_t C);
+void launch_gen_data(hipStream_t s, float* X, const int32_t* y, int64_t N, int64_t IN, int64_t INp,
+                     uint64_t key_mean, uint64_t key_noise, float sigma);
+void launch_init_matrix(hipStream_t s, float* W, int64_t rows, int64_t cols, int64_t ld, uint64_t key,
+                        uint64_t layer, float scale);
+void launch_init_vector(hipStream_t s, float* w, int64_t D, uint64_t key, float std);
+void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int T, uint64_t key, float std);
+void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
+                         int T, uint64_t N, uint64_t key);
+
+// GEMMs (k_gemm.hip).
+struct FwdArgs {
+  const float* A;       // gathered: dataset X [N][lda]; relu: Z [P][Mp][lda]
+  const int32_t* idx;   // [P][M] sample indices (gathered A)
+  int64_t lda;
+  const float* W;       // weight block of replica 0 ([N][ldw]); replica p at W + p*w_pitch
+  int64_t w_pitch, ldw;
+  float* part;          // [KS][P][Mp][N]
+  int P, M, Mp, N, K;   // N multiple of 16, K multiple of 32
+  int KS, cps;          // split count and 32-wide K chunks per split
+};
+enum ASource { A_GATHER = 0, A_RELU = 1 };
+void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src);
+void plan_split(int P, int N, int K, int* KS, int* cps);
+
+struct UpdArgs {
+  const float* G;       // [P][Mp][ldg] error rows (row s = sample, column m = output unit)
+  int64_t ldg;
+  int Mp;               // rows per learner in G and in the relu source
+  const float* Bsrc;    // gathered: dataset X [N][ldb]; relu: Z [P][Mp][ldb]
+  const int32_t* idx;   // [P][Kb]
+  int64_t ldb;
+  float* W;             // weight block of replica 0 ([Mrows][ldw]); replica p at W + p*w_pitch
+  int64_t w_pitch, ldw;
+  float* bias;          // bias block of replica 0 (or nullptr); replica p at bias + p*w_pitch
+  int P, Kb, Mrows, Ncols;
+  float lr;
+};
+void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
+
+// Head of the network (k_head.hip).
+void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
+                        int P, int M, int Mp, int N);
+void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
+                         const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C,
+                         int Cp);
+void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
+                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp);
+
+// Averaging (k_avg.hip).
+void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S);
+void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
+                          bool average, float lr, float mu);
+
+}  // namespace hav

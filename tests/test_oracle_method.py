@@ -285,3 +285,14 @@ def test_groups_are_contiguous_and_independent(S):
             w = np.mean([torch_sgd_run(p, w, j, b * K1, K1) for j in range(q * S, q * S + S)], axis=0)
         for j in range(q * S, q * S + S):
             assert relerr(st.W[j], w) < 1e-12
+
+
+def test_averaging_column_sampling_is_exact():
+    """Restricting the averaging-only workload to a subset of coordinates
+    gives exactly those coordinates of the full run."""
+    p = small(M.AVERAGING, 4, 2, 2, 2, lr=0.1, momentum=0.9, IN=777)
+    full = M.run(p, 2)
+    cols = np.array([0, 5, 300, 776])
+    part = M.run(p, 2, cols=cols)
+    assert np.array_equal(part.W, full.W[:, cols])
+    assert np.array_equal(part.V, full.V[:, cols])
