@@ -27,9 +27,9 @@ thread_local std::string g_last_error;
 void set_error(const std::string& s) { g_last_error = s; }
 
 const char* kClassNames[KC_COUNT] = {
-    "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",  "softmax_grad",     "bwd_hidden",
-    "update2_gemm", "update1_gemm", "group_mean",   "global_mean", "momentum",        "momentum_group_mean",
-    "momentum_global_mean"};
+    "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",   "softmax_grad", "bwd_hidden",
+    "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
+    "momentum",     "momentum_group_mean",          "momentum_global_mean"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -63,6 +63,7 @@ struct hieravg {
   int32_t* idx = nullptr;  // [K2][K1][P][B] indices of the current round
   float* part = nullptr;   // split-K partial sums
   float* Z1 = nullptr;     // [P][Bp][Hp] hidden pre-activations
+  float* PL = nullptr;     // [P][Bp][Cp][Hp/32] partial logits (small-C MLP)
   float* G2 = nullptr;     // [P][Bp][Cp] output error
   float* G1 = nullptr;     // [P][Bp][Hp] hidden error
   uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
@@ -95,24 +96,24 @@ void run(hieravg* h, int kc, F&& launch) {
       return;
     }
   }
-  hipEventRecord(ev[0], h->stream);
+  (void)hipEventRecord(ev[0], h->stream);
   launch();
-  hipEventRecord(ev[1], h->stream);
+  (void)hipEventRecord(ev[1], h->stream);
   h->recs.push_back({ev[0], ev[1], kc});
 }
 
 void release(hieravg* h) {
   if (!h) return;
-  if (h->stream) hipStreamSynchronize(h->stream);
-  void* bufs[] = {h->W, h->V, h->Gr, h->X, h->y, h->idx, h->part, h->Z1, h->G2, h->G1, h->ctr};
+  if (h->stream) (void)hipStreamSynchronize(h->stream);
+  void* bufs[] = {h->W, h->V, h->Gr, h->X, h->y, h->idx, h->part, h->Z1, h->PL, h->G2, h->G1, h->ctr};
   for (void* b : bufs)
-    if (b) hipFree(b);
+    if (b) (void)hipFree(b);
   for (auto& r : h->recs) {
-    hipEventDestroy(r.a);
-    hipEventDestroy(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
   }
-  for (auto e : h->pool) hipEventDestroy(e);
-  if (h->own_stream) hipStreamDestroy(h->own_stream);
+  for (auto e : h->pool) (void)hipEventDestroy(e);
+  if (h->own_stream) (void)hipStreamDestroy(h->own_stream);
   delete h;
 }
 
@@ -201,14 +202,14 @@ int build(hieravg* h) {
       h->off_b2 = h->off_W2 + h->Cp * h->Hp;
       h->Dp = round_up(h->off_b2 + h->Cp, 64);
       h->D = h->H * h->IN + h->H + h->C * h->H + h->C;
-      plan_split(P, (int)h->Hp, (int)h->INp, &h->KS1, &h->cps1);
-      plan_split(P, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
+      plan_split(P, h->Bp, (int)h->Hp, (int)h->INp, &h->KS1, &h->cps1);
+      plan_split(P, h->Bp, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
     } else {
       h->off_W1 = 0;
       h->off_b1 = h->Cp * h->INp;
       h->Dp = round_up(h->off_b1 + h->Cp, 64);
       h->D = h->C * h->IN + h->C;
-      plan_split(P, (int)h->Cp, (int)h->INp, &h->KS1, &h->cps1);
+      plan_split(P, h->Bp, (int)h->Cp, (int)h->INp, &h->KS1, &h->cps1);
     }
     const int T = c.K1 * c.K2;
     const int64_t n1 = mlp ? h->Hp : h->Cp;
@@ -221,6 +222,9 @@ int build(hieravg* h) {
     if ((rc = alloc_zero(h, (void**)&h->idx, sizeof(int32_t) * (size_t)T * P * c.B, "indices"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->part, sizeof(float) * part_floats, "split-K partials"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->G2, sizeof(float) * P * h->Bp * h->Cp, "output error"))) return rc;
+    if (mlp && h->C <= kSmallC &&
+        (rc = alloc_zero(h, (void**)&h->PL, sizeof(float) * P * (h->Hp / 32) * h->Bp * h->Cp, "partial logits")))
+      return rc;
     if (mlp) {
       if ((rc = alloc_zero(h, (void**)&h->Z1, sizeof(float) * P * h->Bp * h->Hp, "hidden activations"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
@@ -254,41 +258,44 @@ void enqueue_step(hieravg* h, int tt) {
   const int P = c.P, B = c.B;
   const int32_t* ix = h->idx + (int64_t)tt * P * B;
   hipStream_t s = h->stream;
+  float* W = h->W;
+  const int Bp = h->Bp, C = (int)h->C, Cp = (int)h->Cp, Hp = (int)h->Hp, INp = (int)h->INp;
   if (c.kind == HIERAVG_KIND_SOFTMAX) {
-    FwdArgs f{h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->part, P, B, h->Bp, (int)h->Cp, (int)h->INp,
-              h->KS1, h->cps1};
+    FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, Cp, INp, h->KS1, h->cps1};
     run(h, KC_FWD1, [&] { launch_fwd(s, f, A_GATHER); });
     run(h, KC_SOFTMAX, [&] {
-      launch_softmax_grad(s, h->part, h->KS1, h->W + h->off_b1, h->Dp, h->y, ix, h->G2, P, B, h->Bp, (int)h->C,
-                          (int)h->Cp);
+      launch_softmax_grad(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->y, ix, h->G2, P, B, Bp, C, Cp);
     });
-    UpdArgs u{h->G2, h->Cp, h->Bp, h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->W + h->off_b1,
-              P, B, (int)h->Cp, (int)h->INp, c.lr};
+    UpdArgs u{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp, c.lr};
     run(h, KC_UPDATE1, [&] { launch_update(s, u, A_GATHER); });
     return;
   }
-  FwdArgs f1{h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->part, P, B, h->Bp, (int)h->Hp, (int)h->INp,
-             h->KS1, h->cps1};
+  FwdArgs f1{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, Hp, INp, h->KS1, h->cps1};
   run(h, KC_FWD1, [&] { launch_fwd(s, f1, A_GATHER); });
-  run(h, KC_REDUCE1, [&] {
-    launch_reduce_bias(s, h->part, h->KS1, h->W + h->off_b1, h->Dp, h->Z1, P, B, h->Bp, (int)h->Hp);
-  });
-  FwdArgs f2{h->Z1, nullptr, h->Hp, h->W + h->off_W2, h->Dp, h->Hp, h->part, P, B, h->Bp, (int)h->Cp, (int)h->Hp,
-             h->KS2, h->cps2};
-  run(h, KC_FWD2, [&] { launch_fwd(s, f2, A_RELU); });
-  run(h, KC_SOFTMAX, [&] {
-    launch_softmax_grad(s, h->part, h->KS2, h->W + h->off_b2, h->Dp, h->y, ix, h->G2, P, B, h->Bp, (int)h->C,
-                        (int)h->Cp);
-  });
-  run(h, KC_BWD_HIDDEN, [&] {
-    launch_bwd_hidden(s, h->G2, h->W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, h->Bp, (int)h->C, (int)h->Cp,
-                      (int)h->Hp);
-  });
-  UpdArgs u2{h->G2, h->Cp, h->Bp, h->Z1, nullptr, h->Hp, h->W + h->off_W2, h->Dp, h->Hp, h->W + h->off_b2,
-             P, B, (int)h->Cp, (int)h->Hp, c.lr};
-  run(h, KC_UPDATE2, [&] { launch_update(s, u2, A_RELU); });
-  UpdArgs u1{h->G1, h->Hp, h->Bp, h->X, ix, h->INp, h->W + h->off_W1, h->Dp, h->INp, h->W + h->off_b1,
-             P, B, (int)h->Hp, (int)h->INp, c.lr};
+  const bool small = C <= kSmallC;
+  if (small) {
+    run(h, KC_HEAD_A, [&] {
+      launch_head_a(s, h->part, h->KS1, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
+    });
+    run(h, KC_HEAD_B, [&] {
+      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, h->G1, h->y, ix, P, B, Bp,
+                    C, Cp, Hp, c.lr);
+    });
+  } else {
+    run(h, KC_REDUCE1, [&] { launch_reduce_bias(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp); });
+    FwdArgs f2{h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, h->part, P, B, Bp, Cp, Hp, h->KS2, h->cps2};
+    run(h, KC_FWD2, [&] { launch_fwd(s, f2, A_RELU); });
+    run(h, KC_SOFTMAX, [&] {
+      launch_softmax_grad(s, h->part, h->KS2, W + h->off_b2, h->Dp, h->y, ix, h->G2, P, B, Bp, C, Cp);
+    });
+    run(h, KC_BWD_HIDDEN, [&] { launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp); });
+    UpdArgs u2{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
+               c.lr};
+    run(h, KC_UPDATE2, [&] { launch_update(s, u2, A_RELU); });
+  }
+  // With the small-C head, b1 took its step in k_head_b.
+  UpdArgs u1{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, small ? nullptr : W + h->off_b1,
+             P, B, Hp, INp, c.lr};
   run(h, KC_UPDATE1, [&] { launch_update(s, u1, A_GATHER); });
 }
 

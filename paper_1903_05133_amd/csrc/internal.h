@@ -70,10 +70,12 @@ __device__ inline int xcd_remap(int bid, int nblocks) {
 enum KernelClass {
   KC_DRAW = 0,       // minibatch index draw (once per round)
   KC_FWD1,           // layer-1 forward GEMM (split-K partials)
-  KC_REDUCE1,        // split-K reduction + bias of layer 1
-  KC_FWD2,           // layer-2 forward GEMM (split-K partials)
-  KC_SOFTMAX,        // logits reduction, softmax, loss gradient
-  KC_BWD_HIDDEN,     // hidden-layer error: (G2 W2) masked by ReLU'
+  KC_REDUCE1,        // large C: split-K reduction + bias of layer 1
+  KC_FWD2,           // large C: layer-2 forward GEMM (split-K partials)
+  KC_SOFTMAX,        // logits reduction, softmax cross-entropy gradient
+  KC_BWD_HIDDEN,     // large C: hidden-layer error (G2 W2) masked by ReLU'
+  KC_HEAD_A,         // small C: layer-1 reduction + bias, partial logits
+  KC_HEAD_B,         // small C: softmax, hidden error, layer-2 and bias updates
   KC_UPDATE2,        // layer-2 weight gradient fused with the SGD update
   KC_UPDATE1,        // layer-1 weight gradient fused with the SGD update
   KC_GROUP_MEAN,     // local mean over each cluster of S replicas
@@ -83,6 +85,9 @@ enum KernelClass {
   KC_MOMENTUM_GLOBAL,// averaging kind: momentum update fused with the global mean
   KC_COUNT
 };
+
+// Largest class count handled by the fused small-C head kernels.
+constexpr int kSmallC = 32;
 
 // ------------------------------------------------------------ launchers
 // Data and initial state (k_data.hip).
@@ -103,13 +108,14 @@ struct FwdArgs {
   int64_t lda;
   const float* W;       // weight block of replica 0 ([N][ldw]); replica p at W + p*w_pitch
   int64_t w_pitch, ldw;
-  float* part;          // [KS][P][Mp][N]
-  int P, M, Mp, N, K;   // N multiple of 16, K multiple of 32
-  int KS, cps;          // split count and 32-wide K chunks per split
+  float* part;          // [KS][P][Mp][N] split-K partial sums
+  int P, M, Mp, N, K;   // N multiple of 16, K multiple of 64
+  int KS, cps;          // split count and 64-wide K chunks per split
 };
 enum ASource { A_GATHER = 0, A_RELU = 1 };
 void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src);
-void plan_split(int P, int N, int K, int* KS, int* cps);
+void plan_split(int P, int Mp, int N, int K, int* KS, int* cps);
+int fwd_tiles(int P, int Mp, int N);
 
 struct UpdArgs {
   const float* G;       // [P][Mp][ldg] error rows (row s = sample, column m = output unit)
@@ -130,10 +136,14 @@ void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
                         int P, int M, int Mp, int N);
 void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
-                         const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C,
-                         int Cp);
+                         const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp);
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp);
+void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp);
+void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
+                   const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
+                   int Cp, int Hp, float lr);
 
 // Averaging (k_avg.hip).
 void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S);

@@ -1,29 +1,22 @@
-// Loss-side work of one local SGD step: split-K reduction with the bias, the
-// softmax cross-entropy gradient (mean over the minibatch, Algorithm 1 in
-// Sec. 3.1 scales the summed gradient by 1/B), and the hidden-layer error.
+// Loss-side work of one local SGD step: the softmax cross-entropy gradient
+// (mean over the minibatch: Algorithm 1 in Sec. 3.1 scales the summed
+// gradient by 1/B), the hidden-layer error, and the second layer's update.
+//
+// Two forms:
+//  * small class count (C <= kSmallC): two fused kernels per step, each with
+//    one workgroup per learner and 32 hidden units.  k_head_a sums the
+//    layer-1 split-K partials with the bias (Z1) and forms this slice's
+//    partial logits; k_head_b adds the slices' partial logits, takes the
+//    softmax gradient, the hidden error, and the second-layer weight and both
+//    bias updates;
+//  * any class count: k_reduce_bias, the layer-2 forward GEMM,
+//    k_softmax_grad and k_bwd_hidden; the second-layer update is the update
+//    GEMM.
+// Every kernel issues its global loads in batches before using them, so a
+// workgroup waits for memory a few times, not once per element.
 #include "internal.h"
 
 namespace hav {
-
-// Z[p][m][n] = sum_ks part[ks][p][m][n] + b_p[n] for m < M; rows M..Mp-1 = 0.
-__global__ __launch_bounds__(256) void k_reduce_bias(const float* __restrict__ part, int KS,
-                                                     const float* __restrict__ bias, int64_t w_pitch,
-                                                     float* __restrict__ Z, int P, int M, int Mp, int N) {
-  const int64_t per = (int64_t)Mp * N;
-  const int64_t total = (int64_t)P * per;
-  const int64_t stride = total;  // part is [KS][P][Mp][N]
-  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int p = (int)(e / per);
-    const int64_t r = e - (int64_t)p * per;
-    const int m = (int)(r / N), n = (int)(r % N);
-    float v = 0.0f;
-    if (m < M) {
-      for (int ks = 0; ks < KS; ++ks) v += part[ks * stride + e];
-      v += bias[(int64_t)p * w_pitch + n];
-    }
-    Z[e] = v;
-  }
-}
 
 __device__ inline float wave_max(float v) {
 #pragma unroll
@@ -36,7 +29,27 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-// One wave per (learner p, sample m < M): logits l_c = sum_ks part + b_c for
+// Z[p][m][n] = b_p[n] + sum_ks part[ks][p][m][n] for m < M; rows M..Mp-1 = 0.
+__global__ __launch_bounds__(256) void k_reduce_bias(const float* __restrict__ part, int KS,
+                                                     const float* __restrict__ bias, int64_t w_pitch,
+                                                     float* __restrict__ Z, int P, int M, int Mp, int N) {
+  const int64_t per = (int64_t)Mp * N;
+  const int64_t total = (int64_t)P * per;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int p = (int)(e / per);
+    const int64_t r = e - (int64_t)p * per;
+    const int m = (int)(r / N), n = (int)(r % N);
+    float v = 0.0f;
+    if (m < M) {
+      v = bias[(int64_t)p * w_pitch + n];
+#pragma unroll 8
+      for (int ks = 0; ks < KS; ++ks) v += part[ks * total + e];
+    }
+    Z[e] = v;
+  }
+}
+
+// One wave per (learner p, sample m < M): logits l_c = b_c + sum_ks part for
 // c < C, G[c] = (softmax(l)_c - [c == y]) / M.  Columns C..Cp-1 stay zero.
 __global__ __launch_bounds__(256) void k_softmax_grad(const float* __restrict__ part, int KS,
                                                       const float* __restrict__ bias, int64_t w_pitch,
@@ -54,6 +67,7 @@ __global__ __launch_bounds__(256) void k_softmax_grad(const float* __restrict__ 
   float mx = -INFINITY;
   for (int c = lane; c < C; c += 64) {
     float v = b[c];
+#pragma unroll 8
     for (int ks = 0; ks < KS; ++ks) v += part[ks * stride + base + c];
     g[c] = v;
     mx = fmaxf(mx, v);
@@ -117,19 +131,183 @@ __global__ __launch_bounds__(256) void k_bwd_hidden(const float* __restrict__ G2
   }
 }
 
-static int grid_cap(int64_t n, int cap) {
-  int64_t g = (n + 255) / 256;
-  return (int)(g < 1 ? 1 : (g < cap ? g : cap));
+// ------------------------------------------------------------ small C
+// Tile = learner p (blockIdx.x / htiles) and hidden units [32*ht, 32*ht + 32);
+// samples in chunks of 32.  KC (16 or 32) is the class capacity, C <= KC.
+// Loads never sit behind a branch: out-of-range rows read a clamped, in-range
+// address and are zeroed by a select, so the compiler can keep many loads in
+// flight and wait for exactly the ones it needs.
+constexpr int kHU = 32;  // hidden units per workgroup
+constexpr int kHM = 32;  // samples per chunk
+
+// Z1 = b1 + sum of the layer-1 partials (stored for k_head_b and the ReLU
+// masks), and this slice's partial logits
+//   PL[p][m][c][ht] = sum_{h in slice} ReLU(Z1[m][h]) * W2[c][h].
+// Thread t reads 16-byte pieces (units 4*(t%8) .. +3) of row t/8 of the chunk.
+template <int KC>
+__global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, int KS, const float* __restrict__ b1,
+                                                const float* __restrict__ W2, int64_t w_pitch,
+                                                float* __restrict__ Z1, float* __restrict__ PL, int P, int M, int Mp,
+                                                int C, int Cp, int Hp, int htiles) {
+  __shared__ float zs[kHM][kHU + 1];
+  __shared__ float ws[KC][kHU + 1];
+  const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
+  const int tid = threadIdx.x, u4 = tid & 7, rr = tid >> 3;
+  const int h4 = ht * kHU + 4 * u4;
+  const float* w2 = W2 + (int64_t)p * w_pitch;
+#pragma unroll
+  for (int i = 0; i < KC * kHU / 256; ++i) {
+    const int e = tid + 256 * i;
+    const int c = e / kHU, hh = e % kHU;
+    const float v = w2[(int64_t)(c < C ? c : 0) * Hp + ht * kHU + hh];
+    ws[c][hh] = c < C ? v : 0.0f;
+  }
+  const f32x4 bias = *(const f32x4*)(b1 + (int64_t)p * w_pitch + h4);
+  const int64_t split = (int64_t)P * Mp * Hp;
+  const float* p0 = part + (int64_t)p * Mp * Hp + h4;
+  for (int m0 = 0; m0 < M; m0 += kHM) {
+    const int m = m0 + rr;
+    const bool mok = m < M;
+    const float* pm = p0 + (int64_t)(mok ? m : 0) * Hp;
+    f32x4 z = bias;
+#pragma unroll 8
+    for (int ks = 0; ks < KS; ++ks) z += *(const f32x4*)(pm + ks * split);
+    if (mok) *(f32x4*)(Z1 + ((int64_t)p * Mp + m) * Hp + h4) = z;
+    zs[rr][4 * u4 + 0] = mok ? fmaxf(z.x, 0.0f) : 0.0f;
+    zs[rr][4 * u4 + 1] = mok ? fmaxf(z.y, 0.0f) : 0.0f;
+    zs[rr][4 * u4 + 2] = mok ? fmaxf(z.z, 0.0f) : 0.0f;
+    zs[rr][4 * u4 + 3] = mok ? fmaxf(z.w, 0.0f) : 0.0f;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kHM * KC / 256; ++k) {
+      const int e = tid + 256 * k, mm = e / KC, c = e % KC;
+      float acc = 0.0f;
+#pragma unroll
+      for (int hh = 0; hh < kHU; ++hh) acc += zs[mm][hh] * ws[c][hh];
+      if (m0 + mm < M && c < C) PL[(((int64_t)p * Mp + m0 + mm) * Cp + c) * htiles + ht] = acc;
+    }
+    __syncthreads();
+  }
+}
+
+// Per 32-sample chunk: the logits of each sample (b2 + the slices' partial
+// logits, added in slice order), its softmax cross-entropy gradient
+// G2 = (softmax - onehot) / M (kept in LDS), then for this slice of units the
+// hidden error G1 = (G2 W2)[m][h] * [Z1 > 0] (W2[:, h] held in registers)
+// and the gradients of b1[h] and W2[:, h].  Thread (u = t%32, g = t/32) owns
+// unit h = 32*ht + u and samples g + 8i of the chunk.  The eight sample groups
+// are combined in LDS in a fixed order; then W2[:, h] and b1[h] take their SGD
+// step after every use of the old column (no other workgroup touches column
+// h).  Slice ht = 0 also updates b2.
+template <int KC>
+__global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, float* __restrict__ W2,
+                                                float* __restrict__ b1, float* __restrict__ b2, int64_t w_pitch,
+                                                const float* __restrict__ Z1, float* __restrict__ G1,
+                                                const int32_t* __restrict__ labels, const int32_t* __restrict__ idx,
+                                                int P, int M, int Mp, int C, int Cp, int Hp, int htiles, float lr) {
+  constexpr int kG = 256 / kHU;     // sample groups
+  constexpr int kR = kHM / kG;      // samples per thread per chunk
+  __shared__ float gs[kHM][KC + 1];
+  __shared__ float red[kG][KC + 1][kHU];
+  __shared__ int ys[kHM];
+  const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
+  const int tid = threadIdx.x, u = tid % kHU, g = tid / kHU;
+  const int h = ht * kHU + u;
+  float* w2 = W2 + (int64_t)p * w_pitch;
+  const float* bb2 = b2 + (int64_t)p * w_pitch;
+  float wc[KC];
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    const float v = w2[(int64_t)(c < C ? c : 0) * Hp + h];
+    wc[c] = c < C ? v : 0.0f;
+  }
+  float db1 = 0.0f, db2 = 0.0f;
+  float dw2[KC];
+#pragma unroll
+  for (int c = 0; c < KC; ++c) dw2[c] = 0.0f;
+  const float invB = 1.0f / (float)M;
+  for (int m0 = 0; m0 < M; m0 += kHM) {
+    const int mn = min(kHM, M - m0);
+    if (tid < kHM) ys[tid] = labels[idx[(int64_t)p * M + m0 + min(tid, mn - 1)]];
+    float z[kR];
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      const int mm = g + kG * i;
+      const float v = Z1[((int64_t)p * Mp + m0 + (mm < mn ? mm : 0)) * Hp + h];
+      z[i] = mm < mn ? v : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kHM * KC / 256; ++k) {
+      const int e = tid + 256 * k, mm = e / KC, c = e % KC;
+      const bool ok = mm < mn && c < C;
+      const float* pl = PL + (((int64_t)p * Mp + m0 + (mm < mn ? mm : 0)) * Cp + (c < C ? c : 0)) * htiles;
+      float l = bb2[c < C ? c : 0];
+#pragma unroll 8
+      for (int t = 0; t < htiles; ++t) l += pl[t];
+      gs[mm][c] = ok ? l : 0.0f;
+    }
+    __syncthreads();
+    if (tid < mn) {
+      float mx = -INFINITY;
+      for (int c = 0; c < C; ++c) mx = fmaxf(mx, gs[tid][c]);
+      float sum = 0.0f;
+      for (int c = 0; c < C; ++c) {
+        const float e = expf(gs[tid][c] - mx);
+        gs[tid][c] = e;
+        sum += e;
+      }
+      const int y = ys[tid];
+      for (int c = 0; c < C; ++c) gs[tid][c] = (gs[tid][c] / sum - (c == y ? 1.0f : 0.0f)) * invB;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      const int mm = g + kG * i;
+      if (mm < mn) {
+        const float a = fmaxf(z[i], 0.0f);
+        float da = 0.0f;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) da += gs[mm][c] * wc[c];
+        const float g1 = z[i] > 0.0f ? da : 0.0f;
+        G1[((int64_t)p * Mp + m0 + mm) * Hp + h] = g1;
+        db1 += g1;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) dw2[c] += gs[mm][c] * a;
+      }
+    }
+    if (ht == 0 && tid < C)
+      for (int mm = 0; mm < mn; ++mm) db2 += gs[mm][tid];
+    __syncthreads();
+  }
+  red[g][KC][u] = db1;
+#pragma unroll
+  for (int c = 0; c < KC; ++c) red[g][c][u] = dw2[c];
+  __syncthreads();
+  if (g == 0) {
+    float s = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kG; ++k) s += red[k][KC][u];
+    b1[(int64_t)p * w_pitch + h] -= lr * s;
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+      if (c < C) {
+        float gsum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < kG; ++k) gsum += red[k][c][u];
+        w2[(int64_t)c * Hp + h] = wc[c] - lr * gsum;
+      }
+  }
+  if (ht == 0 && tid < C) b2[(int64_t)p * w_pitch + tid] -= lr * db2;
 }
 
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
                         int P, int M, int Mp, int N) {
-  k_reduce_bias<<<grid_cap((int64_t)P * Mp * N, 4096), 256, 0, s>>>(part, KS, bias, w_pitch, Z, P, M, Mp, N);
+  int64_t g = ((int64_t)P * Mp * N + 255) / 256;
+  k_reduce_bias<<<(unsigned)(g < 4096 ? g : 4096), 256, 0, s>>>(part, KS, bias, w_pitch, Z, P, M, Mp, N);
 }
 
 void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
-                         const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C,
-                         int Cp) {
+                         const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp) {
   const int rows = P * M;
   k_softmax_grad<<<(rows + 3) / 4, 256, 0, s>>>(part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
 }
@@ -138,6 +316,27 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp) {
   const int htiles = (Hp + 255) / 256;
   k_bwd_hidden<<<P * htiles, 256, 0, s>>>(G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles);
+}
+
+void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp) {
+  const int htiles = Hp / kHU;
+  if (C <= 16)
+    k_head_a<16><<<P * htiles, 256, 0, s>>>(part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+  else
+    k_head_a<32><<<P * htiles, 256, 0, s>>>(part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+}
+
+void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
+                   const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
+                   int Cp, int Hp, float lr) {
+  const int htiles = Hp / kHU;
+  if (C <= 16)
+    k_head_b<16><<<P * htiles, 256, 0, s>>>(PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
+                                            htiles, lr);
+  else
+    k_head_b<32><<<P * htiles, 256, 0, s>>>(PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
+                                            htiles, lr);
 }
 
 }  // namespace hav
