@@ -1,104 +1,185 @@
 // Averaging of replicas (Algorithm 1, Sec. 3.1): the local mean over each
 // cluster of S learners after every block of K1 steps, and the global mean
 // over all P learners at the end of the round.  Both are HBM streams over the
-// [P][Dp] replica array: every lane owns one 16-byte column slice and walks
-// the S rows of its group, so each row is read once, coalesced along D, the
-// sum over replicas stays in registers in the fixed order 0..S-1 (identical
-// results on every run), and the mean is written back to all S rows.
+// [P][Dp] replica array, coalesced along D: a workgroup owns a run of 16-byte
+// column pieces of one cluster; each thread takes one column piece and RG
+// consecutive rows of the cluster (NG = S / RG threads per column), keeps its
+// rows' partial sum in registers (rows in order), and the NG partial sums of a
+// column are added through LDS in group order, so every run produces the same
+// bits.  The mean is then written back to all S rows.
 //
-// The averaging-only workload fuses its heavy-ball update v <- mu*v + g,
+// The averaging-only workload fuses its heavy-ball step v <- mu*v + g,
 // w <- w - lr*v into the same pass (momentum buffers are per learner and are
 // not averaged: Algorithm 1 averages parameters only).
+#include <algorithm>
+
 #include "internal.h"
 
 namespace hav {
 
+#ifndef HAV_AVG_RG
+#define HAV_AVG_RG 1
+#endif
+#ifndef HAV_AVG_NT
+#define HAV_AVG_NT 1
+#endif
+#if HAV_AVG_NT
 __device__ inline f32x4 ld_stream(const f32x4* p) { return __builtin_nontemporal_load(p); }
 __device__ inline void st_stream(f32x4* p, f32x4 v) { __builtin_nontemporal_store(v, p); }
+#else
+__device__ inline f32x4 ld_stream(const f32x4* p) { return *p; }
+__device__ inline void st_stream(f32x4* p, f32x4 v) { *p = v; }
+#endif
 
-// grid (x: column blocks, y: group).  Rows g*S .. g*S+S-1, columns [0, n4) in
-// float4 units, row pitch pitch4.
-__global__ __launch_bounds__(256) void k_group_mean(f32x4* __restrict__ W, int64_t pitch4, int64_t n4, int S) {
-  f32x4* base = W + (int64_t)blockIdx.y * S * pitch4;
-  const float inv = 1.0f / (float)S;
-  const bool pow2 = (S & (S - 1)) == 0;
-  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-    f32x4 sum = ld_stream(base + i);
-    int u = 1;
-    for (; u + 4 <= S; u += 4) {
-      f32x4 a = ld_stream(base + (int64_t)u * pitch4 + i);
-      f32x4 b = ld_stream(base + (int64_t)(u + 1) * pitch4 + i);
-      f32x4 c = ld_stream(base + (int64_t)(u + 2) * pitch4 + i);
-      f32x4 d = ld_stream(base + (int64_t)(u + 3) * pitch4 + i);
-      sum += a;
-      sum += b;
-      sum += c;
-      sum += d;
+// grid (x: column runs, y: cluster).  MOM: apply the heavy-ball step with the
+// given gradients Gr first.  MEAN: replace the S rows by their mean (else each
+// updated row is written back as it is).
+template <bool MOM, bool MEAN, int RG, int NG, int TB>
+__global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __restrict__ V,
+                                             const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4, float lr,
+                                             float mu) {
+  constexpr int S = RG * NG;
+  constexpr int CPB = TB / NG;  // columns per workgroup
+  __shared__ f32x4 part[NG > 1 ? NG : 1][CPB];
+  const int tid = threadIdx.x, cl = tid % CPB, g = tid / CPB;
+  const int64_t row0 = (int64_t)blockIdx.y * S + g * RG;
+  for (int64_t c0 = (int64_t)blockIdx.x * CPB; c0 < n4; c0 += (int64_t)gridDim.x * CPB) {
+    const int64_t i = c0 + cl;
+    const bool ok = i < n4;
+    const int64_t ic = ok ? i : 0;
+    f32x4 w[RG];
+#pragma unroll
+    for (int u = 0; u < RG; ++u) w[u] = ld_stream(W + (row0 + u) * pitch4 + ic);
+    if (MOM) {
+      f32x4 v[RG], gr[RG];
+#pragma unroll
+      for (int u = 0; u < RG; ++u) {
+        v[u] = ld_stream(V + (row0 + u) * pitch4 + ic);
+        gr[u] = ld_stream(Gr + (row0 + u) * pitch4 + ic);
+      }
+#pragma unroll
+      for (int u = 0; u < RG; ++u) {
+        v[u] = mu * v[u] + gr[u];
+        w[u] = w[u] - lr * v[u];
+        if (ok) st_stream(V + (row0 + u) * pitch4 + i, v[u]);
+      }
     }
-    for (; u < S; ++u) sum += ld_stream(base + (int64_t)u * pitch4 + i);
-    // Exact division by S (a power of two is an exact scaling either way).
-    f32x4 mean = pow2 ? sum * inv : sum / (float)S;
-    for (int v = 0; v < S; ++v) st_stream(base + (int64_t)v * pitch4 + i, mean);
+    if (!MEAN) {
+#pragma unroll
+      for (int u = 0; u < RG; ++u)
+        if (ok) st_stream(W + (row0 + u) * pitch4 + i, w[u]);
+      continue;
+    }
+    f32x4 sum = w[0];
+#pragma unroll
+    for (int u = 1; u < RG; ++u) sum += w[u];
+    if (NG > 1) {
+      part[g][cl] = sum;
+      __syncthreads();
+      sum = part[0][cl];
+#pragma unroll
+      for (int k = 1; k < NG; ++k) sum += part[k][cl];
+      __syncthreads();
+    }
+    // S is a power of two here, so the scaling by 1/S is exact.
+    const f32x4 mean = sum * (1.0f / (float)S);
+#pragma unroll
+    for (int u = 0; u < RG; ++u)
+      if (ok) st_stream(W + (row0 + u) * pitch4 + i, mean);
   }
 }
 
-// Heavy-ball step of rows g*S .. g*S+S-1 with the given gradients Gr (row
-// pitch pitch4); with `average`, the S updated rows are replaced by their mean
-// in the same pass.
-template <bool AVERAGE>
-__global__ __launch_bounds__(256) void k_momentum(f32x4* __restrict__ W, f32x4* __restrict__ V,
+// Any S: one thread per column piece walks all S rows (runtime count).
+template <bool MOM>
+__global__ __launch_bounds__(256) void k_rows_any(f32x4* __restrict__ W, f32x4* __restrict__ V,
                                                   const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4, int S,
                                                   float lr, float mu) {
   const int64_t row0 = (int64_t)blockIdx.y * S;
-  const bool pow2 = (S & (S - 1)) == 0;
-  const float inv = 1.0f / (float)S;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
     f32x4 sum = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
     for (int u = 0; u < S; ++u) {
       const int64_t o = (row0 + u) * pitch4 + i;
       f32x4 w = ld_stream(W + o);
-      f32x4 v = ld_stream(V + o);
-      const f32x4 g = ld_stream(Gr + o);
-      v = mu * v + g;
-      w = w - lr * v;
-      st_stream(V + o, v);
-      if (AVERAGE)
-        sum += w;
-      else
-        st_stream(W + o, w);
+      if (MOM) {
+        f32x4 v = ld_stream(V + o);
+        const f32x4 g = ld_stream(Gr + o);
+        v = mu * v + g;
+        w = w - lr * v;
+        st_stream(V + o, v);
+      }
+      sum += w;
     }
-    if (AVERAGE) {
-      const f32x4 mean = pow2 ? sum * inv : sum / (float)S;
-      for (int u = 0; u < S; ++u) st_stream(W + (row0 + u) * pitch4 + i, mean);
-    }
+    const f32x4 mean = sum / (float)S;
+    for (int u = 0; u < S; ++u) st_stream(W + (row0 + u) * pitch4 + i, mean);
   }
 }
 
-static unsigned col_blocks(int64_t n4, int groups) {
-  // About 8 resident workgroups per CU over the whole launch.
-  int64_t want = (2048 + groups - 1) / groups;
-  int64_t need = (n4 + 255) / 256;
-  int64_t g = want < need ? want : need;
-  return (unsigned)(g < 1 ? 1 : g);
+static unsigned col_runs(int64_t n4, int cpb, int groups) {
+  // One column piece per thread, up to about 2^20 workgroups in all.
+  int64_t need = (n4 + cpb - 1) / cpb;
+  int64_t cap = std::max<int64_t>(1, (int64_t(1) << 20) / groups);
+  return (unsigned)(need < cap ? need : cap);
+}
+
+template <bool MOM, bool MEAN, int RG, int NG, int TB = 256>
+static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int groups, float lr,
+                        float mu) {
+  dim3 grid(col_runs(n4, TB / NG, groups), (unsigned)groups);
+  k_rows<MOM, MEAN, RG, NG, TB><<<grid, TB, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, lr, mu);
+}
+
+// Cluster of S rows with S a power of two up to 64.  Up to 16 rows: one row per
+// thread and S threads per column (more threads keep more loads in flight than
+// more rows per thread); 32 and 64 rows: four rows per thread in 1024-thread
+// workgroups (longer row segments per workgroup).  Measured on MI355X.
+// Returns false for other S.
+#ifndef HAV_AVG_RG_BIG
+#define HAV_AVG_RG_BIG 4
+#endif
+#ifndef HAV_AVG_TB_BIG
+#define HAV_AVG_TB_BIG 1024
+#endif
+template <bool MOM, int S>
+static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int groups, float lr, float mu) {
+  constexpr int kR = S <= 16 ? HAV_AVG_RG : HAV_AVG_RG_BIG;
+  constexpr int RG = S < kR ? S : kR;
+  constexpr int TB = S <= 16 ? 256 : HAV_AVG_TB_BIG;
+  launch_rows<MOM, true, RG, S / RG, TB>(s, W, V, Gr, n4, groups, lr, mu);
+}
+
+template <bool MOM>
+static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int P, int S, float lr,
+                             float mu) {
+  const int groups = P / S;
+  switch (S) {
+    case 2: launch_s<MOM, 2>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 4: launch_s<MOM, 4>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 8: launch_s<MOM, 8>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 16: launch_s<MOM, 16>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 32: launch_s<MOM, 32>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 64: launch_s<MOM, 64>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    default: return false;
+  }
 }
 
 void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S) {
   const int64_t n4 = Dp / 4;
-  dim3 grid(col_blocks(n4, P / S), (unsigned)(P / S));
-  k_group_mean<<<grid, 256, 0, s>>>((f32x4*)W, n4, n4, S);
+  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, n4, P, S, 0.0f, 0.0f)) return;
+  dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
+  k_rows_any<false><<<grid, 256, 0, s>>>((f32x4*)W, nullptr, nullptr, n4, n4, S, 0.0f, 0.0f);
 }
 
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, float lr, float mu) {
   const int64_t n4 = Dp / 4;
-  const int groups = average ? P / S : P;
-  const int rows = average ? S : 1;
-  dim3 grid(col_blocks(n4, groups), (unsigned)groups);
-  if (average)
-    k_momentum<true><<<grid, 256, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, rows, lr, mu);
-  else
-    k_momentum<false><<<grid, 256, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, rows, lr, mu);
+  if (!average) {
+    launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, P, lr, mu);
+    return;
+  }
+  if (launch_mean_pow2<true>(s, W, V, Gr, n4, P, S, lr, mu)) return;
+  dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
+  k_rows_any<true><<<grid, 256, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu);
 }
 
 }  // namespace hav
