@@ -8,9 +8,10 @@ synthetic data (N=50000 rows: class-mean pattern + N(0, 0.5) noise).
 and replicas resident in HBM.
 
 Also reported, on the same JSON line:
-  roofline      the dominant kernel of the round: algorithmic bytes (or flops)
-                per launch over its mean duration from HIP events recorded on
-                the handle's stream around every launch of a second timed pass
+  roofline      the dominant kernel of the round (largest launches x duration):
+                algorithmic bytes (or flops) per launch over its mean duration,
+                timed with HIP events on the handle's stream around 200
+                back-to-back launches of it after the timed rounds
   averaging     the averaging-only workload (P=32 replicas of 11.7M floats,
                 S=4, K1=1, K2=4, heavy-ball momentum 0.9, lr 0.1): HBM GB/s of
                 the fused update + cluster mean and update + global mean
@@ -59,6 +60,21 @@ def mean_bytes(P, D):
     return 2 * 4 * P * D
 
 
+def counter_traffic(kernel_class):
+    """HBM bytes per launch of `kernel_class` from the committed counter
+    summary (profiles/traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled by
+    a calibration stream), or None when the kernel's source has changed since
+    the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))["kernels"][kernel_class]
+        cur = hashlib.sha256(open(os.path.join(ROOT, rec["source"]), "rb").read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    return rec["bytes"] if cur == rec["source_sha256"] else None
+
+
 # ---------------------------------------------------------------- main workload
 def bench_mlp(args):
     import torch
@@ -97,6 +113,11 @@ def bench_mlp(args):
     h.profile(False)
     torch.cuda.synchronize()
     ms_prof = start.elapsed_time(end)
+    # Per-launch durations: every kernel class of the round timed over 200
+    # back-to-back launches between two HIP events on the handle's stream (the
+    # event pair adds a few microseconds to a single launch; here it is spread
+    # over 200).  This changes the replicas, so it comes last.
+    dur_ms = {name: h.time_kernel(name, 200) for name in stats if name != "draw_indices"}
     h.close()
 
     work = mlp_kernel_work(P, B, IN, H, C)
@@ -105,20 +126,20 @@ def bench_mlp(args):
     work["global_mean"] = (mean_bytes(P, D), P * D)
     kernels = {}
     for name, (n, tot) in stats.items():
-        avg = tot / n
+        avg = dur_ms.get(name, tot / n)
         b, fl = work.get(name, (0, 0))
-        kernels[name] = {"launches": n, "avg_us": round(avg * 1e3, 3), "share": None,
-                         "GBps": round(b / (avg * 1e-3) / 1e9, 1) if b else None,
+        kernels[name] = {"launches": n, "avg_us": round(avg * 1e3, 3), "share": None, "GBps": round(b / (avg * 1e-3) / 1e9, 1) if b else None,
                          "TFLOPs": round(fl / (avg * 1e-3) / 1e12, 2) if fl else None}
     total = sum(t for _, t in stats.values())
     for name, (n, tot) in stats.items():
         kernels[name]["share"] = round(tot / total, 4)
-    dom = max(stats, key=lambda k: stats[k][1])
-    n, tot = stats[dom]
-    avg_s = tot / n * 1e-3
+    dom = max(dur_ms, key=lambda k: dur_ms[k] * stats[k][0])
+    avg_s = dur_ms[dom] * 1e-3
     b, fl = work[dom]
+    traffic = counter_traffic(dom)
     roof = {"kernel": dom, "bound": "hbm", "achieved": round(b / avg_s / 1e9, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(b / avg_s / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+            "unit": "GB/s", "frac": round(b / avg_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": None if traffic is None else round(traffic),
             "alg_bytes_per_launch": b, "avg_us": round(avg_s * 1e6, 3),
             "mfma_tflops": round(fl / avg_s / 1e12, 2) if fl else None,
             "mfma_frac": round(fl / avg_s / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4) if fl else None}
@@ -161,13 +182,14 @@ def bench_averaging(args):
         h.round()
     stats = h.profile_read()
     h.profile(False)
+    dur_ms = {name: h.time_kernel(name, 20) for name in stats}
     h.close()
     per_launch = 20 * P * D  # read w, v, g; write w, v
     out = {"config": {"workload": "averaging_11_7M", "P": P, "S": c["S"], "K1": c["K1"], "K2": c["K2"], "D": D,
                       "momentum": c["momentum"], "lr": c["lr"]},
            "ms_per_round": ms / rounds, "alg_bytes_per_launch": per_launch, "kernels": {}}
     for name, (n, tot) in stats.items():
-        avg_s = tot / n * 1e-3
+        avg_s = dur_ms[name] * 1e-3
         gbs = per_launch / avg_s / 1e9
         out["kernels"][name] = {"launches": n, "avg_us": round(avg_s * 1e6, 2), "GBps": round(gbs, 1),
                                 "frac": round(gbs / HBM_PEAK_GBS, 4)}

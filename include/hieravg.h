@@ -154,15 +154,27 @@ int hieravg_set_stream(hieravg_t h, void* hip_stream);
 int hieravg_sync(hieravg_t h);
 
 /*
- * Per-kernel timing with HIP events recorded on the handle's stream around
- * every launch.  enable != 0 starts recording (clearing earlier records);
- * enable == 0 stops.  hieravg_profile_read synchronises and writes, for every
+ * Per-kernel timing with HIP events: while enabled, every launch carries two
+ * events that its dispatch packet stamps at kernel start and end, so the
+ * recorded durations are the kernels' execution times.  enable != 0 starts
+ * recording (clearing earlier records); enable == 0 stops.  hieravg_profile_read synchronises and writes, for every
  * kernel class c < min(n, hieravg_kernel_classes()), the number of launches
  * and their summed duration in milliseconds.
  */
 int hieravg_profile(hieravg_t h, int enable);
 int hieravg_profile_read(hieravg_t h, int64_t* launches, double* total_ms, int n);
 int hieravg_kernel_classes(void);
+
+/*
+ * Mean duration in milliseconds of one launch of kernel class
+ * `kernel_class` (see hieravg_kernel_class_name), from HIP events around one
+ * launch of a graph of `reps` back-to-back launches of it (captured on the
+ * handle's stream) with the arguments of step 0 of the current round.  For measurement only: the launches act on the replicas as
+ * `reps` extra applications of that kernel would.  HIERAVG_EINVAL for a class
+ * the workload does not launch, for the index draw, or while profiling.
+ * Synchronises.
+ */
+int hieravg_time_kernel(hieravg_t h, int kernel_class, int reps, double* mean_ms);
 const char* hieravg_kernel_class_name(int c);
 
 #ifdef __cplusplus

@@ -20,6 +20,10 @@
 
 using namespace hav;
 
+namespace hav {
+thread_local LaunchTiming g_launch_timing;
+}
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -80,10 +84,15 @@ struct hieravg {
 
 namespace {
 
+// Run `fn`, which makes exactly one kernel launch.  When profiling, the launch
+// goes out with two events that its dispatch packet stamps; the recorded
+// interval includes a few microseconds of dispatch latency per launch, so
+// profiling gives launch counts and time shares, and hieravg_time_kernel
+// gives per-launch durations.
 template <class F>
-void run(hieravg* h, int kc, F&& launch) {
+void run(hieravg* h, int kc, F&& fn) {
   if (!h->profiling) {
-    launch();
+    fn();
     return;
   }
   hipEvent_t ev[2];
@@ -92,13 +101,14 @@ void run(hieravg* h, int kc, F&& launch) {
       ev[i] = h->pool.back();
       h->pool.pop_back();
     } else if (hipEventCreate(&ev[i]) != hipSuccess) {
-      launch();
+      if (i == 1) h->pool.push_back(ev[0]);
+      fn();
       return;
     }
   }
-  (void)hipEventRecord(ev[0], h->stream);
-  launch();
-  (void)hipEventRecord(ev[1], h->stream);
+  g_launch_timing = {ev[0], ev[1]};
+  fn();
+  g_launch_timing = {};
   h->recs.push_back({ev[0], ev[1], kc});
 }
 
@@ -251,52 +261,115 @@ int build(hieravg* h) {
   return HIERAVG_OK;
 }
 
+// The single kernel launch of class `kc` for step tt of the current round
+// (tt selects the step's sample indices, or the averaging workload's given
+// gradients).  Returns false for a class this workload does not launch.
+bool launch_class(hieravg* h, int kc, int tt) {
+  const hieravg_config& c = h->cfg;
+  const int P = c.P, B = c.B, S = c.S;
+  hipStream_t s = h->stream;
+  float* W = h->W;
+  if (c.kind == HIERAVG_KIND_AVERAGING) {
+    const float* g = h->Gr + (int64_t)tt * P * h->Dp;
+    switch (kc) {
+      case KC_MOMENTUM: launch_momentum_step(s, W, h->V, g, h->Dp, P, 1, false, c.lr, c.momentum); return true;
+      case KC_MOMENTUM_GROUP: launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, c.lr, c.momentum); return true;
+      case KC_MOMENTUM_GLOBAL: launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, c.lr, c.momentum); return true;
+      default: return false;
+    }
+  }
+  const int32_t* ix = h->idx + (int64_t)tt * P * B;
+  const int Bp = h->Bp, C = (int)h->C, Cp = (int)h->Cp, Hp = (int)h->Hp, INp = (int)h->INp;
+  const bool mlp = c.kind == HIERAVG_KIND_MLP, small = mlp && C <= kSmallC;
+  switch (kc) {
+    case KC_DRAW:
+      launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, c.K1 * c.K2, (uint64_t)h->N,
+                          h->key_index);
+      return true;
+    case KC_FWD1: {
+      FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, mlp ? Hp : Cp, INp, h->KS1,
+                h->cps1};
+      launch_fwd(s, f, A_GATHER);
+      return true;
+    }
+    case KC_SOFTMAX:
+      if (small) return false;
+      launch_softmax_grad(s, h->part, mlp ? h->KS2 : h->KS1, W + (mlp ? h->off_b2 : h->off_b1), h->Dp, h->y, ix,
+                          h->G2, P, B, Bp, C, Cp);
+      return true;
+    case KC_UPDATE1: {
+      // With the small-C head, b1 took its step in k_head_b; the softmax
+      // model's layer is the first and only one.
+      if (!mlp) {
+        UpdArgs u{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp,
+                  c.lr};
+        launch_update(s, u, A_GATHER);
+      } else {
+        UpdArgs u{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
+                  small ? nullptr : W + h->off_b1, P, B, Hp, INp, c.lr};
+        launch_update(s, u, A_GATHER);
+      }
+      return true;
+    }
+    case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, P, S); return true;
+    case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, P, P); return true;
+    default: break;
+  }
+  if (!mlp) return false;
+  switch (kc) {
+    case KC_HEAD_A:
+      if (!small) return false;
+      launch_head_a(s, h->part, h->KS1, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
+      return true;
+    case KC_HEAD_B:
+      if (!small) return false;
+      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, h->G1, h->y, ix, P, B, Bp,
+                    C, Cp, Hp, c.lr);
+      return true;
+    case KC_REDUCE1:
+      if (small) return false;
+      launch_reduce_bias(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp);
+      return true;
+    case KC_FWD2: {
+      if (small) return false;
+      FwdArgs f{h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, h->part, P, B, Bp, Cp, Hp, h->KS2, h->cps2};
+      launch_fwd(s, f, A_RELU);
+      return true;
+    }
+    case KC_BWD_HIDDEN:
+      if (small) return false;
+      launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp);
+      return true;
+    case KC_UPDATE2: {
+      if (small) return false;
+      UpdArgs u{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
+                c.lr};
+      launch_update(s, u, A_RELU);
+      return true;
+    }
+    default: return false;
+  }
+}
+
 // One local SGD step of all P learners at step tt of the round (Algorithm 1:
 // w <- w - lr/B * sum_s grad f(w; xi_s) for every learner concurrently).
 void enqueue_step(hieravg* h, int tt) {
-  const hieravg_config& c = h->cfg;
-  const int P = c.P, B = c.B;
-  const int32_t* ix = h->idx + (int64_t)tt * P * B;
-  hipStream_t s = h->stream;
-  float* W = h->W;
-  const int Bp = h->Bp, C = (int)h->C, Cp = (int)h->Cp, Hp = (int)h->Hp, INp = (int)h->INp;
-  if (c.kind == HIERAVG_KIND_SOFTMAX) {
-    FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, Cp, INp, h->KS1, h->cps1};
-    run(h, KC_FWD1, [&] { launch_fwd(s, f, A_GATHER); });
-    run(h, KC_SOFTMAX, [&] {
-      launch_softmax_grad(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->y, ix, h->G2, P, B, Bp, C, Cp);
-    });
-    UpdArgs u{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp, c.lr};
-    run(h, KC_UPDATE1, [&] { launch_update(s, u, A_GATHER); });
-    return;
-  }
-  FwdArgs f1{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, Hp, INp, h->KS1, h->cps1};
-  run(h, KC_FWD1, [&] { launch_fwd(s, f1, A_GATHER); });
-  const bool small = C <= kSmallC;
-  if (small) {
-    run(h, KC_HEAD_A, [&] {
-      launch_head_a(s, h->part, h->KS1, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
-    });
-    run(h, KC_HEAD_B, [&] {
-      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, h->G1, h->y, ix, P, B, Bp,
-                    C, Cp, Hp, c.lr);
-    });
+  static const int kSoftmax[] = {KC_FWD1, KC_SOFTMAX, KC_UPDATE1};
+  static const int kSmall[] = {KC_FWD1, KC_HEAD_A, KC_HEAD_B, KC_UPDATE1};
+  static const int kLarge[] = {KC_FWD1, KC_REDUCE1, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2, KC_UPDATE1};
+  const int* seq;
+  int n;
+  if (h->cfg.kind == HIERAVG_KIND_SOFTMAX) {
+    seq = kSoftmax;
+    n = 3;
+  } else if (h->C <= kSmallC) {
+    seq = kSmall;
+    n = 4;
   } else {
-    run(h, KC_REDUCE1, [&] { launch_reduce_bias(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp); });
-    FwdArgs f2{h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, h->part, P, B, Bp, Cp, Hp, h->KS2, h->cps2};
-    run(h, KC_FWD2, [&] { launch_fwd(s, f2, A_RELU); });
-    run(h, KC_SOFTMAX, [&] {
-      launch_softmax_grad(s, h->part, h->KS2, W + h->off_b2, h->Dp, h->y, ix, h->G2, P, B, Bp, C, Cp);
-    });
-    run(h, KC_BWD_HIDDEN, [&] { launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp); });
-    UpdArgs u2{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
-               c.lr};
-    run(h, KC_UPDATE2, [&] { launch_update(s, u2, A_RELU); });
+    seq = kLarge;
+    n = 7;
   }
-  // With the small-C head, b1 took its step in k_head_b.
-  UpdArgs u1{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, small ? nullptr : W + h->off_b1,
-             P, B, Hp, INp, c.lr};
-  run(h, KC_UPDATE1, [&] { launch_update(s, u1, A_GATHER); });
+  for (int i = 0; i < n; ++i) run(h, seq[i], [&] { launch_class(h, seq[i], tt); });
 }
 
 struct Segment {
@@ -398,30 +471,26 @@ int hieravg_round(hieravg_t h) {
   const hieravg_config& c = h->cfg;
   const int T = c.K1 * c.K2;
   const int P = c.P, S = c.S;
-  hipStream_t s = h->stream;
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     for (int b = 0; b < c.K2; ++b) {
       for (int k = 0; k < c.K1; ++k) {
         const int tt = b * c.K1 + k;
-        const float* g = h->Gr + (int64_t)tt * P * h->Dp;
         const bool end_block = k == c.K1 - 1, end_round = end_block && b == c.K2 - 1;
+        int kc = KC_MOMENTUM;
         if (end_round && P > 1)
-          run(h, KC_MOMENTUM_GLOBAL, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, P, true, c.lr, c.momentum); });
+          kc = KC_MOMENTUM_GLOBAL;
         else if (end_block && !end_round && S > 1)
-          run(h, KC_MOMENTUM_GROUP, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, S, true, c.lr, c.momentum); });
-        else
-          run(h, KC_MOMENTUM, [&] { launch_momentum_step(s, h->W, h->V, g, h->Dp, P, 1, false, c.lr, c.momentum); });
+          kc = KC_MOMENTUM_GROUP;
+        run(h, kc, [&] { launch_class(h, kc, tt); });
       }
     }
   } else {
-    run(h, KC_DRAW, [&] {
-      launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, c.B, T, (uint64_t)h->N, h->key_index);
-    });
+    run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
     for (int b = 0; b < c.K2; ++b) {
       for (int k = 0; k < c.K1; ++k) enqueue_step(h, b * c.K1 + k);
-      if (b < c.K2 - 1 && S > 1) run(h, KC_GROUP_MEAN, [&] { launch_group_mean(s, h->W, h->Dp, P, S); });
+      if (b < c.K2 - 1 && S > 1) run(h, KC_GROUP_MEAN, [&] { launch_class(h, KC_GROUP_MEAN, 0); });
     }
-    if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_group_mean(s, h->W, h->Dp, P, P); });
+    if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
   }
   HAV_CHECK(hipGetLastError());
   h->steps += T;
@@ -558,6 +627,53 @@ int hieravg_profile_read(hieravg_t h, int64_t* launches, double* total_ms, int n
       total_ms[r.kc] += ms;
     }
   }
+  return HIERAVG_OK;
+}
+
+int hieravg_time_kernel(hieravg_t h, int kernel_class, int reps, double* mean_ms) {
+  if (!h || !mean_ms || reps < 1 || reps > 100000 || kernel_class < 0 || kernel_class >= KC_COUNT ||
+      kernel_class == KC_DRAW) {
+    set_error("bad arguments");
+    return HIERAVG_EINVAL;
+  }
+  if (h->profiling) {
+    set_error("disable hieravg_profile first");
+    return HIERAVG_EINVAL;
+  }
+  // The launches are captured into a graph (kernel nodes only) and the graph
+  // is launched once between the two events, so the host's per-launch cost
+  // stays out of the timed interval.
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  HAV_CHECK(hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
+  bool ok = true;
+  for (int i = 0; i < reps && ok; ++i) ok = launch_class(h, kernel_class, 0);
+  hipGraph_t graph = nullptr;
+  HAV_CHECK(hipStreamEndCapture(h->stream, &graph));
+  if (!ok) {
+    (void)hipGraphDestroy(graph);
+    set_error("this workload does not launch that kernel class");
+    return HIERAVG_EINVAL;
+  }
+  hipGraphExec_t exec = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
+  int rc = HIERAVG_OK;
+  if (hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0) != hipSuccess) rc = HIERAVG_EHIP;
+  if (rc == HIERAVG_OK && (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess)) rc = HIERAVG_EHIP;
+  if (rc == HIERAVG_OK && hipEventRecord(a, h->stream) != hipSuccess) rc = HIERAVG_EHIP;
+  if (rc == HIERAVG_OK && hipGraphLaunch(exec, h->stream) != hipSuccess) rc = HIERAVG_EHIP;
+  if (rc == HIERAVG_OK && hipEventRecord(b, h->stream) != hipSuccess) rc = HIERAVG_EHIP;
+  if (rc == HIERAVG_OK && hipEventSynchronize(b) != hipSuccess) rc = HIERAVG_EHIP;
+  float ms = 0.0f;
+  if (rc == HIERAVG_OK && hipEventElapsedTime(&ms, a, b) != hipSuccess) rc = HIERAVG_EHIP;
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (exec) (void)hipGraphExecDestroy(exec);
+  (void)hipGraphDestroy(graph);
+  if (rc != HIERAVG_OK) {
+    set_error("timing the kernel failed");
+    return rc;
+  }
+  *mean_ms = ms / reps;
   return HIERAVG_OK;
 }
 

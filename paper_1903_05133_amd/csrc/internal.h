@@ -10,6 +10,7 @@
 // softmax) all receive zero gradient, and means of zeros are zero.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -88,6 +89,23 @@ enum KernelClass {
 
 // Largest class count handled by the fused small-C head kernels.
 constexpr int kSmallC = 32;
+
+// ------------------------------------------------------------ launching
+// Events that time the next launch on this thread (both null: not timing).
+// When set, the launch goes through hipExtLaunchKernelGGL, whose dispatch
+// packet itself records the kernel's start and end in the two events.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchTiming g_launch_timing;
+
+template <class K, class... Args>
+inline void launch(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  if (g_launch_timing.start)
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, g_launch_timing.start, g_launch_timing.stop, 0u, args...);
+  else
+    kernel<<<grid, block, shmem, s>>>(args...);
+}
 
 // ------------------------------------------------------------ launchers
 // Data and initial state (k_data.hip).

@@ -126,7 +126,7 @@ template <bool MOM, bool MEAN, int RG, int NG, int TB = 256>
 static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int groups, float lr,
                         float mu) {
   dim3 grid(col_runs(n4, TB / NG, groups), (unsigned)groups);
-  k_rows<MOM, MEAN, RG, NG, TB><<<grid, TB, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, lr, mu);
+  launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, lr, mu);
 }
 
 // Cluster of S rows with S a power of two up to 64.  Up to 16 rows: one row per
@@ -167,7 +167,7 @@ void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S) {
   const int64_t n4 = Dp / 4;
   if (launch_mean_pow2<false>(s, W, nullptr, nullptr, n4, P, S, 0.0f, 0.0f)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  k_rows_any<false><<<grid, 256, 0, s>>>((f32x4*)W, nullptr, nullptr, n4, n4, S, 0.0f, 0.0f);
+  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, n4, n4, S, 0.0f, 0.0f);
 }
 
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
@@ -179,7 +179,7 @@ void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, in
   }
   if (launch_mean_pow2<true>(s, W, V, Gr, n4, P, S, lr, mu)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  k_rows_any<true><<<grid, 256, 0, s>>>((f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu);
+  launch(k_rows_any<true>, grid, 256, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu);
 }
 
 }  // namespace hav

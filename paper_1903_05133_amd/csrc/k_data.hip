@@ -97,31 +97,31 @@ static int grid_for(int64_t n, int cap = 8192) {
 }
 
 void launch_gen_labels(hipStream_t s, int32_t* y, int64_t N, uint64_t key, uint64_t C) {
-  k_gen_labels<<<grid_for(N), 256, 0, s>>>(y, N, key, C);
+  launch(k_gen_labels, grid_for(N), 256, 0, s, y, N, key, C);
 }
 
 void launch_gen_data(hipStream_t s, float* X, const int32_t* y, int64_t N, int64_t IN, int64_t INp,
                      uint64_t key_mean, uint64_t key_noise, float sigma) {
-  k_gen_data<<<(unsigned)N, 256, 0, s>>>(X, y, IN, INp, key_mean, key_noise, sigma);
+  launch(k_gen_data, (unsigned)N, 256, 0, s, X, y, IN, INp, key_mean, key_noise, sigma);
 }
 
 void launch_init_matrix(hipStream_t s, float* W, int64_t rows, int64_t cols, int64_t ld, uint64_t key,
                         uint64_t layer, float scale) {
-  k_init_matrix<<<(unsigned)rows, 256, 0, s>>>(W, cols, ld, key, layer, scale);
+  launch(k_init_matrix, (unsigned)rows, 256, 0, s, W, cols, ld, key, layer, scale);
 }
 
 void launch_init_vector(hipStream_t s, float* w, int64_t D, uint64_t key, float std) {
-  k_init_vector<<<grid_for(D), 256, 0, s>>>(w, D, key, std);
+  launch(k_init_vector, grid_for(D), 256, 0, s, w, D, key, std);
 }
 
 void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int T, uint64_t key, float std) {
   dim3 grid((unsigned)grid_for(Dp, 1024), (unsigned)(T * P));
-  k_gen_grads<<<grid, 256, 0, s>>>(G, D, Dp, P, key, std);
+  launch(k_gen_grads, grid, 256, 0, s, G, D, Dp, P, key, std);
 }
 
 void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
                          int T, uint64_t N, uint64_t key) {
-  k_draw_indices<<<grid_for((int64_t)T * P * B, 1024), 256, 0, s>>>(idx, step_ctr, done_ctr, P, B, T, N, key);
+  launch(k_draw_indices, grid_for((int64_t)T * P * B, 1024), 256, 0, s, idx, step_ctr, done_ctr, P, B, T, N, key);
 }
 
 }  // namespace hav

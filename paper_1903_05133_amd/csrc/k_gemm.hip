@@ -201,7 +201,7 @@ void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src) {
   const int mtiles = (a.Mp + MB * 16 - 1) / (MB * 16);
   const int ntiles = (a.N + 127) / 128;
   const unsigned grid = (unsigned)((int64_t)a.P * a.KS * mtiles * ntiles);
-#define HAV_FWD(S_, MB_) k_fwd_nt<S_, MB_><<<grid, 256, 0, s>>>(a, ntiles, mtiles)
+#define HAV_FWD(S_, MB_) launch(k_fwd_nt<S_, MB_>, grid, 256, 0, s, a, ntiles, mtiles)
 #define HAV_FWD_MB(S_)   \
   switch (MB) {          \
     case 1: HAV_FWD(S_, 1); break; \
@@ -388,9 +388,9 @@ void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc) {
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)a.P * mtiles * ntiles);
   if (bsrc == A_GATHER)
-    k_update_tn<A_GATHER><<<grid, 256, 0, s>>>(a, mtiles, ntiles);
+    launch(k_update_tn<A_GATHER>, grid, 256, 0, s, a, mtiles, ntiles);
   else
-    k_update_tn<A_RELU><<<grid, 256, 0, s>>>(a, mtiles, ntiles);
+    launch(k_update_tn<A_RELU>, grid, 256, 0, s, a, mtiles, ntiles);
 }
 
 }  // namespace hav

@@ -303,28 +303,28 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
                         int P, int M, int Mp, int N) {
   int64_t g = ((int64_t)P * Mp * N + 255) / 256;
-  k_reduce_bias<<<(unsigned)(g < 4096 ? g : 4096), 256, 0, s>>>(part, KS, bias, w_pitch, Z, P, M, Mp, N);
+  launch(k_reduce_bias, (unsigned)(g < 4096 ? g : 4096), 256, 0, s, part, KS, bias, w_pitch, Z, P, M, Mp, N);
 }
 
 void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp) {
   const int rows = P * M;
-  k_softmax_grad<<<(rows + 3) / 4, 256, 0, s>>>(part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  launch(k_softmax_grad, (rows + 3) / 4, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
 }
 
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp) {
   const int htiles = (Hp + 255) / 256;
-  k_bwd_hidden<<<P * htiles, 256, 0, s>>>(G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles);
+  launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles);
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
                    float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp) {
   const int htiles = Hp / kHU;
   if (C <= 16)
-    k_head_a<16><<<P * htiles, 256, 0, s>>>(part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+    launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
   else
-    k_head_a<32><<<P * htiles, 256, 0, s>>>(part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+    launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
 }
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
@@ -332,10 +332,10 @@ void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* 
                    int Cp, int Hp, float lr) {
   const int htiles = Hp / kHU;
   if (C <= 16)
-    k_head_b<16><<<P * htiles, 256, 0, s>>>(PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
+    launch(k_head_b<16>, P * htiles, 256, 0, s, PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
                                             htiles, lr);
   else
-    k_head_b<32><<<P * htiles, 256, 0, s>>>(PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
+    launch(k_head_b<32>, P * htiles, 256, 0, s, PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
                                             htiles, lr);
 }
 

@@ -99,6 +99,15 @@ class HierAvg:
     def profile(self, enable=True):
         native.check(native.lib().hieravg_profile(self._h, 1 if enable else 0))
 
+    def time_kernel(self, name, reps=100):
+        """Mean ms of one launch of kernel class `name` over `reps` back-to-back
+        launches (changes the replicas: measurement only)."""
+        L = native.lib()
+        names = [L.hieravg_kernel_class_name(i).decode() for i in range(L.hieravg_kernel_classes())]
+        ms = ctypes.c_double()
+        native.check(L.hieravg_time_kernel(self._h, names.index(name), reps, ctypes.byref(ms)))
+        return ms.value
+
     def profile_read(self):
         """{kernel class name: (launches, total ms)} of the recorded launches."""
         L = native.lib()

@@ -44,6 +44,7 @@ SIGNATURES = {
     "hieravg_profile_read": (ctypes.c_int, [_H, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                                             ctypes.c_int]),
     "hieravg_kernel_classes": (ctypes.c_int, []),
+    "hieravg_time_kernel": (ctypes.c_int, [_H, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]),
     "hieravg_kernel_class_name": (ctypes.c_char_p, [ctypes.c_int]),
 }
 
