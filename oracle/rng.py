@@ -2,8 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-Algorithm 1 (Sec. 3.1) has every learner "randomly sample a mini-batch of size
-B"; Sec. 2 makes the samples i.i.d. across learners and iterations.  The paper
+In Algorithm 1 (Sec. 3.1) every learner draws a fresh random minibatch of B
+samples at each local step; Sec. 2 makes the samples i.i.d. across learners
+and iterations.  The paper
 names no generator, so the reading used here is a counter-based one that any
 implementation can reproduce bit for bit:
 

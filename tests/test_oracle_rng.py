@@ -1,8 +1,8 @@
 """Pins of the oracle's counter-based generator and synthetic-data recipe.
 
-The generator is SplitMix64 (Steele, Lea & Flood, OOPSLA 2014); the minibatch
-draw of Algorithm 1 (Sec. 3.1, "randomly sample a mini-batch") is read as
-i.i.d. draws with replacement (Sec. 2, i.i.d. realisations of xi).
+The generator is SplitMix64 (Steele, Lea & Flood, OOPSLA 2014); the random
+minibatch of Algorithm 1 (Sec. 3.1) is read as i.i.d. draws with replacement
+(Sec. 2 makes the samples i.i.d. realisations).
 """
 
 import os
