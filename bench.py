@@ -53,6 +53,11 @@ def mlp_kernel_work(P, B, IN, H, C):
         "bwd_hidden": (P * f * (B * C + C * H + 2 * B * H), P * 2 * B * C * H),
         "update2_gemm": (P * f * (2 * C * H + B * C + B * H + 2 * C), P * 2 * B * C * H),
         "update1_gemm": (P * f * (2 * H * IN + B * H + B * IN + 2 * H), P * 2 * B * H * IN),
+        # update of W1 at step t and forward of step t+1: W1 read and written
+        # once, G1 and the two minibatches read, the next pre-activations
+        # written once; the group-mean variant moves the same bytes
+        "step1_gemm": (P * f * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
+        "step1_gemm_group_mean": (P * f * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
     }
 
 
@@ -124,6 +129,7 @@ def bench_mlp(args):
     D = H * IN + H + C * H + C
     work["group_mean"] = (mean_bytes(P, D), P * D)
     work["global_mean"] = (mean_bytes(P, D), P * D)
+    work["tail_group_mean"] = (mean_bytes(P, D - H * IN), P * (D - H * IN))
     kernels = {}
     for name, (n, tot) in stats.items():
         avg = dur_ms.get(name, tot / n)

@@ -10,6 +10,14 @@
 // The local mean right before the global mean is left out: means of
 // equal-size cluster means equal the global mean, so it changes nothing but
 // rounding.
+//
+// Where the fused step kernel applies (padded minibatch up to 64), the update
+// of the first weight block at step t also computes the first-layer forward
+// partials of step t+1 from the new weights, and at the end of a block also
+// takes the cluster mean of that block in between; a small kernel then takes
+// the cluster mean of the remaining parameters.  Only step 0 of a round runs
+// the stand-alone forward kernel, and the last step the plain update before
+// the global mean.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -33,7 +41,8 @@ void set_error(const std::string& s) { g_last_error = s; }
 const char* kClassNames[KC_COUNT] = {
     "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",   "softmax_grad", "bwd_hidden",
     "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
-    "momentum",     "momentum_group_mean",          "momentum_global_mean"};
+    "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
+    "step1_gemm_group_mean",     "tail_group_mean"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -74,6 +83,10 @@ struct hieravg {
 
   uint64_t key_index = 0;
   int KS1 = 1, cps1 = 1, KS2 = 1, cps2 = 1;
+  bool fused = false;       // the fused step kernel applies (SG = 1)
+  bool fused_mean = false;  // ... and also with the cluster mean (SG = S)
+  int KS_step = 1, KS_mean = 1;  // forward splits written by the fused kernel
+  int ks_cur = 1;                // splits of the partials currently in `part`
   hipStream_t own_stream = nullptr, stream = nullptr;
   int64_t steps = 0;
 
@@ -223,8 +236,20 @@ int build(hieravg* h) {
     }
     const int T = c.K1 * c.K2;
     const int64_t n1 = mlp ? h->Hp : h->Cp;
+    h->fused = T >= 2 && step_w1_supported(h->Bp, 1);
+    h->fused_mean = h->fused && c.S > 1 && step_w1_supported(h->Bp, c.S);
+    int ks_max = h->KS1;
+    if (h->fused) {
+      h->KS_step = step_w1_splits(P, 1, (int)n1, (int)h->INp);
+      ks_max = std::max(ks_max, h->KS_step);
+    }
+    if (h->fused_mean) {
+      h->KS_mean = step_w1_splits(P, c.S, (int)n1, (int)h->INp);
+      ks_max = std::max(ks_max, h->KS_mean);
+    }
+    h->ks_cur = h->KS1;
     const int64_t part_floats =
-        std::max<int64_t>((int64_t)h->KS1 * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
+        std::max<int64_t>((int64_t)ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
     int rc;
     if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->X, sizeof(float) * h->N * h->INp, "dataset"))) return rc;
@@ -290,11 +315,12 @@ bool launch_class(hieravg* h, int kc, int tt) {
       FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, mlp ? Hp : Cp, INp, h->KS1,
                 h->cps1};
       launch_fwd(s, f, A_GATHER);
+      h->ks_cur = h->KS1;
       return true;
     }
     case KC_SOFTMAX:
       if (small) return false;
-      launch_softmax_grad(s, h->part, mlp ? h->KS2 : h->KS1, W + (mlp ? h->off_b2 : h->off_b1), h->Dp, h->y, ix,
+      launch_softmax_grad(s, h->part, mlp ? h->KS2 : h->ks_cur, W + (mlp ? h->off_b2 : h->off_b1), h->Dp, h->y, ix,
                           h->G2, P, B, Bp, C, Cp);
       return true;
     case KC_UPDATE1: {
@@ -311,15 +337,34 @@ bool launch_class(hieravg* h, int kc, int tt) {
       }
       return true;
     }
-    case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, P, S); return true;
-    case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, P, P); return true;
+    case KC_STEP1:
+    case KC_STEP1_MEAN: {
+      const bool mean = kc == KC_STEP1_MEAN;
+      if (!(mean ? h->fused_mean : h->fused) || tt + 1 >= c.K1 * c.K2) return false;
+      StepArgs a{};
+      if (!mlp)
+        a.u = UpdArgs{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp,
+                      c.lr};
+      else
+        a.u = UpdArgs{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
+                      small ? nullptr : W + h->off_b1, P, B, Hp, INp, c.lr};
+      a.idx_next = ix + (int64_t)P * B;
+      a.part = h->part;
+      a.SG = mean ? S : 1;
+      launch_step_w1(s, a);
+      h->ks_cur = mean ? h->KS_mean : h->KS_step;
+      return true;
+    }
+    case KC_TAIL_MEAN: launch_group_mean(s, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P, S); return true;
+    case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, S); return true;
+    case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, P); return true;
     default: break;
   }
   if (!mlp) return false;
   switch (kc) {
     case KC_HEAD_A:
       if (!small) return false;
-      launch_head_a(s, h->part, h->KS1, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
+      launch_head_a(s, h->part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
       return true;
     case KC_HEAD_B:
       if (!small) return false;
@@ -328,7 +373,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     case KC_REDUCE1:
       if (small) return false;
-      launch_reduce_bias(s, h->part, h->KS1, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp);
+      launch_reduce_bias(s, h->part, h->ks_cur, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp);
       return true;
     case KC_FWD2: {
       if (small) return false;
@@ -352,24 +397,46 @@ bool launch_class(hieravg* h, int kc, int tt) {
 }
 
 // One local SGD step of all P learners at step tt of the round (Algorithm 1:
-// w <- w - lr/B * sum_s grad f(w; xi_s) for every learner concurrently).
-void enqueue_step(hieravg* h, int tt) {
-  static const int kSoftmax[] = {KC_FWD1, KC_SOFTMAX, KC_UPDATE1};
-  static const int kSmall[] = {KC_FWD1, KC_HEAD_A, KC_HEAD_B, KC_UPDATE1};
-  static const int kLarge[] = {KC_FWD1, KC_REDUCE1, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2, KC_UPDATE1};
+// w <- w - lr/B * sum_s grad f(w; xi_s) for every learner concurrently),
+// followed by the cluster mean when the step ends a block that is not the
+// last one.  `have_fwd`: the first-layer forward partials of this step are
+// already in `part` (computed by the previous step's fused kernel); on return
+// it says the same of the next step.
+void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
+  static const int kSoftmax[] = {KC_SOFTMAX};
+  static const int kSmall[] = {KC_HEAD_A, KC_HEAD_B};
+  static const int kLarge[] = {KC_REDUCE1, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2};
+  const hieravg_config& c = h->cfg;
   const int* seq;
   int n;
-  if (h->cfg.kind == HIERAVG_KIND_SOFTMAX) {
+  if (c.kind == HIERAVG_KIND_SOFTMAX) {
     seq = kSoftmax;
-    n = 3;
+    n = 1;
   } else if (h->C <= kSmallC) {
     seq = kSmall;
-    n = 4;
+    n = 2;
   } else {
     seq = kLarge;
-    n = 7;
+    n = 5;
   }
-  for (int i = 0; i < n; ++i) run(h, seq[i], [&] { launch_class(h, seq[i], tt); });
+  auto go = [&](int kc) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
+  if (!have_fwd) go(KC_FWD1);
+  for (int i = 0; i < n; ++i) go(seq[i]);
+  const int T = c.K1 * c.K2;
+  const bool last = tt == T - 1;
+  const bool mean = !last && (tt + 1) % c.K1 == 0 && c.S > 1;
+  have_fwd = false;
+  if (last || !h->fused || (mean && !h->fused_mean)) {
+    go(KC_UPDATE1);
+    if (mean) go(KC_GROUP_MEAN);
+  } else if (mean) {
+    go(KC_STEP1_MEAN);
+    go(KC_TAIL_MEAN);
+    have_fwd = true;
+  } else {
+    go(KC_STEP1);
+    have_fwd = true;
+  }
 }
 
 struct Segment {
@@ -486,10 +553,8 @@ int hieravg_round(hieravg_t h) {
     }
   } else {
     run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
-    for (int b = 0; b < c.K2; ++b) {
-      for (int k = 0; k < c.K1; ++k) enqueue_step(h, b * c.K1 + k);
-      if (b < c.K2 - 1 && S > 1) run(h, KC_GROUP_MEAN, [&] { launch_class(h, KC_GROUP_MEAN, 0); });
-    }
+    bool have_fwd = false;
+    for (int tt = 0; tt < T; ++tt) enqueue_step(h, tt, have_fwd);
     if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
   }
   HAV_CHECK(hipGetLastError());

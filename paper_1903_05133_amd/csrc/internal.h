@@ -84,6 +84,9 @@ enum KernelClass {
   KC_MOMENTUM,       // averaging kind: momentum update (no mean)
   KC_MOMENTUM_GROUP, // averaging kind: momentum update fused with the local mean
   KC_MOMENTUM_GLOBAL,// averaging kind: momentum update fused with the global mean
+  KC_STEP1,          // layer-1 update fused with the next step's layer-1 forward
+  KC_STEP1_MEAN,     // same, with the local mean of layer 1 in between
+  KC_TAIL_MEAN,      // local mean of the parameters after layer 1
   KC_COUNT
 };
 
@@ -150,6 +153,23 @@ struct UpdArgs {
 };
 void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
 
+// Fused step of the first weight block: the update of step t (Bsrc = the
+// dataset gathered through u.idx), optionally the mean over each group of SG
+// learners, and optionally the forward of step t+1 on the new weights.
+struct StepArgs {
+  UpdArgs u;                // u.Bsrc is the dataset, gathered through u.idx
+  const int32_t* idx_next;  // [P][Kb] sample indices of the next step
+  float* part;              // [KS][P][Mp][Mrows] forward partials of the next step
+  int SG;                   // learners averaged per group (1: no mean); SG | P
+  int NT;                   // set by the launcher: 128-column tiles per workgroup
+};
+// Whether the fused kernel handles this shape (Mp a multiple of 16 up to 64,
+// SG in {1, 2, 4, 8}, SG * Mp / 16 <= 16).
+bool step_w1_supported(int Mp, int SG);
+// Number of forward splits KS the fused kernel writes for this shape.
+int step_w1_splits(int P, int SG, int Mrows, int Ncols);
+void launch_step_w1(hipStream_t s, StepArgs a);
+
 // Head of the network (k_head.hip).
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
                         int P, int M, int Mp, int N);
@@ -164,7 +184,9 @@ void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* 
                    int Cp, int Hp, float lr);
 
 // Averaging (k_avg.hip).
-void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S);
+// Mean over each cluster of S rows of the columns [0, len) of W (row pitch
+// `pitch`, both multiples of 4 floats).
+void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, float lr, float mu);
 

@@ -123,10 +123,10 @@ static unsigned col_runs(int64_t n4, int cpb, int groups) {
 }
 
 template <bool MOM, bool MEAN, int RG, int NG, int TB = 256>
-static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int groups, float lr,
-                        float mu) {
+static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
+                        float lr, float mu) {
   dim3 grid(col_runs(n4, TB / NG, groups), (unsigned)groups);
-  launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, lr, mu);
+  launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, p4, n4, lr, mu);
 }
 
 // Cluster of S rows with S a power of two up to 64.  Up to 16 rows: one row per
@@ -141,43 +141,44 @@ static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int6
 #define HAV_AVG_TB_BIG 1024
 #endif
 template <bool MOM, int S>
-static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int groups, float lr, float mu) {
+static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
+                     float lr, float mu) {
   constexpr int kR = S <= 16 ? HAV_AVG_RG : HAV_AVG_RG_BIG;
   constexpr int RG = S < kR ? S : kR;
   constexpr int TB = S <= 16 ? 256 : HAV_AVG_TB_BIG;
-  launch_rows<MOM, true, RG, S / RG, TB>(s, W, V, Gr, n4, groups, lr, mu);
+  launch_rows<MOM, true, RG, S / RG, TB>(s, W, V, Gr, p4, n4, groups, lr, mu);
 }
 
 template <bool MOM>
-static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr, int64_t n4, int P, int S, float lr,
-                             float mu) {
+static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int P,
+                             int S, float lr, float mu) {
   const int groups = P / S;
   switch (S) {
-    case 2: launch_s<MOM, 2>(s, W, V, Gr, n4, groups, lr, mu); return true;
-    case 4: launch_s<MOM, 4>(s, W, V, Gr, n4, groups, lr, mu); return true;
-    case 8: launch_s<MOM, 8>(s, W, V, Gr, n4, groups, lr, mu); return true;
-    case 16: launch_s<MOM, 16>(s, W, V, Gr, n4, groups, lr, mu); return true;
-    case 32: launch_s<MOM, 32>(s, W, V, Gr, n4, groups, lr, mu); return true;
-    case 64: launch_s<MOM, 64>(s, W, V, Gr, n4, groups, lr, mu); return true;
+    case 2: launch_s<MOM, 2>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 4: launch_s<MOM, 4>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 8: launch_s<MOM, 8>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 16: launch_s<MOM, 16>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 32: launch_s<MOM, 32>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 64: launch_s<MOM, 64>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
     default: return false;
   }
 }
 
-void launch_group_mean(hipStream_t s, float* W, int64_t Dp, int P, int S) {
-  const int64_t n4 = Dp / 4;
-  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, n4, P, S, 0.0f, 0.0f)) return;
+void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S) {
+  const int64_t p4 = pitch / 4, n4 = len / 4;
+  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, p4, n4, P, S, 0.0f, 0.0f)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, n4, n4, S, 0.0f, 0.0f);
+  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, 0.0f, 0.0f);
 }
 
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, float lr, float mu) {
   const int64_t n4 = Dp / 4;
   if (!average) {
-    launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, P, lr, mu);
+    launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, n4, P, lr, mu);
     return;
   }
-  if (launch_mean_pow2<true>(s, W, V, Gr, n4, P, S, lr, mu)) return;
+  if (launch_mean_pow2<true>(s, W, V, Gr, n4, n4, P, S, lr, mu)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
   launch(k_rows_any<true>, grid, 256, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu);
 }

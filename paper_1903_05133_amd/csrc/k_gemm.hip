@@ -11,6 +11,12 @@
 // k_update_tn: W_p[m][n] -= lr * sum_s G_p[s][m] * Bsrc_p[s][n], the weight
 //              gradient of a layer fused with the SGD update (the gradient is
 //              never stored), plus b_p[m] -= lr * sum_s G_p[s][m].
+// k_step_w1:   the update of the first weight block at one step, optionally
+//              followed by the mean over each group of SG learners (the local
+//              average of Algorithm 1 for this block), and the forward
+//              partials of the next step computed from the new tile while it
+//              is still on chip, so the block is read and written once per
+//              step instead of twice.
 #include <algorithm>
 
 #include "internal.h"
@@ -391,6 +397,343 @@ void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc) {
     launch(k_update_tn<A_GATHER>, grid, 256, 0, s, a, mtiles, ntiles);
   else
     launch(k_update_tn<A_RELU>, grid, 256, 0, s, a, mtiles, ntiles);
+}
+
+// ------------------------------------------------------------ fused step
+// Workgroup: one 64-row x kSN-column tile range of W1 for one group of SG
+// learners, over NT consecutive column tiles (one split of the next step's
+// forward contraction).  Per tile:
+//   1. for each learner of the group: the update of k_update_tn (the same
+//      stage layout; each wave owns a 32 x kSN/2 block of 32x32x2 MFMAs); the
+//      new tile stays in registers;
+//   2. SG > 1: the group mean of the new tiles (learners in order), written
+//      to every learner of the group;
+//   3. the new tile goes to LDS; for each learner, its next-step minibatch
+//      rows (gathered, this tile's columns) are staged in LDS and the 16x16x4
+//      MFMAs add X'[s][cols] . W[h][cols] to the learner's accumulators (same
+//      k permutation as k_fwd_nt).
+// After the last tile the accumulators are the split's partial sums of the
+// next step's first-layer outputs, [split][P][Mp][Mrows].
+//
+// Loads run one work item ahead: as soon as the registers of the current
+// item's stage operands, W tile and next-step rows have been consumed, the
+// same registers receive the next item's (the next learner of the group, or
+// the next tile), so every load is in flight through at least one block of
+// MFMAs.  Past the last item the prefetch reads the last item again (in range,
+// cached, unused), so no load depends on a branch.  The sample indices of the
+// group are copied to LDS once.  The narrow tile keeps the registers and LDS
+// of a workgroup small, so several workgroups share a CU and one's MFMAs run
+// while another waits for memory.
+#ifndef HAV_STEP_SN
+#define HAV_STEP_SN 64
+#endif
+constexpr int kSN = HAV_STEP_SN;  // W1 columns per tile
+static_assert(kSN == 64 || kSN == 128, "fused step tile width");
+constexpr int kSL = kSN + 4;      // LDS row length of tile-wide rows
+constexpr int kSP = kSN / 4;      // 16-byte pieces per tile-wide row
+constexpr int kRP = 256 / kSP;    // tile-wide rows per pass of the workgroup
+constexpr int kNA = kSN / 64;     // 32x32 update accumulators per wave
+constexpr int kSU = (kUM * kSL > kSC * (kLA + kSL)) ? kUM * kSL : kSC * (kLA + kSL);
+#ifndef HAV_STEP_TARGET_WG
+#define HAV_STEP_TARGET_WG 768
+#endif
+constexpr int kStepTargetWG = HAV_STEP_TARGET_WG;
+#ifndef HAV_STEP_UNROLL_U
+#define HAV_STEP_UNROLL_U 4
+#endif
+#ifndef HAV_STEP_UNROLL_F
+#define HAV_STEP_UNROLL_F 2
+#endif
+constexpr int kStepMaxB = 64;  // largest minibatch of the fused step
+
+template <int SG, int MBF>
+__global__ __launch_bounds__(256) void k_step_w1(StepArgs a, int mtiles, int ntiles, int nchunks) {
+  constexpr int MP = MBF * 16;        // rows of the next-step forward (padded minibatch)
+  constexpr int kWL = kUM / kRP;      // W pieces per thread
+  constexpr int kXL = kSC / kRP;      // stage input pieces per thread
+  constexpr int kXN = (MP + kRP - 1) / kRP;  // next-step input pieces per thread
+  __shared__ __attribute__((aligned(16))) float lds[kSU + MP * kSL];
+  __shared__ int32_t rows_t[SG][kStepMaxB], rows_n[SG][kStepMaxB];
+  float* As = lds;               // [kSC][kLA] error rows of a stage
+  float* Bs = lds + kSC * kLA;   // [kSC][kSL] input rows of a stage
+  float* Wt = lds;               // [kUM][kSL] gradient tile, then the new tile
+  float* Xs = lds + kSU;         // [MP][kSL] next-step input rows
+  const UpdArgs& u = a.u;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = bid % mtiles;
+  const int chunk = (bid / mtiles) % nchunks;
+  const int pg = bid / (mtiles * nchunks);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int mrow0 = mt * kUM;
+  const int wn = (wave & 1) * (kSN / 2), wm = (wave >> 1) * 32;  // update: the wave's block
+  const int pc4 = tid % kSP, pr0 = tid / kSP;            // 16-byte piece of tile-wide rows
+  const bool fwd_on = mrow0 + 16 * wave < u.Mrows;       // forward: the wave's 16 rows of W
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  const float lr = u.lr;
+  const int Kb = u.Kb;
+
+  for (int e = tid; e < SG * Kb; e += 256) {
+    const int64_t g = (int64_t)pg * SG * Kb + e;
+    rows_t[e / Kb][e % Kb] = u.idx[g];
+    rows_n[e / Kb][e % Kb] = a.idx_next[g];
+  }
+  __syncthreads();
+
+  f32x4 ga[2], xb[kXL], wv[kWL], xn[kXN];
+  bool gok[2], xok[kXL], xnok[kXN];
+  // Stage s0 of item (tile n, learner j): G[s0 .. s0+32)[mrow0 .. +64) and
+  // X[idx[s]][tile columns] for s = s0 + pr0 + kRP*i.
+  auto load_stage = [&](int n, int j, int s0) {
+    const float* Gp = u.G + (int64_t)(pg * SG + j) * u.Mp * u.ldg;
+    const int col = n * kSN + 4 * pc4;
+    const bool cok = col < u.Ncols;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      const int s = s0 + (q >> 4), m = mrow0 + 4 * (q & 15);
+      gok[i] = s < Kb && m < u.Mrows;
+      ga[i] = *(const f32x4*)(Gp + (gok[i] ? (int64_t)s * u.ldg + m : 0));
+    }
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {
+      const int s = s0 + pr0 + kRP * i;
+      xok[i] = s < Kb && cok;
+      const int64_t row = rows_t[j][s < Kb ? s : 0];
+      xb[i] = *(const f32x4*)(u.Bsrc + (xok[i] ? row * u.ldb + col : 0));
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      *(f32x4*)&As[(q >> 4) * kLA + 4 * (q & 15)] = gok[i] ? ga[i] : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(pr0 + kRP * i) * kSL + 4 * pc4] = xok[i] ? xb[i] : zero4;
+  };
+  auto load_w = [&](int n, int j) {
+    const float* Wp = u.W + (int64_t)(pg * SG + j) * u.w_pitch;
+    const int col = n * kSN + 4 * pc4;
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) {
+      const int row = mrow0 + pr0 + kRP * i;
+      const bool ok = row < u.Mrows && col < u.Ncols;
+      wv[i] = *(const f32x4*)(Wp + (ok ? (int64_t)row * u.ldw + col : 0));
+    }
+  };
+  auto load_next = [&](int n, int j) {  // X'[s][tile columns], s = pr0 + kRP*i
+    const int col = n * kSN + 4 * pc4;
+    const bool cok = col < u.Ncols;
+#pragma unroll
+    for (int i = 0; i < kXN; ++i) {
+      const int s = pr0 + kRP * i;
+      xnok[i] = s < Kb && cok;
+      const int64_t row = rows_n[j][s < Kb ? s : 0];
+      xn[i] = *(const f32x4*)(u.Bsrc + (xnok[i] ? row * u.ldb + col : 0));
+    }
+  };
+
+  f32x4 accf[SG][MBF];
+#pragma unroll
+  for (int j = 0; j < SG; ++j)
+#pragma unroll
+    for (int b = 0; b < MBF; ++b) accf[j][b] = zero4;
+  f32x16 acc[kNA];
+  auto mfma_stage = [&](bool on) {
+    if (!on) return;
+#pragma unroll HAV_STEP_UNROLL_U
+    for (int ss = 0; ss < kSC; ss += 2) {
+      const int sr = ss + lhi;
+      const float av = As[sr * kLA + wm + l32];
+#pragma unroll
+      for (int jj = 0; jj < kNA; ++jj)
+        acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kSL + wn + 32 * jj + l32], acc[jj], 0, 0, 0);
+    }
+  };
+
+  const int n_begin = chunk * a.NT, n_end = min(ntiles, n_begin + a.NT);
+  load_stage(n_begin, 0, 0);
+  load_w(n_begin, 0);
+  load_next(n_begin, 0);
+  f32x4 msum[kWL];
+  for (int n = n_begin; n < n_end; ++n) {
+    const int ncol0 = n * kSN;
+    const bool wave_on = ncol0 + wn < u.Ncols;
+    const int col = ncol0 + 4 * pc4;
+    const bool col_ok = col < u.Ncols;
+
+#pragma unroll 1
+    for (int j = 0; j < SG; ++j) {
+      // next item: the next learner, else the next tile, else this item again
+      const bool more = j + 1 < SG || n + 1 < n_end;
+      const int jn = j + 1 < SG ? j + 1 : more ? 0 : j;
+      const int nn = j + 1 < SG ? n : more ? n + 1 : n;
+#pragma unroll
+      for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[jj][r] = 0.0f;
+      store_stage();
+      for (int s0 = kSC; s0 < Kb; s0 += kSC) {  // minibatches over 32: further stages
+        __syncthreads();
+        mfma_stage(wave_on);
+        __syncthreads();
+        load_stage(n, j, s0);
+        store_stage();
+      }
+      load_stage(nn, jn, 0);
+      __builtin_amdgcn_sched_barrier(0);  // the prefetch goes out before the MFMAs
+      __syncthreads();
+      mfma_stage(wave_on);
+      __syncthreads();
+#pragma unroll
+      for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+          Wt[row * kSL + wn + 32 * jj + l32] = acc[jj][r];
+        }
+      __syncthreads();
+      // New tile: each thread reads its gradient pieces and, for SG == 1,
+      // writes the new values over them (the same LDS words), so no other
+      // thread's data is touched.  Rows past Mrows and columns past Ncols hold
+      // zeros in LDS.
+      float* Wp = u.W + (int64_t)(pg * SG + j) * u.w_pitch;
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) {
+        const int rl = pr0 + kRP * i, row = mrow0 + rl;
+        const bool ok = col_ok && row < u.Mrows;
+        f32x4* t = (f32x4*)&Wt[rl * kSL + 4 * pc4];
+        const f32x4 wnew = wv[i] - lr * *t;
+        if (SG == 1) {
+          if (ok) *(f32x4*)(Wp + (int64_t)row * u.ldw + col) = wnew;
+          *t = ok ? wnew : zero4;
+        } else {
+          msum[i] = j == 0 ? wnew : msum[i] + wnew;
+        }
+      }
+      load_w(nn, jn);
+      __builtin_amdgcn_sched_barrier(0);
+      if (SG > 1) __syncthreads();  // the next learner's stage overwrites the gradient tile
+    }
+
+    if (SG > 1) {
+      // SG is a power of two: scaling by 1/SG is exact.
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) {
+        const int rl = pr0 + kRP * i, row = mrow0 + rl;
+        const bool ok = col_ok && row < u.Mrows;
+        const f32x4 mean = msum[i] * (1.0f / (float)SG);
+        if (ok)
+          for (int j = 0; j < SG; ++j)
+            *(f32x4*)(u.W + (int64_t)(pg * SG + j) * u.w_pitch + (int64_t)row * u.ldw + col) = mean;
+        *(f32x4*)&Wt[rl * kSL + 4 * pc4] = ok ? mean : zero4;
+      }
+    }
+
+    // Forward partials of the next step for every learner of the group.
+#pragma unroll
+    for (int j = 0; j < SG; ++j) {
+#pragma unroll
+      for (int i = 0; i < kXN; ++i)
+        if (pr0 + kRP * i < MP) *(f32x4*)&Xs[(pr0 + kRP * i) * kSL + 4 * pc4] = xnok[i] ? xn[i] : zero4;
+      const bool more = j + 1 < SG || n + 1 < n_end;
+      load_next(j + 1 < SG ? n : more ? n + 1 : n, j + 1 < SG ? j + 1 : more ? 0 : j);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      if (fwd_on) {
+#pragma unroll HAV_STEP_UNROLL_F
+        for (int q = 0; q < kSN / 16; ++q) {
+          const f32x4 b = *(const f32x4*)&Wt[(16 * wave + lrow) * kSL + 16 * q + 4 * lgrp];
+          f32x4 af[MBF];
+#pragma unroll
+          for (int m = 0; m < MBF; ++m) af[m] = *(const f32x4*)&Xs[(16 * m + lrow) * kSL + 16 * q + 4 * lgrp];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int m = 0; m < MBF; ++m)
+              accf[j][m] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[m][i], b[i], accf[j][m], 0, 0, 0);
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  if (fwd_on) {
+    const int h = mrow0 + 16 * wave + lrow;
+#pragma unroll
+    for (int j = 0; j < SG; ++j) {
+      float* part = a.part + ((int64_t)chunk * u.P + pg * SG + j) * u.Mp * u.Mrows;
+#pragma unroll
+      for (int m = 0; m < MBF; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * m + 4 * lgrp + r;
+          if (s < u.Mp) part[(int64_t)s * u.Mrows + h] = accf[j][m][r];
+        }
+    }
+  }
+  // Bias step (softmax model, large-C MLP), once per learner and row tile.
+  if (chunk == 0 && u.bias != nullptr && tid < kUM) {
+    const int m = mrow0 + tid;
+    if (m < u.Mrows)
+      for (int j = 0; j < SG; ++j) {
+        const int p = pg * SG + j;
+        const float* Gp = u.G + (int64_t)p * u.Mp * u.ldg;
+        float sum = 0.0f;
+        for (int s = 0; s < Kb; ++s) sum += Gp[(int64_t)s * u.ldg + m];
+        u.bias[(int64_t)p * u.w_pitch + m] -= lr * sum;
+      }
+  }
+}
+
+bool step_w1_supported(int Mp, int SG) {
+  if (Mp < 1 || Mp > kStepMaxB || Mp % 16 != 0) return false;
+  if (SG != 1 && SG != 2 && SG != 4 && SG != 8) return false;
+  return SG * (Mp / 16) <= 16;
+}
+
+static void step_plan(int P, int SG, int Mrows, int Ncols, int* mtiles, int* ntiles, int* nchunks, int* NT) {
+  *mtiles = (Mrows + kUM - 1) / kUM;
+  *ntiles = (Ncols + kSN - 1) / kSN;
+  const int64_t base = (int64_t)(P / SG) * *mtiles;
+  int nc = (int)std::min<int64_t>(*ntiles, std::max<int64_t>(1, (kStepTargetWG + base - 1) / base));
+  *NT = (*ntiles + nc - 1) / nc;
+  *nchunks = (*ntiles + *NT - 1) / *NT;
+}
+
+int step_w1_splits(int P, int SG, int Mrows, int Ncols) {
+  int mt, ntl, nc, NT;
+  step_plan(P, SG, Mrows, Ncols, &mt, &ntl, &nc, &NT);
+  return nc;
+}
+
+void launch_step_w1(hipStream_t s, StepArgs a) {
+  int mtiles, ntiles, nchunks;
+  step_plan(a.u.P, a.SG, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
+  const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
+#define HAV_STEP(SG_, MBF_) launch(k_step_w1<SG_, MBF_>, grid, 256, 0, s, a, mtiles, ntiles, nchunks)
+#define HAV_STEP_MBF(SG_)           \
+  switch (a.u.Mp / 16) {            \
+    case 1: HAV_STEP(SG_, 1); break; \
+    case 2: HAV_STEP(SG_, 2); break; \
+    case 3: HAV_STEP(SG_, 3); break; \
+    default: HAV_STEP(SG_, 4); break; \
+  }
+  switch (a.SG) {
+    case 1: HAV_STEP_MBF(1) break;
+    case 2: HAV_STEP_MBF(2) break;
+    case 4: HAV_STEP_MBF(4) break;
+    default:
+      if (a.u.Mp / 16 == 1)
+        HAV_STEP(8, 1);
+      else
+        HAV_STEP(8, 2);
+      break;
+  }
+#undef HAV_STEP_MBF
+#undef HAV_STEP
 }
 
 }  // namespace hav

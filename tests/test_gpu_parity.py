@@ -58,6 +58,10 @@ SMALL = {
     "mlp_ragged": cases.case("mlp", 6, 3, 2, 3, B=5, IN=100, H=70, C=3, N=37, sigma=0.5, lr=0.1, seed=1),
     "mlp_batch1_S1": cases.case("mlp", 2, 1, 1, 2, B=1, IN=64, H=64, C=16, N=10, lr=0.1, seed=2),
     "mlp_batch_150": cases.case("mlp", 2, 2, 1, 1, B=150, IN=200, H=130, C=7, N=300, lr=0.05, seed=6),
+    # fused step kernel with the cluster mean of 8 learners, one 16-row batch tile
+    "mlp_group_mean_S8": cases.case("mlp", 16, 8, 2, 2, B=12, IN=200, H=70, C=5, N=300, lr=0.1, seed=13),
+    # fused step with the mean of 4 learners on the softmax model; ragged last column tile
+    "softmax_group_mean_S4": cases.case("softmax", 8, 4, 1, 3, B=20, IN=130, C=12, N=90, lr=0.2, seed=14),
     "mlp_one_learner": cases.case("mlp", 1, 1, 3, 2, B=8, IN=96, H=33, C=5, N=64, lr=0.1, seed=7),
     "mlp_one_sample_dataset": cases.case("mlp", 4, 4, 2, 1, B=3, IN=50, H=20, C=2, N=1, lr=0.1, seed=8),
     "softmax_ragged": cases.case("softmax", 3, 3, 3, 1, B=17, IN=33, C=17, N=50, lr=0.2, seed=3),
@@ -199,8 +203,25 @@ def test_torch_stream_and_profile(gpu_lib):
         stats = h.profile_read()
         h.set_stream(None)
         assert np.array_equal(h.params(), ref)
-    steps = c["K1"] * c["K2"]
-    assert stats["fwd1_gemm"][0] == steps and stats["update1_gemm"][0] == steps
+    # P=4 S=2 K1=2 K2=2, padded batch 48: the stand-alone forward at step 0,
+    # the fused step (with the cluster mean at the end of block 0) at steps
+    # 0-2, the plain update at the last step, then the global mean.
+    assert stats["fwd1_gemm"][0] == 1 and stats["update1_gemm"][0] == 1
+    assert stats["step1_gemm"][0] == 2 and stats["step1_gemm_group_mean"][0] == 1
+    assert stats["tail_group_mean"][0] == 1 and "group_mean" not in stats
     assert stats["draw_indices"][0] == 1 and stats["global_mean"][0] == 1
-    assert stats["group_mean"][0] == c["K2"] - 1
     assert all(ms >= 0.0 for _, ms in stats.values())
+
+
+def test_unfused_schedule_profile(gpu_lib):
+    """S = 3 has no fused-mean kernel: block ends run the plain update, the
+    whole-replica cluster mean and the stand-alone forward of the next step."""
+    from paper_1903_05133_amd import HierAvg
+    c = SMALL["mlp_ragged"]  # P=6 S=3 K1=2 K2=3
+    with HierAvg(config=cases.native_config(c)) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+    assert stats["group_mean"][0] == 2 and stats["fwd1_gemm"][0] == 3
+    assert stats["update1_gemm"][0] == 3 and stats["step1_gemm"][0] == 3
+    assert "step1_gemm_group_mean" not in stats
