@@ -54,6 +54,27 @@ typedef struct hieravg* hieravg_t;
 #define HIERAVG_MODEL_AVERAGING_11_7M 3      /* D=11.7e6, momentum 0.9, stds 0.01  */
 
 /*
+ * How the first weight block (W1 of the MLP) takes its SGD steps inside a
+ * round.  Both give the result of Algorithm 1 up to float32 rounding.
+ *  EAGER:   every step reads and writes each learner's W1 (the fused
+ *           update-and-next-forward kernel).
+ *  DELAYED: within a block of K1 steps each learner's W1 is its cluster's
+ *           block-start copy minus lr times the sum of its steps' rank-B
+ *           updates G^T X.  The forward uses the block-start copy plus the
+ *           correction -lr * sum_{k'<k} (X_k X_k'^T) G_k' and the cluster
+ *           mean at the block end is one update of the copy by the summed
+ *           G^T X of the cluster's learners and steps.  Needs the MLP with at
+ *           most 32 classes, B <= 32 and K1 <= 8, and a round that starts
+ *           with equal W1 in every replica (true after create and after every
+ *           round; after hieravg_set_params the next round runs EAGER).
+ *  AUTO:    DELAYED where it applies and its extra Gram products cost at most
+ *           an eighth of the step's flops ((K1 - 1) * B <= H / 2), else EAGER.
+ */
+#define HIERAVG_UPDATE_AUTO 0
+#define HIERAVG_UPDATE_EAGER 1
+#define HIERAVG_UPDATE_DELAYED 2
+
+/*
  * Full description of a workload.  Synthetic data, minibatch draws, initial
  * parameters and (averaging kind) the given gradients are all generated on
  * the GPU from `seed` with the SplitMix64 counter generator (Steele, Lea &
@@ -84,6 +105,7 @@ typedef struct hieravg_config {
   float init_std;   /* averaging kind: std of the initial replica           */
   float grad_std;   /* averaging kind: std of the given gradients           */
   uint64_t seed;
+  int32_t update_mode; /* HIERAVG_UPDATE_* (how the first weight block is updated) */
 } hieravg_config;
 
 /*
@@ -97,7 +119,8 @@ typedef struct hieravg_config {
 hieravg_t hieravg_create(int32_t P, int32_t S, int32_t K1, int32_t K2, int32_t model, float lr,
                          int32_t B, uint64_t seed);
 
-/* Same, for an explicit workload description (any dimensions). */
+/* Same, for an explicit workload description (any dimensions).  Also NULL for
+ * an update_mode outside HIERAVG_UPDATE_* or DELAYED where it does not apply. */
 hieravg_t hieravg_create_config(const hieravg_config* cfg);
 
 /*
@@ -105,7 +128,10 @@ hieravg_t hieravg_create_config(const hieravg_config* cfg);
  * local SGD steps, a local mean over each cluster after every block but the
  * last, and the global mean at the end (the local mean right before the
  * global mean does not change the exact result and is skipped).
- * Asynchronous with respect to the host.  Returns HIERAVG_OK or an error.
+ * Asynchronous with respect to the host.  The first call captures the
+ * round's kernels into a HIP graph; later calls launch that graph on the
+ * handle's current stream (while profiling, the kernels are launched one by
+ * one instead).  Returns HIERAVG_OK or an error.
  */
 int hieravg_round(hieravg_t h);
 

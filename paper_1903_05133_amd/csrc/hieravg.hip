@@ -42,7 +42,8 @@ const char* kClassNames[KC_COUNT] = {
     "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",   "softmax_grad", "bwd_hidden",
     "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
-    "step1_gemm_group_mean",     "tail_group_mean"};
+    "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_shared_gemm", "block_update_gemm",
+    "w1_global_mean", "tail_global_mean", "gram_reduce"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -87,8 +88,21 @@ struct hieravg {
   bool fused_mean = false;  // ... and also with the cluster mean (SG = S)
   int KS_step = 1, KS_mean = 1;  // forward splits written by the fused kernel
   int ks_cur = 1;                // splits of the partials currently in `part`
+  // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
+  bool delayed = false;    // the handle uses them for rounds that start with equal W1
+  bool w1_shared = true;   // every learner's W1 equals replica 0's (other rows may be stale)
+  bool in_delayed = false; // the round being enqueued uses them
+  int SGf = 1;             // learners per row group of the shared forward (divides S)
+  int KS_d = 1, cps_d = 1; // splits of the shared forward
+  float* Wc = nullptr;     // [P/S][Hp*INp] cluster copies of W1
+  float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
+  float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
+  int KSG = 1;             // feature splits of the Gram blocks
   hipStream_t own_stream = nullptr, stream = nullptr;
   int64_t steps = 0;
+  // One round's kernels, captured on first use and replayed for every round
+  // that is not profiled (every launch argument is the same in every round).
+  hipGraphExec_t round_exec[2] = {nullptr, nullptr};  // [eager, delayed]
 
   bool profiling = false;
   std::vector<ProfRec> recs;
@@ -128,7 +142,8 @@ void run(hieravg* h, int kc, F&& fn) {
 void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
-  void* bufs[] = {h->W, h->V, h->Gr, h->X, h->y, h->idx, h->part, h->Z1, h->PL, h->G2, h->G1, h->ctr};
+  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1,
+                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   for (auto& r : h->recs) {
@@ -136,6 +151,8 @@ void release(hieravg* h) {
     (void)hipEventDestroy(r.b);
   }
   for (auto e : h->pool) (void)hipEventDestroy(e);
+  for (auto e : h->round_exec)
+    if (e) (void)hipGraphExecDestroy(e);
   if (h->own_stream) (void)hipStreamDestroy(h->own_stream);
   delete h;
 }
@@ -157,6 +174,10 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
   return HIERAVG_OK;
 }
 
+bool delayed_applies(const hieravg_config& c) {
+  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8;
+}
+
 int validate(const hieravg_config& c) {
   auto bad = [](const char* m) {
     set_error(m);
@@ -169,6 +190,10 @@ int validate(const hieravg_config& c) {
   if (c.K2 < 1) return bad("K2 must be >= 1");
   if ((int64_t)c.K1 * c.K2 > (1 << 20)) return bad("K1*K2 must be <= 2^20");
   if (!std::isfinite(c.lr) || c.lr < 0.0f) return bad("lr must be finite and >= 0");
+  if (c.update_mode < HIERAVG_UPDATE_AUTO || c.update_mode > HIERAVG_UPDATE_DELAYED)
+    return bad("update_mode must be one of HIERAVG_UPDATE_*");
+  if (c.update_mode == HIERAVG_UPDATE_DELAYED && !delayed_applies(c))
+    return bad("delayed updates need the MLP with at most 32 classes, B <= 32 and K1 <= 8");
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
     if (!std::isfinite(c.momentum) || c.momentum < 0.0f || c.momentum >= 1.0f)
@@ -247,6 +272,19 @@ int build(hieravg* h) {
       h->KS_mean = step_w1_splits(P, c.S, (int)n1, (int)h->INp);
       ks_max = std::max(ks_max, h->KS_mean);
     }
+    if (mlp && delayed_applies(c)) {
+      const bool cheap = (int64_t)(c.K1 - 1) * h->Bp * 2 <= h->Hp;
+      h->delayed = c.update_mode == HIERAVG_UPDATE_DELAYED || (c.update_mode == HIERAVG_UPDATE_AUTO && cheap);
+    }
+    if (h->delayed) {
+      // Row groups of up to 128 rows that share one cluster copy.
+      h->SGf = 1;
+      for (int d = 1; d <= c.S; ++d)
+        if (c.S % d == 0 && d * h->Bp <= 128) h->SGf = d;
+      plan_split(P / h->SGf, h->SGf * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_d, &h->cps_d, HAV_FWD_SHARED_TARGET,
+                 HAV_FWD_SHARED_MB);
+      ks_max = std::max(ks_max, h->KS_d);
+    }
     h->ks_cur = h->KS1;
     const int64_t part_floats =
         std::max<int64_t>((int64_t)ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
@@ -265,6 +303,15 @@ int build(hieravg* h) {
       if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
     }
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
+    if (h->delayed) {
+      const int64_t w1 = h->Hp * h->INp;
+      if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
+      if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * h->Bp * h->Hp, "block errors"))) return rc;
+      h->KSG = gram_splits(P, c.K2, (int)h->INp);
+      if (c.K1 > 1 && (rc = alloc_zero(h, (void**)&h->gram,
+                                       sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * h->Bp * h->Bp, "Gram blocks")))
+        return rc;
+    }
     h->key_index = hash64(seed, kTagIndex);
     launch_gen_labels(h->stream, h->y, h->N, hash64(seed, kTagLabel), (uint64_t)h->C);
     launch_gen_data(h->stream, h->X, h->y, h->N, h->IN, h->INp, hash64(seed, kTagMean), hash64(seed, kTagNoise),
@@ -356,21 +403,70 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     }
     case KC_TAIL_MEAN: launch_group_mean(s, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P, S); return true;
+    case KC_TAIL_GLOBAL: launch_group_mean(s, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P, P); return true;
+    case KC_GRAM:
+      if (!h->delayed || h->gram == nullptr) return false;
+      launch_gram(s, h->X, h->INp, INp, h->idx, h->gram, P, c.K1, c.K2, B, Bp, h->KSG);
+      return true;
+    case KC_GRAM_REDUCE:
+      if (!h->delayed || h->gram == nullptr || h->KSG < 2) return false;
+      launch_gram_reduce(s, h->gram, P, c.K1, c.K2, Bp, h->KSG);
+      return true;
+    case KC_FWD1_SHARED: {
+      if (!h->delayed) return false;
+      // Block b reads the round-start W1 (replica 0) for b = 0, else its
+      // cluster's copy.
+      const int b = tt / c.K1;
+      FwdArgs f{h->X, ix, h->INp, b == 0 ? W + h->off_W1 : h->Wc, b == 0 ? 0 : h->Hp * h->INp, h->INp, h->part, P,
+                B, Bp, Hp, INp, h->KS_d, h->cps_d};
+      f.SG = h->SGf;
+      f.wdiv = S / h->SGf;
+      f.mb_max = HAV_FWD_SHARED_MB;
+      launch_fwd(s, f, A_GATHER);
+      h->ks_cur = h->KS_d;
+      return true;
+    }
+    case KC_BLOCK_UPDATE: {
+      if (!h->delayed) return false;
+      const int b = tt / c.K1;
+      const int64_t w1 = h->Hp * h->INp;
+      BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
+                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, c.lr / (float)S};
+      launch_block_update(s, a);
+      return true;
+    }
+    case KC_W1_MEAN:
+      if (!h->delayed) return false;
+      launch_mean_rows(s, W + h->off_W1, h->Wc, h->Hp * h->INp, h->Hp * h->INp, P / S);
+      return true;
     case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, S); return true;
     case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, P); return true;
     default: break;
   }
   if (!mlp) return false;
   switch (kc) {
-    case KC_HEAD_A:
+    case KC_HEAD_A: {
       if (!small) return false;
-      launch_head_a(s, h->part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp);
+      HeadCorr corr;
+      if (h->in_delayed && h->gram != nullptr) {
+        corr.gram = h->gram + (int64_t)(tt / c.K1) * P * c.K1 * c.K1 * Bp * Bp;
+        corr.gs = h->Gs;
+        corr.k = tt % c.K1;
+        corr.K1 = c.K1;
+        corr.lr = c.lr;
+      }
+      launch_head_a(s, h->part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp,
+                    corr);
       return true;
-    case KC_HEAD_B:
+    }
+    case KC_HEAD_B: {
       if (!small) return false;
-      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, h->G1, h->y, ix, P, B, Bp,
+      // Under delayed updates the hidden errors are kept for the block end.
+      float* g1 = h->in_delayed ? h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp : h->G1;
+      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, g1, h->y, ix, P, B, Bp,
                     C, Cp, Hp, c.lr);
       return true;
+    }
     case KC_REDUCE1:
       if (small) return false;
       launch_reduce_bias(s, h->part, h->ks_cur, W + h->off_b1, h->Dp, h->Z1, P, B, Bp, Hp);
@@ -530,11 +626,12 @@ hieravg_t hieravg_create(int32_t P, int32_t S, int32_t K1, int32_t K2, int32_t m
   return hieravg_create_config(&c);
 }
 
-int hieravg_round(hieravg_t h) {
-  if (!h) {
-    set_error("NULL handle");
-    return HIERAVG_EINVAL;
-  }
+}  // extern "C"
+
+namespace {
+
+// Every kernel of one round, enqueued on the handle's stream.
+void enqueue_round(hieravg* h) {
   const hieravg_config& c = h->cfg;
   const int T = c.K1 * c.K2;
   const int P = c.P, S = c.S;
@@ -551,14 +648,73 @@ int hieravg_round(hieravg_t h) {
         run(h, kc, [&] { launch_class(h, kc, tt); });
       }
     }
+  } else if (h->in_delayed) {
+    // Delayed first-layer updates: per block, K1 steps of forward from the
+    // block-start copies (with the Gram corrections), head and hidden error,
+    // then one update of each cluster's copy; at the end the global mean of
+    // the copies goes to replica 0 (every learner's W1) and the other
+    // parameters take their global mean.
+    auto go = [&](int kc, int tt) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
+    go(KC_DRAW, 0);
+    if (c.K1 > 1) {
+      go(KC_GRAM, 0);
+      if (h->KSG > 1) go(KC_GRAM_REDUCE, 0);
+    }
+    for (int b = 0; b < c.K2; ++b) {
+      for (int k = 0; k < c.K1; ++k) {
+        const int tt = b * c.K1 + k;
+        go(KC_FWD1_SHARED, tt);
+        go(KC_HEAD_A, tt);
+        go(KC_HEAD_B, tt);
+      }
+      go(KC_BLOCK_UPDATE, b * c.K1);
+      if (b < c.K2 - 1 && S > 1) go(KC_TAIL_MEAN, 0);
+    }
+    go(KC_W1_MEAN, 0);
+    if (P > 1) go(KC_TAIL_GLOBAL, 0);
   } else {
     run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
     bool have_fwd = false;
     for (int tt = 0; tt < T; ++tt) enqueue_step(h, tt, have_fwd);
     if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+int hieravg_round(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  // Delayed updates need every learner to start the round from replica 0's W1.
+  h->in_delayed = h->delayed && h->w1_shared;
+  if (h->profiling) {
+    enqueue_round(h);
+  } else {
+    hipGraphExec_t& exec = h->round_exec[h->in_delayed ? 1 : 0];
+    if (!exec) {
+      HAV_CHECK(hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
+      enqueue_round(h);
+      hipGraph_t graph = nullptr;
+      HAV_CHECK(hipStreamEndCapture(h->stream, &graph));
+      const hipError_t e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (e != hipSuccess) {
+        exec = nullptr;
+        set_error(std::string("hipGraphInstantiate of the round failed: ") + hipGetErrorString(e));
+        return HIERAVG_EHIP;
+      }
+    }
+    HAV_CHECK(hipGraphLaunch(exec, h->stream));
+  }
   HAV_CHECK(hipGetLastError());
-  h->steps += T;
+  // After the global mean every learner holds replica 0's W1 (under delayed
+  // updates only replica 0's copy is written).
+  h->w1_shared = true;
+  h->steps += (int64_t)h->cfg.K1 * h->cfg.K2;
   return HIERAVG_OK;
 }
 
@@ -574,11 +730,16 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {
     return HIERAVG_ESIZE;
   }
   HAV_CHECK(hipStreamSynchronize(h->stream));
+  const std::vector<Segment> segs = segments(h);
   for (int p = 0; p < P; ++p)
-    for (const Segment& g : segments(h))
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const Segment& g = segs[i];
+      // Under delayed updates only replica 0 holds the (common) W1.
+      const int64_t src_row = (i == 0 && h->delayed && h->w1_shared) ? 0 : p;
       HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
-                                 h->W + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
+                                 h->W + src_row * h->Dp + g.src_off, sizeof(float) * g.src_ld,
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+    }
   HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
 }
@@ -600,6 +761,7 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
                                  src + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
   HAV_CHECK(hipStreamSynchronize(h->stream));
+  h->w1_shared = false;  // the rows may differ: the next round updates W1 eagerly
   return HIERAVG_OK;
 }
 

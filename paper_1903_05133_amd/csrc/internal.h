@@ -87,6 +87,12 @@ enum KernelClass {
   KC_STEP1,          // layer-1 update fused with the next step's layer-1 forward
   KC_STEP1_MEAN,     // same, with the local mean of layer 1 in between
   KC_TAIL_MEAN,      // local mean of the parameters after layer 1
+  KC_GRAM,           // delayed updates: Gram blocks of the round's minibatches
+  KC_FWD1_SHARED,    // delayed updates: layer-1 forward from the cluster copies
+  KC_BLOCK_UPDATE,   // delayed updates: block-end update of the cluster copies
+  KC_W1_MEAN,        // delayed updates: global mean of the cluster copies
+  KC_TAIL_GLOBAL,    // global mean of the parameters after layer 1
+  KC_GRAM_REDUCE,    // delayed updates: sum of the Gram blocks' feature splits
   KC_COUNT
 };
 
@@ -127,15 +133,27 @@ struct FwdArgs {
   const float* A;       // gathered: dataset X [N][lda]; relu: Z [P][Mp][lda]
   const int32_t* idx;   // [P][M] sample indices (gathered A)
   int64_t lda;
-  const float* W;       // weight block of replica 0 ([N][ldw]); replica p at W + p*w_pitch
+  const float* W;       // weight block of copy 0 ([N][ldw]); copy c at W + c*w_pitch
   int64_t w_pitch, ldw;
   float* part;          // [KS][P][Mp][N] split-K partial sums
   int P, M, Mp, N, K;   // N multiple of 16, K multiple of 64
   int KS, cps;          // split count and 64-wide K chunks per split
+  // Learners p = g*SG .. g*SG+SG-1 form row group g (SG*Mp rows of one GEMM)
+  // and read weight copy g / wdiv (w_pitch 0: one copy for all).
+  int SG = 1, wdiv = 1;
+  int mb_max = 8;  // largest row tile, in 16-row blocks (1, 2, 4 or 8)
 };
 enum ASource { A_GATHER = 0, A_RELU = 1 };
 void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src);
-void plan_split(int P, int Mp, int N, int K, int* KS, int* cps);
+// Split count for a forward over P row groups of Mp rows each.
+void plan_split(int P, int Mp, int N, int K, int* KS, int* cps, int target_wg = 0, int mb_max = 8);
+// Workgroup target and row tile of the forward from shared cluster copies.
+#ifndef HAV_FWD_SHARED_TARGET
+#define HAV_FWD_SHARED_TARGET 256
+#endif
+#ifndef HAV_FWD_SHARED_MB
+#define HAV_FWD_SHARED_MB 4
+#endif
 int fwd_tiles(int P, int Mp, int N);
 
 struct UpdArgs {
@@ -152,6 +170,37 @@ struct UpdArgs {
   float lr;
 };
 void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
+
+// Delayed first-layer update at the end of a block of K1 steps (the local
+// averaging of Algorithm 1 applied to the first weight block): for each group
+// g of SG learners,
+//   Wo_g = Wb_g - lr_eff * sum_{k<K1, j in g, s<B} G[k][j][s][:]^T X[idx[k][j][s]][:]
+// with lr_eff = lr / SG (the mean of the SG learners' K1 updates).
+struct BlkArgs {
+  const float* G;       // [K1][P][Mp][ldg] hidden errors of the block's steps
+  int64_t ldg;
+  const float* X;       // dataset [N][ldx]
+  const int32_t* idx;   // [K1][P][B] indices of the block's steps
+  int64_t ldx;
+  const float* Wb;      // base of group g at Wb + g*wb_pitch (0: one base for all)
+  int64_t wb_pitch;
+  float* Wo;            // result of group g at Wo + g*wo_pitch (may equal the base)
+  int64_t wo_pitch, ldw;
+  int P, SG, K1, B, Mp, Mrows, Ncols;
+  float lr_eff;
+};
+void launch_block_update(hipStream_t s, const BlkArgs& a);
+
+// Gram blocks of each learner's minibatches within each block of a round, as
+// KSG partial sums over splits of the input features:
+// sum_ks gram[ks][b][p][k][k2][s][s2] = X[idx_(b,k,p,s)] . X[idx_(b,k2,p,s2)]
+// for k2 < k (rows and columns past B are zero), shape
+// [KSG][K2][P][K1][K1][Bp][Bp]; launch_gram_reduce then adds the partial sums
+// into split 0.  K1 * Bp <= 256.
+int gram_splits(int P, int K2, int K);
+void launch_gram(hipStream_t s, const float* X, int64_t ldx, int K, const int32_t* idx, float* gram, int P,
+                 int K1, int K2, int B, int Bp, int KSG);
+void launch_gram_reduce(hipStream_t s, float* gram, int P, int K1, int K2, int Bp, int KSG);
 
 // Fused step of the first weight block: the update of step t (Bsrc = the
 // dataset gathered through u.idx), optionally the mean over each group of SG
@@ -177,8 +226,18 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp);
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp);
+// Correction of the first-layer pre-activations under delayed updates: at
+// step k of a block the learner's first weight block is its block base minus
+// lr times the sum of its previous steps' G^T X, so
+//   Z1 = X Wb^T + b1 - lr * sum_{k2<k} gram[k][k2] G[k2].
+struct HeadCorr {
+  const float* gram = nullptr;  // [P][K1][K1][Bp][Bp] of the block (nullptr: none)
+  const float* gs = nullptr;    // [K1][P][Bp][Hp] hidden errors of the block's steps
+  int k = 0, K1 = 1;
+  float lr = 0.0f;
+};
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp);
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr());
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, float lr);
@@ -187,6 +246,8 @@ void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* 
 // Mean over each cluster of S rows of the columns [0, len) of W (row pitch
 // `pitch`, both multiples of 4 floats).
 void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S);
+// dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4 floats).
+void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, float lr, float mu);
 

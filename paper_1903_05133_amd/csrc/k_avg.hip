@@ -171,6 +171,20 @@ void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int 
   launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, 0.0f, 0.0f);
 }
 
+__global__ __launch_bounds__(256) void k_mean_rows(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
+                                                   int64_t pitch4, int64_t n4, int n) {
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    f32x4 sum = src[i];
+    for (int r = 1; r < n; ++r) sum += src[r * pitch4 + i];
+    dst[i] = sum / (float)n;
+  }
+}
+
+void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n) {
+  const int64_t n4 = len / 4;
+  launch(k_mean_rows, col_runs(n4, 256, 1), 256, 0, s, (f32x4*)dst, (const f32x4*)src, pitch / 4, n4, n);
+}
+
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, float lr, float mu) {
   const int64_t n4 = Dp / 4;

@@ -144,13 +144,20 @@ constexpr int kHM = 32;  // samples per chunk
 // masks), and this slice's partial logits
 //   PL[p][m][c][ht] = sum_{h in slice} ReLU(Z1[m][h]) * W2[c][h].
 // Thread t reads 16-byte pieces (units 4*(t%8) .. +3) of row t/8 of the chunk.
+// With delayed first-layer updates (corr.gram set) the pre-activations also
+// take the correction -lr * sum_{k2<k} gram[k][k2] G[k2] of the learner's
+// earlier steps in the block (M <= 32: one chunk; the errors' slice for this
+// workgroup's units is staged in LDS, the Gram rows are read per thread).
+constexpr int kCorrMaxK = 7;  // earlier steps in a block (K1 <= 8)
 template <int KC>
 __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, int KS, const float* __restrict__ b1,
                                                 const float* __restrict__ W2, int64_t w_pitch,
                                                 float* __restrict__ Z1, float* __restrict__ PL, int P, int M, int Mp,
-                                                int C, int Cp, int Hp, int htiles) {
+                                                int C, int Cp, int Hp, int htiles, HeadCorr corr) {
   __shared__ float zs[kHM][kHU + 1];
   __shared__ float ws[KC][kHU + 1];
+  __shared__ __attribute__((aligned(16))) float gsl[kCorrMaxK][kHM][kHU];
+  __shared__ float grl[kCorrMaxK][kHM][kHM + 1];
   const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
   const int tid = threadIdx.x, u4 = tid & 7, rr = tid >> 3;
   const int h4 = ht * kHU + 4 * u4;
@@ -165,13 +172,37 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
   const f32x4 bias = *(const f32x4*)(b1 + (int64_t)p * w_pitch + h4);
   const int64_t split = (int64_t)P * Mp * Hp;
   const float* p0 = part + (int64_t)p * Mp * Hp + h4;
+  const int kc = corr.gram != nullptr ? corr.k : 0;
+  if (kc > 0) {
+    // errors of the earlier steps, this slice: gsl[k2][s][u] = G[k2][p][s][32*ht + u],
+    // and the learner's Gram rows: grl[k2][s][s2] = gram[k][k2][s][s2]
+    for (int e = tid; e < kc * kHM * (kHU / 4); e += 256) {
+      const int k2 = e / (kHM * (kHU / 4)), rem = e % (kHM * (kHU / 4));
+      const int sm = rem / (kHU / 4), c4 = rem % (kHU / 4);
+      const f32x4 v = *(const f32x4*)(corr.gs + (((int64_t)k2 * P + p) * Mp + (sm < Mp ? sm : 0)) * Hp + ht * kHU + 4 * c4);
+      *(f32x4*)&gsl[k2][sm][4 * c4] = sm < M ? v : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const float* gk = corr.gram + (((int64_t)p * corr.K1 + corr.k) * corr.K1) * Mp * Mp;
+    for (int e = tid; e < kc * Mp * Mp; e += 256) {
+      const int k2 = e / (Mp * Mp), rem = e % (Mp * Mp);
+      grl[k2][rem / Mp][rem % Mp] = gk[(int64_t)k2 * Mp * Mp + rem];
+    }
+    __syncthreads();
+  }
   for (int m0 = 0; m0 < M; m0 += kHM) {
     const int m = m0 + rr;
     const bool mok = m < M;
     const float* pm = p0 + (int64_t)(mok ? m : 0) * Hp;
-    f32x4 z = bias;
+    f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
     for (int ks = 0; ks < KS; ++ks) z += *(const f32x4*)(pm + ks * split);
+    z += bias;
+    if (kc > 0) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+      for (int k2 = 0; k2 < kc; ++k2)
+        for (int s2 = 0; s2 < M; ++s2) c += grl[k2][rr][s2] * *(const f32x4*)&gsl[k2][s2][4 * u4];
+      z -= corr.lr * c;
+    }
     if (mok) *(f32x4*)(Z1 + ((int64_t)p * Mp + m) * Hp + h4) = z;
     zs[rr][4 * u4 + 0] = mok ? fmaxf(z.x, 0.0f) : 0.0f;
     zs[rr][4 * u4 + 1] = mok ? fmaxf(z.y, 0.0f) : 0.0f;
@@ -319,12 +350,14 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp) {
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr) {
   const int htiles = Hp / kHU;
   if (C <= 16)
-    launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+    launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
+           corr);
   else
-    launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles);
+    launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
+           corr);
 }
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,

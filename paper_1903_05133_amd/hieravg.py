@@ -120,7 +120,7 @@ class HierAvg:
 
 
 def config(kind, P, S, K1, K2, B=1, in_dim=0, hidden=0, classes=0, n_samples=0, noise_std=1.0, lr=0.05,
-           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0):
+           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0, update_mode=0):
     return native.Config(P=P, S=S, K1=K1, K2=K2, B=B, kind=kind, in_dim=in_dim, hidden=hidden, classes=classes,
                          n_samples=n_samples, noise_std=noise_std, lr=lr, momentum=momentum, init_std=init_std,
-                         grad_std=grad_std, seed=seed)
+                         grad_std=grad_std, seed=seed, update_mode=update_mode)

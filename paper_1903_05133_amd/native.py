@@ -21,6 +21,7 @@ class Config(ctypes.Structure):
         ("noise_std", ctypes.c_float), ("lr", ctypes.c_float), ("momentum", ctypes.c_float),
         ("init_std", ctypes.c_float), ("grad_std", ctypes.c_float),
         ("seed", ctypes.c_uint64),
+        ("update_mode", ctypes.c_int32),
     ]
 
 

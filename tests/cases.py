@@ -29,11 +29,15 @@ def named(name, P, S, K1, K2, B, lr, seed=0):
     return case(kind, P, S, K1, K2, B=B, lr=lr, seed=seed, **d)
 
 
-def native_config(c):
+UPDATE_MODES = {"auto": 0, "eager": 1, "delayed": 2}
+
+
+def native_config(c, update_mode="auto"):
     from paper_1903_05133_amd import config
     return config(KINDS[c["kind"]], c["P"], c["S"], c["K1"], c["K2"], B=c["B"], in_dim=c["IN"], hidden=c["H"],
                   classes=c["C"], n_samples=c["N"], noise_std=c["sigma"], lr=c["lr"], momentum=c["momentum"],
-                  init_std=c["init_std"], grad_std=c["grad_std"], seed=c["seed"])
+                  init_std=c["init_std"], grad_std=c["grad_std"], seed=c["seed"],
+                  update_mode=UPDATE_MODES[update_mode])
 
 
 def oracle_problem(c):

@@ -63,6 +63,25 @@ def test_invalid_config_rejected():
     assert not L.hieravg_create_config(ctypes.byref(c))
     assert "momentum" in L.hieravg_last_error().decode()
     assert not L.hieravg_create_config(None)
+    c = config(1, 4, 2, 1, 1, B=8, in_dim=10, hidden=5, classes=3, n_samples=10, update_mode=3)
+    assert not L.hieravg_create_config(ctypes.byref(c))
+    assert "update_mode" in L.hieravg_last_error().decode()
+    # delayed first-layer updates: MLP with at most 32 classes, B <= 32, K1 <= 8
+    for kw in (dict(classes=33, B=8, K1=1), dict(classes=3, B=33, K1=1), dict(classes=3, B=8, K1=9)):
+        c = config(1, 4, 2, kw["K1"], 1, B=kw["B"], in_dim=10, hidden=5, classes=kw["classes"], n_samples=10,
+                   update_mode=2)
+        assert not L.hieravg_create_config(ctypes.byref(c))
+        assert "delayed" in L.hieravg_last_error().decode()
+    c = config(0, 4, 2, 1, 1, B=8, in_dim=10, classes=3, n_samples=10, update_mode=2)
+    assert not L.hieravg_create_config(ctypes.byref(c))
+
+
+def test_kernel_class_names():
+    L = native.lib()
+    n = L.hieravg_kernel_classes()
+    names = [L.hieravg_kernel_class_name(i) for i in range(n)]
+    assert all(names) and len(set(names)) == n
+    assert L.hieravg_kernel_class_name(n) == b""
 
 
 def test_null_handles_are_safe():

@@ -22,10 +22,10 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-4
 
 
-def _run_gpu(c, rounds=1):
+def _run_gpu(c, rounds=1, mode="auto"):
     from paper_1903_05133_amd import HierAvg
-    print(f"[gpu case] {c}", flush=True)
-    h = HierAvg(config=cases.native_config(c))
+    print(f"[gpu case] {mode} {c}", flush=True)
+    h = HierAvg(config=cases.native_config(c, mode))
     for _ in range(rounds):
         h.round()
     got = h.params()
@@ -76,9 +76,29 @@ SMALL = {
 @pytest.mark.parametrize("name", sorted(SMALL))
 def test_small_cases_match_oracle(name, gpu_lib):
     c = SMALL[name]
-    got, idx, steps = _run_gpu(c, rounds=2)
+    got, idx, steps = _run_gpu(c, rounds=2, mode="eager")
     assert steps == 2 * c["K1"] * c["K2"]
     _check(c, got, idx, *_oracle(c, 2))
+
+
+# MLP cases within the delayed-update limits (at most 32 classes, B <= 32, K1 <= 8)
+DELAYED = sorted(n for n, c in SMALL.items() if c["kind"] == "mlp" and c["C"] <= 32 and c["B"] <= 32)
+
+
+@pytest.mark.parametrize("name", DELAYED)
+def test_small_cases_delayed_updates_match_oracle(name, gpu_lib):
+    c = SMALL[name]
+    got, idx, steps = _run_gpu(c, rounds=2, mode="delayed")
+    assert steps == 2 * c["K1"] * c["K2"]
+    _check(c, got, idx, *_oracle(c, 2))
+
+
+def test_delayed_updates_long_block(gpu_lib):
+    """K1 = 8 earlier-step corrections (the largest block the delayed path
+    takes), B = 32, S = 2, three blocks."""
+    c = cases.case("mlp", 4, 2, 8, 3, B=32, IN=130, H=96, C=7, N=400, sigma=0.5, lr=0.05, seed=15)
+    got, idx, _ = _run_gpu(c, rounds=1, mode="delayed")
+    _check(c, got, idx, *_oracle(c, 1))
 
 
 def test_named_softmax_workload(gpu_lib):
@@ -88,11 +108,13 @@ def test_named_softmax_workload(gpu_lib):
     _check(c, got, idx, *_oracle(c))
 
 
-def test_named_mlp_workload(gpu_lib):
+@pytest.mark.parametrize("mode", ["auto", "eager"])
+def test_named_mlp_workload(mode, gpu_lib):
     """MLP 3072 -> 512 -> 10, N = 50000, P=16 S=4 K1=4 K2=4 B=32, lr 0.05 (the
-    configuration the benchmark times), one full round."""
+    configuration the benchmark times; auto takes delayed updates), one full
+    round."""
     c = cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0)
-    got, idx, _ = _run_gpu(c)
+    got, idx, _ = _run_gpu(c, mode=mode)
     _check(c, got, idx, *_oracle(c))
 
 
@@ -181,12 +203,17 @@ def test_resume_from_params_continues_the_trajectory(gpu_lib):
         w1 = h.params()
     with HierAvg(config=cases.native_config(c)) as h2:
         h2.set_params(w1)
-        h2.round()
+        h2.round()  # rows set by the caller: eager first-layer updates
         got = h2.params()
+        h2.round()  # equal rows again: delayed updates
+        got2 = h2.params()
     st = M.create(prob)
     st.W = w1.astype(np.float64)
     M.hieravg_round(prob, st)
     ok, det = cases.parity_report(prob, got, st.W)
+    assert ok, det
+    M.hieravg_round(prob, st)
+    ok, det = cases.parity_report(prob, got2, st.W)
     assert ok, det
 
 
@@ -213,12 +240,38 @@ def test_torch_stream_and_profile(gpu_lib):
     assert all(ms >= 0.0 for _, ms in stats.values())
 
 
+def test_delayed_schedule_profile(gpu_lib):
+    """Delayed updates, P=6 S=3 K1=2 K2=3: per step the shared forward and the
+    two head kernels; per block one update of the cluster copies; the Gram
+    blocks once per round; eager round after set_params, delayed again after."""
+    from paper_1903_05133_amd import HierAvg
+    c = SMALL["mlp_ragged"]
+    ref, _, _ = _run_gpu(c, mode="delayed")
+    with HierAvg(config=cases.native_config(c, "delayed")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+        h.profile(False)
+        assert np.array_equal(h.params(), ref)
+        assert stats["fwd1_shared_gemm"][0] == 6 and stats["head_a"][0] == 6 and stats["head_b"][0] == 6
+        assert stats["block_update_gemm"][0] == 3 and stats["gram"][0] == 1
+        assert stats["tail_group_mean"][0] == 2 and stats["tail_global_mean"][0] == 1
+        assert stats["w1_global_mean"][0] == 1
+        assert not {"fwd1_gemm", "update1_gemm", "step1_gemm", "global_mean"} & set(stats)
+        h.set_params(h.params())
+        h.profile(True)
+        h.round()
+        assert "fwd1_gemm" in h.profile_read()
+        h.round()
+        assert "fwd1_shared_gemm" in h.profile_read()
+
+
 def test_unfused_schedule_profile(gpu_lib):
     """S = 3 has no fused-mean kernel: block ends run the plain update, the
     whole-replica cluster mean and the stand-alone forward of the next step."""
     from paper_1903_05133_amd import HierAvg
     c = SMALL["mlp_ragged"]  # P=6 S=3 K1=2 K2=3
-    with HierAvg(config=cases.native_config(c)) as h:
+    with HierAvg(config=cases.native_config(c, "eager")) as h:
         h.profile(True)
         h.round()
         stats = h.profile_read()
