@@ -50,9 +50,9 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
     G = P // S
     pairs = K1 * (K1 - 1) // 2
     return {
-        # forward of one step from the common W1: W1 once, the P minibatches,
-        # the P pre-activation blocks
-        "fwd1_shared_gemm": (f * (H * IN + P * B * IN + P * B * H), P * 2 * B * H * IN),
+        # forward of block 0's K1 steps from the common W1: W1 once, the
+        # K1*P minibatches, the K1*P pre-activation blocks
+        "fwd1_block_gemm": (f * (H * IN + K1 * P * B * IN + K1 * P * B * H), K1 * P * 2 * B * H * IN),
         # block end: the base read once, G cluster copies written, the block's
         # hidden errors and minibatch rows read
         "block_update_gemm": (f * (H * IN + G * H * IN + K1 * P * B * (H + IN)), K1 * P * 2 * B * H * IN),

@@ -42,7 +42,7 @@ const char* kClassNames[KC_COUNT] = {
     "draw_indices", "fwd1_gemm",    "reduce1",      "fwd2_gemm",   "softmax_grad", "bwd_hidden",
     "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
-    "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_shared_gemm", "block_update_gemm",
+    "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
     "w1_global_mean", "tail_global_mean", "gram_reduce"};
 
 struct ProfRec {
@@ -92,8 +92,7 @@ struct hieravg {
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
   bool w1_shared = true;   // every learner's W1 equals replica 0's (other rows may be stale)
   bool in_delayed = false; // the round being enqueued uses them
-  int SGf = 1;             // learners per row group of the shared forward (divides S)
-  int KS_d = 1, cps_d = 1; // splits of the shared forward
+  int KS_b = 1, cps_b = 1; // splits of the block-wide forward
   float* Wc = nullptr;     // [P/S][Hp*INp] cluster copies of W1
   float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
   float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
@@ -277,13 +276,9 @@ int build(hieravg* h) {
       h->delayed = c.update_mode == HIERAVG_UPDATE_DELAYED || (c.update_mode == HIERAVG_UPDATE_AUTO && cheap);
     }
     if (h->delayed) {
-      // Row groups of up to 128 rows that share one cluster copy.
-      h->SGf = 1;
-      for (int d = 1; d <= c.S; ++d)
-        if (c.S % d == 0 && d * h->Bp <= 128) h->SGf = d;
-      plan_split(P / h->SGf, h->SGf * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_d, &h->cps_d, HAV_FWD_SHARED_TARGET,
-                 HAV_FWD_SHARED_MB);
-      ks_max = std::max(ks_max, h->KS_d);
+      // One GEMM per cluster and block: the K1*S minibatches against the copy.
+      plan_split(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b, HAV_FWD_BLOCK_TARGET);
+      ks_max = std::max(ks_max, h->KS_b * c.K1);
     }
     h->ks_cur = h->KS1;
     const int64_t part_floats =
@@ -412,18 +407,19 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (!h->delayed || h->gram == nullptr || h->KSG < 2) return false;
       launch_gram_reduce(s, h->gram, P, c.K1, c.K2, Bp, h->KSG);
       return true;
-    case KC_FWD1_SHARED: {
+    case KC_FWD1_BLOCK: {
       if (!h->delayed) return false;
-      // Block b reads the round-start W1 (replica 0) for b = 0, else its
-      // cluster's copy.
+      // All K1 steps of block b at once: they read the block-start copy
+      // (the round-start W1 in replica 0 for b = 0, else the cluster's copy);
+      // partials go to part[ks][k][P][Bp][Hp].
       const int b = tt / c.K1;
-      FwdArgs f{h->X, ix, h->INp, b == 0 ? W + h->off_W1 : h->Wc, b == 0 ? 0 : h->Hp * h->INp, h->INp, h->part, P,
-                B, Bp, Hp, INp, h->KS_d, h->cps_d};
-      f.SG = h->SGf;
-      f.wdiv = S / h->SGf;
-      f.mb_max = HAV_FWD_SHARED_MB;
+      FwdArgs f{h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
+                b == 0 ? 0 : h->Hp * h->INp, h->INp, h->part, P, B, Bp, Hp, INp, h->KS_b, h->cps_b};
+      f.SG = c.K1 * S;
+      f.vS = S;
+      f.PT = c.K1 * P;
       launch_fwd(s, f, A_GATHER);
-      h->ks_cur = h->KS_d;
+      h->ks_cur = h->KS_b;
       return true;
     }
     case KC_BLOCK_UPDATE: {
@@ -455,8 +451,14 @@ bool launch_class(hieravg* h, int kc, int tt) {
         corr.K1 = c.K1;
         corr.lr = c.lr;
       }
-      launch_head_a(s, h->part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp,
-                    corr);
+      const float* part = h->part;
+      int64_t split = 0;
+      if (h->in_delayed) {  // the block-wide forward's layout
+        part += (int64_t)(tt % c.K1) * P * Bp * Hp;
+        split = (int64_t)c.K1 * P * Bp * Hp;
+      }
+      launch_head_a(s, part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp,
+                    corr, split);
       return true;
     }
     case KC_HEAD_B: {
@@ -649,11 +651,12 @@ void enqueue_round(hieravg* h) {
       }
     }
   } else if (h->in_delayed) {
-    // Delayed first-layer updates: per block, K1 steps of forward from the
-    // block-start copies (with the Gram corrections), head and hidden error,
-    // then one update of each cluster's copy; at the end the global mean of
-    // the copies goes to replica 0 (every learner's W1) and the other
-    // parameters take their global mean.
+    // Delayed first-layer updates: per block, the forward of its K1 steps
+    // from the block-start copies, then per step the head (with the Gram
+    // corrections of the earlier steps) and the hidden error, then one update
+    // of each cluster's copy; at the end the global mean of the copies goes
+    // to replica 0 (every learner's W1) and the other parameters take their
+    // global mean.
     auto go = [&](int kc, int tt) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
     go(KC_DRAW, 0);
     if (c.K1 > 1) {
@@ -661,9 +664,9 @@ void enqueue_round(hieravg* h) {
       if (h->KSG > 1) go(KC_GRAM_REDUCE, 0);
     }
     for (int b = 0; b < c.K2; ++b) {
+      go(KC_FWD1_BLOCK, b * c.K1);
       for (int k = 0; k < c.K1; ++k) {
         const int tt = b * c.K1 + k;
-        go(KC_FWD1_SHARED, tt);
         go(KC_HEAD_A, tt);
         go(KC_HEAD_B, tt);
       }

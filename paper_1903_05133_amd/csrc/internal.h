@@ -88,7 +88,7 @@ enum KernelClass {
   KC_STEP1_MEAN,     // same, with the local mean of layer 1 in between
   KC_TAIL_MEAN,      // local mean of the parameters after layer 1
   KC_GRAM,           // delayed updates: Gram blocks of the round's minibatches
-  KC_FWD1_SHARED,    // delayed updates: layer-1 forward from the cluster copies
+  KC_FWD1_BLOCK,     // delayed updates: layer-1 forward of a block's steps from the cluster copies
   KC_BLOCK_UPDATE,   // delayed updates: block-end update of the cluster copies
   KC_W1_MEAN,        // delayed updates: global mean of the cluster copies
   KC_TAIL_GLOBAL,    // global mean of the parameters after layer 1
@@ -142,17 +142,19 @@ struct FwdArgs {
   // and read weight copy g / wdiv (w_pitch 0: one copy for all).
   int SG = 1, wdiv = 1;
   int mb_max = 8;  // largest row tile, in 16-row blocks (1, 2, 4 or 8)
+  // vS > 0: the SG members of group g are (step k, learner g*vS + j) for
+  // v = k*vS + j, whose sample indices sit at idx + (k*P + g*vS + j)*M and
+  // whose outputs go to part[ks][k][P][Mp][N] (PT = steps * P members per
+  // split).  idx then points at the first step's indices.
+  int vS = 0, PT = 0;
 };
 enum ASource { A_GATHER = 0, A_RELU = 1 };
 void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src);
 // Split count for a forward over P row groups of Mp rows each.
 void plan_split(int P, int Mp, int N, int K, int* KS, int* cps, int target_wg = 0, int mb_max = 8);
-// Workgroup target and row tile of the forward from shared cluster copies.
-#ifndef HAV_FWD_SHARED_TARGET
-#define HAV_FWD_SHARED_TARGET 256
-#endif
-#ifndef HAV_FWD_SHARED_MB
-#define HAV_FWD_SHARED_MB 4
+// Workgroup target of the block-wide forward from the cluster copies.
+#ifndef HAV_FWD_BLOCK_TARGET
+#define HAV_FWD_BLOCK_TARGET 256
 #endif
 int fwd_tiles(int P, int Mp, int N);
 
@@ -236,8 +238,10 @@ struct HeadCorr {
   int k = 0, K1 = 1;
   float lr = 0.0f;
 };
+// part_split: floats between split-K partial sums (0: P * Mp * Hp).
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr());
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr(),
+                   int64_t part_split = 0);
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, float lr);

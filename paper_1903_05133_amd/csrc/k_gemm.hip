@@ -85,7 +85,8 @@ __global__ __launch_bounds__(256) void k_fwd_nt(FwdArgs a, int ntiles, int mtile
     const int m = mbase + r;
     const int jj = m / a.Mp, sm = m - jj * a.Mp;
     aok[i] = m < GM && sm < a.M;
-    const int64_t p = (int64_t)g * a.SG + (aok[i] ? jj : 0);
+    const int v = aok[i] ? jj : 0;
+    const int64_t p = a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
     const int sc = aok[i] ? sm : 0;
     int64_t row;
     if (ASRC == A_GATHER)
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(256) void k_fwd_nt(FwdArgs a, int ntiles, int mtile
     }
   }
 
-  float* part = a.part + ((int64_t)ks * a.P + (int64_t)g * a.SG) * a.Mp * a.N;
+  const int64_t PT = a.PT > 0 ? a.PT : a.P;
 #pragma unroll
   for (int m = 0; m < MB; ++m)
 #pragma unroll
@@ -179,7 +180,11 @@ __global__ __launch_bounds__(256) void k_fwd_nt(FwdArgs a, int ntiles, int mtile
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = mbase + 16 * m + 4 * lgrp + r;
-        if (row < GM) part[(int64_t)row * a.N + nw + 16 * j + lrow] = acc[m][j][r];
+        if (row >= GM) continue;
+        const int v = row / a.Mp, sm = row - v * a.Mp;
+        const int64_t p =
+            a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+        a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + nw + 16 * j + lrow] = acc[m][j][r];
       }
     }
 }
@@ -215,7 +220,8 @@ void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src) {
   const int MB = pick_mb(GM, a.mb_max);
   const int mtiles = (GM + MB * 16 - 1) / (MB * 16);
   const int ntiles = (a.N + 127) / 128;
-  const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * a.KS * mtiles * ntiles);
+  const int groups = a.vS > 0 ? a.P / a.vS : a.P / a.SG;
+  const unsigned grid = (unsigned)((int64_t)groups * a.KS * mtiles * ntiles);
 #define HAV_FWD(S_, MB_) launch(k_fwd_nt<S_, MB_>, grid, 256, 0, s, a, ntiles, mtiles)
 #define HAV_FWD_MB(S_)   \
   switch (MB) {          \
@@ -427,20 +433,34 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   const int xc4 = tid % kXP, xr0 = tid / kXP;
   const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
   const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
-  // Row r of the contraction: step k, learner g*SG + j, sample s.
+  // Row r of the contraction: step k, learner g*SG + j, sample s.  The
+  // quotients come from a float reciprocal (r < 2^24) and one correction step.
+  const float inv_sb = 1.0f / (float)SB, inv_b = 1.0f / (float)a.B;
+  auto qdiv = [](int n, int d, float inv) {
+    int q = (int)((float)n * inv);
+    q += (q + 1) * d <= n ? 1 : 0;
+    q -= q * d > n ? 1 : 0;
+    return q;
+  };
   auto gx_row = [&](int r, int64_t& grow, int64_t& irow) {
-    const int k = r / SB, rem = r - k * SB;
-    const int j = rem / a.B, sm = rem - j * a.B;
+    const int k = qdiv(r, SB, inv_sb), rem = r - k * SB;
+    const int j = qdiv(rem, a.B, inv_b), sm = rem - j * a.B;
     const int64_t kp = (int64_t)k * a.P + (int64_t)g * a.SG + j;
     grow = kp * a.Mp + sm;
     irow = kp * a.B + sm;
   };
-  f32x4 ga[2], xb[kXL];
-  bool gok[2], xok[kXL];
+  // Stage registers: two sets, so each stage's loads are issued two stages
+  // before its rows go to LDS (two blocks of MFMAs of latency hiding).
+  struct StageRegs {
+    f32x4 ga[2], xb[kXL];
+    bool gok[2], xok[kXL];
+  };
+  StageRegs RA, RB;
   // Sample indices are loaded one stage before the rows they select, so the
   // loads of a stage never wait for another load issued with them.
   int32_t xrow[kXL];
-  auto load_idx = [&](int s0) {
+  auto load_idx = [&](int st) {
+    const int s0 = (st < nst ? st : nst - 1) * kSC;
 #pragma unroll
     for (int i = 0; i < kXL; ++i) {
       const int r = s0 + xr0 + kXR * i;
@@ -449,33 +469,34 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
       xrow[i] = a.idx[irow];
     }
   };
-  auto load_stage = [&](int s0) {
+  auto load_stage = [&](int st, StageRegs& q) {
+    const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
 #pragma unroll
     for (int i = 0; i < 2; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
-      const int q = tid + 256 * i;
-      const int r = s0 + (q >> 4), m = mrow0 + 4 * (q & 15);
-      gok[i] = r < R && m < a.Mrows;
+      const int qq = tid + 256 * i;
+      const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
+      q.gok[i] = r < R && m < a.Mrows;
       int64_t grow, irow;
-      gx_row(gok[i] ? r : 0, grow, irow);
-      ga[i] = *(const f32x4*)(a.G + (gok[i] ? grow * a.ldg + m : 0));
+      gx_row(q.gok[i] ? r : 0, grow, irow);
+      q.ga[i] = *(const f32x4*)(a.G + (q.gok[i] ? grow * a.ldg + m : 0));
     }
 #pragma unroll
     for (int i = 0; i < kXL; ++i) {  // X rows of contraction rows s0 + xr0 + kXR*i
       const int r = s0 + xr0 + kXR * i;
-      xok[i] = r < R && xcol_ok;
-      xb[i] = *(const f32x4*)(a.X + (xok[i] ? (int64_t)xrow[i] * a.ldx + xcol : 0));
+      q.xok[i] = r < R && xcol_ok;
+      q.xb[i] = *(const f32x4*)(a.X + (q.xok[i] ? (int64_t)xrow[i] * a.ldx + xcol : 0));
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int buf, const StageRegs& q) {
     float* As = lds + buf * kStage;
     float* Bs = As + kSC * kLA;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int q = tid + 256 * i;
-      *(f32x4*)&As[(q >> 4) * kLA + 4 * (q & 15)] = gok[i] ? ga[i] : zero4;
+      const int qq = tid + 256 * i;
+      *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = q.gok[i] ? q.ga[i] : zero4;
     }
 #pragma unroll
-    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = xok[i] ? xb[i] : zero4;
+    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xok[i] ? q.xb[i] : zero4;
   };
 
   f32x16 acc[kMI][2];
@@ -485,10 +506,29 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  auto mfma_stage = [&](int buf) {
+    if (!wave_on) return;
+    const float* As = lds + buf * kStage;
+    const float* Bs = As + kSC * kLA;
+#pragma unroll 4
+    for (int ss = 0; ss < kSC; ss += 2) {
+      const int sr = ss + lhi;
+      const float b0 = Bs[sr * kLB + wn + l32];
+      const float b1 = Bs[sr * kLB + wn + 32 + l32];
+#pragma unroll
+      for (int i = 0; i < kMI; ++i) {
+        const float av = As[sr * kLA + wm + 32 * i + l32];
+        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b0, acc[i][0], 0, 0, 0);
+        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b1, acc[i][1], 0, 0, 0);
+      }
+    }
+  };
 
   load_idx(0);
-  load_stage(0);
-  load_idx(nst > 1 ? kSC : 0);
+  load_stage(0, RA);
+  load_idx(1);
+  load_stage(1, RB);
+  load_idx(2);
   __builtin_amdgcn_sched_barrier(0);
   // Base tile (16-byte pieces, thread t: column piece t%kXP of rows t/kXP + kXR*i).
   constexpr int kWL = kUM / kXR;
@@ -499,31 +539,24 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
     const int row = mrow0 + xr0 + kXR * i;
     wv[i] = *(const f32x4*)(Wb + (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
   }
-  store_stage(0);
+  store_stage(0, RA);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    // Prefetch the next stage (the last stage again at the end: in range,
-    // unused) and the indices of the one after.
-    load_stage((st + 1 < nst ? st + 1 : st) * kSC);
-    load_idx((st + 2 < nst ? st + 2 : nst - 1) * kSC);
+  // Iteration st: loads of stage st+2 and indices of stage st+3 go out, the
+  // MFMAs of stage st (LDS buffer st&1) run, stage st+1 goes to the other
+  // buffer.  Unrolled by two so each register set is named statically.
+  for (int st = 0; st < nst; st += 2) {
+    load_stage(st + 2, RA);
+    load_idx(st + 3);
     __builtin_amdgcn_sched_barrier(0);
-    if (wave_on) {
-      const float* As = lds + (st & 1) * kStage;
-      const float* Bs = As + kSC * kLA;
-#pragma unroll 4
-      for (int ss = 0; ss < kSC; ss += 2) {
-        const int sr = ss + lhi;
-        const float b0 = Bs[sr * kLB + wn + l32];
-        const float b1 = Bs[sr * kLB + wn + 32 + l32];
-#pragma unroll
-        for (int i = 0; i < kMI; ++i) {
-          const float av = As[sr * kLA + wm + 32 * i + l32];
-          acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b0, acc[i][0], 0, 0, 0);
-          acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b1, acc[i][1], 0, 0, 0);
-        }
-      }
-    }
-    store_stage((st + 1) & 1);
+    mfma_stage(0);
+    store_stage(1, RB);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    load_stage(st + 3, RB);
+    load_idx(st + 4);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(1);
+    store_stage(0, RA);
     __syncthreads();
   }
 

@@ -153,7 +153,8 @@ template <int KC>
 __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, int KS, const float* __restrict__ b1,
                                                 const float* __restrict__ W2, int64_t w_pitch,
                                                 float* __restrict__ Z1, float* __restrict__ PL, int P, int M, int Mp,
-                                                int C, int Cp, int Hp, int htiles, HeadCorr corr) {
+                                                int C, int Cp, int Hp, int htiles, HeadCorr corr,
+                                                int64_t split) {
   __shared__ float zs[kHM][kHU + 1];
   __shared__ float ws[KC][kHU + 1];
   __shared__ __attribute__((aligned(16))) float gsl[kCorrMaxK][kHM][kHU];
@@ -170,7 +171,6 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
     ws[c][hh] = c < C ? v : 0.0f;
   }
   const f32x4 bias = *(const f32x4*)(b1 + (int64_t)p * w_pitch + h4);
-  const int64_t split = (int64_t)P * Mp * Hp;
   const float* p0 = part + (int64_t)p * Mp * Hp + h4;
   const int kc = corr.gram != nullptr ? corr.k : 0;
   if (kc > 0) {
@@ -350,14 +350,16 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr) {
+                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr,
+                   int64_t part_split) {
   const int htiles = Hp / kHU;
+  const int64_t split = part_split > 0 ? part_split : (int64_t)P * Mp * Hp;
   if (C <= 16)
     launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
-           corr);
+           corr, split);
   else
     launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
-           corr);
+           corr, split);
 }
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,

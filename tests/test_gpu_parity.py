@@ -241,9 +241,10 @@ def test_torch_stream_and_profile(gpu_lib):
 
 
 def test_delayed_schedule_profile(gpu_lib):
-    """Delayed updates, P=6 S=3 K1=2 K2=3: per step the shared forward and the
-    two head kernels; per block one update of the cluster copies; the Gram
-    blocks once per round; eager round after set_params, delayed again after."""
+    """Delayed updates, P=6 S=3 K1=2 K2=3: per block one forward of its steps
+    and one update of the cluster copies, per step the two head kernels; the
+    Gram blocks once per round; eager round after set_params, delayed again
+    after."""
     from paper_1903_05133_amd import HierAvg
     c = SMALL["mlp_ragged"]
     ref, _, _ = _run_gpu(c, mode="delayed")
@@ -253,7 +254,7 @@ def test_delayed_schedule_profile(gpu_lib):
         stats = h.profile_read()
         h.profile(False)
         assert np.array_equal(h.params(), ref)
-        assert stats["fwd1_shared_gemm"][0] == 6 and stats["head_a"][0] == 6 and stats["head_b"][0] == 6
+        assert stats["fwd1_block_gemm"][0] == 3 and stats["head_a"][0] == 6 and stats["head_b"][0] == 6
         assert stats["block_update_gemm"][0] == 3 and stats["gram"][0] == 1
         assert stats["tail_group_mean"][0] == 2 and stats["tail_global_mean"][0] == 1
         assert stats["w1_global_mean"][0] == 1
@@ -263,7 +264,7 @@ def test_delayed_schedule_profile(gpu_lib):
         h.round()
         assert "fwd1_gemm" in h.profile_read()
         h.round()
-        assert "fwd1_shared_gemm" in h.profile_read()
+        assert "fwd1_block_gemm" in h.profile_read()
 
 
 def test_unfused_schedule_profile(gpu_lib):
