@@ -277,7 +277,8 @@ int build(hieravg* h) {
     }
     if (h->delayed) {
       // One GEMM per cluster and block: the K1*S minibatches against the copy.
-      plan_split(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b, HAV_FWD_BLOCK_TARGET);
+      plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
+                     HAV_FWD_BLOCK_TARGET);
       ks_max = std::max(ks_max, h->KS_b * c.K1);
     }
     h->ks_cur = h->KS1;
@@ -418,7 +419,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       f.SG = c.K1 * S;
       f.vS = S;
       f.PT = c.K1 * P;
-      launch_fwd(s, f, A_GATHER);
+      launch_fwd_blk(s, f);
       h->ks_cur = h->KS_b;
       return true;
     }

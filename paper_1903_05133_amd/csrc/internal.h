@@ -152,6 +152,10 @@ enum ASource { A_GATHER = 0, A_RELU = 1 };
 void launch_fwd(hipStream_t s, const FwdArgs& a, ASource src);
 // Split count for a forward over P row groups of Mp rows each.
 void plan_split(int P, int Mp, int N, int K, int* KS, int* cps, int target_wg = 0, int mb_max = 8);
+// Large-tile forward (128 x 128 tiles, 1024 threads) for many rows per weight
+// copy, and its split count.
+void launch_fwd_blk(hipStream_t s, const FwdArgs& a);
+void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg);
 // Workgroup target of the block-wide forward from the cluster copies.
 #ifndef HAV_FWD_BLOCK_TARGET
 #define HAV_FWD_BLOCK_TARGET 256

@@ -189,6 +189,141 @@ __global__ __launch_bounds__(256) void k_fwd_nt(FwdArgs a, int ntiles, int mtile
     }
 }
 
+// Large-tile variant for the block-wide forward of delayed updates (many rows
+// per weight copy): 1024 threads, output tile 128 rows x 128 columns, both
+// operands staged through LDS (double-buffered, one barrier per 64-wide K
+// chunk, the next chunk's loads in flight during the current chunk's MFMAs).
+// Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4)) as 2 x 2
+// 16x16x4 MFMA blocks, so each SIMD interleaves four waves.
+constexpr int kBT = 128;  // tile rows and columns
+__global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mtiles) {
+  __shared__ __attribute__((aligned(16))) float As[2][kBT * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float Ws[2][kBT * kLdsStride];
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int nt = bid % ntiles;
+  const int mt = (bid / ntiles) % mtiles;
+  const int ks = (bid / (ntiles * mtiles)) % a.KS;
+  const int g = bid / (ntiles * mtiles * a.KS);
+  const int GM = a.SG * a.Mp;
+  const int nch = a.K / kKC;
+  const int c0 = ks * a.cps;
+  const int c1 = min(nch, c0 + a.cps);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int wm = (wave >> 2) * 32, wn = (wave & 3) * 32;
+  const int mbase = mt * kBT, nbase = nt * kBT;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+
+  // Thread t stages pieces t and t + 1024 of each 128 x 64 chunk: row q/16,
+  // 16-byte column piece q%16.
+  const float* arow[2];
+  const float* wrow[2];
+  bool aok[2], wok[2];
+  int off[2];
+  const float* wp = a.W + (int64_t)(g / a.wdiv) * a.w_pitch;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = tid + 1024 * i;
+    const int r = q >> 4, c4 = q & 15;
+    off[i] = r * kLdsStride + 4 * c4;
+    const int m = mbase + r;
+    const int jj = m / a.Mp, sm = m - jj * a.Mp;
+    aok[i] = m < GM && sm < a.M;
+    const int v = aok[i] ? jj : 0;
+    const int64_t p = a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+    arow[i] = a.A + (int64_t)a.idx[p * a.M + (aok[i] ? sm : 0)] * a.lda + 4 * c4;
+    const int n = nbase + r;
+    wok[i] = n < a.N;
+    wrow[i] = wp + (int64_t)(wok[i] ? n : 0) * a.ldw + 4 * c4;
+  }
+  f32x4 av[2], wv[2];
+  auto load = [&](int c) {
+    const int64_t o = (int64_t)c * kKC;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      av[i] = *(const f32x4*)(arow[i] + o);
+      wv[i] = *(const f32x4*)(wrow[i] + o);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *(f32x4*)&As[buf][off[i]] = aok[i] ? av[i] : zero4;
+      *(f32x4*)&Ws[buf][off[i]] = wok[i] ? wv[i] : zero4;
+    }
+  };
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = zero4;
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < kKC / 16; ++q) {
+      f32x4 x[2], y[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        x[i] = *(const f32x4*)&As[buf][(wm + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
+        y[i] = *(const f32x4*)&Ws[buf][(wn + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[i][e], y[j][e], acc[i][j], 0, 0, 0);
+    }
+  };
+  if (c0 < c1) {
+    load(c0);
+    store(0);
+    __syncthreads();
+    for (int c = c0; c < c1; ++c) {
+      load(c + 1 < c1 ? c + 1 : c);  // the last chunk again at the end: in range, unused
+      __builtin_amdgcn_sched_barrier(0);
+      compute((c - c0) & 1);
+      store((c - c0 + 1) & 1);
+      __syncthreads();
+    }
+  }
+  const int64_t PT = a.PT > 0 ? a.PT : a.P;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = nbase + wn + 16 * j + lrow;
+      if (col >= a.N) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = mbase + wm + 16 * i + 4 * lgrp + r;
+        if (row >= GM) continue;
+        const int v = row / a.Mp, sm = row - v * a.Mp;
+        const int64_t p =
+            a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+        a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col] = acc[i][j][r];
+      }
+    }
+}
+
+void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
+  const int GM = a.SG * a.Mp;
+  const int mtiles = (GM + kBT - 1) / kBT;
+  const int ntiles = (a.N + kBT - 1) / kBT;
+  const int groups = a.vS > 0 ? a.P / a.vS : a.P / a.SG;
+  const unsigned grid = (unsigned)((int64_t)groups * a.KS * mtiles * ntiles);
+  launch(k_fwd_blk, grid, 1024, 0, s, a, ntiles, mtiles);
+}
+
+// Split count of k_fwd_blk: about target_wg workgroups, no empty split.
+void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg) {
+  const int64_t tiles = (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
+  const int nch = K / kKC;
+  int ks = (int)std::max<int64_t>(1, (target_wg + tiles - 1) / tiles);
+  ks = std::min(ks, nch);
+  const int c = (nch + ks - 1) / ks;
+  *KS = (nch + c - 1) / c;
+  *cps = c;
+}
+
 static int pick_mb(int Mp, int mb_max = 8) {
   const int mb = Mp >= 128 ? 8 : Mp >= 64 ? 4 : Mp >= 32 ? 2 : 1;
   return mb < mb_max ? mb : mb_max;
@@ -407,9 +542,16 @@ __global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int nt
 // ------------------------------------------------------------ delayed update
 // Tile of k_update_tn (64 rows x kUN columns of one group's W1), contracted
 // over the K1*SG*B rows (step k, learner j, sample s) of the group in stages
-// of 32 rows through two LDS buffers: the next stage's loads are in flight
-// while the current stage's MFMAs run, and each stage costs one barrier.
-__global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int ntiles) {
+// of 32 rows through two LDS buffers: each stage's loads are issued two
+// stages ahead (two register sets) and each stage costs one barrier.  NTH/64
+// waves split the tile into 32-row x (2*kUN/NW)-column blocks of 32x32x2
+// MFMAs.
+template <int NTH>
+__global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int ntiles) {
+  constexpr int NW = NTH / 64;            // waves
+  constexpr int kWCn = NW / 2;            // waves across the columns (two 32-row blocks)
+  constexpr int kWN = kUN / kWCn;         // columns per wave
+  constexpr int kNA = kWN / 32;           // 32x32 accumulators per wave
   constexpr int kStage = kSC * (kLA + kLB);
   constexpr int kLds = 2 * kStage > kUM * kLB ? 2 * kStage : kUM * kLB;
   __shared__ __attribute__((aligned(16))) float lds[kLds];
@@ -422,14 +564,15 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l32 = lane & 31, lhi = lane >> 5;
   const int mrow0 = mt * kUM, ncol0 = nt * kUN;
-  const int wn = (wave % kWC) * 64, wm = (wave / kWC) * kMI * 32;
+  const int wn = (wave % kWCn) * kWN, wm = (wave / kWCn) * 32;
   const bool wave_on = ncol0 + wn < a.Ncols;
   const int SB = a.SG * a.B;
   const int R = a.K1 * SB;  // contraction rows
   const int nst = (R + kSC - 1) / kSC;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
-  constexpr int kXP = kUN / 4, kXR = 256 / kXP, kXL = kSC / kXR;
+  constexpr int kXP = kUN / 4, kXR = NTH / kXP, kXL = kSC / kXR;
+  constexpr int kGL = kSC * (kUM / 4) / NTH;  // G pieces per thread per stage
   const int xc4 = tid % kXP, xr0 = tid / kXP;
   const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
   const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
@@ -452,8 +595,8 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   // Stage registers: two sets, so each stage's loads are issued two stages
   // before its rows go to LDS (two blocks of MFMAs of latency hiding).
   struct StageRegs {
-    f32x4 ga[2], xb[kXL];
-    bool gok[2], xok[kXL];
+    f32x4 ga[kGL], xb[kXL];
+    bool gok[kGL], xok[kXL];
   };
   StageRegs RA, RB;
   // Sample indices are loaded one stage before the rows they select, so the
@@ -472,8 +615,8 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   auto load_stage = [&](int st, StageRegs& q) {
     const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
-      const int qq = tid + 256 * i;
+    for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
+      const int qq = tid + NTH * i;
       const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
       q.gok[i] = r < R && m < a.Mrows;
       int64_t grow, irow;
@@ -491,21 +634,19 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
     float* As = lds + buf * kStage;
     float* Bs = As + kSC * kLA;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int qq = tid + 256 * i;
+    for (int i = 0; i < kGL; ++i) {
+      const int qq = tid + NTH * i;
       *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = q.gok[i] ? q.ga[i] : zero4;
     }
 #pragma unroll
     for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xok[i] ? q.xb[i] : zero4;
   };
 
-  f32x16 acc[kMI][2];
+  f32x16 acc[kNA];
 #pragma unroll
-  for (int i = 0; i < kMI; ++i)
+  for (int j = 0; j < kNA; ++j)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
   auto mfma_stage = [&](int buf) {
     if (!wave_on) return;
     const float* As = lds + buf * kStage;
@@ -513,14 +654,10 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
 #pragma unroll 4
     for (int ss = 0; ss < kSC; ss += 2) {
       const int sr = ss + lhi;
-      const float b0 = Bs[sr * kLB + wn + l32];
-      const float b1 = Bs[sr * kLB + wn + 32 + l32];
+      const float av = As[sr * kLA + wm + l32];
 #pragma unroll
-      for (int i = 0; i < kMI; ++i) {
-        const float av = As[sr * kLA + wm + 32 * i + l32];
-        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b0, acc[i][0], 0, 0, 0);
-        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b1, acc[i][1], 0, 0, 0);
-      }
+      for (int j = 0; j < kNA; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kLB + wn + 32 * j + l32], acc[j], 0, 0, 0);
     }
   };
 
@@ -561,14 +698,12 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   }
 
 #pragma unroll
-  for (int i = 0; i < kMI; ++i)
+  for (int j = 0; j < kNA; ++j)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lhi + (r & 3);
-        Gt[row * kLB + wn + 32 * j + l32] = acc[i][j][r];
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      Gt[row * kLB + wn + 32 * j + l32] = acc[j][r];
+    }
   __syncthreads();
   float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
 #pragma unroll
@@ -581,11 +716,14 @@ __global__ __launch_bounds__(256) void k_block_update(BlkArgs a, int mtiles, int
   }
 }
 
+#ifndef HAV_BLK_THREADS
+#define HAV_BLK_THREADS 512
+#endif
 void launch_block_update(hipStream_t s, const BlkArgs& a) {
   const int mtiles = (a.Mrows + kUM - 1) / kUM;
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
-  launch(k_block_update, grid, 256, 0, s, a, mtiles, ntiles);
+  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, 0, s, a, mtiles, ntiles);
 }
 
 // ------------------------------------------------------------ Gram blocks
