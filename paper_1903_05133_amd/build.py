@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhieravg.so")
-SOURCES = ["hieravg.hip", "k_data.hip", "k_gemm.hip", "k_head.hip", "k_avg.hip"]
+SOURCES = ["hieravg.hip", "k_data.hip", "k_gemm.hip", "k_delayed.hip", "k_head.hip", "k_avg.hip"]
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 arithmetic.
 HIPCC_FLAGS = [

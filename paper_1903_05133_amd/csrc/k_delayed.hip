@@ -1,0 +1,510 @@
+// Kernels of the delayed first-layer update (include/hieravg.h,
+// HIERAVG_UPDATE_DELAYED): within a block of K1 local steps (Algorithm 1,
+// Sec. 3.1) every learner of a cluster starts from the same first weight
+// block Wb, and after k steps its block is Wb - lr * sum_{k'<k} G_k'^T X_k'.
+//
+// k_fwd_blk:      the first-layer forward partials of all K1 steps of a block
+//                 from the cluster copies (one GEMM per cluster and block).
+// k_gram:         the Gram blocks X_k X_k'^T (k' < k) of each learner's
+//                 minibatches in each block, which turn the forward from Wb
+//                 into the forward from the learner's current block.
+// k_block_update: the block-end cluster mean of the first weight block, as one
+//                 update of the copy by the summed G^T X of the cluster.
+#include <algorithm>
+
+#include "internal.h"
+
+namespace hav {
+
+constexpr int kKC = 64;         // K floats per LDS chunk
+constexpr int kLdsStride = 68;  // LDS row stride in floats (64 + 4: conflict-free 128-bit reads)
+constexpr int kUM = 64;         // W rows per block-update workgroup
+constexpr int kUN = 128;        // W columns per block-update workgroup
+constexpr int kSC = 32;         // contraction rows per LDS stage
+constexpr int kLA = kUM + 4;    // LDS row length of the error stage
+constexpr int kLB = kUN + 4;    // LDS row length of the input stage and of the gradient tile
+
+// Large-tile variant for the block-wide forward of delayed updates (many rows
+// per weight copy): 1024 threads, output tile 128 rows x 128 columns, both
+// operands staged through LDS (double-buffered, one barrier per 64-wide K
+// chunk, the next chunk's loads in flight during the current chunk's MFMAs).
+// Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4)) as 2 x 2
+// 16x16x4 MFMA blocks, so each SIMD interleaves four waves.
+constexpr int kBT = 128;  // tile rows and columns
+__global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mtiles) {
+  __shared__ __attribute__((aligned(16))) float As[2][kBT * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float Ws[2][kBT * kLdsStride];
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int nt = bid % ntiles;
+  const int mt = (bid / ntiles) % mtiles;
+  const int ks = (bid / (ntiles * mtiles)) % a.KS;
+  const int g = bid / (ntiles * mtiles * a.KS);
+  const int GM = a.SG * a.Mp;
+  const int nch = a.K / kKC;
+  const int c0 = ks * a.cps;
+  const int c1 = min(nch, c0 + a.cps);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int wm = (wave >> 2) * 32, wn = (wave & 3) * 32;
+  const int mbase = mt * kBT, nbase = nt * kBT;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+
+  // Thread t stages pieces t and t + 1024 of each 128 x 64 chunk: row q/16,
+  // 16-byte column piece q%16.
+  const float* arow[2];
+  const float* wrow[2];
+  bool aok[2], wok[2];
+  int off[2];
+  const float* wp = a.W + (int64_t)(g / a.wdiv) * a.w_pitch;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = tid + 1024 * i;
+    const int r = q >> 4, c4 = q & 15;
+    off[i] = r * kLdsStride + 4 * c4;
+    const int m = mbase + r;
+    const int jj = m / a.Mp, sm = m - jj * a.Mp;
+    aok[i] = m < GM && sm < a.M;
+    const int v = aok[i] ? jj : 0;
+    const int64_t p = a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+    arow[i] = a.A + (int64_t)a.idx[p * a.M + (aok[i] ? sm : 0)] * a.lda + 4 * c4;
+    const int n = nbase + r;
+    wok[i] = n < a.N;
+    wrow[i] = wp + (int64_t)(wok[i] ? n : 0) * a.ldw + 4 * c4;
+  }
+  f32x4 av[2], wv[2];
+  auto load = [&](int c) {
+    const int64_t o = (int64_t)c * kKC;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      av[i] = *(const f32x4*)(arow[i] + o);
+      wv[i] = *(const f32x4*)(wrow[i] + o);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *(f32x4*)&As[buf][off[i]] = aok[i] ? av[i] : zero4;
+      *(f32x4*)&Ws[buf][off[i]] = wok[i] ? wv[i] : zero4;
+    }
+  };
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = zero4;
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < kKC / 16; ++q) {
+      f32x4 x[2], y[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        x[i] = *(const f32x4*)&As[buf][(wm + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
+        y[i] = *(const f32x4*)&Ws[buf][(wn + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[i][e], y[j][e], acc[i][j], 0, 0, 0);
+    }
+  };
+  if (c0 < c1) {
+    load(c0);
+    store(0);
+    __syncthreads();
+    for (int c = c0; c < c1; ++c) {
+      load(c + 1 < c1 ? c + 1 : c);  // the last chunk again at the end: in range, unused
+      __builtin_amdgcn_sched_barrier(0);
+      compute((c - c0) & 1);
+      store((c - c0 + 1) & 1);
+      __syncthreads();
+    }
+  }
+  const int64_t PT = a.PT > 0 ? a.PT : a.P;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = nbase + wn + 16 * j + lrow;
+      if (col >= a.N) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = mbase + wm + 16 * i + 4 * lgrp + r;
+        if (row >= GM) continue;
+        const int v = row / a.Mp, sm = row - v * a.Mp;
+        const int64_t p =
+            a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+        a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col] = acc[i][j][r];
+      }
+    }
+}
+
+void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
+  const int GM = a.SG * a.Mp;
+  const int mtiles = (GM + kBT - 1) / kBT;
+  const int ntiles = (a.N + kBT - 1) / kBT;
+  const int groups = a.vS > 0 ? a.P / a.vS : a.P / a.SG;
+  const unsigned grid = (unsigned)((int64_t)groups * a.KS * mtiles * ntiles);
+  launch(k_fwd_blk, grid, 1024, 0, s, a, ntiles, mtiles);
+}
+
+// Split count of k_fwd_blk: about target_wg workgroups, no empty split.
+void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg) {
+  const int64_t tiles = (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
+  const int nch = K / kKC;
+  int ks = (int)std::max<int64_t>(1, (target_wg + tiles - 1) / tiles);
+  ks = std::min(ks, nch);
+  const int c = (nch + ks - 1) / ks;
+  *KS = (nch + c - 1) / c;
+  *cps = c;
+}
+
+// ------------------------------------------------------------ delayed update
+// Tile of k_update_tn (64 rows x kUN columns of one group's W1), contracted
+// over the K1*SG*B rows (step k, learner j, sample s) of the group in stages
+// of 32 rows through two LDS buffers: each stage's loads are issued two
+// stages ahead (two register sets) and each stage costs one barrier.  NTH/64
+// waves split the tile into 32-row x (2*kUN/NW)-column blocks of 32x32x2
+// MFMAs.
+template <int NTH>
+__global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int ntiles) {
+  constexpr int NW = NTH / 64;            // waves
+  constexpr int kWCn = NW / 2;            // waves across the columns (two 32-row blocks)
+  constexpr int kWN = kUN / kWCn;         // columns per wave
+  constexpr int kNA = kWN / 32;           // 32x32 accumulators per wave
+  constexpr int kStage = kSC * (kLA + kLB);
+  constexpr int kLds = 2 * kStage > kUM * kLB ? 2 * kStage : kUM * kLB;
+  __shared__ __attribute__((aligned(16))) float lds[kLds];
+  float* Gt = lds;  // [kUM][kLB] gradient tile (after the stages)
+  // Tiles that share minibatch rows (same group and columns) are neighbours.
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = bid % mtiles;
+  const int nt = (bid / mtiles) % ntiles;
+  const int g = bid / (ntiles * mtiles);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int mrow0 = mt * kUM, ncol0 = nt * kUN;
+  const int wn = (wave % kWCn) * kWN, wm = (wave / kWCn) * 32;
+  const bool wave_on = ncol0 + wn < a.Ncols;
+  const int SB = a.SG * a.B;
+  const int R = a.K1 * SB;  // contraction rows
+  const int nst = (R + kSC - 1) / kSC;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+
+  constexpr int kXP = kUN / 4, kXR = NTH / kXP, kXL = kSC / kXR;
+  constexpr int kGL = kSC * (kUM / 4) / NTH;  // G pieces per thread per stage
+  const int xc4 = tid % kXP, xr0 = tid / kXP;
+  const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
+  const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
+  // Row r of the contraction: step k, learner g*SG + j, sample s.  The
+  // quotients come from a float reciprocal (r < 2^24) and one correction step.
+  const float inv_sb = 1.0f / (float)SB, inv_b = 1.0f / (float)a.B;
+  auto qdiv = [](int n, int d, float inv) {
+    int q = (int)((float)n * inv);
+    q += (q + 1) * d <= n ? 1 : 0;
+    q -= q * d > n ? 1 : 0;
+    return q;
+  };
+  auto gx_row = [&](int r, int64_t& grow, int64_t& irow) {
+    const int k = qdiv(r, SB, inv_sb), rem = r - k * SB;
+    const int j = qdiv(rem, a.B, inv_b), sm = rem - j * a.B;
+    const int64_t kp = (int64_t)k * a.P + (int64_t)g * a.SG + j;
+    grow = kp * a.Mp + sm;
+    irow = kp * a.B + sm;
+  };
+  // Stage registers: two sets, so each stage's loads are issued two stages
+  // before its rows go to LDS (two blocks of MFMAs of latency hiding).
+  struct StageRegs {
+    f32x4 ga[kGL], xb[kXL];
+    bool gok[kGL], xok[kXL];
+  };
+  StageRegs RA, RB;
+  // Sample indices are loaded one stage before the rows they select, so the
+  // loads of a stage never wait for another load issued with them.
+  int32_t xrow[kXL];
+  auto load_idx = [&](int st) {
+    const int s0 = (st < nst ? st : nst - 1) * kSC;
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {
+      const int r = s0 + xr0 + kXR * i;
+      int64_t grow, irow;
+      gx_row(r < R ? r : 0, grow, irow);
+      xrow[i] = a.idx[irow];
+    }
+  };
+  auto load_stage = [&](int st, StageRegs& q) {
+    const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
+#pragma unroll
+    for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
+      const int qq = tid + NTH * i;
+      const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
+      q.gok[i] = r < R && m < a.Mrows;
+      int64_t grow, irow;
+      gx_row(q.gok[i] ? r : 0, grow, irow);
+      q.ga[i] = *(const f32x4*)(a.G + (q.gok[i] ? grow * a.ldg + m : 0));
+    }
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {  // X rows of contraction rows s0 + xr0 + kXR*i
+      const int r = s0 + xr0 + kXR * i;
+      q.xok[i] = r < R && xcol_ok;
+      q.xb[i] = *(const f32x4*)(a.X + (q.xok[i] ? (int64_t)xrow[i] * a.ldx + xcol : 0));
+    }
+  };
+  auto store_stage = [&](int buf, const StageRegs& q) {
+    float* As = lds + buf * kStage;
+    float* Bs = As + kSC * kLA;
+#pragma unroll
+    for (int i = 0; i < kGL; ++i) {
+      const int qq = tid + NTH * i;
+      *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = q.gok[i] ? q.ga[i] : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xok[i] ? q.xb[i] : zero4;
+  };
+
+  f32x16 acc[kNA];
+#pragma unroll
+  for (int j = 0; j < kNA; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
+  auto mfma_stage = [&](int buf) {
+    if (!wave_on) return;
+    const float* As = lds + buf * kStage;
+    const float* Bs = As + kSC * kLA;
+#pragma unroll 4
+    for (int ss = 0; ss < kSC; ss += 2) {
+      const int sr = ss + lhi;
+      const float av = As[sr * kLA + wm + l32];
+#pragma unroll
+      for (int j = 0; j < kNA; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kLB + wn + 32 * j + l32], acc[j], 0, 0, 0);
+    }
+  };
+
+  load_idx(0);
+  load_stage(0, RA);
+  load_idx(1);
+  load_stage(1, RB);
+  load_idx(2);
+  __builtin_amdgcn_sched_barrier(0);
+  // Base tile (16-byte pieces, thread t: column piece t%kXP of rows t/kXP + kXR*i).
+  constexpr int kWL = kUM / kXR;
+  const float* Wb = a.Wb + (int64_t)g * a.wb_pitch;
+  f32x4 wv[kWL];
+#pragma unroll
+  for (int i = 0; i < kWL; ++i) {
+    const int row = mrow0 + xr0 + kXR * i;
+    wv[i] = *(const f32x4*)(Wb + (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
+  }
+  store_stage(0, RA);
+  __syncthreads();
+  // Iteration st: loads of stage st+2 and indices of stage st+3 go out, the
+  // MFMAs of stage st (LDS buffer st&1) run, stage st+1 goes to the other
+  // buffer.  Unrolled by two so each register set is named statically.
+  for (int st = 0; st < nst; st += 2) {
+    load_stage(st + 2, RA);
+    load_idx(st + 3);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(0);
+    store_stage(1, RB);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    load_stage(st + 3, RB);
+    load_idx(st + 4);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(1);
+    store_stage(0, RA);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int j = 0; j < kNA; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      Gt[row * kLB + wn + 32 * j + l32] = acc[j][r];
+    }
+  __syncthreads();
+  float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
+#pragma unroll
+  for (int i = 0; i < kWL; ++i) {
+    const int rl = xr0 + kXR * i, row = mrow0 + rl;
+    if (xcol_ok && row < a.Mrows) {
+      const f32x4 gsum = *(const f32x4*)&Gt[rl * kLB + 4 * xc4];
+      *(f32x4*)(Wo + (int64_t)row * a.ldw + xcol) = wv[i] - a.lr_eff * gsum;
+    }
+  }
+}
+
+#ifndef HAV_BLK_THREADS
+#define HAV_BLK_THREADS 512
+#endif
+void launch_block_update(hipStream_t s, const BlkArgs& a) {
+  const int mtiles = (a.Mrows + kUM - 1) / kUM;
+  const int ntiles = (a.Ncols + kUN - 1) / kUN;
+  const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
+  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, 0, s, a, mtiles, ntiles);
+}
+
+// ------------------------------------------------------------ Gram blocks
+// One workgroup per (learner p, block b, K split ks): all step pairs k2 < k of
+// the block at once.  The K1*Bp minibatch rows of the block (gathered, this
+// split's input features) are staged through LDS 64 features at a time, the
+// next chunk's loads in flight during the current chunk's MFMAs; each wave
+// owns a fixed set of the 16x16 output blocks of the lower block triangle
+// (16x16x4 MFMAs, the k permutation of k_fwd_nt).  Every minibatch row is
+// read once per split; the consumer adds the KSG partial sums.
+constexpr int kGramMaxBlocks = 28;  // 16x16 output blocks per wave (K1 <= 8, Bp <= 32)
+template <int NB, int ROWS>
+__global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t ldx, int K,
+                                              const int32_t* __restrict__ idx, float* __restrict__ gram, int P,
+                                              int K1, int B, int Bp, int KSG) {
+  constexpr int kRows = ROWS;         // LDS capacity in rows (K1 * Bp <= ROWS)
+  constexpr int kL = kKC + 4;         // LDS row length
+  constexpr int kLPT = kRows * (kKC / 4) / 256;  // 16-byte pieces per thread per chunk (at most)
+  __shared__ __attribute__((aligned(16))) float xs[kRows * kL];
+  const int ks = blockIdx.x % KSG;
+  const int pb = blockIdx.x / KSG;  // p + P * b
+  const int p = pb % P, b = pb / P;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int rows = K1 * Bp;
+  const int nch = K / kKC;
+  const int c0 = (int)((int64_t)nch * ks / KSG), c1 = (int)((int64_t)nch * (ks + 1) / KSG);
+  // Row r = k*Bp + s of the block: sample s of step b*K1 + k (rows past B: zero).
+  const float* src[kLPT];
+  bool ok[kLPT];
+  int off[kLPT];
+#pragma unroll
+  for (int i = 0; i < kLPT; ++i) {
+    const int q = tid + 256 * i;
+    const int r = q >> 4, c4 = q & 15;
+    const int k = r / Bp, sm = r - k * Bp;
+    ok[i] = r < rows && sm < B;
+    const int64_t e = ((int64_t)(b * K1 + (ok[i] ? k : 0)) * P + p) * B + (ok[i] ? sm : 0);
+    src[i] = X + (int64_t)idx[e] * ldx + 4 * c4;
+    off[i] = (r < kRows ? r : 0) * kL + 4 * c4;
+  }
+  // Output blocks of this wave: block e = wave + 4*t over the lower triangle
+  // (pair (k, k2), row block mb, column block nb).
+  const int mbs = Bp / 16;
+  const int nblk = K1 * (K1 - 1) / 2 * mbs * mbs;
+  int arow[NB], brow[NB];
+  bool bon[NB];
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    const int e = wave + 4 * t;
+    bon[t] = e < nblk;
+    int pr = (bon[t] ? e : 0) / (mbs * mbs), rem = (bon[t] ? e : 0) % (mbs * mbs);
+    int k = 1, k2 = pr;
+    while (k2 >= k) {
+      k2 -= k;
+      ++k;
+    }
+    arow[t] = (k * Bp + 16 * (rem / mbs) + lrow) * kL + 4 * lgrp;
+    brow[t] = (k2 * Bp + 16 * (rem % mbs) + lrow) * kL + 4 * lgrp;
+  }
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 acc[NB];
+#pragma unroll
+  for (int t = 0; t < NB; ++t) acc[t] = zero4;
+  f32x4 v[kLPT];
+  auto load = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < kLPT; ++i) v[i] = *(const f32x4*)(src[i] + (int64_t)c * kKC);
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < kLPT; ++i)
+      if (tid + 256 * i < rows * (kKC / 4)) *(f32x4*)&xs[off[i]] = ok[i] ? v[i] : zero4;
+  };
+  if (c0 < c1) {
+    load(c0);
+    for (int c = c0; c < c1; ++c) {
+      store();
+      __syncthreads();
+      load(c + 1 < c1 ? c + 1 : c);  // next chunk in flight (the last again at the end)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        if (!bon[t]) continue;
+#pragma unroll
+        for (int q = 0; q < kKC / 16; ++q) {
+          const f32x4 x = *(const f32x4*)&xs[arow[t] + 16 * q];
+          const f32x4 y = *(const f32x4*)&xs[brow[t] + 16 * q];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[i], y[i], acc[t], 0, 0, 0);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // gram[ks][b][p][k][k2][s][s2]
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    if (!bon[t]) continue;
+    const int e = wave + 4 * t;
+    const int pr = e / (mbs * mbs), rem = e % (mbs * mbs);
+    int k = 1, k2 = pr;
+    while (k2 >= k) {
+      k2 -= k;
+      ++k;
+    }
+    const int K2n = gridDim.x / (KSG * P);
+    float* out = gram + (((((int64_t)ks * K2n + b) * P + p) * K1 + k) * K1 + k2) * Bp * Bp;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      out[(16 * (rem / mbs) + 4 * lgrp + r) * Bp + 16 * (rem % mbs) + lrow] = acc[t][r];
+  }
+}
+
+// gram[0] += gram[1] + ... + gram[KSG-1] over the blocks k2 < k (added in
+// split order), so the consumer reads one sum.
+__global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ gram, int64_t split, int64_t n4, int KSG) {
+  f32x4* g = (f32x4*)gram;
+  const int64_t s4 = split / 4;
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    f32x4 v = g[i];
+    for (int t = 1; t < KSG; ++t) v += g[t * s4 + i];
+    g[i] = v;
+  }
+}
+
+int gram_splits(int P, int K2, int K) {
+  // about two workgroups per CU, at least two 64-wide chunks per split
+  const int target = 512;
+  int ksg = (target + P * K2 - 1) / (P * K2);
+  return std::max(1, std::min(ksg, K / kKC / 2));
+}
+
+void launch_gram(hipStream_t s, const float* X, int64_t ldx, int K, const int32_t* idx, float* gram, int P, int K1,
+                 int K2, int B, int Bp, int KSG) {
+  const int nblk = K1 * (K1 - 1) / 2 * (Bp / 16) * (Bp / 16);
+  if (nblk == 0) return;
+  const unsigned grid = (unsigned)((int64_t)P * K2 * KSG);
+  const int nb = (nblk + 3) / 4;
+#define HAV_GRAM(N_, R_) launch(k_gram<N_, R_>, grid, 256, 0, s, X, ldx, K, idx, gram, P, K1, B, Bp, KSG)
+  if (K1 * Bp <= 128) {
+    if (nb <= 2)
+      HAV_GRAM(2, 128);
+    else if (nb <= 6)
+      HAV_GRAM(6, 128);
+    else
+      HAV_GRAM(12, 128);
+  } else {
+    if (nb <= 12)
+      HAV_GRAM(12, 256);
+    else
+      HAV_GRAM(kGramMaxBlocks, 256);
+  }
+#undef HAV_GRAM
+}
+
+void launch_gram_reduce(hipStream_t s, float* gram, int P, int K1, int K2, int Bp, int KSG) {
+  const int64_t split = (int64_t)K2 * P * K1 * K1 * Bp * Bp;
+  const int64_t n4 = split / 4;
+  const int64_t g = std::min<int64_t>((n4 + 255) / 256, 2048);
+  launch(k_gram_reduce, (unsigned)g, 256, 0, s, gram, split, n4, KSG);
+}
+
+}  // namespace hav
