@@ -158,7 +158,7 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
   __shared__ float zs[kHM][kHU + 1];
   __shared__ float ws[KC][kHU + 1];
   __shared__ __attribute__((aligned(16))) float gsl[kCorrMaxK][kHM][kHU];
-  __shared__ float grl[kCorrMaxK][kHM][kHM + 1];
+  __shared__ __attribute__((aligned(16))) float grl[kCorrMaxK][kHM][kHM + 4];
   const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
   const int tid = threadIdx.x, u4 = tid & 7, rr = tid >> 3;
   const int h4 = ht * kHU + 4 * u4;
@@ -172,6 +172,17 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
   }
   const f32x4 bias = *(const f32x4*)(b1 + (int64_t)p * w_pitch + h4);
   const float* p0 = part + (int64_t)p * Mp * Hp + h4;
+  auto part_sum = [&](int m0) {  // sum of the split-K partials of row m0 + rr, in split order
+    const int m = m0 + rr;
+    const float* pm = p0 + (int64_t)(m < M ? m : 0) * Hp;
+    f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int ks = 0; ks < KS; ++ks) z += *(const f32x4*)(pm + ks * split);
+    return z;
+  };
+  // The first chunk's partials are read before the correction operands are
+  // staged, so the two sets of loads overlap.
+  const f32x4 z_first = part_sum(0);
   const int kc = corr.gram != nullptr ? corr.k : 0;
   if (kc > 0) {
     // errors of the earlier steps, this slice: gsl[k2][s][u] = G[k2][p][s][32*ht + u],
@@ -192,15 +203,19 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
   for (int m0 = 0; m0 < M; m0 += kHM) {
     const int m = m0 + rr;
     const bool mok = m < M;
-    const float* pm = p0 + (int64_t)(mok ? m : 0) * Hp;
-    f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-    for (int ks = 0; ks < KS; ++ks) z += *(const f32x4*)(pm + ks * split);
+    f32x4 z = m0 == 0 ? z_first : part_sum(m0);
     z += bias;
     if (kc > 0) {
+      // Rows and columns past M are zero in both staged operands, so the
+      // sum runs over the padded minibatch in fours.
       f32x4 c = {0.f, 0.f, 0.f, 0.f};
       for (int k2 = 0; k2 < kc; ++k2)
-        for (int s2 = 0; s2 < M; ++s2) c += grl[k2][rr][s2] * *(const f32x4*)&gsl[k2][s2][4 * u4];
+#pragma unroll 2
+        for (int s2 = 0; s2 < Mp; s2 += 4) {
+          const f32x4 g = *(const f32x4*)&grl[k2][rr][s2];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) c += g[i] * *(const f32x4*)&gsl[k2][s2 + i][4 * u4];
+        }
       z -= corr.lr * c;
     }
     if (mok) *(f32x4*)(Z1 + ((int64_t)p * Mp + m) * Hp + h4) = z;
