@@ -149,6 +149,21 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats);
  * Synchronous. */
 int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats);
 
+/*
+ * Quality of one replica's model (softmax or MLP kinds): the mean softmax
+ * cross-entropy F(w; xi) over `n_rows` rows (the empirical risk of Sec. 2)
+ * and the number of rows whose first largest logit is the label's.  split 0
+ * takes the training rows 0 .. n_rows-1 (n_rows <= N); split 1 takes held-out
+ * rows 0 .. n_rows-1 of a second synthetic set with the same class means and
+ * its own label and noise streams (labels H(k_tlabel, i) mod C, noise
+ * z(k_tnoise, i*IN + d)), generated on the GPU at the first call that needs
+ * them.  Runs on the handle's stream and synchronises; allocates its
+ * buffers at the first call.  HIERAVG_EINVAL for the averaging kind, a bad
+ * replica or split, or n_rows out of range.
+ */
+int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
+                     int64_t* correct);
+
 /* Release every resource of the handle.  NULL-safe. */
 void hieravg_destroy(hieravg_t h);
 

@@ -39,6 +39,9 @@ TAG_MEAN = int.from_bytes(b"hv.cmean", "big")
 TAG_NOISE = int.from_bytes(b"hv.noise", "big")
 TAG_INIT = int.from_bytes(b"hv.winit", "big")
 TAG_GRAD = int.from_bytes(b"hv.grads", "big")
+# held-out rows: same class means, their own labels and noise
+TAG_TEST_LABEL = int.from_bytes(b"hv.tlabl", "big")
+TAG_TEST_NOISE = int.from_bytes(b"hv.tnois", "big")
 
 IRWIN_HALL_OFFSET = 393210  # 12 * (2^16 - 1) / 2
 IRWIN_HALL_SCALE = 65536.0
@@ -113,8 +116,8 @@ def normal_surrogate(key: int, e):
     return (acc - IRWIN_HALL_OFFSET).astype(np.float64) / IRWIN_HALL_SCALE
 
 
-def labels(seed: int, rows, C: int):
-    key = stream_key(seed, TAG_LABEL)
+def labels(seed: int, rows, C: int, split: int = 0):
+    key = stream_key(seed, TAG_LABEL if split == 0 else TAG_TEST_LABEL)
     return (h(key, _u64(rows)) % np.uint64(C)).astype(np.int64)
 
 
@@ -126,14 +129,16 @@ def class_means(seed: int, classes, IN: int):
     return normal_surrogate(key, classes * np.uint64(IN) + d)
 
 
-def data_rows(seed: int, rows, IN: int, C: int, sigma: float):
-    """Rows X[i, :] and labels y[i] of the synthetic dataset, regenerated on
-    demand (the dataset is never materialised): X = fp32(mu[y] + sigma * z)."""
+def data_rows(seed: int, rows, IN: int, C: int, sigma: float, split: int = 0):
+    """Rows X[i, :] and labels y[i] of the synthetic dataset (split 0) or of
+    the held-out set (split 1: the same class means, its own label and noise
+    streams), regenerated on demand (never materialised):
+    X = fp32(mu[y] + sigma * z)."""
     rows = np.asarray(rows, dtype=np.int64).reshape(-1)
-    y = labels(seed, rows, C)
+    y = labels(seed, rows, C, split)
     uniq, inv = np.unique(y, return_inverse=True)
     mu = class_means(seed, uniq, IN)[inv]
-    key = stream_key(seed, TAG_NOISE)
+    key = stream_key(seed, TAG_NOISE if split == 0 else TAG_TEST_NOISE)
     d = np.arange(IN, dtype=np.uint64).reshape(1, -1)
     z = normal_surrogate(key, rows.astype(np.uint64).reshape(-1, 1) * np.uint64(IN) + d)
     sig = float(np.float32(sigma))

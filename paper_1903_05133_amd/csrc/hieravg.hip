@@ -96,6 +96,14 @@ struct hieravg {
   float* Wc = nullptr;     // [P/S][Hp*INp] cluster copies of W1
   float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
   float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
+  // Evaluation (allocated at the first hieravg_evaluate).
+  int eval_rows = 0;                  // chunk capacity (multiple of 16)
+  int32_t* eval_iota = nullptr;       // [eval_rows] 0, 1, 2, ...
+  float *eval_part = nullptr, *eval_part2 = nullptr, *eval_Z1 = nullptr, *eval_loss = nullptr;
+  int32_t* eval_hit = nullptr;
+  int64_t n_test = 0;                 // held-out rows generated so far
+  float* Xtest = nullptr;             // [n_test][INp]
+  int32_t* ytest = nullptr;           // [n_test]
   int KSG = 1;             // feature splits of the Gram blocks
   hipStream_t own_stream = nullptr, stream = nullptr;
   int64_t steps = 0;
@@ -142,7 +150,8 @@ void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1,
-                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram};
+                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->eval_iota,
+                  h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   for (auto& r : h->recs) {
@@ -719,6 +728,117 @@ int hieravg_round(hieravg_t h) {
   // updates only replica 0's copy is written).
   h->w1_shared = true;
   h->steps += (int64_t)h->cfg.K1 * h->cfg.K2;
+  return HIERAVG_OK;
+}
+
+int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
+                     int64_t* correct) {
+  if (!h || !mean_loss || !correct) {
+    set_error("NULL handle or output");
+    return HIERAVG_EINVAL;
+  }
+  const hieravg_config& c = h->cfg;
+  if (c.kind == HIERAVG_KIND_AVERAGING) {
+    set_error("the averaging-only workload has no model to evaluate");
+    return HIERAVG_EINVAL;
+  }
+  if (replica < 0 || replica >= c.P || (split != 0 && split != 1) || n_rows < 1 ||
+      (split == 0 && n_rows > h->N) || n_rows > (int64_t(1) << 31)) {
+    set_error("bad replica, split or row count (split 0 takes at most N rows)");
+    return HIERAVG_EINVAL;
+  }
+  const bool mlp = c.kind == HIERAVG_KIND_MLP;
+  const int Hp = (int)h->Hp, Cp = (int)h->Cp, INp = (int)h->INp, C = (int)h->C;
+  hipStream_t s = h->stream;
+  HAV_CHECK(hipStreamSynchronize(s));
+  // Buffers for chunks of up to 4096 rows.
+  const int chunk = (int)std::min<int64_t>(4096, round_up(n_rows, 16));
+  int KS1e, cps1e, KS2e = 1, cps2e = 1;
+  plan_split(1, chunk, mlp ? Hp : Cp, INp, &KS1e, &cps1e);
+  if (mlp) plan_split(1, chunk, Cp, Hp, &KS2e, &cps2e);
+  if (chunk > h->eval_rows) {
+    void* old[] = {h->eval_iota, h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit};
+    for (void* b : old)
+      if (b) (void)hipFree(b);
+    h->eval_iota = nullptr;
+    h->eval_part = h->eval_part2 = h->eval_Z1 = h->eval_loss = nullptr;
+    h->eval_hit = nullptr;
+    h->eval_rows = 0;
+    int rc;
+    // KS for a chunk is at most the number of 64-wide K chunks.
+    const int64_t ks1 = std::max<int64_t>(KS1e, INp / 64), ks2 = mlp ? std::max<int64_t>(KS2e, Hp / 64) : 1;
+    if ((rc = alloc_zero(h, (void**)&h->eval_iota, sizeof(int32_t) * chunk, "evaluation rows")) ||
+        (rc = alloc_zero(h, (void**)&h->eval_part, sizeof(float) * ks1 * chunk * (mlp ? Hp : Cp), "evaluation partials")) ||
+        (rc = alloc_zero(h, (void**)&h->eval_loss, sizeof(float) * chunk, "evaluation losses")) ||
+        (rc = alloc_zero(h, (void**)&h->eval_hit, sizeof(int32_t) * chunk, "evaluation hits")))
+      return rc;
+    if (mlp && ((rc = alloc_zero(h, (void**)&h->eval_part2, sizeof(float) * ks2 * chunk * Cp, "evaluation logits")) ||
+                (rc = alloc_zero(h, (void**)&h->eval_Z1, sizeof(float) * chunk * Hp, "evaluation activations"))))
+      return rc;
+    std::vector<int32_t> iota(chunk);
+    for (int i = 0; i < chunk; ++i) iota[i] = i;
+    HAV_CHECK(hipMemcpyAsync(h->eval_iota, iota.data(), sizeof(int32_t) * chunk, hipMemcpyHostToDevice, s));
+    HAV_CHECK(hipStreamSynchronize(s));
+    h->eval_rows = chunk;
+  }
+  // Held-out rows: the dataset recipe with its own label and noise streams.
+  if (split == 1 && n_rows > h->n_test) {
+    if (h->Xtest) (void)hipFree(h->Xtest);
+    if (h->ytest) (void)hipFree(h->ytest);
+    h->Xtest = nullptr;
+    h->ytest = nullptr;
+    h->n_test = 0;
+    int rc;
+    if ((rc = alloc_zero(h, (void**)&h->Xtest, sizeof(float) * n_rows * h->INp, "held-out rows")) ||
+        (rc = alloc_zero(h, (void**)&h->ytest, sizeof(int32_t) * n_rows, "held-out labels")))
+      return rc;
+    launch_gen_labels(s, h->ytest, n_rows, hash64(c.seed, kTagTestLabel), (uint64_t)C);
+    launch_gen_data(s, h->Xtest, h->ytest, n_rows, h->IN, h->INp, hash64(c.seed, kTagMean),
+                    hash64(c.seed, kTagTestNoise), c.noise_std);
+    HAV_CHECK(hipGetLastError());
+    h->n_test = n_rows;
+  }
+  const float* Xs = split == 0 ? h->X : h->Xtest;
+  const int32_t* ys = split == 0 ? h->y : h->ytest;
+  // Replica `replica`; its first weight block lives in replica 0 while the
+  // learners share it under delayed updates.
+  const float* Wr = h->W + (int64_t)replica * h->Dp;
+  const float* W1r = (h->delayed && h->w1_shared ? h->W : Wr) + h->off_W1;
+  double total = 0.0;
+  int64_t hits = 0;
+  std::vector<float> lh(chunk);
+  std::vector<int32_t> hh(chunk);
+  for (int64_t r0 = 0; r0 < n_rows; r0 += chunk) {
+    const int M = (int)std::min<int64_t>(chunk, n_rows - r0);
+    const int Mp = (int)round_up(M, 16);
+    int KS1, cps1;
+    plan_split(1, Mp, mlp ? Hp : Cp, INp, &KS1, &cps1);
+    FwdArgs f{Xs + r0 * h->INp, h->eval_iota, h->INp, W1r, 0, h->INp, h->eval_part, 1, M, Mp, mlp ? Hp : Cp, INp,
+              KS1, cps1};
+    launch_fwd(s, f, A_GATHER);
+    if (mlp) {
+      launch_reduce_bias(s, h->eval_part, KS1, Wr + h->off_b1, 0, h->eval_Z1, 1, M, Mp, Hp);
+      int KS2, cps2;
+      plan_split(1, Mp, Cp, Hp, &KS2, &cps2);
+      FwdArgs f2{h->eval_Z1, nullptr, h->Hp, Wr + h->off_W2, 0, h->Hp, h->eval_part2, 1, M, Mp, Cp, Hp, KS2, cps2};
+      launch_fwd(s, f2, A_RELU);
+      launch_eval_rows(s, h->eval_part2, KS2, (int64_t)Mp * Cp, Wr + h->off_b2, ys + r0, M, Cp, C, h->eval_loss,
+                       h->eval_hit);
+    } else {
+      launch_eval_rows(s, h->eval_part, KS1, (int64_t)Mp * Cp, Wr + h->off_b1, ys + r0, M, Cp, C, h->eval_loss,
+                       h->eval_hit);
+    }
+    HAV_CHECK(hipGetLastError());
+    HAV_CHECK(hipMemcpyAsync(lh.data(), h->eval_loss, sizeof(float) * M, hipMemcpyDeviceToHost, s));
+    HAV_CHECK(hipMemcpyAsync(hh.data(), h->eval_hit, sizeof(int32_t) * M, hipMemcpyDeviceToHost, s));
+    HAV_CHECK(hipStreamSynchronize(s));
+    for (int i = 0; i < M; ++i) {
+      total += lh[i];
+      hits += hh[i];
+    }
+  }
+  *mean_loss = total / (double)n_rows;
+  *correct = hits;
   return HIERAVG_OK;
 }
 

@@ -54,6 +54,8 @@ constexpr uint64_t kTagMean = 0x68762e636d65616eull;   // "hv.cmean"
 constexpr uint64_t kTagNoise = 0x68762e6e6f697365ull;  // "hv.noise"
 constexpr uint64_t kTagInit = 0x68762e77696e6974ull;   // "hv.winit"
 constexpr uint64_t kTagGrad = 0x68762e6772616473ull;   // "hv.grads"
+constexpr uint64_t kTagTestLabel = 0x68762e746c61626cull;  // "hv.tlabl" (held-out rows)
+constexpr uint64_t kTagTestNoise = 0x68762e746e6f6973ull;  // "hv.tnois"
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -249,6 +251,11 @@ void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, co
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, float lr);
+
+// Per-row softmax cross-entropy and first-argmax hit of an evaluation chunk
+// from split-K logit partials part[ks][m][Cp] (split floats apart) and bias.
+void launch_eval_rows(hipStream_t s, const float* part, int KS, int64_t split, const float* bias, const int32_t* y,
+                      int M, int Cp, int C, float* loss, int32_t* hit);
 
 // Averaging (k_avg.hip).
 // Mean over each cluster of S rows of the columns [0, len) of W (row pitch

@@ -346,6 +346,56 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
   if (ht == 0 && tid < C) b2[(int64_t)p * w_pitch + tid] -= lr * db2;
 }
 
+// Evaluation: one wave per row m < M of a chunk.  Logits l_c = b_c + sum_ks
+// part[ks][m][c] for c < C (splits added in order); the row's softmax
+// cross-entropy log(sum_c exp(l_c - max)) + max - l_y and whether the first
+// largest logit is the label's.
+__global__ __launch_bounds__(256) void k_eval_rows(const float* __restrict__ part, int KS, int64_t split,
+                                                   const float* __restrict__ bias, const int32_t* __restrict__ y,
+                                                   int M, int Cp, int C, float* __restrict__ loss,
+                                                   int32_t* __restrict__ hit) {
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (m >= M) return;
+  const float* pr = part + (int64_t)m * Cp;
+  auto logit = [&](int c) {
+    float v = bias[c];
+    for (int ks = 0; ks < KS; ++ks) v += pr[ks * split + c];
+    return v;
+  };
+  float best = -INFINITY;
+  int bestc = 0x7fffffff;
+  for (int c = lane; c < C; c += 64) {
+    const float v = logit(c);
+    if (v > best) {  // c increases within a lane: the first index wins ties
+      best = v;
+      bestc = c;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oc = __shfl_xor(bestc, o, 64);
+    if (ob > best || (ob == best && oc < bestc)) {
+      best = ob;
+      bestc = oc;
+    }
+  }
+  float sum = 0.0f;
+  for (int c = lane; c < C; c += 64) sum += expf(logit(c) - best);
+  sum = wave_sum(sum);
+  if (lane == 0) {
+    const int yy = y[m];
+    loss[m] = logf(sum) + best - logit(yy);
+    hit[m] = bestc == yy ? 1 : 0;
+  }
+}
+
+void launch_eval_rows(hipStream_t s, const float* part, int KS, int64_t split, const float* bias, const int32_t* y,
+                      int M, int Cp, int C, float* loss, int32_t* hit) {
+  launch(k_eval_rows, (M + 3) / 4, 256, 0, s, part, KS, split, bias, y, M, Cp, C, loss, hit);
+}
+
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,
                         int P, int M, int Mp, int N) {
   int64_t g = ((int64_t)P * Mp * N + 255) / 256;

@@ -85,6 +85,15 @@ class HierAvg:
             a = np.ascontiguousarray(arr, dtype=np.float32)
             native.check(native.lib().hieravg_set_params(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
 
+    def evaluate(self, replica=0, split=1, n_rows=4096):
+        """(mean cross-entropy, correct count) of replica `replica` on
+        `n_rows` training (split 0) or held-out (split 1) rows."""
+        loss = ctypes.c_double()
+        correct = ctypes.c_int64()
+        native.check(native.lib().hieravg_evaluate(self._h, replica, split, n_rows, ctypes.byref(loss),
+                                                   ctypes.byref(correct)))
+        return loss.value, correct.value
+
     def last_indices(self):
         out = np.empty((self.K2, self.K1, self.P, self.B), dtype=np.int32)
         native.check(native.lib().hieravg_last_indices(self._h, ctypes.c_void_p(out.ctypes.data), out.size))

@@ -35,6 +35,8 @@ SIGNATURES = {
     "hieravg_params": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_set_params": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_destroy": (None, [_H]),
+    "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "hieravg_last_error": (ctypes.c_char_p, []),
     "hieravg_dim": (ctypes.c_int64, [_H]),
     "hieravg_step_count": (ctypes.c_int64, [_H]),

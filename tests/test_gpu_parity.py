@@ -279,3 +279,38 @@ def test_unfused_schedule_profile(gpu_lib):
     assert stats["group_mean"][0] == 2 and stats["fwd1_gemm"][0] == 3
     assert stats["update1_gemm"][0] == 3 and stats["step1_gemm"][0] == 3
     assert "step1_gemm_group_mean" not in stats
+
+
+# ---------------------------------------------------------------- evaluation
+EVAL_CASES = {
+    "softmax_ragged": (SMALL["softmax_ragged"], "auto"),
+    "mlp_ragged_delayed": (SMALL["mlp_ragged"], "delayed"),
+    "mlp_multi_tile_large_C": (SMALL["mlp_multi_tile"], "eager"),
+    "mlp_3072_512_10": (cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0), "auto"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EVAL_CASES))
+def test_evaluate_matches_oracle(name, gpu_lib):
+    """Loss and accuracy of replicas after a round, on training and held-out
+    rows, against the oracle evaluating the same parameters: loss within
+    1e-4 relative; hit counts equal except rows whose two largest logits are
+    within 1e-5 (relative) of each other, where float32 may decide either way."""
+    from paper_1903_05133_amd import HierAvg
+    c, mode = EVAL_CASES[name]
+    prob = cases.oracle_problem(c)
+    with HierAvg(config=cases.native_config(c, mode)) as h:
+        h.round()
+        W = h.params().astype(np.float64)
+        # more rows than one 4096-row chunk on the held-out split of the small cases
+        plan = [(0, 0, min(c["N"], 300)), (c["P"] - 1, 1, 300 if c["IN"] > 1000 else 5000)]
+        for replica, split, n in plan:
+            print(f"[gpu case] evaluate {name} replica {replica} split {split} rows {n}", flush=True)
+            loss, correct = h.evaluate(replica, split, n)
+            want, wc, gaps = M.evaluate(prob, W[replica], np.arange(n), split)
+            assert abs(loss - want) <= 1e-4 * max(1.0, abs(want)), (loss, want)
+            assert abs(correct - wc) <= int(np.sum(gaps < 1e-5)), (correct, wc)
+        with pytest.raises(Exception):
+            h.evaluate(c["P"], 0, 10)
+        with pytest.raises(Exception):
+            h.evaluate(0, 0, c["N"] + 1)

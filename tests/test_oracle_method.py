@@ -296,3 +296,44 @@ def test_averaging_column_sampling_is_exact():
     part = M.run(p, 2, cols=cols)
     assert np.array_equal(part.W, full.W[:, cols])
     assert np.array_equal(part.V, full.V[:, cols])
+
+
+# ---------------------------------------------------------------- evaluation
+def test_evaluate_matches_torch_cross_entropy_and_argmax():
+    """The evaluation loss is torch's softmax cross-entropy (float64, CPU) of
+    the model's logits, and the count is torch's argmax accuracy."""
+    import torch
+    for kind in (M.MLP, M.SOFTMAX):
+        p = M.Problem(kind, 2, 1, 1, 1, 4, IN=20, H=9, C=6, N=50, sigma=0.7, seed=21)
+        st = M.create(p)
+        row = st.W[0] + np.random.default_rng(0).normal(0, 0.3, p.D)  # off the initial point
+        rows = np.arange(37)
+        for split in (0, 1):
+            loss, correct, gaps = M.evaluate(p, row, rows, split, chunk=10)
+            X, y = rng.data_rows(p.seed, rows, p.IN, p.C, p.sigma, split)
+            blk = M.unpack(p, row)
+            Xt = torch.tensor(X)
+            if kind == M.SOFTMAX:
+                z = Xt @ torch.tensor(blk["W"]).T + torch.tensor(blk["b"])
+            else:
+                a = torch.relu(Xt @ torch.tensor(blk["W1"]).T + torch.tensor(blk["b1"]))
+                z = a @ torch.tensor(blk["W2"]).T + torch.tensor(blk["b2"])
+            want = torch.nn.functional.cross_entropy(z, torch.tensor(y)).item()
+            assert abs(loss - want) <= 1e-12 * max(1.0, abs(want))
+            assert correct == int((z.argmax(dim=1) == torch.tensor(y)).sum())
+            assert gaps.shape == (37,) and np.all(gaps >= 0)
+
+
+def test_held_out_rows_recipe():
+    """Split 1 keeps the class means and takes its own label and noise
+    streams; one element written out from the definition."""
+    seed, IN, C, sigma = 4, 16, 3, 0.5
+    X0, y0 = rng.data_rows(seed, np.arange(200), IN, C, sigma, 0)
+    X1, y1 = rng.data_rows(seed, np.arange(200), IN, C, sigma, 1)
+    assert not np.array_equal(y0, y1) and not np.array_equal(X0, X1)
+    i, d = 17, 5
+    key_n = rng.stream_key(seed, rng.TAG_TEST_NOISE)
+    z = rng.normal_surrogate(key_n, np.array([i * IN + d], dtype=np.uint64))[0]
+    mu = rng.class_means(seed, np.arange(C), IN)
+    assert y1[i] == rng.h_scalar(rng.stream_key(seed, rng.TAG_TEST_LABEL), i) % C
+    assert X1[i, d] == float(np.float32(mu[y1[i], d] + sigma * z))
