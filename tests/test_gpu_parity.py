@@ -314,3 +314,21 @@ def test_evaluate_matches_oracle(name, gpu_lib):
             h.evaluate(c["P"], 0, 10)
         with pytest.raises(Exception):
             h.evaluate(0, 0, c["N"] + 1)
+
+
+def test_convergence_runner(gpu_lib):
+    """The multi-round runner: one JSON line per round plus a summary; the
+    global model's training loss falls over the rounds."""
+    import io
+    import json
+    from paper_1903_05133_amd import convergence
+    buf = io.StringIO()
+    # softmax model with noisy data (std 5) and lr 0.005: the loss falls from
+    # about 1.6 to 0.3 over three rounds (oracle)
+    summ = convergence.run("t", 0, 4, 2, 2, 2, 8, 0.005, 3, 256, noise=5.0, out=buf)
+    lines = [json.loads(x) for x in buf.getvalue().splitlines()]
+    per_round = [x for x in lines if "summary" not in x]
+    assert [x["round"] for x in per_round] == [1, 2, 3] and lines[-1]["summary"]
+    assert [x["steps"] for x in per_round] == [4, 8, 12]
+    assert per_round[-1]["train_loss"] < per_round[0]["train_loss"]
+    assert 0.0 <= summ["final_test_acc"] <= 1.0
