@@ -106,6 +106,12 @@ typedef struct hieravg_config {
   float grad_std;   /* averaging kind: std of the given gradients           */
   uint64_t seed;
   int32_t update_mode; /* HIERAVG_UPDATE_* (how the first weight block is updated) */
+  int32_t k_global;    /* SGD steps per round (the paper's global interval K2 in steps,
+                          Sec. 3.1); 0: K1*K2.  When set, K2 is not used: a local mean
+                          follows every K1 steps of the round except its last step, which
+                          takes the global mean, so a round of k_global steps that K1
+                          does not divide ends with a shorter block (a non-integer beta);
+                          the count of local steps restarts at every global mean */
 } hieravg_config;
 
 /*
@@ -150,6 +156,24 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats);
 int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats);
 
 /*
+ * Minibatch size of the rounds enqueued from now on (a per-round schedule
+ * B_n, Thm 3.3), 1 <= B <= the B given at create (the buffers' capacity).
+ * The draws of sample s keep their counters, so the first B samples of a
+ * step are the same for any B.  Synchronises; the next round rebuilds its
+ * launch plan.  HIERAVG_EINVAL for the averaging kind or B out of range.
+ */
+int hieravg_set_batch(hieravg_t h, int32_t B);
+
+/*
+ * Step size of the rounds enqueued from now on (a per-round schedule, e.g.
+ * the step decay 0.1 -> 0.01 of Sec. 4 or the gamma_n of Thm 3.3).  The value
+ * lives in device memory and every kernel reads it, so a change needs no new
+ * launch plan.  Synchronises the handle's stream.  HIERAVG_EINVAL for a
+ * non-finite or negative lr.
+ */
+int hieravg_set_lr(hieravg_t h, float lr);
+
+/*
  * Quality of one replica's model (softmax or MLP kinds): the mean softmax
  * cross-entropy F(w; xi) over `n_rows` rows (the empirical risk of Sec. 2)
  * and the number of rows whose first largest logit is the label's.  split 0
@@ -177,9 +201,11 @@ int64_t hieravg_dim(hieravg_t h);
 int64_t hieravg_step_count(hieravg_t h);
 
 /*
- * Copy the minibatch indices the last round drew, as int32 [K2][K1][P][B],
- * to `dst` (host or device, n >= K2*K1*P*B).  Synchronises.  HIERAVG_EINVAL
- * for the averaging kind (it draws no samples).
+ * Copy the minibatch indices the last round drew, as int32 [T][P][B] with T
+ * the steps per round (K2*K1 or k_global) and B the current minibatch size
+ * (hieravg_set_batch), to `dst` (host or device,
+ * n >= T*P*B).  Synchronises.  HIERAVG_EINVAL for the averaging kind (it
+ * draws no samples).
  */
 int hieravg_last_indices(hieravg_t h, int32_t* dst, size_t n);
 

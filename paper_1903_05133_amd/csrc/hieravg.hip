@@ -81,9 +81,12 @@ struct hieravg {
   float* G2 = nullptr;     // [P][Bp][Cp] output error
   float* G1 = nullptr;     // [P][Bp][Hp] hidden error
   uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
+  float* hyper = nullptr;   // [0]: step size lr read by the kernels (hieravg_set_lr)
 
   uint64_t key_index = 0;
   int KS1 = 1, cps1 = 1, KS2 = 1, cps2 = 1;
+  int Bmax = 0;             // minibatch size at create: the buffers' capacity
+  bool rows_stale = false;  // replicas 1..P-1 hold an old W1 (after a delayed round)
   bool fused = false;       // the fused step kernel applies (SG = 1)
   bool fused_mean = false;  // ... and also with the cluster mean (SG = S)
   int KS_step = 1, KS_mean = 1;  // forward splits written by the fused kernel
@@ -107,6 +110,7 @@ struct hieravg {
   int KSG = 1;             // feature splits of the Gram blocks
   hipStream_t own_stream = nullptr, stream = nullptr;
   int64_t steps = 0;
+  int T = 1;  // SGD steps per round
   // One round's kernels, captured on first use and replayed for every round
   // that is not profiled (every launch argument is the same in every round).
   hipGraphExec_t round_exec[2] = {nullptr, nullptr};  // [eager, delayed]
@@ -149,7 +153,7 @@ void run(hieravg* h, int kc, F&& fn) {
 void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
-  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1,
+  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
@@ -183,7 +187,8 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
 }
 
 bool delayed_applies(const hieravg_config& c) {
-  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8;
+  const bool whole_blocks = c.k_global == 0 || c.k_global % c.K1 == 0;
+  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8 && whole_blocks;
 }
 
 int validate(const hieravg_config& c) {
@@ -195,19 +200,21 @@ int validate(const hieravg_config& c) {
   if (c.S < 1) return bad("S must be >= 1");
   if (c.P % c.S != 0) return bad("S must divide P (Sec. 2: S | P)");
   if (c.K1 < 1) return bad("K1 must be >= 1");
-  if (c.K2 < 1) return bad("K2 must be >= 1");
-  if ((int64_t)c.K1 * c.K2 > (1 << 20)) return bad("K1*K2 must be <= 2^20");
+  if (c.k_global < 0) return bad("k_global must be >= 0");
+  if (c.k_global == 0 && c.K2 < 1) return bad("K2 must be >= 1");
+  const int64_t T = c.k_global > 0 ? (int64_t)c.k_global : (int64_t)c.K1 * c.K2;
+  if (T > (1 << 20)) return bad("steps per round (K1*K2 or k_global) must be <= 2^20");
   if (!std::isfinite(c.lr) || c.lr < 0.0f) return bad("lr must be finite and >= 0");
   if (c.update_mode < HIERAVG_UPDATE_AUTO || c.update_mode > HIERAVG_UPDATE_DELAYED)
     return bad("update_mode must be one of HIERAVG_UPDATE_*");
   if (c.update_mode == HIERAVG_UPDATE_DELAYED && !delayed_applies(c))
-    return bad("delayed updates need the MLP with at most 32 classes, B <= 32 and K1 <= 8");
+    return bad("delayed updates need the MLP with at most 32 classes, B <= 32, K1 <= 8 and whole blocks");
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
     if (!std::isfinite(c.momentum) || c.momentum < 0.0f || c.momentum >= 1.0f)
       return bad("averaging: momentum must be in [0, 1)");
     if (!std::isfinite(c.init_std) || !std::isfinite(c.grad_std)) return bad("averaging: stds must be finite");
-    if ((int64_t)c.K1 * c.K2 * c.P > 65535) return bad("averaging: K1*K2*P must be <= 65535");
+    if (T * c.P > 65535) return bad("averaging: steps per round * P must be <= 65535");
     return HIERAVG_OK;
   }
   if (c.kind != HIERAVG_KIND_SOFTMAX && c.kind != HIERAVG_KIND_MLP) return bad("unknown model kind");
@@ -217,23 +224,68 @@ int validate(const hieravg_config& c) {
   if (c.kind == HIERAVG_KIND_MLP && (c.hidden < 1 || c.hidden > (1 << 20))) return bad("hidden must be in [1, 2^20]");
   if (c.n_samples < 1 || c.n_samples > 0x7fffffffLL) return bad("n_samples must be in [1, 2^31 - 1]");
   if (!std::isfinite(c.noise_std)) return bad("noise_std must be finite");
-  if ((int64_t)c.K1 * c.K2 * c.P * c.B > 0x7fffffffLL) return bad("K1*K2*P*B must be < 2^31");
+  if (T * c.P * c.B > 0x7fffffffLL) return bad("steps per round * P * B must be < 2^31");
   return HIERAVG_OK;
 }
 
 float fan_in_scale(int64_t fan_in) { return (float)(1.0 / std::sqrt((double)fan_in)); }
 
+// Launch plan for minibatch size B (softmax / MLP kinds): padded batch,
+// split counts, which fused and delayed kernels apply.  Returns the partial
+// buffer size the plan needs, in floats.
+int64_t plan(hieravg* h, int B) {
+  const hieravg_config& c = h->cfg;
+  const int P = c.P;
+  const bool mlp = c.kind == HIERAVG_KIND_MLP;
+  const int64_t n1 = mlp ? h->Hp : h->Cp;
+  h->Bp = (int)round_up(B, 16);
+  h->KS2 = h->cps2 = 1;
+  plan_split(P, h->Bp, (int)n1, (int)h->INp, &h->KS1, &h->cps1);
+  if (mlp) plan_split(P, h->Bp, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
+  h->fused = h->T >= 2 && step_w1_supported(h->Bp, 1);
+  h->fused_mean = h->fused && c.S > 1 && step_w1_supported(h->Bp, c.S);
+  int64_t ks_max = h->KS1;
+  if (h->fused) {
+    h->KS_step = step_w1_splits(P, 1, (int)n1, (int)h->INp);
+    ks_max = std::max<int64_t>(ks_max, h->KS_step);
+  }
+  if (h->fused_mean) {
+    h->KS_mean = step_w1_splits(P, c.S, (int)n1, (int)h->INp);
+    ks_max = std::max<int64_t>(ks_max, h->KS_mean);
+  }
+  h->delayed = false;
+  hieravg_config cb = c;
+  cb.B = B;
+  if (mlp && delayed_applies(cb)) {
+    const bool cheap = (int64_t)(c.K1 - 1) * h->Bp * 2 <= h->Hp;
+    h->delayed = c.update_mode == HIERAVG_UPDATE_DELAYED || (c.update_mode == HIERAVG_UPDATE_AUTO && cheap);
+  }
+  if (h->delayed) {
+    // One GEMM per cluster and block: the K1*S minibatches against the copy.
+    plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
+                   HAV_FWD_BLOCK_TARGET);
+    ks_max = std::max<int64_t>(ks_max, (int64_t)h->KS_b * c.K1);
+  }
+  h->ks_cur = h->KS1;
+  return std::max<int64_t>(ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
+}
+
 int build(hieravg* h) {
   const hieravg_config& c = h->cfg;
   HAV_CHECK(hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
   h->stream = h->own_stream;
+  {
+    int rc;
+    if ((rc = alloc_zero(h, (void**)&h->hyper, 4 * sizeof(float), "hyperparameters"))) return rc;
+    HAV_CHECK(hipMemcpyAsync(h->hyper, &c.lr, sizeof(float), hipMemcpyHostToDevice, h->stream));
+  }
   const int P = c.P;
   const uint64_t seed = c.seed;
 
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     h->D = c.in_dim;
     h->Dp = round_up(h->D, 64);
-    const int T = c.K1 * c.K2;
+    const int T = h->T;
     int rc;
     if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->V, sizeof(float) * P * h->Dp, "momentum buffers"))) return rc;
@@ -250,7 +302,6 @@ int build(hieravg* h) {
     h->INp = round_up(h->IN, 64);
     h->Cp = round_up(h->C, 16);
     h->Hp = mlp ? round_up(h->H, 64) : 0;
-    h->Bp = (int)round_up(c.B, 16);
     if (mlp) {
       h->off_W1 = 0;
       h->off_b1 = h->Hp * h->INp;
@@ -258,41 +309,29 @@ int build(hieravg* h) {
       h->off_b2 = h->off_W2 + h->Cp * h->Hp;
       h->Dp = round_up(h->off_b2 + h->Cp, 64);
       h->D = h->H * h->IN + h->H + h->C * h->H + h->C;
-      plan_split(P, h->Bp, (int)h->Hp, (int)h->INp, &h->KS1, &h->cps1);
-      plan_split(P, h->Bp, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
     } else {
       h->off_W1 = 0;
       h->off_b1 = h->Cp * h->INp;
       h->Dp = round_up(h->off_b1 + h->Cp, 64);
       h->D = h->C * h->IN + h->C;
-      plan_split(P, h->Bp, (int)h->Cp, (int)h->INp, &h->KS1, &h->cps1);
     }
-    const int T = c.K1 * c.K2;
-    const int64_t n1 = mlp ? h->Hp : h->Cp;
-    h->fused = T >= 2 && step_w1_supported(h->Bp, 1);
-    h->fused_mean = h->fused && c.S > 1 && step_w1_supported(h->Bp, c.S);
-    int ks_max = h->KS1;
-    if (h->fused) {
-      h->KS_step = step_w1_splits(P, 1, (int)n1, (int)h->INp);
-      ks_max = std::max(ks_max, h->KS_step);
+    const int T = h->T;
+    // Buffers hold the largest launch plan over every batch size up to the
+    // create-time B (hieravg_set_batch may lower it).
+    h->Bmax = c.B;
+    int64_t part_floats = 0;
+    bool any_delayed = false;
+    int Bp_del = 0;
+    for (int b = 16; b <= round_up(c.B, 16); b += 16) {
+      const int64_t pf = plan(h, std::min(b, c.B));
+      part_floats = std::max(part_floats, pf);
+      if (h->delayed) {
+        any_delayed = true;
+        Bp_del = std::max(Bp_del, h->Bp);
+      }
     }
-    if (h->fused_mean) {
-      h->KS_mean = step_w1_splits(P, c.S, (int)n1, (int)h->INp);
-      ks_max = std::max(ks_max, h->KS_mean);
-    }
-    if (mlp && delayed_applies(c)) {
-      const bool cheap = (int64_t)(c.K1 - 1) * h->Bp * 2 <= h->Hp;
-      h->delayed = c.update_mode == HIERAVG_UPDATE_DELAYED || (c.update_mode == HIERAVG_UPDATE_AUTO && cheap);
-    }
-    if (h->delayed) {
-      // One GEMM per cluster and block: the K1*S minibatches against the copy.
-      plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
-                     HAV_FWD_BLOCK_TARGET);
-      ks_max = std::max(ks_max, h->KS_b * c.K1);
-    }
-    h->ks_cur = h->KS1;
-    const int64_t part_floats =
-        std::max<int64_t>((int64_t)ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
+    plan(h, c.B);
+    h->Bp = (int)round_up(c.B, 16);
     int rc;
     if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->X, sizeof(float) * h->N * h->INp, "dataset"))) return rc;
@@ -308,13 +347,13 @@ int build(hieravg* h) {
       if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
     }
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
-    if (h->delayed) {
+    if (any_delayed) {
       const int64_t w1 = h->Hp * h->INp;
       if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
-      if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * h->Bp * h->Hp, "block errors"))) return rc;
+      if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
       h->KSG = gram_splits(P, c.K2, (int)h->INp);
       if (c.K1 > 1 && (rc = alloc_zero(h, (void**)&h->gram,
-                                       sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * h->Bp * h->Bp, "Gram blocks")))
+                                       sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * Bp_del * Bp_del, "Gram blocks")))
         return rc;
     }
     h->key_index = hash64(seed, kTagIndex);
@@ -349,9 +388,13 @@ bool launch_class(hieravg* h, int kc, int tt) {
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     const float* g = h->Gr + (int64_t)tt * P * h->Dp;
     switch (kc) {
-      case KC_MOMENTUM: launch_momentum_step(s, W, h->V, g, h->Dp, P, 1, false, c.lr, c.momentum); return true;
-      case KC_MOMENTUM_GROUP: launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, c.lr, c.momentum); return true;
-      case KC_MOMENTUM_GLOBAL: launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, c.lr, c.momentum); return true;
+      case KC_MOMENTUM: launch_momentum_step(s, W, h->V, g, h->Dp, P, 1, false, h->hyper, c.momentum); return true;
+      case KC_MOMENTUM_GROUP:
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, h->hyper, c.momentum);
+        return true;
+      case KC_MOMENTUM_GLOBAL:
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, h->hyper, c.momentum);
+        return true;
       default: return false;
     }
   }
@@ -360,7 +403,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
   const bool mlp = c.kind == HIERAVG_KIND_MLP, small = mlp && C <= kSmallC;
   switch (kc) {
     case KC_DRAW:
-      launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, c.K1 * c.K2, (uint64_t)h->N,
+      launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, h->T, (uint64_t)h->N,
                           h->key_index);
       return true;
     case KC_FWD1: {
@@ -380,11 +423,11 @@ bool launch_class(hieravg* h, int kc, int tt) {
       // model's layer is the first and only one.
       if (!mlp) {
         UpdArgs u{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp,
-                  c.lr};
+                  h->hyper};
         launch_update(s, u, A_GATHER);
       } else {
         UpdArgs u{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
-                  small ? nullptr : W + h->off_b1, P, B, Hp, INp, c.lr};
+                  small ? nullptr : W + h->off_b1, P, B, Hp, INp, h->hyper};
         launch_update(s, u, A_GATHER);
       }
       return true;
@@ -392,14 +435,14 @@ bool launch_class(hieravg* h, int kc, int tt) {
     case KC_STEP1:
     case KC_STEP1_MEAN: {
       const bool mean = kc == KC_STEP1_MEAN;
-      if (!(mean ? h->fused_mean : h->fused) || tt + 1 >= c.K1 * c.K2) return false;
+      if (!(mean ? h->fused_mean : h->fused) || tt + 1 >= h->T) return false;
       StepArgs a{};
       if (!mlp)
         a.u = UpdArgs{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp,
-                      c.lr};
+                      h->hyper};
       else
         a.u = UpdArgs{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
-                      small ? nullptr : W + h->off_b1, P, B, Hp, INp, c.lr};
+                      small ? nullptr : W + h->off_b1, P, B, Hp, INp, h->hyper};
       a.idx_next = ix + (int64_t)P * B;
       a.part = h->part;
       a.SG = mean ? S : 1;
@@ -437,7 +480,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       const int b = tt / c.K1;
       const int64_t w1 = h->Hp * h->INp;
       BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
-                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, c.lr / (float)S};
+                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S};
       launch_block_update(s, a);
       return true;
     }
@@ -459,7 +502,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
         corr.gs = h->Gs;
         corr.k = tt % c.K1;
         corr.K1 = c.K1;
-        corr.lr = c.lr;
+        corr.lr = h->hyper;
       }
       const float* part = h->part;
       int64_t split = 0;
@@ -476,7 +519,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       // Under delayed updates the hidden errors are kept for the block end.
       float* g1 = h->in_delayed ? h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp : h->G1;
       launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, g1, h->y, ix, P, B, Bp,
-                    C, Cp, Hp, c.lr);
+                    C, Cp, Hp, h->hyper);
       return true;
     }
     case KC_REDUCE1:
@@ -496,7 +539,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
     case KC_UPDATE2: {
       if (small) return false;
       UpdArgs u{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
-                c.lr};
+                h->hyper};
       launch_update(s, u, A_RELU);
       return true;
     }
@@ -530,7 +573,7 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   auto go = [&](int kc) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
   if (!have_fwd) go(KC_FWD1);
   for (int i = 0; i < n; ++i) go(seq[i]);
-  const int T = c.K1 * c.K2;
+  const int T = h->T;
   const bool last = tt == T - 1;
   const bool mean = !last && (tt + 1) % c.K1 == 0 && c.S > 1;
   have_fwd = false;
@@ -580,6 +623,11 @@ hieravg_t hieravg_create_config(const hieravg_config* cfg) {
     return nullptr;
   }
   h->cfg = *cfg;
+  // Steps per round; K2 becomes the number of blocks (the last one shorter
+  // when K1 does not divide k_global).
+  h->T = cfg->k_global > 0 ? cfg->k_global : cfg->K1 * cfg->K2;
+  h->cfg.k_global = h->T;
+  h->cfg.K2 = (h->T + cfg->K1 - 1) / cfg->K1;
   if (build(h) != HIERAVG_OK) {
     std::string msg = g_last_error;
     release(h);
@@ -645,20 +693,17 @@ namespace {
 // Every kernel of one round, enqueued on the handle's stream.
 void enqueue_round(hieravg* h) {
   const hieravg_config& c = h->cfg;
-  const int T = c.K1 * c.K2;
+  const int T = h->T;
   const int P = c.P, S = c.S;
   if (c.kind == HIERAVG_KIND_AVERAGING) {
-    for (int b = 0; b < c.K2; ++b) {
-      for (int k = 0; k < c.K1; ++k) {
-        const int tt = b * c.K1 + k;
-        const bool end_block = k == c.K1 - 1, end_round = end_block && b == c.K2 - 1;
-        int kc = KC_MOMENTUM;
-        if (end_round && P > 1)
-          kc = KC_MOMENTUM_GLOBAL;
-        else if (end_block && !end_round && S > 1)
-          kc = KC_MOMENTUM_GROUP;
-        run(h, kc, [&] { launch_class(h, kc, tt); });
-      }
+    for (int tt = 0; tt < T; ++tt) {
+      const bool end_round = tt == T - 1, end_block = (tt + 1) % c.K1 == 0;
+      int kc = KC_MOMENTUM;
+      if (end_round && P > 1)
+        kc = KC_MOMENTUM_GLOBAL;
+      else if (end_block && !end_round && S > 1)
+        kc = KC_MOMENTUM_GROUP;
+      run(h, kc, [&] { launch_class(h, kc, tt); });
     }
   } else if (h->in_delayed) {
     // Delayed first-layer updates: per block, the forward of its K1 steps
@@ -704,6 +749,14 @@ int hieravg_round(hieravg_t h) {
   }
   // Delayed updates need every learner to start the round from replica 0's W1.
   h->in_delayed = h->delayed && h->w1_shared;
+  if (!h->in_delayed && h->rows_stale) {
+    // An eager round reads every replica's W1: copy replica 0's to the others.
+    const size_t w1 = sizeof(float) * h->Hp * h->INp;
+    for (int p = 1; p < h->cfg.P; ++p)
+      HAV_CHECK(hipMemcpyAsync(h->W + (int64_t)p * h->Dp + h->off_W1, h->W + h->off_W1, w1,
+                               hipMemcpyDeviceToDevice, h->stream));
+    h->rows_stale = false;
+  }
   if (h->profiling) {
     enqueue_round(h);
   } else {
@@ -727,7 +780,48 @@ int hieravg_round(hieravg_t h) {
   // After the global mean every learner holds replica 0's W1 (under delayed
   // updates only replica 0's copy is written).
   h->w1_shared = true;
-  h->steps += (int64_t)h->cfg.K1 * h->cfg.K2;
+  if (h->in_delayed) h->rows_stale = true;
+  h->steps += h->T;
+  return HIERAVG_OK;
+}
+
+int hieravg_set_batch(hieravg_t h, int32_t B) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  if (h->cfg.kind == HIERAVG_KIND_AVERAGING) {
+    set_error("the averaging-only workload has no minibatch");
+    return HIERAVG_EINVAL;
+  }
+  if (B < 1 || B > h->Bmax) {
+    set_error("B must be in [1, the minibatch size given at create]");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  h->cfg.B = B;
+  plan(h, B);
+  // The captured rounds carry the old launch shapes.
+  for (auto& e : h->round_exec)
+    if (e) {
+      (void)hipGraphExecDestroy(e);
+      e = nullptr;
+    }
+  return HIERAVG_OK;
+}
+
+int hieravg_set_lr(hieravg_t h, float lr) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  if (!std::isfinite(lr) || lr < 0.0f) {
+    set_error("lr must be finite and >= 0");
+    return HIERAVG_EINVAL;
+  }
+  h->cfg.lr = lr;
+  HAV_CHECK(hipMemcpyAsync(h->hyper, &h->cfg.lr, sizeof(float), hipMemcpyHostToDevice, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
 }
 
@@ -803,7 +897,7 @@ int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows
   // Replica `replica`; its first weight block lives in replica 0 while the
   // learners share it under delayed updates.
   const float* Wr = h->W + (int64_t)replica * h->Dp;
-  const float* W1r = (h->delayed && h->w1_shared ? h->W : Wr) + h->off_W1;
+  const float* W1r = (h->rows_stale ? h->W : Wr) + h->off_W1;
   double total = 0.0;
   int64_t hits = 0;
   std::vector<float> lh(chunk);
@@ -858,8 +952,8 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {
   for (int p = 0; p < P; ++p)
     for (size_t i = 0; i < segs.size(); ++i) {
       const Segment& g = segs[i];
-      // Under delayed updates only replica 0 holds the (common) W1.
-      const int64_t src_row = (i == 0 && h->delayed && h->w1_shared) ? 0 : p;
+      // After delayed updates only replica 0 holds the (common) W1.
+      const int64_t src_row = (i == 0 && h->rows_stale) ? 0 : p;
       HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
                                  h->W + src_row * h->Dp + g.src_off, sizeof(float) * g.src_ld,
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
@@ -886,6 +980,7 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
   HAV_CHECK(hipStreamSynchronize(h->stream));
   h->w1_shared = false;  // the rows may differ: the next round updates W1 eagerly
+  h->rows_stale = false;
   return HIERAVG_OK;
 }
 
@@ -916,9 +1011,9 @@ int hieravg_last_indices(hieravg_t h, int32_t* dst, size_t n) {
     set_error("the averaging-only workload draws no samples");
     return HIERAVG_EINVAL;
   }
-  const size_t need = (size_t)h->cfg.K1 * h->cfg.K2 * h->cfg.P * h->cfg.B;
+  const size_t need = (size_t)h->T * h->cfg.P * h->cfg.B;
   if (n < need) {
-    set_error("destination holds fewer than K2*K1*P*B indices");
+    set_error("destination holds fewer than T*P*B indices");
     return HIERAVG_ESIZE;
   }
   HAV_CHECK(hipStreamSynchronize(h->stream));

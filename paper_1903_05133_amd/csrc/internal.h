@@ -175,7 +175,7 @@ struct UpdArgs {
   int64_t w_pitch, ldw;
   float* bias;          // bias block of replica 0 (or nullptr); replica p at bias + p*w_pitch
   int P, Kb, Mrows, Ncols;
-  float lr;
+  const float* lr;      // device scalar: the step size (read at kernel start)
 };
 void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
 
@@ -195,7 +195,8 @@ struct BlkArgs {
   float* Wo;            // result of group g at Wo + g*wo_pitch (may equal the base)
   int64_t wo_pitch, ldw;
   int P, SG, K1, B, Mp, Mrows, Ncols;
-  float lr_eff;
+  const float* lr;      // device scalar step size; the mean takes lr / lr_div
+  float lr_div;
 };
 void launch_block_update(hipStream_t s, const BlkArgs& a);
 
@@ -242,7 +243,7 @@ struct HeadCorr {
   const float* gram = nullptr;  // [P][K1][K1][Bp][Bp] of the block (nullptr: none)
   const float* gs = nullptr;    // [K1][P][Bp][Hp] hidden errors of the block's steps
   int k = 0, K1 = 1;
-  float lr = 0.0f;
+  const float* lr = nullptr;    // device scalar step size
 };
 // part_split: floats between split-K partial sums (0: P * Mp * Hp).
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
@@ -250,7 +251,7 @@ void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, co
                    int64_t part_split = 0);
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
-                   int Cp, int Hp, float lr);
+                   int Cp, int Hp, const float* lr);
 
 // Per-row softmax cross-entropy and first-argmax hit of an evaluation chunk
 // from split-K logit partials part[ks][m][Cp] (split floats apart) and bias.
@@ -264,6 +265,6 @@ void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int 
 // dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4 floats).
 void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
-                          bool average, float lr, float mu);
+                          bool average, const float* lr, float mu);
 
 }  // namespace hav

@@ -36,8 +36,9 @@ __device__ inline void st_stream(f32x4* p, f32x4 v) { *p = v; }
 // updated row is written back as it is).
 template <bool MOM, bool MEAN, int RG, int NG, int TB>
 __global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __restrict__ V,
-                                             const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4, float lr,
-                                             float mu) {
+                                             const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4,
+                                             const float* __restrict__ lr_ptr, float mu) {
+  const float lr = MOM ? *lr_ptr : 0.0f;
   constexpr int S = RG * NG;
   constexpr int CPB = TB / NG;  // columns per workgroup
   __shared__ f32x4 part[NG > 1 ? NG : 1][CPB];
@@ -93,7 +94,8 @@ __global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __res
 template <bool MOM>
 __global__ __launch_bounds__(256) void k_rows_any(f32x4* __restrict__ W, f32x4* __restrict__ V,
                                                   const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4, int S,
-                                                  float lr, float mu) {
+                                                  const float* __restrict__ lr_ptr, float mu) {
+  const float lr = MOM ? *lr_ptr : 0.0f;
   const int64_t row0 = (int64_t)blockIdx.y * S;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
     f32x4 sum = {0.f, 0.f, 0.f, 0.f};
@@ -124,7 +126,7 @@ static unsigned col_runs(int64_t n4, int cpb, int groups) {
 
 template <bool MOM, bool MEAN, int RG, int NG, int TB = 256>
 static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
-                        float lr, float mu) {
+                        const float* lr, float mu) {
   dim3 grid(col_runs(n4, TB / NG, groups), (unsigned)groups);
   launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, p4, n4, lr, mu);
 }
@@ -142,7 +144,7 @@ static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int6
 #endif
 template <bool MOM, int S>
 static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
-                     float lr, float mu) {
+                     const float* lr, float mu) {
   constexpr int kR = S <= 16 ? HAV_AVG_RG : HAV_AVG_RG_BIG;
   constexpr int RG = S < kR ? S : kR;
   constexpr int TB = S <= 16 ? 256 : HAV_AVG_TB_BIG;
@@ -151,7 +153,7 @@ static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t
 
 template <bool MOM>
 static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int P,
-                             int S, float lr, float mu) {
+                             int S, const float* lr, float mu) {
   const int groups = P / S;
   switch (S) {
     case 2: launch_s<MOM, 2>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
@@ -166,9 +168,9 @@ static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr,
 
 void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S) {
   const int64_t p4 = pitch / 4, n4 = len / 4;
-  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, p4, n4, P, S, 0.0f, 0.0f)) return;
+  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, p4, n4, P, S, nullptr, 0.0f)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, 0.0f, 0.0f);
+  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, (const float*)nullptr, 0.0f);
 }
 
 __global__ __launch_bounds__(256) void k_mean_rows(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
@@ -186,7 +188,7 @@ void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch
 }
 
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
-                          bool average, float lr, float mu) {
+                          bool average, const float* lr, float mu) {
   const int64_t n4 = Dp / 4;
   if (!average) {
     launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, n4, P, lr, mu);

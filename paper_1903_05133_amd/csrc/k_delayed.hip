@@ -326,12 +326,13 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     }
   __syncthreads();
   float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
+  const float lr_eff = *a.lr / a.lr_div;
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {
     const int rl = xr0 + kXR * i, row = mrow0 + rl;
     if (xcol_ok && row < a.Mrows) {
       const f32x4 gsum = *(const f32x4*)&Gt[rl * kLB + 4 * xc4];
-      *(f32x4*)(Wo + (int64_t)row * a.ldw + xcol) = wv[i] - a.lr_eff * gsum;
+      *(f32x4*)(Wo + (int64_t)row * a.ldw + xcol) = wv[i] - lr_eff * gsum;
     }
   }
 }

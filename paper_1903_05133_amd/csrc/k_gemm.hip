@@ -384,7 +384,7 @@ __global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int nt
         Gt[row * kLB + wn + 32 * j + l32] = acc[i][j][r];
       }
   __syncthreads();
-  const float lr = a.lr;
+  const float lr = *a.lr;
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {
     const int rl = wr0 + kXR * i, row = mrow0 + rl;
@@ -399,7 +399,7 @@ __global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int nt
     if (m < a.Mrows) {
       float sum = 0.0f;
       for (int s = 0; s < a.Kb; ++s) sum += Gp[(int64_t)s * a.ldg + m];
-      a.bias[(int64_t)p * a.w_pitch + m] -= a.lr * sum;
+      a.bias[(int64_t)p * a.w_pitch + m] -= lr * sum;
     }
   }
 }
@@ -486,7 +486,7 @@ __global__ __launch_bounds__(256) void k_step_w1(StepArgs a, int mtiles, int nti
   const int pc4 = tid % kSP, pr0 = tid / kSP;            // 16-byte piece of tile-wide rows
   const bool fwd_on = mrow0 + 16 * wave < u.Mrows;       // forward: the wave's 16 rows of W
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-  const float lr = u.lr;
+  const float lr = *u.lr;
   const int Kb = u.Kb;
 
   for (int e = tid; e < SG * Kb; e += 256) {

@@ -216,7 +216,7 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
 #pragma unroll
           for (int i = 0; i < 4; ++i) c += g[i] * *(const f32x4*)&gsl[k2][s2 + i][4 * u4];
         }
-      z -= corr.lr * c;
+      z -= *corr.lr * c;
     }
     if (mok) *(f32x4*)(Z1 + ((int64_t)p * Mp + m) * Hp + h4) = z;
     zs[rr][4 * u4 + 0] = mok ? fmaxf(z.x, 0.0f) : 0.0f;
@@ -250,7 +250,9 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
                                                 float* __restrict__ b1, float* __restrict__ b2, int64_t w_pitch,
                                                 const float* __restrict__ Z1, float* __restrict__ G1,
                                                 const int32_t* __restrict__ labels, const int32_t* __restrict__ idx,
-                                                int P, int M, int Mp, int C, int Cp, int Hp, int htiles, float lr) {
+                                                int P, int M, int Mp, int C, int Cp, int Hp, int htiles,
+                                                const float* __restrict__ lr_ptr) {
+  const float lr = *lr_ptr;
   constexpr int kG = 256 / kHU;     // sample groups
   constexpr int kR = kHM / kG;      // samples per thread per chunk
   __shared__ float gs[kHM][KC + 1];
@@ -429,7 +431,7 @@ void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, co
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
-                   int Cp, int Hp, float lr) {
+                   int Cp, int Hp, const float* lr) {
   const int htiles = Hp / kHU;
   if (C <= 16)
     launch(k_head_b<16>, P * htiles, 256, 0, s, PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,

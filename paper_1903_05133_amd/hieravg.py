@@ -31,6 +31,7 @@ class HierAvg:
         self.K1 = K1 if config is None else config.K1
         self.K2 = K2 if config is None else config.K2
         self.B = B if config is None else config.B
+        self.T = self.K1 * self.K2 if config is None or config.k_global == 0 else config.k_global
         self.D = int(L.hieravg_dim(h))
 
     # -------------------------------------------------------------- lifecycle
@@ -85,6 +86,15 @@ class HierAvg:
             a = np.ascontiguousarray(arr, dtype=np.float32)
             native.check(native.lib().hieravg_set_params(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
 
+    def set_batch(self, B):
+        """Minibatch size of the rounds that follow (at most the B at create)."""
+        native.check(native.lib().hieravg_set_batch(self._h, B))
+        self.B = B
+
+    def set_lr(self, lr):
+        """Step size of the rounds that follow."""
+        native.check(native.lib().hieravg_set_lr(self._h, lr))
+
     def evaluate(self, replica=0, split=1, n_rows=4096):
         """(mean cross-entropy, correct count) of replica `replica` on
         `n_rows` training (split 0) or held-out (split 1) rows."""
@@ -95,7 +105,10 @@ class HierAvg:
         return loss.value, correct.value
 
     def last_indices(self):
-        out = np.empty((self.K2, self.K1, self.P, self.B), dtype=np.int32)
+        """Indices of the last round: [K2, K1, P, B], or [T, P, B] when the
+        round length T is not K1 * K2."""
+        shape = (self.K2, self.K1, self.P, self.B) if self.T == self.K1 * self.K2 else (self.T, self.P, self.B)
+        out = np.empty(shape, dtype=np.int32)
         native.check(native.lib().hieravg_last_indices(self._h, ctypes.c_void_p(out.ctypes.data), out.size))
         return out
 
@@ -129,7 +142,7 @@ class HierAvg:
 
 
 def config(kind, P, S, K1, K2, B=1, in_dim=0, hidden=0, classes=0, n_samples=0, noise_std=1.0, lr=0.05,
-           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0, update_mode=0):
+           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0, update_mode=0, k_global=0):
     return native.Config(P=P, S=S, K1=K1, K2=K2, B=B, kind=kind, in_dim=in_dim, hidden=hidden, classes=classes,
                          n_samples=n_samples, noise_std=noise_std, lr=lr, momentum=momentum, init_std=init_std,
-                         grad_std=grad_std, seed=seed, update_mode=update_mode)
+                         grad_std=grad_std, seed=seed, update_mode=update_mode, k_global=k_global)

@@ -22,6 +22,7 @@ class Config(ctypes.Structure):
         ("init_std", ctypes.c_float), ("grad_std", ctypes.c_float),
         ("seed", ctypes.c_uint64),
         ("update_mode", ctypes.c_int32),
+        ("k_global", ctypes.c_int32),
     ]
 
 
@@ -35,6 +36,8 @@ SIGNATURES = {
     "hieravg_params": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_set_params": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_destroy": (None, [_H]),
+    "hieravg_set_lr": (ctypes.c_int, [_H, ctypes.c_float]),
+    "hieravg_set_batch": (ctypes.c_int, [_H, ctypes.c_int32]),
     "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "hieravg_last_error": (ctypes.c_char_p, []),

@@ -332,3 +332,74 @@ def test_convergence_runner(gpu_lib):
     assert [x["steps"] for x in per_round] == [4, 8, 12]
     assert per_round[-1]["train_loss"] < per_round[0]["train_loss"]
     assert 0.0 <= summ["final_test_acc"] <= 1.0
+
+
+def _schedule_run(c, schedule, mode="auto"):
+    """Rounds with a per-round (lr, B) schedule through set_lr / set_batch,
+    and the oracle's rounds with the same Problem changed per round."""
+    import dataclasses
+    from paper_1903_05133_amd import HierAvg
+    prob = cases.oracle_problem(c)
+    mon = M.KinkMonitor(prob.H) if prob.kind == M.MLP else None
+    st = M.create(prob)
+    data = M.Dataset(prob) if prob.kind != M.AVERAGING else None
+    print(f"[gpu case] schedule {mode} {schedule} {c}", flush=True)
+    with HierAvg(config=cases.native_config(c, mode)) as h:
+        for lr, B in schedule:
+            h.set_lr(lr)
+            if prob.kind != M.AVERAGING:
+                h.set_batch(B)
+            h.round()
+            pr = dataclasses.replace(prob, lr=lr, B=B)
+            M.hieravg_round(pr, st, data, mon)
+            got = h.params()
+            if prob.kind != M.AVERAGING:
+                assert np.array_equal(h.last_indices().astype(np.int64), st.last_indices)
+            assert np.array_equal(got, np.repeat(got[:1], got.shape[0], axis=0))
+            ok, det = cases.parity_report(pr, got, st.W, mon)
+            print(f"[gpu case] lr={lr} B={B} worst {det['worst']}", flush=True)
+            assert ok, det
+        assert h.steps == len(schedule) * prob.T
+
+
+@pytest.mark.parametrize("mode", ["auto", "eager"])
+def test_lr_schedule_matches_oracle(mode, gpu_lib):
+    c = cases.case("mlp", 4, 2, 2, 2, B=12, IN=150, H=70, C=6, N=200, sigma=0.5, lr=0.1, seed=21)
+    _schedule_run(c, [(0.1, 12), (0.05, 12), (0.02, 12)], mode)
+
+
+def test_lr_schedule_softmax_and_momentum(gpu_lib):
+    c = cases.case("softmax", 4, 2, 2, 1, B=10, IN=90, C=7, N=100, lr=0.2, seed=22)
+    _schedule_run(c, [(0.2, 10), (0.07, 10)], "auto")
+    c = cases.case("averaging", 4, 2, 2, 2, IN=777, lr=0.1, momentum=0.9, seed=23)
+    _schedule_run(c, [(0.1, 1), (0.03, 1)], "auto")
+
+
+def test_batch_schedule_switches_update_modes(gpu_lib):
+    """B = 40 updates eagerly (beyond the delayed path's 32), B = 16 and 9
+    take delayed updates; each switch back to eager first copies replica 0's
+    common first layer to every learner.  Indices: the first B draws of a
+    step do not depend on B."""
+    c = cases.case("mlp", 4, 2, 2, 2, B=40, IN=150, H=70, C=6, N=300, sigma=0.5, lr=0.05, seed=24)
+    _schedule_run(c, [(0.05, 40), (0.05, 16), (0.05, 40), (0.05, 9), (0.05, 16), (0.05, 33)], "auto")
+
+
+K_GLOBAL_CASES = {
+    "mlp_T5_K1_2": cases.case("mlp", 4, 2, 2, 1, B=8, IN=100, H=70, C=5, N=200, sigma=0.5, lr=0.1, seed=25,
+                              k_global=5),
+    "mlp_T7_K1_3_S4": cases.case("mlp", 8, 4, 3, 1, B=6, IN=64, H=40, C=3, N=90, sigma=0.5, lr=0.1, seed=26,
+                                 k_global=7),
+    "softmax_T3_K1_2": cases.case("softmax", 4, 4, 2, 1, B=5, IN=40, C=4, N=50, lr=0.2, seed=27, k_global=3),
+    "averaging_T5_K1_2": cases.case("averaging", 4, 2, 2, 1, IN=999, lr=0.1, momentum=0.9, seed=28, k_global=5),
+}
+
+
+@pytest.mark.parametrize("name", sorted(K_GLOBAL_CASES))
+def test_global_interval_not_multiple_of_k1(name, gpu_lib):
+    """A round of k_global steps with a shorter last block (non-integer beta)."""
+    c = K_GLOBAL_CASES[name]
+    got, idx, steps = _run_gpu(c, rounds=2)
+    assert steps == 2 * c["k_global"]
+    if idx is not None:
+        assert idx.shape == (c["k_global"], c["P"], c["B"])
+    _check(c, got, idx, *_oracle(c, 2))

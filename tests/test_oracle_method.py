@@ -337,3 +337,38 @@ def test_held_out_rows_recipe():
     mu = rng.class_means(seed, np.arange(C), IN)
     assert y1[i] == rng.h_scalar(rng.stream_key(seed, rng.TAG_TEST_LABEL), i) % C
     assert X1[i, d] == float(np.float32(mu[y1[i], d] + sigma * z))
+
+
+# ------------------------------------------------ generalised global interval
+@pytest.mark.parametrize("kind", [M.SOFTMAX, M.MLP])
+def test_global_interval_in_steps_with_s_one_is_kavg(kind):
+    """S = 1 with a global interval of T = 5 steps and K1 = 2 (a non-integer
+    beta): local means are identities, so a round is K-AVG with K = 5
+    (torch.optim.SGD per learner, then the mean)."""
+    p = small(kind, 3, 1, 2, 1, k_global=5)
+    st = M.run(p, 2)
+    want = kavg_reference(p, 5, 2)
+    for j in range(p.P):
+        assert relerr(st.W[j], want) < 1e-12
+
+
+def test_global_interval_in_steps_with_s_equal_p():
+    """S = P, K1 = 2, T = 5: the local mean is the global mean, so a round is
+    K-AVG rounds of 2, 2 and 1 steps (each ends with the mean of all P)."""
+    p = small(M.MLP, 3, 3, 2, 1, k_global=5)
+    st = M.run(p, 1)
+    w = M.initial_replica(p)
+    t = 0
+    for K in (2, 2, 1):
+        rows = [torch_sgd_run(p, w, j, t, K) for j in range(p.P)]
+        w = np.mean(rows, axis=0)
+        t += K
+    for j in range(p.P):
+        assert relerr(st.W[j], w) < 1e-12
+
+
+def test_global_interval_equal_to_blocks_is_the_block_round():
+    """T = K1 * K2 given as a step count reproduces the block round bit for bit."""
+    a = M.run(small(M.MLP, 4, 2, 2, 3), 1)
+    b = M.run(small(M.MLP, 4, 2, 2, 3, k_global=6), 1)
+    assert np.array_equal(a.W, b.W) and np.array_equal(a.last_indices, b.last_indices)
