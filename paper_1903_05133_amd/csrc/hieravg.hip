@@ -43,7 +43,7 @@ const char* kClassNames[KC_COUNT] = {
     "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
-    "w1_global_mean", "tail_global_mean", "gram_reduce"};
+    "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -340,7 +340,7 @@ int build(hieravg* h) {
     if ((rc = alloc_zero(h, (void**)&h->part, sizeof(float) * part_floats, "split-K partials"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->G2, sizeof(float) * P * h->Bp * h->Cp, "output error"))) return rc;
     if (mlp && h->C <= kSmallC &&
-        (rc = alloc_zero(h, (void**)&h->PL, sizeof(float) * P * (h->Hp / 32) * h->Bp * h->Cp, "partial logits")))
+        (rc = alloc_zero(h, (void**)&h->PL, sizeof(float) * 2 * P * (h->Hp / 32) * h->Bp * h->Cp, "partial logits")))
       return rc;
     if (mlp) {
       if ((rc = alloc_zero(h, (void**)&h->Z1, sizeof(float) * P * h->Bp * h->Hp, "hidden activations"))) return rc;
@@ -510,8 +510,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
         part += (int64_t)(tt % c.K1) * P * Bp * Hp;
         split = (int64_t)c.K1 * P * Bp * Hp;
       }
-      launch_head_a(s, part, h->ks_cur, W + h->off_b1, W + h->off_W2, h->Dp, h->Z1, h->PL, P, B, Bp, C, Cp, Hp,
-                    corr, split);
+      launch_head_a(s, part, h->ks_cur, W + h->off_b1, W + h->off_W2, W + h->off_b2, h->Dp, h->Z1, h->PL, P, B,
+                    Bp, C, Cp, Hp, corr, split);
       return true;
     }
     case KC_HEAD_B: {
@@ -520,6 +520,42 @@ bool launch_class(hieravg* h, int kc, int tt) {
       float* g1 = h->in_delayed ? h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp : h->G1;
       launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, g1, h->y, ix, P, B, Bp,
                     C, Cp, Hp, h->hyper);
+      return true;
+    }
+    case KC_HEAD_STEP:
+    case KC_HEAD_END: {
+      if (!h->in_delayed) return false;
+      // HEAD_STEP at step tt: backward of step tt-1 of the block (if any),
+      // forward and output error of step tt; HEAD_END at a block's last step
+      // tt: its backward.
+      const int k = kc == KC_HEAD_END ? c.K1 : tt % c.K1;
+      const int blk = tt / c.K1;
+      HeadStepArgs a{};
+      a.part = h->part + (int64_t)(k < c.K1 ? k : 0) * P * Bp * Hp;
+      a.KS = h->ks_cur;
+      a.split = (int64_t)c.K1 * P * Bp * Hp;
+      a.W2 = W + h->off_W2;
+      a.b1 = W + h->off_b1;
+      a.b2 = W + h->off_b2;
+      a.w_pitch = h->Dp;
+      a.Z1 = h->Z1;
+      a.PL = h->PL;
+      a.pl_half = (int64_t)P * (Hp / 32) * Bp * Cp;
+      a.gs = h->Gs;
+      a.gram = h->gram ? h->gram + (int64_t)blk * P * c.K1 * c.K1 * Bp * Bp : nullptr;
+      a.labels = h->y;
+      // the previous step's indices (HEAD_END: this step's, the block's last)
+      a.idx_prev = kc == KC_HEAD_END ? ix : ix - (int64_t)P * B;
+      a.lr = h->hyper;
+      a.P = P;
+      a.M = B;
+      a.Mp = Bp;
+      a.C = C;
+      a.Cp = Cp;
+      a.Hp = Hp;
+      a.K1 = c.K1;
+      a.k = k;
+      launch_head_step(s, a);
       return true;
     }
     case KC_REDUCE1:
@@ -720,11 +756,8 @@ void enqueue_round(hieravg* h) {
     }
     for (int b = 0; b < c.K2; ++b) {
       go(KC_FWD1_BLOCK, b * c.K1);
-      for (int k = 0; k < c.K1; ++k) {
-        const int tt = b * c.K1 + k;
-        go(KC_HEAD_A, tt);
-        go(KC_HEAD_B, tt);
-      }
+      for (int k = 0; k < c.K1; ++k) go(KC_HEAD_STEP, b * c.K1 + k);
+      go(KC_HEAD_END, b * c.K1 + c.K1 - 1);
       go(KC_BLOCK_UPDATE, b * c.K1);
       if (b < c.K2 - 1 && S > 1) go(KC_TAIL_MEAN, 0);
     }

@@ -95,6 +95,8 @@ enum KernelClass {
   KC_W1_MEAN,        // delayed updates: global mean of the cluster copies
   KC_TAIL_GLOBAL,    // global mean of the parameters after layer 1
   KC_GRAM_REDUCE,    // delayed updates: sum of the Gram blocks' feature splits
+  KC_HEAD_STEP,      // delayed updates: backward of step k-1 + forward and loss gradient of step k
+  KC_HEAD_END,       // delayed updates: backward of a block's last step
   KC_COUNT
 };
 
@@ -246,12 +248,38 @@ struct HeadCorr {
   const float* lr = nullptr;    // device scalar step size
 };
 // part_split: floats between split-K partial sums (0: P * Mp * Hp).
-void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr(),
+void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
+                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr(),
                    int64_t part_split = 0);
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, const float* lr);
+
+// One launch per local step of the delayed schedule (C <= 32, M <= 32, K1 <= 8):
+// workgroup (p, slice of 32 hidden units) finishes step k-1's backward for its
+// units (logits from every slice's partial logits, softmax gradient, hidden
+// error into gs[k-1], SGD steps of b1, W2 and, on slice 0, b2) and runs step
+// k's forward for them (pre-activations with the Gram correction, partial
+// logits).  k = 0: forward only; k = K1: backward of the block's last step.
+struct HeadStepArgs {
+  const float* part;      // step k's layer-1 split-K partials (split floats apart)
+  int KS;
+  int64_t split;
+  float* W2;              // replica 0's second weight block; replica p at + p*w_pitch
+  float* b1;
+  float* b2;
+  int64_t w_pitch;
+  float* Z1;              // [P][Mp][Hp] pre-activations of the current step
+  float* PL;              // [2][P][Mp][Cp][Hp/32] partial logits (step parity)
+  int64_t pl_half;        // floats per parity
+  float* gs;              // [K1][P][Mp][Hp] hidden errors of the block's steps
+  const float* gram;      // [P][K1][K1][Mp][Mp] of the block
+  const int32_t* labels;  // dataset labels
+  const int32_t* idx_prev;  // [P][M] sample indices of step k-1
+  const float* lr;        // device scalar step size
+  int P, M, Mp, C, Cp, Hp, K1, k;
+};
+void launch_head_step(hipStream_t s, const HeadStepArgs& a);
 
 // Per-row softmax cross-entropy and first-argmax hit of an evaluation chunk
 // from split-K logit partials part[ks][m][Cp] (split floats apart) and bias.

@@ -219,10 +219,11 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     bool gok[kGL], xok[kXL];
   };
   StageRegs RA, RB;
-  // Sample indices are loaded one stage before the rows they select, so the
-  // loads of a stage never wait for another load issued with them.
-  int32_t xrow[kXL];
-  auto load_idx = [&](int st) {
+  // Sample indices are loaded two stages before the rows they select (two
+  // sets, even and odd stages): loads complete in issue order, so waiting for
+  // an index then waits only for loads the previous stage already needed.
+  int32_t xrowA[kXL], xrowB[kXL];
+  auto load_idx = [&](int st, int32_t (&xrow)[kXL]) {
     const int s0 = (st < nst ? st : nst - 1) * kSC;
 #pragma unroll
     for (int i = 0; i < kXL; ++i) {
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
       xrow[i] = a.idx[irow];
     }
   };
-  auto load_stage = [&](int st, StageRegs& q) {
+  auto load_stage = [&](int st, StageRegs& q, const int32_t (&xrow)[kXL]) {
     const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
 #pragma unroll
     for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
@@ -281,13 +282,37 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     }
   };
 
-  load_idx(0);
-  load_stage(0, RA);
-  load_idx(1);
-  load_stage(1, RB);
-  load_idx(2);
-  __builtin_amdgcn_sched_barrier(0);
-  // Base tile (16-byte pieces, thread t: column piece t%kXP of rows t/kXP + kXR*i).
+  load_idx(0, xrowA);
+  load_idx(1, xrowB);
+  load_stage(0, RA, xrowA);
+  load_idx(2, xrowA);
+  load_stage(1, RB, xrowB);
+  load_idx(3, xrowB);
+  store_stage(0, RA);
+  __syncthreads();
+  // Iteration st: loads of stage st+2 and indices of stage st+4 go out, the
+  // MFMAs of stage st (LDS buffer st&1) run, stage st+1 goes to the other
+  // buffer.  Unrolled by two so each register set is named statically.
+  for (int st = 0; st < nst; st += 2) {
+    load_stage(st + 2, RA, xrowA);
+    load_idx(st + 4, xrowA);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(0);
+    store_stage(1, RB);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    load_stage(st + 3, RB, xrowB);
+    load_idx(st + 5, xrowB);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(1);
+    store_stage(0, RA);
+    __syncthreads();
+  }
+
+  // Base tile (16-byte pieces, thread t: column piece t%kXP of rows t/kXP +
+  // kXR*i), loaded only now so that its registers are free during the
+  // contraction (three workgroups per CU); its latency overlaps the
+  // accumulator transfer to LDS.
   constexpr int kWL = kUM / kXR;
   const float* Wb = a.Wb + (int64_t)g * a.wb_pitch;
   f32x4 wv[kWL];
@@ -296,27 +321,6 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     const int row = mrow0 + xr0 + kXR * i;
     wv[i] = *(const f32x4*)(Wb + (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
   }
-  store_stage(0, RA);
-  __syncthreads();
-  // Iteration st: loads of stage st+2 and indices of stage st+3 go out, the
-  // MFMAs of stage st (LDS buffer st&1) run, stage st+1 goes to the other
-  // buffer.  Unrolled by two so each register set is named statically.
-  for (int st = 0; st < nst; st += 2) {
-    load_stage(st + 2, RA);
-    load_idx(st + 3);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_stage(0);
-    store_stage(1, RB);
-    __syncthreads();
-    if (st + 1 >= nst) break;
-    load_stage(st + 3, RB);
-    load_idx(st + 4);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_stage(1);
-    store_stage(0, RA);
-    __syncthreads();
-  }
-
 #pragma unroll
   for (int j = 0; j < kNA; ++j)
 #pragma unroll

@@ -142,7 +142,8 @@ constexpr int kHM = 32;  // samples per chunk
 
 // Z1 = b1 + sum of the layer-1 partials (stored for k_head_b and the ReLU
 // masks), and this slice's partial logits
-//   PL[p][m][c][ht] = sum_{h in slice} ReLU(Z1[m][h]) * W2[c][h].
+//   PL[p][m][c][ht] = [ht == 0] b2[c] + sum_{h in slice} ReLU(Z1[m][h]) * W2[c][h]
+// (b2 is folded into slice 0's, so k_head_b never reads the b2 it updates).
 // Thread t reads 16-byte pieces (units 4*(t%8) .. +3) of row t/8 of the chunk.
 // With delayed first-layer updates (corr.gram set) the pre-activations also
 // take the correction -lr * sum_{k2<k} gram[k][k2] G[k2] of the learner's
@@ -151,7 +152,8 @@ constexpr int kHM = 32;  // samples per chunk
 constexpr int kCorrMaxK = 7;  // earlier steps in a block (K1 <= 8)
 template <int KC>
 __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, int KS, const float* __restrict__ b1,
-                                                const float* __restrict__ W2, int64_t w_pitch,
+                                                const float* __restrict__ W2, const float* __restrict__ b2,
+                                                int64_t w_pitch,
                                                 float* __restrict__ Z1, float* __restrict__ PL, int P, int M, int Mp,
                                                 int C, int Cp, int Hp, int htiles, HeadCorr corr,
                                                 int64_t split) {
@@ -227,7 +229,7 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
 #pragma unroll
     for (int k = 0; k < kHM * KC / 256; ++k) {
       const int e = tid + 256 * k, mm = e / KC, c = e % KC;
-      float acc = 0.0f;
+      float acc = ht == 0 && c < C ? b2[(int64_t)p * w_pitch + c] : 0.0f;
 #pragma unroll
       for (int hh = 0; hh < kHU; ++hh) acc += zs[mm][hh] * ws[c][hh];
       if (m0 + mm < M && c < C) PL[(((int64_t)p * Mp + m0 + mm) * Cp + c) * htiles + ht] = acc;
@@ -236,8 +238,8 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
   }
 }
 
-// Per 32-sample chunk: the logits of each sample (b2 + the slices' partial
-// logits, added in slice order), its softmax cross-entropy gradient
+// Per 32-sample chunk: the logits of each sample (the slices' partial logits,
+// b2 included, added in slice order), its softmax cross-entropy gradient
 // G2 = (softmax - onehot) / M (kept in LDS), then for this slice of units the
 // hidden error G1 = (G2 W2)[m][h] * [Z1 > 0] (W2[:, h] held in registers)
 // and the gradients of b1[h] and W2[:, h].  Thread (u = t%32, g = t/32) owns
@@ -262,7 +264,6 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
   const int tid = threadIdx.x, u = tid % kHU, g = tid / kHU;
   const int h = ht * kHU + u;
   float* w2 = W2 + (int64_t)p * w_pitch;
-  const float* bb2 = b2 + (int64_t)p * w_pitch;
   float wc[KC];
 #pragma unroll
   for (int c = 0; c < KC; ++c) {
@@ -289,7 +290,7 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
       const int e = tid + 256 * k, mm = e / KC, c = e % KC;
       const bool ok = mm < mn && c < C;
       const float* pl = PL + (((int64_t)p * Mp + m0 + (mm < mn ? mm : 0)) * Cp + (c < C ? c : 0)) * htiles;
-      float l = bb2[c < C ? c : 0];
+      float l = 0.0f;
 #pragma unroll 8
       for (int t = 0; t < htiles; ++t) l += pl[t];
       gs[mm][c] = ok ? l : 0.0f;
@@ -346,6 +347,223 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
       }
   }
   if (ht == 0 && tid < C) b2[(int64_t)p * w_pitch + tid] -= lr * db2;
+}
+
+// Fused head of the delayed schedule (HeadStepArgs).  Workgroup (p, ht) owns
+// hidden units h = 32*ht + u of learner p; M <= 32 samples, one chunk.
+//  (A) k > 0, the rest of step k-1: logits of every sample from the partial
+//      logits of all slices (b2 is folded into slice 0's), its softmax
+//      cross-entropy gradient G2 (mean over the minibatch), then for this
+//      slice, with thread (u = t%32, g = t/32) taking samples g + 8i:
+//      G1 = (G2 W2)[m][h] * [Z1 > 0] into gs[k-1] and into LDS for (B); the
+//      eight sample groups' sums give the steps of b1[h] and W2[:, h] (the
+//      new values stay in LDS for (B)); slice 0 steps b2.
+//  (B) k < K1, step k: Z1 = b1 + sum of the split-K partials
+//      - lr * sum_{k2<k} gram[k][k2] G1[k2] for this slice, its ReLU, and the
+//      slice's partial logits into PL[k&1] (slice 0 adds b2).
+// (A) reads PL[(k-1)&1] of every slice while (B) writes PL[k&1], and b2 is
+// read and written by slice 0 only, so no workgroup depends on another
+// within a launch.
+template <int KC>
+__global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
+  constexpr int kG = 256 / kHU, kR = kHM / kG;
+  constexpr int kGsl = kCorrMaxK * kHM * kHU;                 // G1 slices of the block's steps
+  constexpr int kPhaseB = kCorrMaxK * kHM * (kHM + 4) + kHM * (kHU + 1);
+  constexpr int kPhaseA = kHM * (KC + 1) + kG * (KC + 1) * kHU;
+  constexpr int kRegion = kPhaseA > kPhaseB ? kPhaseA : kPhaseB;
+  __shared__ __attribute__((aligned(16))) float lds[kGsl + kRegion + KC * (kHU + 1) + kHU + KC];
+  __shared__ int ys[kHM];
+  auto gsl = [&](int k2, int s, int u) -> float& { return lds[(k2 * kHM + s) * kHU + u]; };
+  float* region = lds + kGsl;
+  float* ws = region + kRegion;     // [KC][kHU + 1] W2 slice (after (A))
+  float* bs = ws + KC * (kHU + 1);  // [kHU] b1 slice (after (A))
+  float* b2l = bs + kHU;            // [KC] b2 (slice 0, after (A))
+
+  const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
+  const int tid = threadIdx.x;
+  const int M = a.M, C = a.C, Cp = a.Cp, Hp = a.Hp, Mp = a.Mp;
+  const float lr = *a.lr;
+  float* w2 = a.W2 + (int64_t)p * a.w_pitch;
+  float* b1 = a.b1 + (int64_t)p * a.w_pitch;
+  float* b2 = a.b2 + (int64_t)p * a.w_pitch;
+
+  // Step k's partial sums are independent of (A): their loads go out first.
+  const int u4 = tid & 7, rr = tid >> 3;
+  const int h4 = ht * kHU + 4 * u4;
+  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  if (a.k < a.K1) {
+    const float* pm = a.part + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+#pragma unroll 8
+    for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
+  }
+
+  if (a.k > 0) {  // (A): the rest of step k-1
+    const int kp = a.k - 1;
+    const int u = tid % kHU, g = tid / kHU, h = ht * kHU + u;
+    float* g2s = region;                   // [kHM][KC + 1]
+    float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
+    if (tid < kHM) ys[tid] = a.labels[a.idx_prev[(int64_t)p * M + (tid < M ? tid : 0)]];
+    float wc[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const float v = w2[(int64_t)(c < C ? c : 0) * Hp + h];
+      wc[c] = c < C ? v : 0.0f;
+    }
+    float zp[kR];
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      const int mm = g + kG * i;
+      const float v = a.Z1[((int64_t)p * Mp + (mm < M ? mm : 0)) * Hp + h];
+      zp[i] = mm < M ? v : 0.0f;
+    }
+    const float b1h = b1[h];
+    const float* plp = a.PL + (int64_t)(kp & 1) * a.pl_half;
+#pragma unroll
+    for (int q = 0; q < kHM * KC / 256; ++q) {
+      const int e = tid + 256 * q, mm = e / KC, c = e % KC;
+      const bool ok = mm < M && c < C;
+      const float* pl = plp + (((int64_t)p * Mp + (ok ? mm : 0)) * Cp + (ok ? c : 0)) * htiles;
+      float l = 0.0f;
+#pragma unroll 8
+      for (int t = 0; t < htiles; ++t) l += pl[t];
+      g2s[mm * (KC + 1) + c] = ok ? l : 0.0f;
+    }
+    __syncthreads();
+    if (tid < M) {
+      float* row = g2s + tid * (KC + 1);
+      float mx = -INFINITY;
+      for (int c = 0; c < C; ++c) mx = fmaxf(mx, row[c]);
+      float sum = 0.0f;
+      for (int c = 0; c < C; ++c) {
+        const float e = expf(row[c] - mx);
+        row[c] = e;
+        sum += e;
+      }
+      const int y = ys[tid];
+      const float invB = 1.0f / (float)M;
+      for (int c = 0; c < C; ++c) row[c] = (row[c] / sum - (c == y ? 1.0f : 0.0f)) * invB;
+    }
+    __syncthreads();
+    float db1 = 0.0f, db2 = 0.0f;
+    float dw2[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) dw2[c] = 0.0f;
+    float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + h;
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      const int mm = g + kG * i;
+      float g1 = 0.0f;
+      if (mm < M) {
+        const float act = fmaxf(zp[i], 0.0f);
+        float da = 0.0f;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) da += g2s[mm * (KC + 1) + c] * wc[c];
+        g1 = zp[i] > 0.0f ? da : 0.0f;
+        g1out[(int64_t)mm * Hp] = g1;
+        db1 += g1;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) dw2[c] += g2s[mm * (KC + 1) + c] * act;
+      }
+      if (a.k < a.K1) gsl(kp, mm, u) = g1;  // for (B) (k-1 <= K1-2 < kCorrMaxK)
+    }
+    if (ht == 0 && tid < C)
+      for (int mm = 0; mm < M; ++mm) db2 += g2s[mm * (KC + 1) + tid];
+    red[(g * (KC + 1) + KC) * kHU + u] = db1;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) red[(g * (KC + 1) + c) * kHU + u] = dw2[c];
+    __syncthreads();
+    if (g == 0) {
+      float sb = 0.0f;
+#pragma unroll
+      for (int q = 0; q < kG; ++q) sb += red[(q * (KC + 1) + KC) * kHU + u];
+      const float nb = b1h - lr * sb;
+      b1[h] = nb;
+      bs[u] = nb;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        float gsum = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kG; ++q) gsum += red[(q * (KC + 1) + c) * kHU + u];
+        const float nw = wc[c] - lr * gsum;
+        if (c < C) w2[(int64_t)c * Hp + h] = nw;
+        ws[c * (kHU + 1) + u] = c < C ? nw : 0.0f;
+      }
+    }
+    if (ht == 0 && tid < KC) {
+      const float nb2 = tid < C ? b2[tid] - lr * db2 : 0.0f;
+      if (tid < C) b2[tid] = nb2;
+      b2l[tid] = nb2;
+    }
+    __syncthreads();
+  } else {
+    for (int e = tid; e < KC * kHU; e += 256) {
+      const int c = e / kHU, hh = e % kHU;
+      const float v = w2[(int64_t)(c < C ? c : 0) * Hp + ht * kHU + hh];
+      ws[c * (kHU + 1) + hh] = c < C ? v : 0.0f;
+    }
+    if (tid < kHU) bs[tid] = b1[ht * kHU + tid];
+    if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2[tid] : 0.0f;
+  }
+  if (a.k >= a.K1) return;
+
+  // (B): step k's forward for this slice.
+  float* grl = region;                               // [kCorrMaxK][kHM][kHM + 4]
+  float* zs = region + kCorrMaxK * kHM * (kHM + 4);  // [kHM][kHU + 1]
+  const int kc = a.k;
+  if (kc > 0) {
+    // G1 slices of steps k2 < k-1 from memory (k-1 is in LDS from (A)),
+    // and the learner's Gram rows grl[k2][s][s2] = gram[k][k2][s][s2].
+    for (int e = tid; e < (kc - 1) * kHM * (kHU / 4); e += 256) {
+      const int k2 = e / (kHM * (kHU / 4)), rem = e % (kHM * (kHU / 4));
+      const int sm = rem / (kHU / 4), c4 = rem % (kHU / 4);
+      const f32x4 v = *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + (sm < M ? sm : 0)) * Hp + ht * kHU + 4 * c4);
+      *(f32x4*)&gsl(k2, sm, 4 * c4) = sm < M ? v : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
+    for (int e = tid; e < kc * Mp * Mp; e += 256) {
+      const int k2 = e / (Mp * Mp), rem = e % (Mp * Mp);
+      grl[(k2 * kHM + rem / Mp) * (kHM + 4) + rem % Mp] = gk[(int64_t)k2 * Mp * Mp + rem];
+    }
+  }
+  __syncthreads();
+  z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
+  if (kc > 0) {
+    // Rows and columns past M are zero in the staged errors, so the sum runs
+    // over the padded minibatch in fours.
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    for (int k2 = 0; k2 < kc; ++k2)
+#pragma unroll 2
+      for (int s2 = 0; s2 < Mp; s2 += 4) {
+        const f32x4 gg = *(const f32x4*)&grl[(k2 * kHM + rr) * (kHM + 4) + s2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c += gg[i] * *(const f32x4*)&gsl(k2, s2 + i, 4 * u4);
+      }
+    z -= lr * c;
+  }
+  const bool mok = rr < M;
+  if (mok) *(f32x4*)(a.Z1 + ((int64_t)p * Mp + rr) * Hp + h4) = z;
+  zs[rr * (kHU + 1) + 4 * u4 + 0] = mok ? fmaxf(z.x, 0.0f) : 0.0f;
+  zs[rr * (kHU + 1) + 4 * u4 + 1] = mok ? fmaxf(z.y, 0.0f) : 0.0f;
+  zs[rr * (kHU + 1) + 4 * u4 + 2] = mok ? fmaxf(z.z, 0.0f) : 0.0f;
+  zs[rr * (kHU + 1) + 4 * u4 + 3] = mok ? fmaxf(z.w, 0.0f) : 0.0f;
+  __syncthreads();
+  float* plo = a.PL + (int64_t)(a.k & 1) * a.pl_half;
+#pragma unroll
+  for (int q = 0; q < kHM * KC / 256; ++q) {
+    const int e = tid + 256 * q, mm = e / KC, c = e % KC;
+    float acc = ht == 0 ? b2l[c] : 0.0f;
+#pragma unroll
+    for (int hh = 0; hh < kHU; ++hh) acc += zs[mm * (kHU + 1) + hh] * ws[c * (kHU + 1) + hh];
+    if (mm < M && c < C) plo[(((int64_t)p * Mp + mm) * Cp + c) * htiles + ht] = acc;
+  }
+}
+
+void launch_head_step(hipStream_t s, const HeadStepArgs& a) {
+  const int htiles = a.Hp / kHU;
+  if (a.C <= 16)
+    launch(k_head_step<16>, a.P * htiles, 256, 0, s, a, htiles);
+  else
+    launch(k_head_step<32>, a.P * htiles, 256, 0, s, a, htiles);
 }
 
 // Evaluation: one wave per row m < M of a chunk.  Logits l_c = b_c + sum_ks
@@ -416,16 +634,16 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
   launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles);
 }
 
-void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, int64_t w_pitch,
-                   float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr,
+void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
+                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr,
                    int64_t part_split) {
   const int htiles = Hp / kHU;
   const int64_t split = part_split > 0 ? part_split : (int64_t)P * Mp * Hp;
   if (C <= 16)
-    launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
+    launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, b2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
            corr, split);
   else
-    launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
+    launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, b2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
            corr, split);
 }
 

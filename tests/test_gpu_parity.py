@@ -242,7 +242,8 @@ def test_torch_stream_and_profile(gpu_lib):
 
 def test_delayed_schedule_profile(gpu_lib):
     """Delayed updates, P=6 S=3 K1=2 K2=3: per block one forward of its steps
-    and one update of the cluster copies, per step the two head kernels; the
+    and one update of the cluster copies, per step one fused head kernel
+    (plus one for the backward of the block's last step); the
     Gram blocks once per round; eager round after set_params, delayed again
     after."""
     from paper_1903_05133_amd import HierAvg
@@ -254,7 +255,8 @@ def test_delayed_schedule_profile(gpu_lib):
         stats = h.profile_read()
         h.profile(False)
         assert np.array_equal(h.params(), ref)
-        assert stats["fwd1_block_gemm"][0] == 3 and stats["head_a"][0] == 6 and stats["head_b"][0] == 6
+        assert stats["fwd1_block_gemm"][0] == 3 and stats["head_step"][0] == 6 and stats["head_step_end"][0] == 3
+        assert not {"head_a", "head_b"} & set(stats)
         assert stats["block_update_gemm"][0] == 3 and stats["gram"][0] == 1
         assert stats["tail_group_mean"][0] == 2 and stats["tail_global_mean"][0] == 1
         assert stats["w1_global_mean"][0] == 1
