@@ -64,7 +64,7 @@ typedef struct hieravg* hieravg_t;
  *           correction -lr * sum_{k'<k} (X_k X_k'^T) G_k' and the cluster
  *           mean at the block end is one update of the copy by the summed
  *           G^T X of the cluster's learners and steps.  Needs the MLP with at
- *           most 32 classes, B <= 32 and K1 <= 8, and a round that starts
+ *           most 32 classes, B <= 32, K1 <= 8 and K1*S*B <= 16384, and a round that starts
  *           with equal W1 in every replica (true after create and after every
  *           round; after hieravg_set_params the next round runs EAGER).
  *  AUTO:    DELAYED where it applies and its extra Gram products cost at most

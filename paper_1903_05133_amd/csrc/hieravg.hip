@@ -188,7 +188,8 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
 
 bool delayed_applies(const hieravg_config& c) {
   const bool whole_blocks = c.k_global == 0 || c.k_global % c.K1 == 0;
-  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8 && whole_blocks;
+  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8 && whole_blocks &&
+         (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows;
 }
 
 int validate(const hieravg_config& c) {

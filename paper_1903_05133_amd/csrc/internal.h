@@ -200,6 +200,9 @@ struct BlkArgs {
   const float* lr;      // device scalar step size; the mean takes lr / lr_div
   float lr_div;
 };
+// Contraction rows (K1 * SG * B) the block update takes: their sample indices
+// live in LDS beside the 50 KB of operand stages.
+constexpr int kBlkMaxRows = 16384;
 void launch_block_update(hipStream_t s, const BlkArgs& a);
 
 // Gram blocks of each learner's minibatches within each block of a round, as

@@ -175,6 +175,7 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
   constexpr int kStage = kSC * (kLA + kLB);
   constexpr int kLds = 2 * kStage > kUM * kLB ? 2 * kStage : kUM * kLB;
   __shared__ __attribute__((aligned(16))) float lds[kLds];
+  extern __shared__ int32_t sidx[];  // [K1*SG*B] sample index of each contraction row
   float* Gt = lds;  // [kUM][kLB] gradient tile (after the stages)
   // Tiles that share minibatch rows (same group and columns) are neighbours.
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -219,21 +220,17 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     bool gok[kGL], xok[kXL];
   };
   StageRegs RA, RB;
-  // Sample indices are loaded two stages before the rows they select (two
-  // sets, even and odd stages): loads complete in issue order, so waiting for
-  // an index then waits only for loads the previous stage already needed.
-  int32_t xrowA[kXL], xrowB[kXL];
-  auto load_idx = [&](int st, int32_t (&xrow)[kXL]) {
-    const int s0 = (st < nst ? st : nst - 1) * kSC;
-#pragma unroll
-    for (int i = 0; i < kXL; ++i) {
-      const int r = s0 + xr0 + kXR * i;
-      int64_t grow, irow;
-      gx_row(r < R ? r : 0, grow, irow);
-      xrow[i] = a.idx[irow];
-    }
-  };
-  auto load_stage = [&](int st, StageRegs& q, const int32_t (&xrow)[kXL]) {
+  // The sample index of every contraction row, read once into LDS: the
+  // stage loads then depend on no other global load (loads complete in issue
+  // order, so an index load in the loop would make the wait for it a wait
+  // for the stage data issued before it).
+  for (int r = tid; r < R; r += NTH) {
+    int64_t grow, irow;
+    gx_row(r, grow, irow);
+    sidx[r] = a.idx[irow];
+  }
+  __syncthreads();
+  auto load_stage = [&](int st, StageRegs& q) {
     const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
 #pragma unroll
     for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
@@ -248,7 +245,8 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     for (int i = 0; i < kXL; ++i) {  // X rows of contraction rows s0 + xr0 + kXR*i
       const int r = s0 + xr0 + kXR * i;
       q.xok[i] = r < R && xcol_ok;
-      q.xb[i] = *(const f32x4*)(a.X + (q.xok[i] ? (int64_t)xrow[i] * a.ldx + xcol : 0));
+      const int xrow = sidx[r < R ? r : 0];
+      q.xb[i] = *(const f32x4*)(a.X + (q.xok[i] ? (int64_t)xrow * a.ldx + xcol : 0));
     }
   };
   auto store_stage = [&](int buf, const StageRegs& q) {
@@ -282,27 +280,21 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     }
   };
 
-  load_idx(0, xrowA);
-  load_idx(1, xrowB);
-  load_stage(0, RA, xrowA);
-  load_idx(2, xrowA);
-  load_stage(1, RB, xrowB);
-  load_idx(3, xrowB);
+  load_stage(0, RA);
+  load_stage(1, RB);
   store_stage(0, RA);
   __syncthreads();
-  // Iteration st: loads of stage st+2 and indices of stage st+4 go out, the
-  // MFMAs of stage st (LDS buffer st&1) run, stage st+1 goes to the other
-  // buffer.  Unrolled by two so each register set is named statically.
+  // Iteration st: loads of stage st+2 go out, the MFMAs of stage st (LDS
+  // buffer st&1) run, stage st+1 goes to the other buffer.  Unrolled by two
+  // so each register set is named statically.
   for (int st = 0; st < nst; st += 2) {
-    load_stage(st + 2, RA, xrowA);
-    load_idx(st + 4, xrowA);
+    load_stage(st + 2, RA);
     __builtin_amdgcn_sched_barrier(0);
     mfma_stage(0);
     store_stage(1, RB);
     __syncthreads();
     if (st + 1 >= nst) break;
-    load_stage(st + 3, RB, xrowB);
-    load_idx(st + 5, xrowB);
+    load_stage(st + 3, RB);
     __builtin_amdgcn_sched_barrier(0);
     mfma_stage(1);
     store_stage(0, RA);
@@ -348,7 +340,8 @@ void launch_block_update(hipStream_t s, const BlkArgs& a) {
   const int mtiles = (a.Mrows + kUM - 1) / kUM;
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
-  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, 0, s, a, mtiles, ntiles);
+  const uint32_t shmem = sizeof(int32_t) * a.K1 * a.SG * a.B;
+  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
 }
 
 // ------------------------------------------------------------ Gram blocks
