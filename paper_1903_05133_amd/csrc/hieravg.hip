@@ -99,6 +99,7 @@ struct hieravg {
   float* Wc = nullptr;     // [P/S][Hp*INp] cluster copies of W1
   float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
   float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
+  int32_t* ylab = nullptr; // [T][P][B] labels of the drawn samples (delayed schedule)
   // Evaluation (allocated at the first hieravg_evaluate).
   int eval_rows = 0;                  // chunk capacity (multiple of 16)
   int32_t* eval_iota = nullptr;       // [eval_rows] 0, 1, 2, ...
@@ -154,7 +155,7 @@ void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper,
-                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->eval_iota,
+                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -352,6 +353,7 @@ int build(hieravg* h) {
       const int64_t w1 = h->Hp * h->INp;
       if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
+      if ((rc = alloc_zero(h, (void**)&h->ylab, sizeof(int32_t) * (size_t)T * P * c.B, "sample labels"))) return rc;
       h->KSG = gram_splits(P, c.K2, (int)h->INp);
       if (c.K1 > 1 && (rc = alloc_zero(h, (void**)&h->gram,
                                        sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * Bp_del * Bp_del, "Gram blocks")))
@@ -405,7 +407,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
   switch (kc) {
     case KC_DRAW:
       launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, h->T, (uint64_t)h->N,
-                          h->key_index);
+                          h->key_index, h->y, h->in_delayed ? h->ylab : nullptr);
       return true;
     case KC_FWD1: {
       FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, mlp ? Hp : Cp, INp, h->KS1,
@@ -544,9 +546,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.pl_half = (int64_t)P * (Hp / 32) * Bp * Cp;
       a.gs = h->Gs;
       a.gram = h->gram ? h->gram + (int64_t)blk * P * c.K1 * c.K1 * Bp * Bp : nullptr;
-      a.labels = h->y;
-      // the previous step's indices (HEAD_END: this step's, the block's last)
-      a.idx_prev = kc == KC_HEAD_END ? ix : ix - (int64_t)P * B;
+      // the previous step's labels (HEAD_END: this step's, the block's last)
+      a.ylab_prev = h->ylab + (int64_t)(kc == KC_HEAD_END ? tt : tt - 1) * P * B;
       a.lr = h->hyper;
       a.P = P;
       a.M = B;

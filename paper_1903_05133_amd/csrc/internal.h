@@ -129,8 +129,9 @@ void launch_init_matrix(hipStream_t s, float* W, int64_t rows, int64_t cols, int
                         uint64_t layer, float scale);
 void launch_init_vector(hipStream_t s, float* w, int64_t D, uint64_t key, float std);
 void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int T, uint64_t key, float std);
+// ylab (optional): the label of every drawn sample, same layout as idx.
 void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
-                         int T, uint64_t N, uint64_t key);
+                         int T, uint64_t N, uint64_t key, const int32_t* labels = nullptr, int32_t* ylab = nullptr);
 
 // GEMMs (k_gemm.hip).
 struct FwdArgs {
@@ -277,8 +278,7 @@ struct HeadStepArgs {
   int64_t pl_half;        // floats per parity
   float* gs;              // [K1][P][Mp][Hp] hidden errors of the block's steps
   const float* gram;      // [P][K1][K1][Mp][Mp] of the block
-  const int32_t* labels;  // dataset labels
-  const int32_t* idx_prev;  // [P][M] sample indices of step k-1
+  const int32_t* ylab_prev;  // [P][M] labels of the samples of step k-1
   const float* lr;        // device scalar step size
   int P, M, Mp, C, Cp, Hp, K1, k;
 };

@@ -68,7 +68,8 @@ __global__ __launch_bounds__(256) void k_gen_grads(float* __restrict__ G, int64_
 // counter lives on the device and a round needs no host-side argument.
 __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx, uint64_t* step_ctr,
                                                       uint32_t* done_ctr, int P, int B, int T, uint64_t N,
-                                                      uint64_t key) {
+                                                      uint64_t key, const int32_t* __restrict__ labels,
+                                                      int32_t* __restrict__ ylab) {
   const uint64_t t0 = *step_ctr;
   const int64_t total = (int64_t)T * P * B;
   for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
@@ -76,7 +77,9 @@ __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx,
     const int64_t j = (e / B) % P;
     const int64_t tt = e / ((int64_t)B * P);
     const uint64_t ctr = ((t0 + (uint64_t)tt) << 32) | ((uint64_t)j << 16) | (uint64_t)s;
-    idx[e] = (int32_t)(hash64(key, ctr) % N);
+    const int32_t i = (int32_t)(hash64(key, ctr) % N);
+    idx[e] = i;
+    if (ylab) ylab[e] = labels[i];
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -120,8 +123,9 @@ void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int
 }
 
 void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
-                         int T, uint64_t N, uint64_t key) {
-  launch(k_draw_indices, grid_for((int64_t)T * P * B, 1024), 256, 0, s, idx, step_ctr, done_ctr, P, B, T, N, key);
+                         int T, uint64_t N, uint64_t key, const int32_t* labels, int32_t* ylab) {
+  launch(k_draw_indices, grid_for((int64_t)T * P * B, 1024), 256, 0, s, idx, step_ctr, done_ctr, P, B, T, N, key,
+         labels, ylab);
 }
 
 }  // namespace hav

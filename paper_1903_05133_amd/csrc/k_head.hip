@@ -353,28 +353,32 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 // hidden units h = 32*ht + u of learner p; M <= 32 samples, one chunk.
 //  (A) k > 0, the rest of step k-1: logits of every sample from the partial
 //      logits of all slices (b2 is folded into slice 0's), its softmax
-//      cross-entropy gradient G2 (mean over the minibatch), then for this
-//      slice, with thread (u = t%32, g = t/32) taking samples g + 8i:
-//      G1 = (G2 W2)[m][h] * [Z1 > 0] into gs[k-1] and into LDS for (B); the
-//      eight sample groups' sums give the steps of b1[h] and W2[:, h] (the
-//      new values stay in LDS for (B)); slice 0 steps b2.
+//      cross-entropy gradient G2 (mean over the minibatch; eight threads per
+//      sample), then for this slice, with thread (u = t%32, g = t/32) taking
+//      samples g + 8i: G1 = (G2 W2)[m][h] * [Z1 > 0] into gs[k-1] and into LDS
+//      for (B); the eight sample groups' sums give the steps of b1[h] and
+//      W2[:, h] (the new values stay in LDS for (B)); slice 0 steps b2.
 //  (B) k < K1, step k: Z1 = b1 + sum of the split-K partials
 //      - lr * sum_{k2<k} gram[k][k2] G1[k2] for this slice, its ReLU, and the
 //      slice's partial logits into PL[k&1] (slice 0 adds b2).
 // (A) reads PL[(k-1)&1] of every slice while (B) writes PL[k&1], and b2 is
 // read and written by slice 0 only, so no workgroup depends on another
-// within a launch.
+// within a launch.  Every global load the launch needs that does not depend
+// on (A) is issued before (A) starts: step k's partials, the Gram rows and
+// the earlier steps' hidden errors of (B).
 template <int KC>
 __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   constexpr int kG = 256 / kHU, kR = kHM / kG;
-  constexpr int kGsl = kCorrMaxK * kHM * kHU;                 // G1 slices of the block's steps
-  constexpr int kPhaseB = kCorrMaxK * kHM * (kHM + 4) + kHM * (kHU + 1);
+  constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
+  constexpr int kGrl = kCorrMaxK * kHM * (kHM + 4);  // Gram rows of step k
   constexpr int kPhaseA = kHM * (KC + 1) + kG * (KC + 1) * kHU;
-  constexpr int kRegion = kPhaseA > kPhaseB ? kPhaseA : kPhaseB;
-  __shared__ __attribute__((aligned(16))) float lds[kGsl + kRegion + KC * (kHU + 1) + kHU + KC];
+  constexpr int kZs = kHM * (kHU + 1);
+  constexpr int kRegion = kPhaseA > kZs ? kPhaseA : kZs;
+  __shared__ __attribute__((aligned(16))) float lds[kGsl + kGrl + kRegion + KC * (kHU + 1) + kHU + KC];
   __shared__ int ys[kHM];
   auto gsl = [&](int k2, int s, int u) -> float& { return lds[(k2 * kHM + s) * kHU + u]; };
-  float* region = lds + kGsl;
+  float* grl = lds + kGsl;          // [kCorrMaxK][kHM][kHM + 4]
+  float* region = grl + kGrl;
   float* ws = region + kRegion;     // [KC][kHU + 1] W2 slice (after (A))
   float* bs = ws + KC * (kHU + 1);  // [kHU] b1 slice (after (A))
   float* b2l = bs + kHU;            // [KC] b2 (slice 0, after (A))
@@ -386,15 +390,34 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   float* w2 = a.W2 + (int64_t)p * a.w_pitch;
   float* b1 = a.b1 + (int64_t)p * a.w_pitch;
   float* b2 = a.b2 + (int64_t)p * a.w_pitch;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
-  // Step k's partial sums are independent of (A): their loads go out first.
+  // Step k's partial sums.
   const int u4 = tid & 7, rr = tid >> 3;
   const int h4 = ht * kHU + 4 * u4;
-  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  f32x4 z = zero4;
+  const int kc = a.k < a.K1 ? a.k : 0;  // earlier steps whose correction (B) applies
   if (a.k < a.K1) {
     const float* pm = a.part + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
 #pragma unroll 8
     for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
+  }
+  // (B)'s operands: the hidden errors of steps k2 < k-1 (16-byte piece tid of
+  // each step's 32 x 32 slice; step k-1 comes from (A)) and the Gram rows
+  // gram[k][k2] (piece tid of each Mp x Mp block).
+  f32x4 gv[kCorrMaxK - 1], gr[kCorrMaxK];
+  const int gsm = tid / (kHU / 4), gc4 = tid % (kHU / 4);
+#pragma unroll
+  for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2) {
+    gv[k2] = zero4;
+    if (k2 < kc - 1 && gsm < M)
+      gv[k2] = *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + gsm) * Hp + ht * kHU + 4 * gc4);
+  }
+  const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
+#pragma unroll
+  for (int k2 = 0; k2 < kCorrMaxK; ++k2) {
+    gr[k2] = zero4;
+    if (k2 < kc && tid < Mp * Mp / 4) gr[k2] = *(const f32x4*)(gk + (int64_t)k2 * Mp * Mp + 4 * tid);
   }
 
   if (a.k > 0) {  // (A): the rest of step k-1
@@ -402,7 +425,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
     const int u = tid % kHU, g = tid / kHU, h = ht * kHU + u;
     float* g2s = region;                   // [kHM][KC + 1]
     float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
-    if (tid < kHM) ys[tid] = a.labels[a.idx_prev[(int64_t)p * M + (tid < M ? tid : 0)]];
+    if (tid < kHM) ys[tid] = a.ylab_prev[(int64_t)p * M + (tid < M ? tid : 0)];
     float wc[KC];
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
@@ -429,19 +452,35 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
       g2s[mm * (KC + 1) + c] = ok ? l : 0.0f;
     }
     __syncthreads();
-    if (tid < M) {
-      float* row = g2s + tid * (KC + 1);
+    {  // softmax gradient: eight threads per sample, KC/8 classes each
+      const int row = tid >> 3, l8 = tid & 7;
+      float* rowp = g2s + row * (KC + 1);
+      float v[KC / 8];
       float mx = -INFINITY;
-      for (int c = 0; c < C; ++c) mx = fmaxf(mx, row[c]);
-      float sum = 0.0f;
-      for (int c = 0; c < C; ++c) {
-        const float e = expf(row[c] - mx);
-        row[c] = e;
-        sum += e;
+#pragma unroll
+      for (int j = 0; j < KC / 8; ++j) {
+        const int c = l8 + 8 * j;
+        v[j] = rowp[c];
+        if (c < C) mx = fmaxf(mx, v[j]);
       }
-      const int y = ys[tid];
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 8));
+      float sum = 0.0f;
+#pragma unroll
+      for (int j = 0; j < KC / 8; ++j) {
+        v[j] = l8 + 8 * j < C ? expf(v[j] - mx) : 0.0f;
+        sum += v[j];
+      }
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) sum += __shfl_xor(sum, o, 8);
+      const int y = ys[row];
       const float invB = 1.0f / (float)M;
-      for (int c = 0; c < C; ++c) row[c] = (row[c] / sum - (c == y ? 1.0f : 0.0f)) * invB;
+      if (row < M)
+#pragma unroll
+        for (int j = 0; j < KC / 8; ++j) {
+          const int c = l8 + 8 * j;
+          if (c < C) rowp[c] = (v[j] / sum - (c == y ? 1.0f : 0.0f)) * invB;
+        }
     }
     __syncthreads();
     float db1 = 0.0f, db2 = 0.0f;
@@ -494,7 +533,6 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
       if (tid < C) b2[tid] = nb2;
       b2l[tid] = nb2;
     }
-    __syncthreads();
   } else {
     for (int e = tid; e < KC * kHU; e += 256) {
       const int c = e / kHU, hh = e % kHU;
@@ -507,30 +545,22 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   if (a.k >= a.K1) return;
 
   // (B): step k's forward for this slice.
-  float* grl = region;                               // [kCorrMaxK][kHM][kHM + 4]
-  float* zs = region + kCorrMaxK * kHM * (kHM + 4);  // [kHM][kHU + 1]
-  const int kc = a.k;
-  if (kc > 0) {
-    // G1 slices of steps k2 < k-1 from memory (k-1 is in LDS from (A)),
-    // and the learner's Gram rows grl[k2][s][s2] = gram[k][k2][s][s2].
-    for (int e = tid; e < (kc - 1) * kHM * (kHU / 4); e += 256) {
-      const int k2 = e / (kHM * (kHU / 4)), rem = e % (kHM * (kHU / 4));
-      const int sm = rem / (kHU / 4), c4 = rem % (kHU / 4);
-      const f32x4 v = *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + (sm < M ? sm : 0)) * Hp + ht * kHU + 4 * c4);
-      *(f32x4*)&gsl(k2, sm, 4 * c4) = sm < M ? v : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2)
+    if (k2 < kc - 1) *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gv[k2];
+#pragma unroll
+  for (int k2 = 0; k2 < kCorrMaxK; ++k2)
+    if (k2 < kc && tid < Mp * Mp / 4) {
+      const int rem = 4 * tid;
+      *(f32x4*)&grl[(k2 * kHM + rem / Mp) * (kHM + 4) + rem % Mp] = gr[k2];
     }
-    const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
-    for (int e = tid; e < kc * Mp * Mp; e += 256) {
-      const int k2 = e / (Mp * Mp), rem = e % (Mp * Mp);
-      grl[(k2 * kHM + rem / Mp) * (kHM + 4) + rem % Mp] = gk[(int64_t)k2 * Mp * Mp + rem];
-    }
-  }
+  float* zs = region;  // [kHM][kHU + 1]
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
   if (kc > 0) {
     // Rows and columns past M are zero in the staged errors, so the sum runs
     // over the padded minibatch in fours.
-    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    f32x4 c = zero4;
     for (int k2 = 0; k2 < kc; ++k2)
 #pragma unroll 2
       for (int s2 = 0; s2 < Mp; s2 += 4) {
