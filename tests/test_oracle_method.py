@@ -372,3 +372,91 @@ def test_global_interval_equal_to_blocks_is_the_block_round():
     a = M.run(small(M.MLP, 4, 2, 2, 3), 1)
     b = M.run(small(M.MLP, 4, 2, 2, 3, k_global=6), 1)
     assert np.array_equal(a.W, b.W) and np.array_equal(a.last_indices, b.last_indices)
+
+
+# ------------------------------------------------ momentum and weight decay (MLP/softmax)
+def torch_schedule_reference(p, rounds):
+    """Algorithm 1's schedule with torch.optim.SGD (momentum, weight_decay,
+    no dampening, no Nesterov) as every learner's step: one optimizer per
+    learner for the whole run; after every K1 steps each group of S learners
+    takes the mean of its parameters (and of its momentum buffers when
+    avg_momentum), at the end of a round all P learners do."""
+    w0 = M.initial_replica(p)
+    prms = [torch_params(p, w0) for _ in range(p.P)]
+    opts = [torch.optim.SGD(list(prm.values()), lr=p.lr64, momentum=p.mu64, weight_decay=p.wd64) for prm in prms]
+
+    def average(groups):
+        for grp in groups:
+            for name in prms[0]:
+                mean = torch.stack([prms[j][name].detach() for j in grp]).mean(dim=0)
+                for j in grp:
+                    prms[j][name].data.copy_(mean)
+            if p.avg_momentum:
+                for i, _ in enumerate(prms[0]):
+                    bufs = [opts[j].state[list(prms[j].values())[i]]["momentum_buffer"] for j in grp]
+                    mean = torch.stack(bufs).mean(dim=0)
+                    for b in bufs:
+                        b.copy_(mean)
+
+    t = 0
+    for _ in range(rounds):
+        for tt in range(p.T):
+            for j in range(p.P):
+                X, y = rng.data_rows(p.seed, rng.draw_indices(p.seed, j, t, p.B, p.N), p.IN, p.C, p.sigma)
+                opts[j].zero_grad()
+                torch_loss(p, prms[j], X, y).backward()
+                opts[j].step()
+            t += 1
+            if (tt + 1) % p.K1 == 0:
+                average([range(q * p.S, q * p.S + p.S) for q in range(p.P // p.S)])
+        average([range(p.P)])
+    W = np.stack([flatten(p, prm) for prm in prms])
+    V = np.stack([np.concatenate([opts[j].state[v]["momentum_buffer"].numpy().reshape(-1)
+                                  for v in prms[j].values()]) for j in range(p.P)])
+    return W, V
+
+
+@pytest.mark.parametrize("kind", [M.SOFTMAX, M.MLP])
+def test_single_learner_momentum_weight_decay_is_torch_sgd(kind):
+    p = small(kind, 1, 1, 3, 2, momentum=0.9, weight_decay=0.01)
+    st = M.run(p, 2)
+    W, V = torch_schedule_reference(p, 2)
+    assert relerr(st.W[0], W[0]) < 1e-12
+    assert relerr(st.V[0], V[0]) < 1e-12
+
+
+@pytest.mark.parametrize("avg", [False, True])
+def test_hierarchical_momentum_buffers(avg):
+    """P = 4 in groups of 2, K1 = 2, two blocks and two rounds: per-learner
+    buffers carried across the means (or averaged with the parameters)."""
+    p = small(M.MLP, 4, 2, 2, 2, momentum=0.8, weight_decay=0.005, avg_momentum=avg)
+    st = M.run(p, 2)
+    W, V = torch_schedule_reference(p, 2)
+    assert relerr(st.W, W) < 1e-12
+    assert relerr(st.V, V) < 1e-12
+    # after the global mean: equal buffers exactly when they are averaged
+    assert np.array_equal(st.V, np.repeat(st.V[:1], 4, axis=0)) == avg
+
+
+def test_momentum_zero_is_plain_step():
+    """mu = lambda = 0 reproduces the plain step bit for bit."""
+    p = small(M.MLP, 4, 2, 2, 2)
+    q = small(M.MLP, 4, 2, 2, 2, momentum=0.0, weight_decay=0.0, avg_momentum=True)
+    assert np.array_equal(M.run(p, 2).W, M.run(q, 2).W)
+
+
+def test_averaged_buffers_with_one_group_per_step_are_large_batch_momentum():
+    """S = P, K1 = 1: every step ends with the mean of parameters and buffers,
+    which is one learner with momentum on the mean gradient of the P*B
+    samples of the step (the buffers being linear in the gradients)."""
+    p = small(M.SOFTMAX, 3, 3, 1, 4, B=3, momentum=0.9, weight_decay=0.01, avg_momentum=True)
+    st = M.run(p, 1)
+    prm = torch_params(p, M.initial_replica(p))
+    opt = torch.optim.SGD(list(prm.values()), lr=p.lr64, momentum=p.mu64, weight_decay=p.wd64)
+    for t in range(4):
+        Xs, ys = zip(*[rng.data_rows(p.seed, rng.draw_indices(p.seed, j, t, p.B, p.N), p.IN, p.C, p.sigma)
+                       for j in range(p.P)])
+        opt.zero_grad()
+        torch_loss(p, prm, np.concatenate(Xs), np.concatenate(ys)).backward()
+        opt.step()
+    assert relerr(st.W[0], flatten(p, prm)) < 1e-12
