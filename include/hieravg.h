@@ -64,9 +64,10 @@ typedef struct hieravg* hieravg_t;
  *           correction -lr * sum_{k'<k} (X_k X_k'^T) G_k' and the cluster
  *           mean at the block end is one update of the copy by the summed
  *           G^T X of the cluster's learners and steps.  Needs the MLP with at
- *           most 32 classes, B <= 32, K1 <= 8 and K1*S*B <= 16384, and a round that starts
- *           with equal W1 in every replica (true after create and after every
- *           round; after hieravg_set_params the next round runs EAGER).
+ *           most 32 classes, B <= 32, K1 <= 8, K1*S*B <= 16384, plain SGD
+ *           (momentum = weight_decay = 0), and a round that starts with equal
+ *           W1 in every replica (true after create and after every round;
+ *           after hieravg_set_params the next round runs EAGER).
  *  AUTO:    DELAYED where it applies and its extra Gram products cost at most
  *           an eighth of the step's flops ((K1 - 1) * B <= H / 2), else EAGER.
  */
@@ -101,7 +102,8 @@ typedef struct hieravg_config {
   int64_t n_samples;/* dataset rows N (softmax/MLP), N < 2^32               */
   float noise_std;  /* data noise std                                       */
   float lr;         /* step size gamma, finite and >= 0                     */
-  float momentum;   /* averaging kind: heavy-ball coefficient mu in [0, 1)  */
+  float momentum;   /* heavy-ball coefficient mu in [0, 1) (every kind):    */
+                    /*   d = g + weight_decay*w, v <- mu*v + d, w <- w - lr*v */
   float init_std;   /* averaging kind: std of the initial replica           */
   float grad_std;   /* averaging kind: std of the given gradients           */
   uint64_t seed;
@@ -112,6 +114,14 @@ typedef struct hieravg_config {
                           takes the global mean, so a round of k_global steps that K1
                           does not divide ends with a shorter block (a non-integer beta);
                           the count of local steps restarts at every global mean */
+  float weight_decay;  /* L2 coefficient lambda >= 0 of the step above; with
+                          momentum = weight_decay = 0 the step is Algorithm 1's
+                          plain SGD step.  The paper states no optimizer beyond
+                          SGD; these follow the usual heavy-ball convention.
+                          Softmax/MLP with either set run EAGER updates. */
+  int32_t avg_momentum; /* 1: every local and global mean also averages the
+                           momentum buffers v; 0: v stays per learner (Algorithm 1
+                           averages parameters only) */
 } hieravg_config;
 
 /*
@@ -154,6 +164,13 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats);
  * or device memory, n_floats >= P*D).  Momentum buffers are left as they are.
  * Synchronous. */
 int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats);
+
+/* The momentum buffers v of all learners, copied out / in as a dense [P][D]
+ * array in the layout of hieravg_params (host or device memory, n_floats >=
+ * P*D, else HIERAVG_ESIZE).  Synchronous.  HIERAVG_EINVAL when the handle has
+ * no buffers (momentum = 0: the step keeps no state). */
+int hieravg_momentum(hieravg_t h, float* dst, size_t n_floats);
+int hieravg_set_momentum(hieravg_t h, const float* src, size_t n_floats);
 
 /*
  * Minibatch size of the rounds enqueued from now on (a per-round schedule

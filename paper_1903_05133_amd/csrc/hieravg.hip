@@ -43,7 +43,8 @@ const char* kClassNames[KC_COUNT] = {
     "head_a",       "head_b",       "update2_gemm", "update1_gemm", "group_mean",  "global_mean",
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
-    "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end"};
+    "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
+    "momentum_buffer_group_mean", "momentum_buffer_global_mean"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -70,7 +71,7 @@ struct hieravg {
   int64_t off_W1 = 0, off_b1 = 0, off_W2 = 0, off_b2 = 0;
 
   float* W = nullptr;    // [P][Dp] replicas
-  float* V = nullptr;    // [P][Dp] momentum buffers (averaging kind)
+  float* V = nullptr;    // [P][Dp] momentum buffers (momentum > 0, or the averaging kind)
   float* Gr = nullptr;   // [K1*K2][P][Dp] given gradients (averaging kind)
   float* X = nullptr;    // [N][INp] dataset
   int32_t* y = nullptr;  // [N] labels
@@ -190,7 +191,7 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
 bool delayed_applies(const hieravg_config& c) {
   const bool whole_blocks = c.k_global == 0 || c.k_global % c.K1 == 0;
   return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8 && whole_blocks &&
-         (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows;
+         (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows && c.momentum == 0.0f && c.weight_decay == 0.0f;
 }
 
 int validate(const hieravg_config& c) {
@@ -209,12 +210,15 @@ int validate(const hieravg_config& c) {
   if (!std::isfinite(c.lr) || c.lr < 0.0f) return bad("lr must be finite and >= 0");
   if (c.update_mode < HIERAVG_UPDATE_AUTO || c.update_mode > HIERAVG_UPDATE_DELAYED)
     return bad("update_mode must be one of HIERAVG_UPDATE_*");
+  if (!std::isfinite(c.momentum) || c.momentum < 0.0f || c.momentum >= 1.0f)
+    return bad("momentum must be in [0, 1)");
+  if (!std::isfinite(c.weight_decay) || c.weight_decay < 0.0f) return bad("weight_decay must be finite and >= 0");
+  if (c.avg_momentum != 0 && c.avg_momentum != 1) return bad("avg_momentum must be 0 or 1");
   if (c.update_mode == HIERAVG_UPDATE_DELAYED && !delayed_applies(c))
-    return bad("delayed updates need the MLP with at most 32 classes, B <= 32, K1 <= 8 and whole blocks");
+    return bad("delayed updates need the MLP with at most 32 classes, B <= 32, K1 <= 8, K1*S*B <= 16384, "
+               "whole blocks and plain SGD (no momentum or weight decay)");
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
-    if (!std::isfinite(c.momentum) || c.momentum < 0.0f || c.momentum >= 1.0f)
-      return bad("averaging: momentum must be in [0, 1)");
     if (!std::isfinite(c.init_std) || !std::isfinite(c.grad_std)) return bad("averaging: stds must be finite");
     if (T * c.P > 65535) return bad("averaging: steps per round * P must be <= 65535");
     return HIERAVG_OK;
@@ -244,7 +248,8 @@ int64_t plan(hieravg* h, int B) {
   h->KS2 = h->cps2 = 1;
   plan_split(P, h->Bp, (int)n1, (int)h->INp, &h->KS1, &h->cps1);
   if (mlp) plan_split(P, h->Bp, (int)h->Cp, (int)h->Hp, &h->KS2, &h->cps2);
-  h->fused = h->T >= 2 && step_w1_supported(h->Bp, 1);
+  // The fused step kernels take the plain SGD step only.
+  h->fused = h->T >= 2 && step_w1_supported(h->Bp, 1) && c.momentum == 0.0f && c.weight_decay == 0.0f;
   h->fused_mean = h->fused && c.S > 1 && step_w1_supported(h->Bp, c.S);
   int64_t ks_max = h->KS1;
   if (h->fused) {
@@ -336,6 +341,9 @@ int build(hieravg* h) {
     h->Bp = (int)round_up(c.B, 16);
     int rc;
     if ((rc = alloc_zero(h, (void**)&h->W, sizeof(float) * P * h->Dp, "replicas"))) return rc;
+    if (c.momentum > 0.0f &&
+        (rc = alloc_zero(h, (void**)&h->V, sizeof(float) * P * h->Dp, "momentum buffers")))
+      return rc;
     if ((rc = alloc_zero(h, (void**)&h->X, sizeof(float) * h->N * h->INp, "dataset"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->y, sizeof(int32_t) * h->N, "labels"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->idx, sizeof(int32_t) * (size_t)T * P * c.B, "indices"))) return rc;
@@ -383,6 +391,17 @@ int build(hieravg* h) {
 // The single kernel launch of class `kc` for step tt of the current round
 // (tt selects the step's sample indices, or the averaging workload's given
 // gradients).  Returns false for a class this workload does not launch.
+// The heavy-ball buffers and decay of an update GEMM over the parameter block
+// at offset `off` (bias at `boff`) of the replica rows.
+void with_momentum(const hieravg* h, UpdArgs& u, int64_t off, int64_t boff) {
+  u.mu = h->cfg.momentum;
+  u.wd = h->cfg.weight_decay;
+  if (h->V) {
+    u.V = h->V + off;
+    u.vbias = u.bias ? h->V + boff : nullptr;
+  }
+}
+
 bool launch_class(hieravg* h, int kc, int tt) {
   const hieravg_config& c = h->cfg;
   const int P = c.P, B = c.B, S = c.S;
@@ -391,13 +410,17 @@ bool launch_class(hieravg* h, int kc, int tt) {
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     const float* g = h->Gr + (int64_t)tt * P * h->Dp;
     switch (kc) {
-      case KC_MOMENTUM: launch_momentum_step(s, W, h->V, g, h->Dp, P, 1, false, h->hyper, c.momentum); return true;
+      case KC_MOMENTUM:
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, 1, false, h->hyper, c.momentum, c.weight_decay);
+        return true;
       case KC_MOMENTUM_GROUP:
-        launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, h->hyper, c.momentum);
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, h->hyper, c.momentum, c.weight_decay);
         return true;
       case KC_MOMENTUM_GLOBAL:
-        launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, h->hyper, c.momentum);
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, h->hyper, c.momentum, c.weight_decay);
         return true;
+      case KC_VMEAN_GROUP:
+      case KC_VMEAN_GLOBAL: launch_group_mean(s, h->V, h->Dp, h->Dp, P, kc == KC_VMEAN_GROUP ? S : P); return true;
       default: return false;
     }
   }
@@ -427,10 +450,12 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (!mlp) {
         UpdArgs u{h->G2, h->Cp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, W + h->off_b1, P, B, Cp, INp,
                   h->hyper};
+        with_momentum(h, u, h->off_W1, h->off_b1);
         launch_update(s, u, A_GATHER);
       } else {
         UpdArgs u{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
                   small ? nullptr : W + h->off_b1, P, B, Hp, INp, h->hyper};
+        with_momentum(h, u, h->off_W1, h->off_b1);
         launch_update(s, u, A_GATHER);
       }
       return true;
@@ -493,6 +518,11 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, S); return true;
     case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, P); return true;
+    case KC_VMEAN_GROUP:
+    case KC_VMEAN_GLOBAL:
+      if (!h->V) return false;
+      launch_group_mean(s, h->V, h->Dp, h->Dp, P, kc == KC_VMEAN_GROUP ? S : P);
+      return true;
     default: break;
   }
   if (!mlp) return false;
@@ -521,8 +551,16 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (!small) return false;
       // Under delayed updates the hidden errors are kept for the block end.
       float* g1 = h->in_delayed ? h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp : h->G1;
+      HeadMom mom;
+      mom.mu = c.momentum;
+      mom.wd = c.weight_decay;
+      if (h->V) {
+        mom.vw2 = h->V + h->off_W2;
+        mom.vb1 = h->V + h->off_b1;
+        mom.vb2 = h->V + h->off_b2;
+      }
       launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, g1, h->y, ix, P, B, Bp,
-                    C, Cp, Hp, h->hyper);
+                    C, Cp, Hp, h->hyper, mom);
       return true;
     }
     case KC_HEAD_STEP:
@@ -578,6 +616,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (small) return false;
       UpdArgs u{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
                 h->hyper};
+      with_momentum(h, u, h->off_W2, h->off_b2);
       launch_update(s, u, A_RELU);
       return true;
     }
@@ -618,6 +657,7 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   if (last || !h->fused || (mean && !h->fused_mean)) {
     go(KC_UPDATE1);
     if (mean) go(KC_GROUP_MEAN);
+    if (mean && h->cfg.avg_momentum && h->V) go(KC_VMEAN_GROUP);
   } else if (mean) {
     go(KC_STEP1_MEAN);
     go(KC_TAIL_MEAN);
@@ -742,6 +782,10 @@ void enqueue_round(hieravg* h) {
       else if (end_block && !end_round && S > 1)
         kc = KC_MOMENTUM_GROUP;
       run(h, kc, [&] { launch_class(h, kc, tt); });
+      if (c.avg_momentum && kc != KC_MOMENTUM) {
+        const int vk = kc == KC_MOMENTUM_GLOBAL ? KC_VMEAN_GLOBAL : KC_VMEAN_GROUP;
+        run(h, vk, [&] { launch_class(h, vk, tt); });
+      }
     }
   } else if (h->in_delayed) {
     // Delayed first-layer updates: per block, the forward of its K1 steps
@@ -770,6 +814,7 @@ void enqueue_round(hieravg* h) {
     bool have_fwd = false;
     for (int tt = 0; tt < T; ++tt) enqueue_step(h, tt, have_fwd);
     if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
+    if (P > 1 && c.avg_momentum && h->V) run(h, KC_VMEAN_GLOBAL, [&] { launch_class(h, KC_VMEAN_GLOBAL, 0); });
   }
 }
 
@@ -1016,6 +1061,54 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
   HAV_CHECK(hipStreamSynchronize(h->stream));
   h->w1_shared = false;  // the rows may differ: the next round updates W1 eagerly
   h->rows_stale = false;
+  return HIERAVG_OK;
+}
+
+int hieravg_momentum(hieravg_t h, float* dst, size_t n_floats) {
+  if (!h || !dst) {
+    set_error("NULL handle or destination");
+    return HIERAVG_EINVAL;
+  }
+  if (!h->V) {
+    set_error("no momentum buffers (momentum is 0)");
+    return HIERAVG_EINVAL;
+  }
+  const int P = h->cfg.P;
+  if (n_floats < (size_t)P * (size_t)h->D) {
+    set_error("destination holds fewer than P*D floats");
+    return HIERAVG_ESIZE;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (int p = 0; p < P; ++p)
+    for (const Segment& g : segments(h))
+      HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
+                                 h->V + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
+                                 sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  return HIERAVG_OK;
+}
+
+int hieravg_set_momentum(hieravg_t h, const float* src, size_t n_floats) {
+  if (!h || !src) {
+    set_error("NULL handle or source");
+    return HIERAVG_EINVAL;
+  }
+  if (!h->V) {
+    set_error("no momentum buffers (momentum is 0)");
+    return HIERAVG_EINVAL;
+  }
+  const int P = h->cfg.P;
+  if (n_floats < (size_t)P * (size_t)h->D) {
+    set_error("source holds fewer than P*D floats");
+    return HIERAVG_ESIZE;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  for (int p = 0; p < P; ++p)
+    for (const Segment& g : segments(h))
+      HAV_CHECK(hipMemcpy2DAsync(h->V + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
+                                 src + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
+                                 sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
 }
 

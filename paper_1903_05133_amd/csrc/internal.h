@@ -97,6 +97,8 @@ enum KernelClass {
   KC_GRAM_REDUCE,    // delayed updates: sum of the Gram blocks' feature splits
   KC_HEAD_STEP,      // delayed updates: backward of step k-1 + forward and loss gradient of step k
   KC_HEAD_END,       // delayed updates: backward of a block's last step
+  KC_VMEAN_GROUP,    // averaged momentum buffers: cluster mean of v
+  KC_VMEAN_GLOBAL,   // averaged momentum buffers: global mean of v
   KC_COUNT
 };
 
@@ -179,6 +181,11 @@ struct UpdArgs {
   float* bias;          // bias block of replica 0 (or nullptr); replica p at bias + p*w_pitch
   int P, Kb, Mrows, Ncols;
   const float* lr;      // device scalar: the step size (read at kernel start)
+  // Heavy-ball step with L2 decay (d = g + wd*w; v <- mu*v + d; w <- w - lr*v):
+  // V, vbias are the buffers laid out like W, bias (nullptr: v = d, no state).
+  float* V = nullptr;
+  float* vbias = nullptr;
+  float mu = 0.0f, wd = 0.0f;
 };
 void launch_update(hipStream_t s, const UpdArgs& a, ASource bsrc);
 
@@ -255,9 +262,17 @@ struct HeadCorr {
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
                    int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr(),
                    int64_t part_split = 0);
+// Heavy-ball step with L2 decay of the second layer and the biases in
+// k_head_b: buffers laid out like W2, b1, b2 (nullptr: no buffers).
+struct HeadMom {
+  float* vw2 = nullptr;
+  float* vb1 = nullptr;
+  float* vb2 = nullptr;
+  float mu = 0.0f, wd = 0.0f;
+};
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
-                   int Cp, int Hp, const float* lr);
+                   int Cp, int Hp, const float* lr, HeadMom mom = HeadMom());
 
 // One launch per local step of the delayed schedule (C <= 32, M <= 32, K1 <= 8):
 // workgroup (p, slice of 32 hidden units) finishes step k-1's backward for its
@@ -296,6 +311,6 @@ void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int 
 // dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4 floats).
 void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
-                          bool average, const float* lr, float mu);
+                          bool average, const float* lr, float mu, float wd);
 
 }  // namespace hav

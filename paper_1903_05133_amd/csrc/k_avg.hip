@@ -8,9 +8,10 @@
 // column are added through LDS in group order, so every run produces the same
 // bits.  The mean is then written back to all S rows.
 //
-// The averaging-only workload fuses its heavy-ball step v <- mu*v + g,
-// w <- w - lr*v into the same pass (momentum buffers are per learner and are
-// not averaged: Algorithm 1 averages parameters only).
+// The averaging-only workload fuses its heavy-ball step v <- mu*v + g +
+// lambda*w, w <- w - lr*v into the same pass (the momentum buffers are per
+// learner; Algorithm 1 averages parameters only, and the variant that also
+// averages the buffers runs the plain mean over them as a second pass).
 #include <algorithm>
 
 #include "internal.h"
@@ -37,7 +38,7 @@ __device__ inline void st_stream(f32x4* p, f32x4 v) { *p = v; }
 template <bool MOM, bool MEAN, int RG, int NG, int TB>
 __global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __restrict__ V,
                                              const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4,
-                                             const float* __restrict__ lr_ptr, float mu) {
+                                             const float* __restrict__ lr_ptr, float mu, float wd) {
   const float lr = MOM ? *lr_ptr : 0.0f;
   constexpr int S = RG * NG;
   constexpr int CPB = TB / NG;  // columns per workgroup
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __res
       }
 #pragma unroll
       for (int u = 0; u < RG; ++u) {
-        v[u] = mu * v[u] + gr[u];
+        v[u] = mu * v[u] + (gr[u] + wd * w[u]);
         w[u] = w[u] - lr * v[u];
         if (ok) st_stream(V + (row0 + u) * pitch4 + i, v[u]);
       }
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(TB) void k_rows(f32x4* __restrict__ W, f32x4* __res
 template <bool MOM>
 __global__ __launch_bounds__(256) void k_rows_any(f32x4* __restrict__ W, f32x4* __restrict__ V,
                                                   const f32x4* __restrict__ Gr, int64_t pitch4, int64_t n4, int S,
-                                                  const float* __restrict__ lr_ptr, float mu) {
+                                                  const float* __restrict__ lr_ptr, float mu, float wd) {
   const float lr = MOM ? *lr_ptr : 0.0f;
   const int64_t row0 = (int64_t)blockIdx.y * S;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
@@ -106,7 +107,7 @@ __global__ __launch_bounds__(256) void k_rows_any(f32x4* __restrict__ W, f32x4* 
       if (MOM) {
         f32x4 v = ld_stream(V + o);
         const f32x4 g = ld_stream(Gr + o);
-        v = mu * v + g;
+        v = mu * v + (g + wd * w);
         w = w - lr * v;
         st_stream(V + o, v);
       }
@@ -126,9 +127,9 @@ static unsigned col_runs(int64_t n4, int cpb, int groups) {
 
 template <bool MOM, bool MEAN, int RG, int NG, int TB = 256>
 static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
-                        const float* lr, float mu) {
+                        const float* lr, float mu, float wd) {
   dim3 grid(col_runs(n4, TB / NG, groups), (unsigned)groups);
-  launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, p4, n4, lr, mu);
+  launch(k_rows<MOM, MEAN, RG, NG, TB>, grid, TB, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, p4, n4, lr, mu, wd);
 }
 
 // Cluster of S rows with S a power of two up to 64.  Up to 16 rows: one row per
@@ -144,33 +145,34 @@ static void launch_rows(hipStream_t s, float* W, float* V, const float* Gr, int6
 #endif
 template <bool MOM, int S>
 static void launch_s(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int groups,
-                     const float* lr, float mu) {
+                     const float* lr, float mu, float wd) {
   constexpr int kR = S <= 16 ? HAV_AVG_RG : HAV_AVG_RG_BIG;
   constexpr int RG = S < kR ? S : kR;
   constexpr int TB = S <= 16 ? 256 : HAV_AVG_TB_BIG;
-  launch_rows<MOM, true, RG, S / RG, TB>(s, W, V, Gr, p4, n4, groups, lr, mu);
+  launch_rows<MOM, true, RG, S / RG, TB>(s, W, V, Gr, p4, n4, groups, lr, mu, wd);
 }
 
 template <bool MOM>
 static bool launch_mean_pow2(hipStream_t s, float* W, float* V, const float* Gr, int64_t p4, int64_t n4, int P,
-                             int S, const float* lr, float mu) {
+                             int S, const float* lr, float mu, float wd) {
   const int groups = P / S;
   switch (S) {
-    case 2: launch_s<MOM, 2>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
-    case 4: launch_s<MOM, 4>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
-    case 8: launch_s<MOM, 8>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
-    case 16: launch_s<MOM, 16>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
-    case 32: launch_s<MOM, 32>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
-    case 64: launch_s<MOM, 64>(s, W, V, Gr, p4, n4, groups, lr, mu); return true;
+    case 2: launch_s<MOM, 2>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
+    case 4: launch_s<MOM, 4>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
+    case 8: launch_s<MOM, 8>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
+    case 16: launch_s<MOM, 16>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
+    case 32: launch_s<MOM, 32>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
+    case 64: launch_s<MOM, 64>(s, W, V, Gr, p4, n4, groups, lr, mu, wd); return true;
     default: return false;
   }
 }
 
 void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S) {
   const int64_t p4 = pitch / 4, n4 = len / 4;
-  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, p4, n4, P, S, nullptr, 0.0f)) return;
+  if (launch_mean_pow2<false>(s, W, nullptr, nullptr, p4, n4, P, S, nullptr, 0.0f, 0.0f)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, (const float*)nullptr, 0.0f);
+  launch(k_rows_any<false>, grid, 256, 0, s, (f32x4*)W, nullptr, nullptr, p4, n4, S, (const float*)nullptr, 0.0f,
+         0.0f);
 }
 
 __global__ __launch_bounds__(256) void k_mean_rows(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
@@ -188,15 +190,15 @@ void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch
 }
 
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
-                          bool average, const float* lr, float mu) {
+                          bool average, const float* lr, float mu, float wd) {
   const int64_t n4 = Dp / 4;
   if (!average) {
-    launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, n4, P, lr, mu);
+    launch_rows<true, false, 1, 1>(s, W, V, Gr, n4, n4, P, lr, mu, wd);
     return;
   }
-  if (launch_mean_pow2<true>(s, W, V, Gr, n4, n4, P, S, lr, mu)) return;
+  if (launch_mean_pow2<true>(s, W, V, Gr, n4, n4, P, S, lr, mu, wd)) return;
   dim3 grid(col_runs(n4, 256, P / S), (unsigned)(P / S));
-  launch(k_rows_any<true>, grid, 256, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu);
+  launch(k_rows_any<true>, grid, 256, 0, s, (f32x4*)W, (f32x4*)V, (const f32x4*)Gr, n4, n4, S, lr, mu, wd);
 }
 
 }  // namespace hav

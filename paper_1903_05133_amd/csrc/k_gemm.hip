@@ -385,12 +385,20 @@ __global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int nt
       }
   __syncthreads();
   const float lr = *a.lr;
+  // d = g + wd*w; with buffers v <- mu*v + d and the step takes v.
+  float* Vp = a.V ? a.V + (int64_t)p * a.w_pitch : nullptr;
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {
     const int rl = wr0 + kXR * i, row = mrow0 + rl;
     if (col_ok && row < a.Mrows) {
-      const f32x4 g = *(const f32x4*)&Gt[rl * kLB + 4 * wc4];
-      *(f32x4*)(Wp + (int64_t)row * a.ldw + wcol) = wv[i] - lr * g;
+      f32x4 d = *(const f32x4*)&Gt[rl * kLB + 4 * wc4];
+      if (a.wd != 0.0f) d += a.wd * wv[i];
+      if (Vp) {
+        f32x4* vp = (f32x4*)(Vp + (int64_t)row * a.ldw + wcol);
+        d = a.mu * *vp + d;
+        *vp = d;
+      }
+      *(f32x4*)(Wp + (int64_t)row * a.ldw + wcol) = wv[i] - lr * d;
     }
   }
 
@@ -399,7 +407,15 @@ __global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int nt
     if (m < a.Mrows) {
       float sum = 0.0f;
       for (int s = 0; s < a.Kb; ++s) sum += Gp[(int64_t)s * a.ldg + m];
-      a.bias[(int64_t)p * a.w_pitch + m] -= lr * sum;
+      float* bp = a.bias + (int64_t)p * a.w_pitch + m;
+      const float b = *bp;
+      float d = sum + a.wd * b;
+      if (a.vbias) {
+        float* vp = a.vbias + (int64_t)p * a.w_pitch + m;
+        d = a.mu * *vp + d;
+        *vp = d;
+      }
+      *bp = b - lr * d;
     }
   }
 }

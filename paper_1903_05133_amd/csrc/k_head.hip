@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
                                                 const float* __restrict__ Z1, float* __restrict__ G1,
                                                 const int32_t* __restrict__ labels, const int32_t* __restrict__ idx,
                                                 int P, int M, int Mp, int C, int Cp, int Hp, int htiles,
-                                                const float* __restrict__ lr_ptr) {
+                                                const float* __restrict__ lr_ptr, HeadMom mom) {
   const float lr = *lr_ptr;
   constexpr int kG = 256 / kHU;     // sample groups
   constexpr int kR = kHM / kG;      // samples per thread per chunk
@@ -332,21 +332,33 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 #pragma unroll
   for (int c = 0; c < KC; ++c) red[g][c][u] = dw2[c];
   __syncthreads();
+  // d = g + wd*w; with buffers v <- mu*v + d and the step takes v.
+  auto step = [&](float* w, float* v, float wold, float gsum) {
+    float d = gsum + mom.wd * wold;
+    if (v) {
+      d = mom.mu * *v + d;
+      *v = d;
+    }
+    *w = wold - lr * d;
+  };
+  const int64_t po = (int64_t)p * w_pitch;
   if (g == 0) {
     float s = 0.0f;
 #pragma unroll
     for (int k = 0; k < kG; ++k) s += red[k][KC][u];
-    b1[(int64_t)p * w_pitch + h] -= lr * s;
+    step(b1 + po + h, mom.vb1 ? mom.vb1 + po + h : nullptr, b1[po + h], s);
 #pragma unroll
     for (int c = 0; c < KC; ++c)
       if (c < C) {
         float gsum = 0.0f;
 #pragma unroll
         for (int k = 0; k < kG; ++k) gsum += red[k][c][u];
-        w2[(int64_t)c * Hp + h] = wc[c] - lr * gsum;
+        const int64_t o = po + (int64_t)c * Hp + h;
+        step(W2 + o, mom.vw2 ? mom.vw2 + o : nullptr, wc[c], gsum);
       }
   }
-  if (ht == 0 && tid < C) b2[(int64_t)p * w_pitch + tid] -= lr * db2;
+  if (ht == 0 && tid < C)
+    step(b2 + po + tid, mom.vb2 ? mom.vb2 + po + tid : nullptr, b2[po + tid], db2);
 }
 
 // Fused head of the delayed schedule (HeadStepArgs).  Workgroup (p, ht) owns
@@ -679,14 +691,14 @@ void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, co
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
-                   int Cp, int Hp, const float* lr) {
+                   int Cp, int Hp, const float* lr, HeadMom mom) {
   const int htiles = Hp / kHU;
   if (C <= 16)
     launch(k_head_b<16>, P * htiles, 256, 0, s, PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
-                                            htiles, lr);
+           htiles, lr, mom);
   else
     launch(k_head_b<32>, P * htiles, 256, 0, s, PL, W2, b1, b2, w_pitch, Z1, G1, labels, idx, P, M, Mp, C, Cp, Hp,
-                                            htiles, lr);
+           htiles, lr, mom);
 }
 
 }  // namespace hav

@@ -86,6 +86,16 @@ class HierAvg:
             a = np.ascontiguousarray(arr, dtype=np.float32)
             native.check(native.lib().hieravg_set_params(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
 
+    def momentum(self):
+        """Momentum buffers of all learners as [P, D] float32 (numpy)."""
+        out = np.empty((self.P, self.D), dtype=np.float32)
+        native.check(native.lib().hieravg_momentum(self._h, ctypes.c_void_p(out.ctypes.data), out.size))
+        return out
+
+    def set_momentum(self, arr):
+        a = np.ascontiguousarray(arr, dtype=np.float32)
+        native.check(native.lib().hieravg_set_momentum(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
+
     def set_batch(self, B):
         """Minibatch size of the rounds that follow (at most the B at create)."""
         native.check(native.lib().hieravg_set_batch(self._h, B))
@@ -142,7 +152,9 @@ class HierAvg:
 
 
 def config(kind, P, S, K1, K2, B=1, in_dim=0, hidden=0, classes=0, n_samples=0, noise_std=1.0, lr=0.05,
-           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0, update_mode=0, k_global=0):
+           momentum=0.0, init_std=0.01, grad_std=0.01, seed=0, update_mode=0, k_global=0, weight_decay=0.0,
+           avg_momentum=False):
     return native.Config(P=P, S=S, K1=K1, K2=K2, B=B, kind=kind, in_dim=in_dim, hidden=hidden, classes=classes,
                          n_samples=n_samples, noise_std=noise_std, lr=lr, momentum=momentum, init_std=init_std,
-                         grad_std=grad_std, seed=seed, update_mode=update_mode, k_global=k_global)
+                         grad_std=grad_std, seed=seed, update_mode=update_mode, k_global=k_global,
+                         weight_decay=weight_decay, avg_momentum=1 if avg_momentum else 0)

@@ -23,6 +23,8 @@ class Config(ctypes.Structure):
         ("seed", ctypes.c_uint64),
         ("update_mode", ctypes.c_int32),
         ("k_global", ctypes.c_int32),
+        ("weight_decay", ctypes.c_float),
+        ("avg_momentum", ctypes.c_int32),
     ]
 
 
@@ -38,6 +40,8 @@ SIGNATURES = {
     "hieravg_destroy": (None, [_H]),
     "hieravg_set_lr": (ctypes.c_int, [_H, ctypes.c_float]),
     "hieravg_set_batch": (ctypes.c_int, [_H, ctypes.c_int32]),
+    "hieravg_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
+    "hieravg_set_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "hieravg_last_error": (ctypes.c_char_p, []),

@@ -18,9 +18,10 @@ MODEL_ID = {"softmax_3072_10": 0, "mlp_3072_512_10": 1, "mlp_150528_1024_1000": 
 
 
 def case(kind, P, S, K1, K2, B=1, IN=0, H=0, C=0, N=0, sigma=1.0, lr=0.05, momentum=0.0, init_std=0.01,
-         grad_std=0.01, seed=0, k_global=0):
+         grad_std=0.01, seed=0, k_global=0, weight_decay=0.0, avg_momentum=False):
     return dict(kind=kind, P=P, S=S, K1=K1, K2=K2, B=B, IN=IN, H=H, C=C, N=N, sigma=sigma, lr=lr,
-                momentum=momentum, init_std=init_std, grad_std=grad_std, seed=seed, k_global=k_global)
+                momentum=momentum, init_std=init_std, grad_std=grad_std, seed=seed, k_global=k_global,
+                weight_decay=weight_decay, avg_momentum=avg_momentum)
 
 
 def named(name, P, S, K1, K2, B, lr, seed=0):
@@ -37,14 +38,16 @@ def native_config(c, update_mode="auto"):
     return config(KINDS[c["kind"]], c["P"], c["S"], c["K1"], c["K2"], B=c["B"], in_dim=c["IN"], hidden=c["H"],
                   classes=c["C"], n_samples=c["N"], noise_std=c["sigma"], lr=c["lr"], momentum=c["momentum"],
                   init_std=c["init_std"], grad_std=c["grad_std"], seed=c["seed"],
-                  update_mode=UPDATE_MODES[update_mode], k_global=c.get("k_global", 0))
+                  update_mode=UPDATE_MODES[update_mode], k_global=c.get("k_global", 0),
+                  weight_decay=c.get("weight_decay", 0.0), avg_momentum=c.get("avg_momentum", False))
 
 
 def oracle_problem(c):
     from oracle import method as M
     return M.Problem(c["kind"], c["P"], c["S"], c["K1"], c["K2"], c["B"], IN=c["IN"], H=c["H"], C=c["C"],
                      N=c["N"], sigma=c["sigma"], lr=c["lr"], momentum=c["momentum"], init_std=c["init_std"],
-                     grad_std=c["grad_std"], seed=c["seed"], k_global=c.get("k_global", 0))
+                     grad_std=c["grad_std"], seed=c["seed"], k_global=c.get("k_global", 0),
+                     weight_decay=c.get("weight_decay", 0.0), avg_momentum=c.get("avg_momentum", False))
 
 
 def block_errors(prob, got, want):

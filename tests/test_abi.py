@@ -74,6 +74,16 @@ def test_invalid_config_rejected():
         assert "delayed" in L.hieravg_last_error().decode()
     c = config(0, 4, 2, 1, 1, B=8, in_dim=10, classes=3, n_samples=10, update_mode=2)
     assert not L.hieravg_create_config(ctypes.byref(c))
+    # the optimizer fields, for every kind; delayed updates take plain SGD only
+    for kw, msg in ((dict(momentum=-0.1), "momentum"), (dict(momentum=1.0), "momentum"),
+                    (dict(weight_decay=-1.0), "weight_decay"), (dict(weight_decay=float("inf")), "weight_decay"),
+                    (dict(avg_momentum=2), "avg_momentum"), (dict(momentum=0.9, update_mode=2), "delayed"),
+                    (dict(weight_decay=0.1, update_mode=2), "delayed")):
+        c = config(1, 4, 2, 2, 1, B=8, in_dim=10, hidden=5, classes=3, n_samples=10, **kw)
+        if "avg_momentum" in kw:
+            c.avg_momentum = kw["avg_momentum"]
+        assert not L.hieravg_create_config(ctypes.byref(c))
+        assert msg in L.hieravg_last_error().decode()
 
 
 def test_kernel_class_names():

@@ -405,3 +405,83 @@ def test_global_interval_not_multiple_of_k1(name, gpu_lib):
     if idx is not None:
         assert idx.shape == (c["k_global"], c["P"], c["B"])
     _check(c, got, idx, *_oracle(c, 2))
+
+
+# ---------------------------------------------------- momentum and weight decay
+MOMENTUM_CASES = {
+    # small-class head (k_head_a/k_head_b) and the update GEMM of the first layer
+    "mlp_head_mom_wd": cases.case("mlp", 4, 2, 2, 2, B=12, IN=150, H=70, C=6, N=200, sigma=0.5, lr=0.05,
+                                  momentum=0.9, weight_decay=0.01, seed=31),
+    # more than 32 classes: layer-2 forward GEMM and the update GEMM with bias
+    "mlp_large_c_mom": cases.case("mlp", 4, 4, 2, 2, B=20, IN=130, H=80, C=40, N=300, sigma=0.5, lr=0.05,
+                                  momentum=0.8, seed=32),
+    "softmax_mom_wd": cases.case("softmax", 6, 3, 2, 2, B=9, IN=70, C=11, N=80, lr=0.1, momentum=0.9,
+                                 weight_decay=0.02, seed=33),
+    "mlp_avg_buffers": cases.case("mlp", 8, 4, 2, 2, B=8, IN=64, H=40, C=5, N=100, sigma=0.5, lr=0.05,
+                                  momentum=0.9, weight_decay=0.005, avg_momentum=True, seed=34),
+    "softmax_decay_only": cases.case("softmax", 4, 2, 3, 1, B=7, IN=50, C=4, N=60, lr=0.1, weight_decay=0.05,
+                                     seed=35),
+    "averaging_wd_avg_buffers": cases.case("averaging", 4, 2, 2, 2, IN=1001, lr=0.1, momentum=0.9,
+                                           weight_decay=0.01, avg_momentum=True, seed=36),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MOMENTUM_CASES))
+def test_momentum_and_weight_decay_match_oracle(name, gpu_lib):
+    """Heavy-ball buffers and L2 decay in every update kernel: parameters and
+    buffers after two rounds against the oracle (AUTO mode: these run eager)."""
+    from paper_1903_05133_amd import HierAvg
+    c = MOMENTUM_CASES[name]
+    print(f"[gpu case] momentum {name} {c}", flush=True)
+    with HierAvg(config=cases.native_config(c)) as h:
+        h.profile(True)
+        h.round()
+        h.round()
+        stats = h.profile_read()
+        got = h.params()
+        vgot = h.momentum() if c["momentum"] > 0 or c["kind"] == "averaging" else None
+        idx = h.last_indices() if c["kind"] != "averaging" else None
+    assert "fwd1_block_gemm" not in stats and "step1_gemm" not in stats
+    if c["avg_momentum"] and c["momentum"] > 0:
+        assert "momentum_buffer_global_mean" in stats
+    st, mon = _oracle(c, 2)
+    _check(c, got, idx, st, mon)
+    if vgot is not None:
+        prob = cases.oracle_problem(c)
+        ok, det = cases.parity_report(prob, vgot, st.V, mon)
+        print(f"[gpu case] buffers: worst block error {det['worst']}", flush=True)
+        assert ok, det
+        if c["avg_momentum"]:
+            assert np.array_equal(vgot, np.repeat(vgot[:1], vgot.shape[0], axis=0))
+
+
+def test_momentum_checkpoint_resume(gpu_lib):
+    """params + momentum buffers copied into a fresh handle continue the
+    trajectory: the round after equals the oracle's second round."""
+    from paper_1903_05133_amd import HierAvg
+    c = MOMENTUM_CASES["mlp_head_mom_wd"]
+    with HierAvg(config=cases.native_config(c)) as h:
+        h.round()
+        w, v = h.params(), h.momentum()
+    with HierAvg(config=cases.native_config(c)) as h2:
+        with pytest.raises(Exception):
+            h2.set_momentum(v[:1])
+        h2.set_params(w)
+        h2.set_momentum(v)
+        assert np.array_equal(h2.momentum(), v)
+        # the oracle's second round draws from step T on; the fresh handle from step 0
+        h2.round()
+        got = h2.params()
+    prob = cases.oracle_problem(c)
+    st = M.create(prob)
+    st.W, st.V = w.astype(np.float64), v.astype(np.float64)
+    M.hieravg_round(prob, st)
+    ok, det = cases.parity_report(prob, got, st.W)
+    assert ok, det
+
+
+def test_no_buffers_without_momentum(gpu_lib):
+    from paper_1903_05133_amd import HierAvg
+    with HierAvg(config=cases.native_config(MOMENTUM_CASES["softmax_decay_only"])) as h:
+        with pytest.raises(Exception):
+            h.momentum()
