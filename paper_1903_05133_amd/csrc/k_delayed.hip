@@ -28,8 +28,12 @@ constexpr int kLB = kUN + 4;    // LDS row length of the input stage and of the 
 // per weight copy): 1024 threads, output tile 128 rows x 128 columns, both
 // operands staged through LDS (double-buffered, one barrier per 64-wide K
 // chunk, the next chunk's loads in flight during the current chunk's MFMAs).
-// Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4)) as 2 x 2
-// 16x16x4 MFMA blocks, so each SIMD interleaves four waves.
+// Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4)) as one
+// chain of 32x32x2 MFMAs (one accumulator chain per wave keeps the matrix
+// pipe fuller than four interleaved 16x16x4 chains), so each SIMD
+// interleaves four waves.  Lane (l, h) reads the 16-byte piece of k values
+// 8q + 4h .. +3 of its row in both operands and feeds them to four MFMAs:
+// MFMA e contracts k = 8q + e and 8q + 4 + e, a permutation of the chunk's k.
 constexpr int kBT = 128;  // tile rows and columns
 __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mtiles) {
   __shared__ __attribute__((aligned(16))) float As[2][kBT * kLdsStride];
@@ -44,7 +48,7 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   const int c0 = ks * a.cps;
   const int c1 = min(nch, c0 + a.cps);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int l32 = lane & 31, lhi = lane >> 5;
   const int wm = (wave >> 2) * 32, wn = (wave & 3) * 32;
   const int mbase = mt * kBT, nbase = nt * kBT;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
@@ -87,25 +91,16 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
       *(f32x4*)&Ws[buf][off[i]] = wok[i] ? wv[i] : zero4;
     }
   };
-  f32x4 acc[2][2];
+  f32x16 acc;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = zero4;
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
   auto compute = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < kKC / 16; ++q) {
-      f32x4 x[2], y[2];
+    for (int q = 0; q < kKC / 8; ++q) {
+      const f32x4 x = *(const f32x4*)&As[buf][(wm + l32) * kLdsStride + 8 * q + 4 * lhi];
+      const f32x4 y = *(const f32x4*)&Ws[buf][(wn + l32) * kLdsStride + 8 * q + 4 * lhi];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        x[i] = *(const f32x4*)&As[buf][(wm + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
-        y[i] = *(const f32x4*)&Ws[buf][(wn + 16 * i + lrow) * kLdsStride + 16 * q + 4 * lgrp];
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[i][e], y[j][e], acc[i][j], 0, 0, 0);
+      for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[e], y[e], acc, 0, 0, 0);
     }
   };
   if (c0 < c1) {
@@ -121,22 +116,18 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
     }
   }
   const int64_t PT = a.PT > 0 ? a.PT : a.P;
+  const int col = nbase + wn + l32;
+  if (col < a.N) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = nbase + wn + 16 * j + lrow;
-      if (col >= a.N) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = mbase + wm + 16 * i + 4 * lgrp + r;
-        if (row >= GM) continue;
-        const int v = row / a.Mp, sm = row - v * a.Mp;
-        const int64_t p =
-            a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
-        a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col] = acc[i][j][r];
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int row = mbase + wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      if (row >= GM) continue;
+      const int v = row / a.Mp, sm = row - v * a.Mp;
+      const int64_t p =
+          a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+      a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col] = acc[r];
     }
+  }
 }
 
 void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
@@ -457,14 +448,26 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
 }
 
 // gram[0] += gram[1] + ... + gram[KSG-1] over the blocks k2 < k (added in
-// split order), so the consumer reads one sum.
-__global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ gram, int64_t split, int64_t n4, int KSG) {
+// split order), so the consumer reads one sum.  Element i enumerates
+// (block and learner bp, step pair, 16-byte piece q of the Bp x Bp block).
+__global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ gram, int64_t split, int64_t n4, int K1,
+                                                     int pairs, int blk4, int KSG) {
   f32x4* g = (f32x4*)gram;
   const int64_t s4 = split / 4;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-    f32x4 v = g[i];
-    for (int t = 1; t < KSG; ++t) v += g[t * s4 + i];
-    g[i] = v;
+    const int q = (int)(i % blk4);
+    const int64_t t = i / blk4;
+    const int pr = (int)(t % pairs);
+    const int64_t bp = t / pairs;
+    int k = 1, k2 = pr;
+    while (k2 >= k) {
+      k2 -= k;
+      ++k;
+    }
+    const int64_t o = ((bp * K1 + k) * K1 + k2) * blk4 + q;
+    f32x4 v = g[o];
+    for (int t2 = 1; t2 < KSG; ++t2) v += g[t2 * s4 + o];
+    g[o] = v;
   }
 }
 
@@ -500,9 +503,10 @@ void launch_gram(hipStream_t s, const float* X, int64_t ldx, int K, const int32_
 
 void launch_gram_reduce(hipStream_t s, float* gram, int P, int K1, int K2, int Bp, int KSG) {
   const int64_t split = (int64_t)K2 * P * K1 * K1 * Bp * Bp;
-  const int64_t n4 = split / 4;
+  const int pairs = K1 * (K1 - 1) / 2, blk4 = Bp * Bp / 4;
+  const int64_t n4 = (int64_t)K2 * P * pairs * blk4;
   const int64_t g = std::min<int64_t>((n4 + 255) / 256, 2048);
-  launch(k_gram_reduce, (unsigned)g, 256, 0, s, gram, split, n4, KSG);
+  launch(k_gram_reduce, (unsigned)g, 256, 0, s, gram, split, n4, K1, pairs, blk4, KSG);
 }
 
 }  // namespace hav
