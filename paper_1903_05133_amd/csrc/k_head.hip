@@ -382,14 +382,16 @@ template <int KC>
 __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   constexpr int kG = 256 / kHU, kR = kHM / kG;
   constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
-  constexpr int kGrl = kCorrMaxK * kHM * (kHM + 4);  // Gram rows of step k
+  constexpr int kGrlS = kHM + 1;                    // Gram row stride (conflict-free column reads)
+  constexpr int kGrl = kCorrMaxK * kHM * kGrlS;      // Gram rows of step k
   constexpr int kPhaseA = kHM * (KC + 1) + kG * (KC + 1) * kHU;
   constexpr int kZs = kHM * (kHU + 1);
-  constexpr int kRegion = kPhaseA > kZs ? kPhaseA : kZs;
+  constexpr int kCbuf = 4 * kHM * (kHM + 1);          // per-wave partial corrections
+  constexpr int kRegion = kPhaseA > kZs + kCbuf ? kPhaseA : kZs + kCbuf;
   __shared__ __attribute__((aligned(16))) float lds[kGsl + kGrl + kRegion + KC * (kHU + 1) + kHU + KC];
   __shared__ int ys[kHM];
   auto gsl = [&](int k2, int s, int u) -> float& { return lds[(k2 * kHM + s) * kHU + u]; };
-  float* grl = lds + kGsl;          // [kCorrMaxK][kHM][kHM + 4]
+  float* grl = lds + kGsl;          // [kCorrMaxK][kHM][kGrlS]
   float* region = grl + kGrl;
   float* ws = region + kRegion;     // [KC][kHU + 1] W2 slice (after (A))
   float* bs = ws + KC * (kHU + 1);  // [kHU] b1 slice (after (A))
@@ -564,22 +566,41 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   for (int k2 = 0; k2 < kCorrMaxK; ++k2)
     if (k2 < kc && tid < Mp * Mp / 4) {
       const int rem = 4 * tid;
-      *(f32x4*)&grl[(k2 * kHM + rem / Mp) * (kHM + 4) + rem % Mp] = gr[k2];
+      float* g = &grl[(k2 * kHM + rem / Mp) * kGrlS + rem % Mp];
+      g[0] = gr[k2].x;
+      g[1] = gr[k2].y;
+      g[2] = gr[k2].z;
+      g[3] = gr[k2].w;
     }
-  float* zs = region;  // [kHM][kHU + 1]
+  float* zs = region;           // [kHM][kHU + 1]
+  float* cbuf = region + kZs;   // [4][kHM][kHM + 1]
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
   if (kc > 0) {
-    // Rows and columns past M are zero in the staged errors, so the sum runs
-    // over the padded minibatch in fours.
-    f32x4 c = zero4;
-    for (int k2 = 0; k2 < kc; ++k2)
-#pragma unroll 2
-      for (int s2 = 0; s2 < Mp; s2 += 4) {
-        const f32x4 gg = *(const f32x4*)&grl[(k2 * kHM + rr) * (kHM + 4) + s2];
+    // The correction sum_{k2<k} gram[k][k2] G1[k2] of this slice is a 32 x 32
+    // product with k*Mp terms: wave w takes the steps k2 = w, w + 4 as 32x32x2
+    // MFMAs (lane (l, h): Gram row l and error row l of unit l at s2 = 2j + h);
+    // the waves' partial tiles are added in wave order.  Staged errors are
+    // zero past row M, so the sum runs over the padded minibatch.
+    const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, lhi = lane >> 5;
+    if (wave < kc) {
+      f32x16 acc;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) c += gg[i] * *(const f32x4*)&gsl(k2, s2 + i, 4 * u4);
-      }
+      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+      for (int k2 = wave; k2 < kc; k2 += 4)
+        for (int j = 0; j < Mp / 2; ++j)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(grl[(k2 * kHM + l32) * kGrlS + 2 * j + lhi],
+                                                     gsl(k2, 2 * j + lhi, l32), acc, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        cbuf[(wave * kHM + 8 * (r >> 2) + 4 * lhi + (r & 3)) * (kHM + 1) + l32] = acc[r];
+    }
+    __syncthreads();
+    f32x4 c = zero4;
+    for (int w = 0; w < (kc < 4 ? kc : 4); ++w) {
+      const float* cr = cbuf + (w * kHM + rr) * (kHM + 1) + 4 * u4;
+      c += f32x4{cr[0], cr[1], cr[2], cr[3]};
+    }
     z -= lr * c;
   }
   const bool mok = rr < M;
