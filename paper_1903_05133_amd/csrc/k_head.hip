@@ -461,8 +461,19 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
       const bool ok = mm < M && c < C;
       const float* pl = plp + (((int64_t)p * Mp + (ok ? mm : 0)) * Cp + (ok ? c : 0)) * htiles;
       float l = 0.0f;
+      if ((htiles & 3) == 0) {  // 16-byte pieces, still added in slice order
+#pragma unroll 4
+        for (int t = 0; t < htiles; t += 4) {
+          const f32x4 v = *(const f32x4*)(pl + t);
+          l += v.x;
+          l += v.y;
+          l += v.z;
+          l += v.w;
+        }
+      } else {
 #pragma unroll 8
-      for (int t = 0; t < htiles; ++t) l += pl[t];
+        for (int t = 0; t < htiles; ++t) l += pl[t];
+      }
       g2s[mm * (KC + 1) + c] = ok ? l : 0.0f;
     }
     __syncthreads();
