@@ -63,8 +63,8 @@ typedef struct hieravg* hieravg_t;
  *           updates G^T X.  The forward uses the block-start copy plus the
  *           correction -lr * sum_{k'<k} (X_k X_k'^T) G_k' and the cluster
  *           mean at the block end is one update of the copy by the summed
- *           G^T X of the cluster's learners and steps.  Needs the MLP with at
- *           most 32 classes, B <= 32, K1 <= 8, K1*S*B <= 16384, plain SGD
+ *           G^T X of the cluster's learners and steps.  Needs the MLP with
+ *           B <= 32, K1 <= 8, K1*S*B <= 16384, plain SGD
  *           (momentum = weight_decay = 0), and a round that starts with equal
  *           W1 in every replica (true after create and after every round;
  *           after hieravg_set_params the next round runs EAGER).

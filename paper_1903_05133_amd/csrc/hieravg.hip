@@ -44,7 +44,7 @@ const char* kClassNames[KC_COUNT] = {
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
-    "momentum_buffer_group_mean", "momentum_buffer_global_mean"};
+    "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -101,6 +101,7 @@ struct hieravg {
   float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
   float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
   int32_t* ylab = nullptr; // [T][P][B] labels of the drawn samples (delayed schedule)
+  float* part2 = nullptr;  // layer-2 split-K partials of the delayed schedule with more than 32 classes
   // Evaluation (allocated at the first hieravg_evaluate).
   int eval_rows = 0;                  // chunk capacity (multiple of 16)
   int32_t* eval_iota = nullptr;       // [eval_rows] 0, 1, 2, ...
@@ -156,7 +157,7 @@ void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper,
-                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->eval_iota,
+                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -190,7 +191,7 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
 
 bool delayed_applies(const hieravg_config& c) {
   const bool whole_blocks = c.k_global == 0 || c.k_global % c.K1 == 0;
-  return c.kind == HIERAVG_KIND_MLP && c.classes <= kSmallC && c.B <= 32 && c.K1 <= 8 && whole_blocks &&
+  return c.kind == HIERAVG_KIND_MLP && c.B <= 32 && c.K1 <= 8 && whole_blocks &&
          (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows && c.momentum == 0.0f && c.weight_decay == 0.0f;
 }
 
@@ -215,8 +216,8 @@ int validate(const hieravg_config& c) {
   if (!std::isfinite(c.weight_decay) || c.weight_decay < 0.0f) return bad("weight_decay must be finite and >= 0");
   if (c.avg_momentum != 0 && c.avg_momentum != 1) return bad("avg_momentum must be 0 or 1");
   if (c.update_mode == HIERAVG_UPDATE_DELAYED && !delayed_applies(c))
-    return bad("delayed updates need the MLP with at most 32 classes, B <= 32, K1 <= 8, K1*S*B <= 16384, "
-               "whole blocks and plain SGD (no momentum or weight decay)");
+    return bad("delayed updates need the MLP with B <= 32, K1 <= 8, K1*S*B <= 16384, whole blocks and plain SGD "
+               "(no momentum or weight decay)");
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
     if (!std::isfinite(c.init_std) || !std::isfinite(c.grad_std)) return bad("averaging: stds must be finite");
@@ -326,7 +327,7 @@ int build(hieravg* h) {
     // Buffers hold the largest launch plan over every batch size up to the
     // create-time B (hieravg_set_batch may lower it).
     h->Bmax = c.B;
-    int64_t part_floats = 0;
+    int64_t part_floats = 0, part2_floats = 0;
     bool any_delayed = false;
     int Bp_del = 0;
     for (int b = 16; b <= round_up(c.B, 16); b += 16) {
@@ -335,6 +336,7 @@ int build(hieravg* h) {
       if (h->delayed) {
         any_delayed = true;
         Bp_del = std::max(Bp_del, h->Bp);
+        part2_floats = std::max<int64_t>(part2_floats, (int64_t)h->KS2 * P * h->Bp * h->Cp);
       }
     }
     plan(h, c.B);
@@ -362,6 +364,11 @@ int build(hieravg* h) {
       if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->ylab, sizeof(int32_t) * (size_t)T * P * c.B, "sample labels"))) return rc;
+      // more than 32 classes: the layer-2 partials of a step must not overwrite
+      // the block forward's partials of the later steps
+      if (h->C > kSmallC &&
+          (rc = alloc_zero(h, (void**)&h->part2, sizeof(float) * part2_floats, "layer-2 partials")))
+        return rc;
       h->KSG = gram_splits(P, c.K2, (int)h->INp);
       if (c.K1 > 1 && (rc = alloc_zero(h, (void**)&h->gram,
                                        sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * Bp_del * Bp_del, "Gram blocks")))
@@ -441,8 +448,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
     }
     case KC_SOFTMAX:
       if (small) return false;
-      launch_softmax_grad(s, h->part, mlp ? h->KS2 : h->ks_cur, W + (mlp ? h->off_b2 : h->off_b1), h->Dp, h->y, ix,
-                          h->G2, P, B, Bp, C, Cp);
+      launch_softmax_grad(s, h->in_delayed ? h->part2 : h->part, mlp ? h->KS2 : h->ks_cur,
+                          W + (mlp ? h->off_b2 : h->off_b1), h->Dp, h->y, ix, h->G2, P, B, Bp, C, Cp);
       return true;
     case KC_UPDATE1: {
       // With the small-C head, b1 took its step in k_head_b; the softmax
@@ -604,14 +611,41 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     case KC_FWD2: {
       if (small) return false;
-      FwdArgs f{h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, h->part, P, B, Bp, Cp, Hp, h->KS2, h->cps2};
+      FwdArgs f{h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, h->in_delayed ? h->part2 : h->part, P, B, Bp, Cp,
+                Hp, h->KS2, h->cps2};
       launch_fwd(s, f, A_RELU);
       return true;
     }
     case KC_BWD_HIDDEN:
       if (small) return false;
-      launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp);
+      if (h->in_delayed)  // the hidden errors are kept for the block end; b1 takes its step here
+        launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp, P, B,
+                          Bp, C, Cp, Hp, W + h->off_b1, h->hyper);
+      else
+        launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp);
       return true;
+    case KC_Z1_DELAYED: {
+      if (!h->in_delayed || small) return false;
+      Z1Args a{};
+      const int k = tt % c.K1;
+      a.part = h->part + (int64_t)k * P * Bp * Hp;
+      a.KS = h->ks_cur;
+      a.split = (int64_t)c.K1 * P * Bp * Hp;
+      a.b1 = W + h->off_b1;
+      a.w_pitch = h->Dp;
+      a.gs = h->Gs;
+      a.gram = h->gram ? h->gram + (int64_t)(tt / c.K1) * P * c.K1 * c.K1 * Bp * Bp : nullptr;
+      a.Z1 = h->Z1;
+      a.lr = h->hyper;
+      a.P = P;
+      a.M = B;
+      a.Mp = Bp;
+      a.Hp = Hp;
+      a.K1 = c.K1;
+      a.k = k;
+      launch_z1_delayed(s, a);
+      return true;
+    }
     case KC_UPDATE2: {
       if (small) return false;
       UpdArgs u{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
@@ -802,8 +836,13 @@ void enqueue_round(hieravg* h) {
     }
     for (int b = 0; b < c.K2; ++b) {
       go(KC_FWD1_BLOCK, b * c.K1);
-      for (int k = 0; k < c.K1; ++k) go(KC_HEAD_STEP, b * c.K1 + k);
-      go(KC_HEAD_END, b * c.K1 + c.K1 - 1);
+      if (h->C <= kSmallC) {
+        for (int k = 0; k < c.K1; ++k) go(KC_HEAD_STEP, b * c.K1 + k);
+        go(KC_HEAD_END, b * c.K1 + c.K1 - 1);
+      } else {  // more than 32 classes: the layer-2 GEMMs of the eager head, per step
+        for (int k = 0; k < c.K1; ++k)
+          for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2}) go(kc, b * c.K1 + k);
+      }
       go(KC_BLOCK_UPDATE, b * c.K1);
       if (b < c.K2 - 1 && S > 1) go(KC_TAIL_MEAN, 0);
     }

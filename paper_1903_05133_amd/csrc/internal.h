@@ -97,6 +97,7 @@ enum KernelClass {
   KC_GRAM_REDUCE,    // delayed updates: sum of the Gram blocks' feature splits
   KC_HEAD_STEP,      // delayed updates: backward of step k-1 + forward and loss gradient of step k
   KC_HEAD_END,       // delayed updates: backward of a block's last step
+  KC_Z1_DELAYED,     // delayed updates, more than 32 classes: pre-activations with the Gram correction
   KC_VMEAN_GROUP,    // averaged momentum buffers: cluster mean of v
   KC_VMEAN_GLOBAL,   // averaged momentum buffers: global mean of v
   KC_COUNT
@@ -246,8 +247,27 @@ void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* b
                         int P, int M, int Mp, int N);
 void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp);
+// b1 (optional, replica 0's; replica p at + p*w_pitch): also take the SGD step
+// b1[h] -= lr * sum_m G1[m][h] (delayed updates, where no update GEMM steps b1).
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
-                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp);
+                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1 = nullptr,
+                       const float* lr = nullptr);
+// Pre-activations of step k of a block under delayed updates for the head
+// with more than 32 classes: Z1 = b1 + sum of the split-K partials
+// - lr * sum_{k2<k} gram[k][k2] G1[k2] (M <= 32, K1 <= 8).
+struct Z1Args {
+  const float* part;      // step k's layer-1 split-K partials (split floats apart)
+  int KS;
+  int64_t split;
+  const float* b1;        // replica 0's b1; replica p at + p*w_pitch
+  int64_t w_pitch;
+  const float* gs;        // [K1][P][Mp][Hp] hidden errors of the block's steps
+  const float* gram;      // [P][K1][K1][Mp][Mp] of the block
+  float* Z1;              // [P][Mp][Hp]
+  const float* lr;
+  int P, M, Mp, Hp, K1, k;
+};
+void launch_z1_delayed(hipStream_t s, const Z1Args& a);
 // Correction of the first-layer pre-activations under delayed updates: at
 // step k of a block the learner's first weight block is its block base minus
 // lr times the sum of its previous steps' G^T X, so

@@ -86,49 +86,128 @@ __global__ __launch_bounds__(256) void k_softmax_grad(const float* __restrict__ 
 }
 
 // G1[p][m][h] = (sum_{c<C} G2[p][m][c] * W2_p[c][h]) * [Z1[p][m][h] > 0] for
-// m < M; one thread per hidden unit h, 16 samples at a time, G2 staged in LDS.
+// m < M.  Workgroup (p, 64 hidden units): lane = unit, wave w = a quarter of
+// each 64-class chunk of G2 (staged in LDS, 16 samples at a time); the four
+// waves' partial sums are added in wave order through LDS.  With b1, the
+// unit's sum over the samples also takes the SGD step of b1[h].
 __global__ __launch_bounds__(256) void k_bwd_hidden(const float* __restrict__ G2, const float* __restrict__ W2,
                                                     int64_t w_pitch, const float* __restrict__ Z1,
                                                     float* __restrict__ G1, int M, int Mp, int C, int Cp, int Hp,
-                                                    int htiles) {
-  constexpr int MC = 16, CC = 64;
+                                                    int htiles, float* __restrict__ b1,
+                                                    const float* __restrict__ lr_ptr) {
+  constexpr int MC = 16, CC = 64, HU = 64, NW = 4, CW = CC / NW;
   __shared__ float gs[MC][CC];
+  __shared__ float red[NW][MC][HU];
   const int p = blockIdx.x / htiles;
-  const int h = (blockIdx.x % htiles) * 256 + threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int h = (blockIdx.x % htiles) * HU + lane;
   const bool hok = h < Hp;
   const float* w2 = W2 + (int64_t)p * w_pitch;
   const float* g2 = G2 + (int64_t)p * Mp * Cp;
+  float db1 = 0.0f;
   for (int m0 = 0; m0 < M; m0 += MC) {
     float acc[MC];
 #pragma unroll
     for (int i = 0; i < MC; ++i) acc[i] = 0.0f;
     for (int c0 = 0; c0 < C; c0 += CC) {
       __syncthreads();
-      for (int e = threadIdx.x; e < MC * CC; e += 256) {
+      for (int e = tid; e < MC * CC; e += 256) {
         const int mm = e / CC, cc = e % CC;
-        gs[mm][cc] = (m0 + mm < M && c0 + cc < C) ? g2[(int64_t)(m0 + mm) * Cp + c0 + cc] : 0.0f;
+        const bool ok = m0 + mm < M && c0 + cc < C;
+        const float v = g2[(int64_t)(ok ? m0 + mm : 0) * Cp + (ok ? c0 + cc : 0)];
+        gs[mm][cc] = ok ? v : 0.0f;
       }
       __syncthreads();
-      if (hok) {
-        const int cn = min(CC, C - c0);
-        for (int cc = 0; cc < cn; ++cc) {
-          const float w = w2[(int64_t)(c0 + cc) * Hp + h];
+      const int cb = c0 + CW * w;
+#pragma unroll 4
+      for (int cc = 0; cc < CW; ++cc) {
+        const int c = cb + cc;
+        const float wv = w2[(int64_t)(c < C ? c : 0) * Hp + (hok ? h : 0)];
+        const float wt = c < C ? wv : 0.0f;
 #pragma unroll
-          for (int i = 0; i < MC; ++i) acc[i] += gs[i][cc] * w;
-        }
+        for (int i = 0; i < MC; ++i) acc[i] += gs[i][CW * w + cc] * wt;
       }
     }
-    if (hok) {
 #pragma unroll
-      for (int i = 0; i < MC; ++i) {
-        const int m = m0 + i;
-        if (m < M) {
-          const int64_t o = ((int64_t)p * Mp + m) * Hp + h;
-          G1[o] = Z1[o] > 0.0f ? acc[i] : 0.0f;
-        }
+    for (int i = 0; i < MC; ++i) red[w][i][lane] = acc[i];
+    __syncthreads();
+    // wave w finishes samples w*4 .. w*4+3 of the chunk
+#pragma unroll
+    for (int j = 0; j < MC / NW; ++j) {
+      const int i = MC / NW * w + j, m = m0 + i;
+      const float g = ((red[0][i][lane] + red[1][i][lane]) + red[2][i][lane]) + red[3][i][lane];
+      if (hok && m < M) {
+        const int64_t o = ((int64_t)p * Mp + m) * Hp + h;
+        const float g1 = Z1[o] > 0.0f ? g : 0.0f;
+        G1[o] = g1;
+        db1 += g1;
       }
     }
   }
+  if (b1) {  // the four waves' sample sums, in wave order
+    __syncthreads();
+    red[w][0][lane] = db1;
+    __syncthreads();
+    if (w == 0 && hok)
+      b1[(int64_t)p * w_pitch + h] -= *lr_ptr * (((red[0][0][lane] + red[1][0][lane]) + red[2][0][lane]) + red[3][0][lane]);
+  }
+}
+
+// Delayed-update pre-activations for the head with more than 32 classes
+// (Z1Args): workgroup (p, slice of 32 hidden units); the Gram correction as in
+// k_head_step (32x32x2 MFMAs over the earlier steps, split over the waves).
+__global__ __launch_bounds__(256) void k_z1_delayed(Z1Args a, int htiles) {
+  constexpr int kHS = 32, kMS = 32, kGrlS = kMS + 1, kMaxK = 7;
+  __shared__ __attribute__((aligned(16))) float gsl[kMaxK][kMS][kHS];
+  __shared__ float grl[kMaxK][kMS][kGrlS];
+  __shared__ float cbuf[4][kMS][kMS + 1];
+  const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
+  const int tid = threadIdx.x, u4 = tid & 7, rr = tid >> 3;
+  const int M = a.M, Mp = a.Mp, Hp = a.Hp, kc = a.k;
+  const int h4 = ht * kHS + 4 * u4;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 z = zero4;
+  const float* pm = a.part + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+#pragma unroll 8
+  for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
+  z += *(const f32x4*)(a.b1 + (int64_t)p * a.w_pitch + h4);
+  if (kc > 0) {
+    const int gsm = tid / (kHS / 4), gc4 = tid % (kHS / 4);
+    for (int k2 = 0; k2 < kc; ++k2) {
+      const f32x4 v =
+          *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + (gsm < M ? gsm : 0)) * Hp + ht * kHS + 4 * gc4);
+      *(f32x4*)&gsl[k2][gsm][4 * gc4] = gsm < M ? v : zero4;
+    }
+    const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
+    for (int e = tid; e < kc * Mp * Mp; e += 256) {
+      const int k2 = e / (Mp * Mp), rem = e % (Mp * Mp);
+      grl[k2][rem / Mp][rem % Mp] = gk[(int64_t)k2 * Mp * Mp + rem];
+    }
+    __syncthreads();
+    const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, lhi = lane >> 5;
+    if (wave < kc) {
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+      for (int k2 = wave; k2 < kc; k2 += 4)
+        for (int j = 0; j < Mp / 2; ++j)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(grl[k2][l32][2 * j + lhi], gsl[k2][2 * j + lhi][l32], acc, 0,
+                                                     0, 0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) cbuf[wave][8 * (r >> 2) + 4 * lhi + (r & 3)][l32] = acc[r];
+    }
+    __syncthreads();
+    f32x4 c = zero4;
+    for (int w = 0; w < (kc < 4 ? kc : 4); ++w)
+      c += f32x4{cbuf[w][rr][4 * u4], cbuf[w][rr][4 * u4 + 1], cbuf[w][rr][4 * u4 + 2], cbuf[w][rr][4 * u4 + 3]};
+    z -= *a.lr * c;
+  }
+  if (rr < M) *(f32x4*)(a.Z1 + ((int64_t)p * Mp + rr) * Hp + h4) = z;
+}
+
+void launch_z1_delayed(hipStream_t s, const Z1Args& a) {
+  const int htiles = a.Hp / 32;
+  launch(k_z1_delayed, a.P * htiles, 256, 0, s, a, htiles);
 }
 
 // ------------------------------------------------------------ small C
@@ -703,9 +782,9 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
 }
 
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
-                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp) {
-  const int htiles = (Hp + 255) / 256;
-  launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles);
+                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr) {
+  const int htiles = (Hp + 63) / 64;
+  launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles, b1, lr);
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,

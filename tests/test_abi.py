@@ -66,8 +66,8 @@ def test_invalid_config_rejected():
     c = config(1, 4, 2, 1, 1, B=8, in_dim=10, hidden=5, classes=3, n_samples=10, update_mode=3)
     assert not L.hieravg_create_config(ctypes.byref(c))
     assert "update_mode" in L.hieravg_last_error().decode()
-    # delayed first-layer updates: MLP with at most 32 classes, B <= 32, K1 <= 8
-    for kw in (dict(classes=33, B=8, K1=1), dict(classes=3, B=33, K1=1), dict(classes=3, B=8, K1=9)):
+    # delayed first-layer updates: MLP with B <= 32, K1 <= 8
+    for kw in (dict(classes=3, B=33, K1=1), dict(classes=3, B=8, K1=9)):
         c = config(1, 4, 2, kw["K1"], 1, B=kw["B"], in_dim=10, hidden=5, classes=kw["classes"], n_samples=10,
                    update_mode=2)
         assert not L.hieravg_create_config(ctypes.byref(c))

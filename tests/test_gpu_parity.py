@@ -93,6 +93,31 @@ def test_small_cases_delayed_updates_match_oracle(name, gpu_lib):
     _check(c, got, idx, *_oracle(c, 2))
 
 
+LARGE_C_DELAYED = {
+    # more than 32 classes: per step the pre-activation kernel with the Gram
+    # correction, then the layer-2 GEMM head; ragged hidden width
+    "mlp_c40_K1_3": cases.case("mlp", 4, 2, 3, 2, B=20, IN=130, H=70, C=40, N=300, sigma=0.5, lr=0.05, seed=41),
+    "mlp_c100_K1_1": cases.case("mlp", 2, 2, 1, 3, B=7, IN=64, H=96, C=100, N=50, sigma=0.5, lr=0.1, seed=42),
+    "mlp_c33_K1_8": cases.case("mlp", 4, 4, 8, 1, B=32, IN=96, H=64, C=33, N=200, sigma=0.5, lr=0.05, seed=43),
+}
+
+
+@pytest.mark.parametrize("name", sorted(LARGE_C_DELAYED))
+def test_large_class_delayed_updates_match_oracle(name, gpu_lib):
+    from paper_1903_05133_amd import HierAvg
+    c = LARGE_C_DELAYED[name]
+    with HierAvg(config=cases.native_config(c, "delayed")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+        h.profile(False)
+        h.round()
+        got = h.params()
+        idx = h.last_indices()
+    assert "block_update_gemm" in stats and "z1_delayed" in stats and "head_step" not in stats
+    _check(c, got, idx, *_oracle(c, 2))
+
+
 def test_delayed_updates_long_block(gpu_lib):
     """K1 = 8 earlier-step corrections (the largest block the delayed path
     takes), B = 32, S = 2, three blocks."""
