@@ -477,8 +477,12 @@ constexpr int kStepTargetWG = HAV_STEP_TARGET_WG;
 #endif
 constexpr int kStepMaxB = 64;  // largest minibatch of the fused step
 
+// Occupancy: at least four waves per SIMD for a single learner per group
+// (its prefetch registers then fit in 128 VGPRs), three with the group mean
+// of up to 8 x 16 forward rows (larger groups would spill).
 template <int SG, int MBF>
-__global__ __launch_bounds__(256) void k_step_w1(StepArgs a, int mtiles, int ntiles, int nchunks) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4 : SG * MBF <= 8 ? 3 : 1))) void k_step_w1(
+    StepArgs a, int mtiles, int ntiles, int nchunks) {
   constexpr int MP = MBF * 16;        // rows of the next-step forward (padded minibatch)
   constexpr int kWL = kUM / kRP;      // W pieces per thread
   constexpr int kXL = kSC / kRP;      // stage input pieces per thread
