@@ -162,7 +162,9 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats);
 
 /* Overwrite all replicas from a dense [P][D] array laid out as above (host
  * or device memory, n_floats >= P*D).  Momentum buffers are left as they are.
- * Synchronous. */
+ * Synchronous.  When every replica's first weight block is then the same
+ * (a checkpoint taken at a round boundary), the next round may take delayed
+ * updates; otherwise it runs EAGER. */
 int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats);
 
 /* The momentum buffers v of all learners, copied out / in as a dense [P][D]
@@ -216,6 +218,12 @@ int64_t hieravg_dim(hieravg_t h);
 
 /* Global SGD steps taken since creation (K1*K2 per round). */
 int64_t hieravg_step_count(hieravg_t h);
+
+/* Set the global step counter t (t >= 0): the next round draws its
+ * minibatches for steps t, t+1, ...  With hieravg_set_params (and
+ * hieravg_set_momentum) this resumes a run exactly from a checkpoint taken
+ * at a round boundary.  Synchronous; HIERAVG_EINVAL for t < 0. */
+int hieravg_set_step_count(hieravg_t h, int64_t t);
 
 /*
  * Copy the minibatch indices the last round drew, as int32 [T][P][B] with T

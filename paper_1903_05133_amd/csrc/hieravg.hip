@@ -82,6 +82,7 @@ struct hieravg {
   float* G2 = nullptr;     // [P][Bp][Cp] output error
   float* G1 = nullptr;     // [P][Bp][Hp] hidden error
   uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
+  int* flag = nullptr;       // result word of device-side checks
   float* hyper = nullptr;   // [0]: step size lr read by the kernels (hieravg_set_lr)
 
   uint64_t key_index = 0;
@@ -157,7 +158,7 @@ void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper,
-                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->eval_iota,
+                  h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -1097,9 +1098,19 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
       HAV_CHECK(hipMemcpy2DAsync(h->W + (int64_t)p * h->Dp + g.src_off, sizeof(float) * g.src_ld,
                                  src + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
-  HAV_CHECK(hipStreamSynchronize(h->stream));
-  h->w1_shared = false;  // the rows may differ: the next round updates W1 eagerly
+  h->w1_shared = false;  // unless every row's W1 equals row 0's (a round-boundary checkpoint)
   h->rows_stale = false;
+  if (h->cfg.kind == HIERAVG_KIND_MLP) {
+    if (!h->flag) HAV_CHECK(hipMalloc((void**)&h->flag, sizeof(int)));
+    HAV_CHECK(hipMemsetAsync(h->flag, 0, sizeof(int), h->stream));
+    launch_rows_differ(h->stream, h->W + h->off_W1, h->Dp, h->Hp * h->INp, P, h->flag);
+    HAV_CHECK(hipGetLastError());
+    int differ = 0;
+    HAV_CHECK(hipMemcpyAsync(&differ, h->flag, sizeof(int), hipMemcpyDeviceToHost, h->stream));
+    HAV_CHECK(hipStreamSynchronize(h->stream));
+    h->w1_shared = differ == 0;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
 }
 
@@ -1159,6 +1170,22 @@ int64_t hieravg_dim(hieravg_t h) {
     return HIERAVG_EINVAL;
   }
   return h->D;
+}
+
+int hieravg_set_step_count(hieravg_t h, int64_t t) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  if (t < 0) {
+    set_error("the step count must be >= 0");
+    return HIERAVG_EINVAL;
+  }
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  const uint64_t v[2] = {(uint64_t)t, 0};
+  HAV_CHECK(hipMemcpy(h->ctr, v, sizeof(v), hipMemcpyHostToDevice));
+  h->steps = t;
+  return HIERAVG_OK;
 }
 
 int64_t hieravg_step_count(hieravg_t h) {

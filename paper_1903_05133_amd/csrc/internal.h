@@ -330,6 +330,9 @@ void launch_eval_rows(hipStream_t s, const float* part, int KS, int64_t split, c
 void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S);
 // dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4 floats).
 void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n);
+// flag = 1 if any of rows 1..n-1 of W (pitch floats apart) differs from row 0
+// in columns [0, len) (bit patterns; len a multiple of 4); flag untouched otherwise.
+void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t len, int n, int* flag);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, const float* lr, float mu, float wd);
 

@@ -189,6 +189,22 @@ void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch
   launch(k_mean_rows, col_runs(n4, 256, 1), 256, 0, s, (f32x4*)dst, (const f32x4*)src, pitch / 4, n4, n);
 }
 
+__global__ __launch_bounds__(256) void k_rows_differ(const int4* __restrict__ W, int64_t pitch4, int64_t n4, int n,
+                                                     int* __restrict__ flag) {
+  const int64_t total = (int64_t)(n - 1) * n4;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int64_t r = 1 + e / n4, i = e % n4;
+    const int4 a = W[r * pitch4 + i], b = W[i];
+    if (a.x != b.x || a.y != b.y || a.z != b.z || a.w != b.w) *flag = 1;
+  }
+}
+
+void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t len, int n, int* flag) {
+  if (n < 2) return;
+  launch(k_rows_differ, col_runs((int64_t)(n - 1) * (len / 4), 256, 1), 256, 0, s, (const int4*)W, pitch / 4,
+         len / 4, n, flag);
+}
+
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, const float* lr, float mu, float wd) {
   const int64_t n4 = Dp / 4;

@@ -86,6 +86,40 @@ class HierAvg:
             a = np.ascontiguousarray(arr, dtype=np.float32)
             native.check(native.lib().hieravg_set_params(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
 
+    def set_step_count(self, t):
+        """Global step counter: the next round draws its minibatches for steps t, t+1, ..."""
+        native.check(native.lib().hieravg_set_step_count(self._h, t))
+
+    def state(self):
+        """Checkpoint at a round boundary: replicas, momentum buffers (None
+        without momentum), global step count."""
+        try:
+            mom = self.momentum()
+        except native.HierAvgError:
+            mom = None
+        return {"params": self.params(), "momentum": mom, "steps": self.steps}
+
+    def load_state(self, st):
+        """Resume from state(): the rounds that follow are those of the
+        uninterrupted run."""
+        self.set_params(st["params"])
+        if st.get("momentum") is not None:
+            self.set_momentum(st["momentum"])
+        self.set_step_count(int(st["steps"]))
+
+    def save(self, path):
+        """Write state() to an .npz file (plain arrays, no pickled objects)."""
+        st = self.state()
+        arrays = {"params": st["params"], "steps": np.array(st["steps"], dtype=np.int64)}
+        if st["momentum"] is not None:
+            arrays["momentum"] = st["momentum"]
+        np.savez(path, **arrays)
+
+    def load(self, path):
+        with np.load(path, allow_pickle=False) as z:
+            self.load_state({"params": z["params"], "steps": int(z["steps"]),
+                             "momentum": z["momentum"] if "momentum" in z.files else None})
+
     def momentum(self):
         """Momentum buffers of all learners as [P, D] float32 (numpy)."""
         out = np.empty((self.P, self.D), dtype=np.float32)

@@ -40,6 +40,7 @@ SIGNATURES = {
     "hieravg_destroy": (None, [_H]),
     "hieravg_set_lr": (ctypes.c_int, [_H, ctypes.c_float]),
     "hieravg_set_batch": (ctypes.c_int, [_H, ctypes.c_int32]),
+    "hieravg_set_step_count": (ctypes.c_int, [_H, ctypes.c_int64]),
     "hieravg_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_set_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,

@@ -228,9 +228,9 @@ def test_resume_from_params_continues_the_trajectory(gpu_lib):
         w1 = h.params()
     with HierAvg(config=cases.native_config(c)) as h2:
         h2.set_params(w1)
-        h2.round()  # rows set by the caller: eager first-layer updates
+        h2.round()  # equal rows (a round-boundary state): delayed updates
         got = h2.params()
-        h2.round()  # equal rows again: delayed updates
+        h2.round()
         got2 = h2.params()
     st = M.create(prob)
     st.W = w1.astype(np.float64)
@@ -286,12 +286,21 @@ def test_delayed_schedule_profile(gpu_lib):
         assert stats["tail_group_mean"][0] == 2 and stats["tail_global_mean"][0] == 1
         assert stats["w1_global_mean"][0] == 1
         assert not {"fwd1_gemm", "update1_gemm", "step1_gemm", "global_mean"} & set(stats)
-        h.set_params(h.params())
+        h.set_params(h.params())  # equal rows: still delayed
+        h.profile(True)
+        h.round()
+        assert "fwd1_block_gemm" in h.profile_read() and "fwd1_gemm" not in h.profile_read()
+        w = h.params()
+        w[1, 0] += 1.0  # rows that differ: one eager round, then delayed again
+        h.set_params(w)
+        h.profile(False)
         h.profile(True)
         h.round()
         assert "fwd1_gemm" in h.profile_read()
+        h.profile(False)
+        h.profile(True)
         h.round()
-        assert "fwd1_block_gemm" in h.profile_read()
+        assert "fwd1_block_gemm" in h.profile_read() and "fwd1_gemm" not in h.profile_read()
 
 
 def test_unfused_schedule_profile(gpu_lib):
@@ -510,3 +519,37 @@ def test_no_buffers_without_momentum(gpu_lib):
     with HierAvg(config=cases.native_config(MOMENTUM_CASES["softmax_decay_only"])) as h:
         with pytest.raises(Exception):
             h.momentum()
+
+
+@pytest.mark.parametrize("name", ["delayed_mlp", "momentum_softmax", "eager_unequal_rows"])
+def test_checkpoint_resume_is_exact(name, gpu_lib, tmp_path):
+    """save() after one round, load() into a fresh handle, one more round:
+    bit for bit the second round of the uninterrupted run (same step counter,
+    parameters, buffers and, for equal first-layer rows, the same schedule)."""
+    from paper_1903_05133_amd import HierAvg
+    c = {"delayed_mlp": SMALL["mlp_ragged"], "momentum_softmax": MOMENTUM_CASES["softmax_mom_wd"],
+         "eager_unequal_rows": SMALL["mlp_ragged"]}[name]
+    cfg = cases.native_config(c)
+    with HierAvg(config=cfg) as h:
+        h.round()
+        if name == "eager_unequal_rows":  # rows that differ: the resumed round must run eager
+            w = h.params()
+            w[1, 0] += 1.0
+            h.set_params(w)
+        h.save(str(tmp_path / "ck.npz"))
+        h.round()
+        ref, steps = h.params(), h.steps
+        vref = h.momentum() if c["momentum"] > 0 else None
+    with HierAvg(config=cfg) as h2:
+        h2.load(str(tmp_path / "ck.npz"))
+        h2.profile(True)
+        h2.round()
+        stats = h2.profile_read()
+        assert h2.steps == steps
+        assert np.array_equal(h2.params(), ref)
+        if vref is not None:
+            assert np.array_equal(h2.momentum(), vref)
+    if name == "delayed_mlp":
+        assert "fwd1_block_gemm" in stats
+    if name == "eager_unequal_rows":
+        assert "fwd1_block_gemm" not in stats
