@@ -20,9 +20,17 @@ data, with the paper's global interval K1*K2 written as ``k_global``:
   * K1 in {4, 8} and S in {2, 4} at P=16, k_global=32;
   * Hier-AVG against K-AVG (S=1) at the same P, K1 and k_global.
 
+Optimizer and schedule options: ``--momentum``, ``--weight-decay``,
+``--avg-momentum`` (heavy-ball buffers, L2 decay, buffers averaged with the
+parameters), ``--lr-drop ROUND:LR`` (step schedule of Sec. 4, repeatable:
+the step size from that round on), ``--k-global`` (round length in steps,
+non-integer beta), ``--checkpoint PATH`` (state after every round, resumable
+with ``--resume PATH``).
+
 Everything runs through the C ABI on the GPU; the oracle is not used.
 
     python -m paper_1903_05133_amd.convergence --model 1 --P 16 --S 4 --K1 4 --K2 4 --rounds 16
+    python -m paper_1903_05133_amd.convergence --momentum 0.9 --lr 0.02 --lr-drop 12:0.002 --rounds 16
     python -m paper_1903_05133_amd.convergence --sweep paper --steps 256
 """
 
@@ -42,14 +50,28 @@ MODELS = {
 }
 
 
-def run(name, model, P, S, K1, K2, B, lr, rounds, eval_rows, noise=None, seed=0, out=sys.stdout):
+def run(name, model, P, S, K1, K2, B, lr, rounds, eval_rows, noise=None, seed=0, out=sys.stdout, momentum=0.0,
+        weight_decay=0.0, avg_momentum=False, lr_drops=(), k_global=0, checkpoint=None, resume=None):
     kind, IN, H, C, N, sigma = MODELS[model]
     cfg = config(kind, P, S, K1, K2, B=B, in_dim=IN, hidden=H, classes=C, n_samples=N,
-                 noise_std=sigma if noise is None else noise, lr=lr, seed=seed)
+                 noise_std=sigma if noise is None else noise, lr=lr, seed=seed, momentum=momentum,
+                 weight_decay=weight_decay, avg_momentum=avg_momentum, k_global=k_global)
     n_train = min(eval_rows, N)
     curve = []
+    drops = dict(lr_drops)
     with HierAvg(config=cfg) as h:
-        for r in range(1, rounds + 1):
+        first = 1
+        if resume:
+            h.load(resume)
+            first = h.steps // h.T + 1
+        cur_lr = lr
+        for r in range(1, first):
+            cur_lr = drops.get(r, cur_lr)
+        h.set_lr(cur_lr)
+        for r in range(first, rounds + 1):
+            if r in drops:
+                cur_lr = drops[r]
+                h.set_lr(cur_lr)
             t0 = time.perf_counter()
             h.round()
             h.sync()
@@ -58,15 +80,19 @@ def run(name, model, P, S, K1, K2, B, lr, rounds, eval_rows, noise=None, seed=0,
             tr_loss, tr_hit = h.evaluate(0, 0, n_train)
             te_loss, te_hit = h.evaluate(0, 1, eval_rows)
             ems = (time.perf_counter() - t1) * 1e3
-            rec = {"run": name, "round": r, "steps": h.steps, "train_loss": float(f"{tr_loss:.7g}"),
+            rec = {"run": name, "round": r, "steps": h.steps, "lr": cur_lr, "train_loss": float(f"{tr_loss:.7g}"),
                    "train_acc": round(tr_hit / n_train, 6), "test_loss": float(f"{te_loss:.7g}"),
                    "test_acc": round(te_hit / eval_rows, 6), "round_ms": round(ms, 3),
                    "eval_ms": round(ems, 3)}
             curve.append(rec)
             print(json.dumps(rec), file=out, flush=True)
+            if checkpoint:
+                h.save(checkpoint)
     last = curve[-1]
     summary = {"run": name, "summary": True, "model": model, "P": P, "S": S, "K1": K1, "K2": K2,
-               "k_global": K1 * K2, "B": B, "lr": lr, "noise": sigma if noise is None else noise,
+               "k_global": k_global or K1 * K2, "B": B, "lr": lr, "lr_drops": sorted(drops.items()),
+               "momentum": momentum, "weight_decay": weight_decay, "avg_momentum": avg_momentum,
+               "noise": sigma if noise is None else noise,
                "rounds": rounds, "steps": last["steps"], "final_test_loss": last["test_loss"],
                "final_test_acc": last["test_acc"],
                "best_test_loss": min(c["test_loss"] for c in curve)}
@@ -107,12 +133,23 @@ def main(argv=None):
     ap.add_argument("--noise", type=float, default=None, help="override the model's data noise std")
     ap.add_argument("--sweep", choices=["paper"], default=None)
     ap.add_argument("--steps", type=int, default=256, help="local SGD steps per learner of each sweep run")
+    ap.add_argument("--momentum", type=float, default=0.0)
+    ap.add_argument("--weight-decay", type=float, default=0.0)
+    ap.add_argument("--avg-momentum", action="store_true")
+    ap.add_argument("--lr-drop", action="append", default=[], metavar="ROUND:LR",
+                    help="step size from round ROUND on (repeatable)")
+    ap.add_argument("--k-global", type=int, default=0, help="SGD steps per round (0: K1*K2)")
+    ap.add_argument("--checkpoint", default=None, help="write the state after every round (.npz)")
+    ap.add_argument("--resume", default=None, help="continue from a --checkpoint file")
     a = ap.parse_args(argv)
+    drops = [(int(d.split(":")[0]), float(d.split(":")[1])) for d in a.lr_drop]
     native.lib()
     if a.sweep == "paper":
         paper_sweep(a.steps, a.model, a.B, a.lr, a.eval_rows, a.noise)
     else:
-        run("single", a.model, a.P, a.S, a.K1, a.K2, a.B, a.lr, a.rounds, a.eval_rows, a.noise)
+        run("single", a.model, a.P, a.S, a.K1, a.K2, a.B, a.lr, a.rounds, a.eval_rows, a.noise,
+            momentum=a.momentum, weight_decay=a.weight_decay, avg_momentum=a.avg_momentum, lr_drops=drops,
+            k_global=a.k_global, checkpoint=a.checkpoint, resume=a.resume)
 
 
 if __name__ == "__main__":

@@ -370,6 +370,26 @@ def test_convergence_runner(gpu_lib):
     assert 0.0 <= summ["final_test_acc"] <= 1.0
 
 
+def test_convergence_runner_momentum_schedule_and_resume(gpu_lib, tmp_path):
+    """Runner with momentum, a step-size drop and checkpoints: a run resumed
+    from the state after round 2 reports exactly the uninterrupted round 3."""
+    import io
+    import json
+    from paper_1903_05133_amd import convergence
+    kw = dict(noise=5.0, momentum=0.9, weight_decay=1e-3, lr_drops=[(3, 0.001)])
+    full, part, rest = io.StringIO(), io.StringIO(), io.StringIO()
+    convergence.run("a", 0, 4, 2, 2, 2, 8, 0.005, 3, 256, out=full, **kw)
+    ck = str(tmp_path / "state.npz")
+    convergence.run("b", 0, 4, 2, 2, 2, 8, 0.005, 2, 256, out=part, checkpoint=ck, **kw)
+    convergence.run("c", 0, 4, 2, 2, 2, 8, 0.005, 3, 256, out=rest, resume=ck, **kw)
+    a = [json.loads(x) for x in full.getvalue().splitlines() if "summary" not in x]
+    c = [json.loads(x) for x in rest.getvalue().splitlines() if "summary" not in x]
+    assert [x["lr"] for x in a] == [0.005, 0.005, 0.001]
+    assert [x["round"] for x in c] == [3]
+    for key in ("steps", "lr", "train_loss", "train_acc", "test_loss", "test_acc"):
+        assert c[0][key] == a[2][key], key
+
+
 def _schedule_run(c, schedule, mode="auto"):
     """Rounds with a per-round (lr, B) schedule through set_lr / set_batch,
     and the oracle's rounds with the same Problem changed per round."""
