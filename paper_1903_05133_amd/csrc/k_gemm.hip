@@ -263,8 +263,10 @@ constexpr int kLA = kUM + 4;      // LDS row length of the G stage
 constexpr int kLB = kUN + 4;      // LDS row length of the input stage and of the gradient tile
 constexpr int kUpdLds = (kUM * kLB > kSC * (kLA + kLB)) ? kUM * kLB : kSC * (kLA + kLB);
 
+// Four waves per SIMD (128 registers: the stage and tile registers fit).
 template <int BSRC>
-__global__ __launch_bounds__(256) void k_update_tn(UpdArgs a, int mtiles, int ntiles) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_update_tn(UpdArgs a, int mtiles,
+                                                                                          int ntiles) {
   __shared__ __attribute__((aligned(16))) float lds[kUpdLds];
   float* As = lds;               // [kSC][kLA]
   float* Bs = lds + kSC * kLA;   // [kSC][kLB]
