@@ -573,3 +573,27 @@ def test_checkpoint_resume_is_exact(name, gpu_lib, tmp_path):
         assert "fwd1_block_gemm" in stats
     if name == "eager_unequal_rows":
         assert "fwd1_block_gemm" not in stats
+
+
+EDGE_CASES = {
+    # many learners in one cluster (S = P = 512), one step per round
+    "softmax_512_learners": cases.case("softmax", 512, 512, 1, 1, B=2, IN=8, C=3, N=16, lr=0.1, seed=51),
+    # many learners in clusters of 2
+    "mlp_256_learners_S2": cases.case("mlp", 256, 2, 2, 1, B=3, IN=10, H=5, C=2, N=40, lr=0.1, seed=52),
+    # large minibatch (eager, several 16-row batch tiles and forward chunks)
+    "mlp_batch_1000": cases.case("mlp", 2, 2, 1, 2, B=1000, IN=40, H=20, C=3, N=5000, sigma=0.5, lr=0.05, seed=53),
+    # one input feature, one hidden unit, two classes
+    "mlp_tiny_dims": cases.case("mlp", 4, 2, 2, 2, B=5, IN=1, H=1, C=2, N=9, lr=0.2, seed=54),
+    # a long round: 100 steps, blocks of 7 (the last one of 2 steps)
+    "softmax_100_steps": cases.case("softmax", 4, 2, 7, 1, B=4, IN=12, C=5, N=30, lr=0.05, seed=55, k_global=100),
+    # averaging kind with 1024 replicas of a short vector
+    "averaging_1024_rows": cases.case("averaging", 1024, 32, 1, 2, IN=300, lr=0.1, momentum=0.9, seed=56),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE_CASES))
+def test_edge_shapes_match_oracle(name, gpu_lib):
+    c = EDGE_CASES[name]
+    got, idx, steps = _run_gpu(c, rounds=1)
+    assert steps == (c["k_global"] or c["K1"] * c["K2"])
+    _check(c, got, idx, *_oracle(c, 1))
