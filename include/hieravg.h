@@ -41,6 +41,7 @@ typedef struct hieravg* hieravg_t;
 #define HIERAVG_EINVAL (-1) /* bad argument or handle                      */
 #define HIERAVG_EHIP (-2)   /* HIP runtime or kernel error                 */
 #define HIERAVG_ESIZE (-3)  /* destination/source size too small / too big */
+#define HIERAVG_ENONFINITE (-4) /* hieravg_check_finite: a replica holds inf or NaN */
 
 /* Model kinds (what one learner's SGD step computes). */
 #define HIERAVG_KIND_SOFTMAX 0   /* softmax regression, IN -> C             */
@@ -218,6 +219,11 @@ int64_t hieravg_dim(hieravg_t h);
 
 /* Global SGD steps taken since creation (K1*K2 per round). */
 int64_t hieravg_step_count(hieravg_t h);
+
+/* Divergence check: synchronise and scan every replica; HIERAVG_OK when all
+ * parameters are finite, HIERAVG_ENONFINITE when any is inf or NaN (for
+ * example after a step size too large for the data). */
+int hieravg_check_finite(hieravg_t h);
 
 /* Set the global step counter t (t >= 0): the next round draws its
  * minibatches for steps t, t+1, ...  With hieravg_set_params (and

@@ -20,6 +20,7 @@
 // the global mean.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -83,6 +84,7 @@ struct hieravg {
   float* G1 = nullptr;     // [P][Bp][Hp] hidden error
   uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
   int* flag = nullptr;       // result word of device-side checks
+  int n_allocs = 0, fail_alloc = 0;  // allocation count of create; the forced failure (debug)
   float* hyper = nullptr;   // [0]: step size lr read by the kernels (hieravg_set_lr)
 
   uint64_t key_index = 0;
@@ -173,8 +175,21 @@ void release(hieravg* h) {
   delete h;
 }
 
+// Debug hook for the failure paths of create: HIERAVG_FAIL_ALLOC=n makes the
+// n-th device allocation of a create (counted from 1) fail.
+int forced_alloc_failure() {
+  const char* v = std::getenv("HIERAVG_FAIL_ALLOC");
+  return v ? std::atoi(v) : 0;
+}
+
 int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
   if (bytes == 0) bytes = 16;
+  ++h->n_allocs;
+  if (h->fail_alloc > 0 && h->n_allocs == h->fail_alloc) {
+    *p = nullptr;
+    set_error(std::string("hipMalloc of ") + what + " failed (HIERAVG_FAIL_ALLOC)");
+    return HIERAVG_EHIP;
+  }
   hipError_t e = hipMalloc(p, bytes);
   if (e != hipSuccess) {
     *p = nullptr;
@@ -736,6 +751,7 @@ hieravg_t hieravg_create_config(const hieravg_config* cfg) {
     return nullptr;
   }
   h->cfg = *cfg;
+  h->fail_alloc = forced_alloc_failure();
   // Steps per round; K2 becomes the number of blocks (the last one shorter
   // when K1 does not divide k_global).
   h->T = cfg->k_global > 0 ? cfg->k_global : cfg->K1 * cfg->K2;
@@ -1170,6 +1186,25 @@ int64_t hieravg_dim(hieravg_t h) {
     return HIERAVG_EINVAL;
   }
   return h->D;
+}
+
+int hieravg_check_finite(hieravg_t h) {
+  if (!h) {
+    set_error("NULL handle");
+    return HIERAVG_EINVAL;
+  }
+  if (!h->flag) HAV_CHECK(hipMalloc((void**)&h->flag, sizeof(int)));
+  HAV_CHECK(hipMemsetAsync(h->flag, 0, sizeof(int), h->stream));
+  launch_any_nonfinite(h->stream, h->W, (int64_t)h->cfg.P * h->Dp, h->flag);
+  HAV_CHECK(hipGetLastError());
+  int bad = 0;
+  HAV_CHECK(hipMemcpyAsync(&bad, h->flag, sizeof(int), hipMemcpyDeviceToHost, h->stream));
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  if (bad) {
+    set_error("a replica holds inf or NaN");
+    return HIERAVG_ENONFINITE;
+  }
+  return HIERAVG_OK;
 }
 
 int hieravg_set_step_count(hieravg_t h, int64_t t) {

@@ -333,6 +333,8 @@ void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch
 // flag = 1 if any of rows 1..n-1 of W (pitch floats apart) differs from row 0
 // in columns [0, len) (bit patterns; len a multiple of 4); flag untouched otherwise.
 void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t len, int n, int* flag);
+// flag = 1 if any of the n floats at W is inf or NaN (n a multiple of 4).
+void launch_any_nonfinite(hipStream_t s, const float* W, int64_t n, int* flag);
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, const float* lr, float mu, float wd);
 

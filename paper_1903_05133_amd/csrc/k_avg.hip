@@ -205,6 +205,21 @@ void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t le
          len / 4, n, flag);
 }
 
+__global__ __launch_bounds__(256) void k_any_nonfinite(const f32x4* __restrict__ W, int64_t n4,
+                                                       int* __restrict__ flag) {
+  bool bad = false;
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const f32x4 v = W[i];
+    bad |= !(isfinite(v.x) && isfinite(v.y) && isfinite(v.z) && isfinite(v.w));
+  }
+  if (bad) *flag = 1;
+}
+
+void launch_any_nonfinite(hipStream_t s, const float* W, int64_t n, int* flag) {
+  launch(k_any_nonfinite, col_runs(n / 4, 256, 1) < 4096 ? col_runs(n / 4, 256, 1) : 4096u, 256, 0, s,
+         (const f32x4*)W, n / 4, flag);
+}
+
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
                           bool average, const float* lr, float mu, float wd) {
   const int64_t n4 = Dp / 4;

@@ -86,6 +86,14 @@ class HierAvg:
             a = np.ascontiguousarray(arr, dtype=np.float32)
             native.check(native.lib().hieravg_set_params(self._h, ctypes.c_void_p(a.ctypes.data), a.size))
 
+    def finite(self):
+        """True when every replica holds finite values (divergence check)."""
+        rc = native.lib().hieravg_check_finite(self._h)
+        if rc == native.ENONFINITE:
+            return False
+        native.check(rc)
+        return True
+
     def set_step_count(self, t):
         """Global step counter: the next round draws its minibatches for steps t, t+1, ..."""
         native.check(native.lib().hieravg_set_step_count(self._h, t))

@@ -7,7 +7,7 @@ import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhieravg.so")
 
-OK, EINVAL, EHIP, ESIZE = 0, -1, -2, -3
+OK, EINVAL, EHIP, ESIZE, ENONFINITE = 0, -1, -2, -3, -4
 KIND_SOFTMAX, KIND_MLP, KIND_AVERAGING = 0, 1, 2
 MODEL_SOFTMAX_3072_10, MODEL_MLP_3072_512_10, MODEL_MLP_150528_1024_1000, MODEL_AVERAGING_11_7M = 0, 1, 2, 3
 
@@ -41,6 +41,7 @@ SIGNATURES = {
     "hieravg_set_lr": (ctypes.c_int, [_H, ctypes.c_float]),
     "hieravg_set_batch": (ctypes.c_int, [_H, ctypes.c_int32]),
     "hieravg_set_step_count": (ctypes.c_int, [_H, ctypes.c_int64]),
+    "hieravg_check_finite": (ctypes.c_int, [_H]),
     "hieravg_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_set_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,

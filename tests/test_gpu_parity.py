@@ -597,3 +597,42 @@ def test_edge_shapes_match_oracle(name, gpu_lib):
     got, idx, steps = _run_gpu(c, rounds=1)
     assert steps == (c["k_global"] or c["K1"] * c["K2"])
     _check(c, got, idx, *_oracle(c, 1))
+
+
+def test_divergence_check(gpu_lib):
+    """hieravg_check_finite: finite replicas pass; a step size far too large
+    for the data drives them to inf/NaN, which the check reports."""
+    from paper_1903_05133_amd import HierAvg
+    ok = cases.case("softmax", 4, 2, 2, 1, B=8, IN=20, C=3, N=40, lr=0.1, seed=61)
+    with HierAvg(config=cases.native_config(ok)) as h:
+        h.round()
+        assert h.finite()
+        h.set_lr(3.0e38)
+        for _ in range(3):
+            h.round()
+        assert not h.finite()
+
+
+def test_forced_allocation_failures_leave_no_broken_state(gpu_lib, monkeypatch):
+    """Every device allocation of create made to fail in turn (debug hook):
+    create returns NULL with a message naming the buffer, nothing leaks into
+    the next handle, which computes the oracle's round."""
+    import ctypes
+    from paper_1903_05133_amd import HierAvg, native
+    c = cases.case("mlp", 4, 2, 2, 2, B=8, IN=50, H=20, C=3, N=40, sigma=0.5, lr=0.1, seed=62)
+    L = native.lib()
+    failed = 0
+    for n in range(1, 40):
+        monkeypatch.setenv("HIERAVG_FAIL_ALLOC", str(n))
+        cfg = cases.native_config(c)
+        h = L.hieravg_create_config(ctypes.byref(cfg))
+        if not h:
+            assert "HIERAVG_FAIL_ALLOC" in L.hieravg_last_error().decode()
+            failed += 1
+        else:
+            L.hieravg_destroy(h)
+            break
+    assert failed >= 5
+    monkeypatch.delenv("HIERAVG_FAIL_ALLOC")
+    got, idx, _ = _run_gpu(c)
+    _check(c, got, idx, *_oracle(c))
