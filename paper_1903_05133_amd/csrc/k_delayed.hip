@@ -261,7 +261,8 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
     if (!wave_on) return;
     const float* As = lds + buf * kStage;
     const float* Bs = As + kSC * kLA;
-#pragma unroll 4
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
     for (int ss = 0; ss < kSC; ss += 2) {
       const int sr = ss + lhi;
       const float av = As[sr * kLA + wm + l32];
@@ -269,6 +270,7 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
       for (int j = 0; j < kNA; ++j)
         acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kLB + wn + 32 * j + l32], acc[j], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
   };
 
   load_stage(0, RA);
