@@ -40,8 +40,8 @@ typedef struct hieravg* hieravg_t;
 #define HIERAVG_OK 0
 #define HIERAVG_EINVAL (-1) /* bad argument or handle                      */
 #define HIERAVG_EHIP (-2)   /* HIP runtime or kernel error                 */
-#define HIERAVG_ESIZE (-3)  /* destination/source size too small / too big */
-#define HIERAVG_ENONFINITE (-4) /* hieravg_check_finite: a replica holds inf or NaN */
+#define HIERAVG_ENONFINITE (-3) /* hieravg_check_finite: a replica holds inf or NaN */
+#define HIERAVG_ESIZE (-4)  /* destination/source size too small / too big */
 
 /* Model kinds (what one learner's SGD step computes). */
 #define HIERAVG_KIND_SOFTMAX 0   /* softmax regression, IN -> C             */

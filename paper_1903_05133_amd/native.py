@@ -7,7 +7,7 @@ import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhieravg.so")
 
-OK, EINVAL, EHIP, ESIZE, ENONFINITE = 0, -1, -2, -3, -4
+OK, EINVAL, EHIP, ENONFINITE, ESIZE = 0, -1, -2, -3, -4
 KIND_SOFTMAX, KIND_MLP, KIND_AVERAGING = 0, 1, 2
 MODEL_SOFTMAX_3072_10, MODEL_MLP_3072_512_10, MODEL_MLP_150528_1024_1000, MODEL_AVERAGING_11_7M = 0, 1, 2, 3
 
