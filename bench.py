@@ -78,6 +78,19 @@ def mean_bytes(P, D):
     return 2 * 4 * P * D
 
 
+def counter_mfma_util(kernel_class):
+    """MfmaUtil (fraction) of `kernel_class` from the committed counter summary
+    (profiles/mfma.json), or None when the kernel's source has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "mfma.json")
+    try:
+        rec = json.load(open(path))["kernels"][kernel_class]
+        cur = hashlib.sha256(open(os.path.join(ROOT, rec["source"]), "rb").read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    return rec["mfma_util"] if cur == rec["source_sha256"] else None
+
+
 def counter_traffic(kernel_class):
     """HBM bytes per launch of `kernel_class` from the committed counter
     summary (profiles/traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled by
@@ -172,6 +185,8 @@ def bench_mlp(args):
                  "alg_bytes_per_launch": b, "alg_flops_per_launch": fl, "avg_us": round(avg_s * 1e6, 3),
                  "hbm_frac": round(b / avg_s / 1e9 / HBM_PEAK_GBS, 4),
                  "mfma_frac": round(fl / avg_s / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4) if fl else None})
+    mu = counter_mfma_util(dom)
+    roof["mfma_util_counter"] = None if mu is None else round(mu, 4)
     steps_per_round = P * K1 * K2
     return {
         "value": steps_per_round * args.steps / (ms * 1e-3),
