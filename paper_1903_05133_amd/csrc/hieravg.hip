@@ -550,30 +550,13 @@ bool launch_class(hieravg* h, int kc, int tt) {
   }
   if (!mlp) return false;
   switch (kc) {
-    case KC_HEAD_A: {
-      if (!small) return false;
-      HeadCorr corr;
-      if (h->in_delayed && h->gram != nullptr) {
-        corr.gram = h->gram + (int64_t)(tt / c.K1) * P * c.K1 * c.K1 * Bp * Bp;
-        corr.gs = h->Gs;
-        corr.k = tt % c.K1;
-        corr.K1 = c.K1;
-        corr.lr = h->hyper;
-      }
-      const float* part = h->part;
-      int64_t split = 0;
-      if (h->in_delayed) {  // the block-wide forward's layout
-        part += (int64_t)(tt % c.K1) * P * Bp * Hp;
-        split = (int64_t)c.K1 * P * Bp * Hp;
-      }
-      launch_head_a(s, part, h->ks_cur, W + h->off_b1, W + h->off_W2, W + h->off_b2, h->Dp, h->Z1, h->PL, P, B,
-                    Bp, C, Cp, Hp, corr, split);
+    case KC_HEAD_A:  // eager schedule (the delayed one runs KC_HEAD_STEP)
+      if (!small || h->in_delayed) return false;
+      launch_head_a(s, h->part, h->ks_cur, W + h->off_b1, W + h->off_W2, W + h->off_b2, h->Dp, h->Z1, h->PL, P, B,
+                    Bp, C, Cp, Hp);
       return true;
-    }
-    case KC_HEAD_B: {
-      if (!small) return false;
-      // Under delayed updates the hidden errors are kept for the block end.
-      float* g1 = h->in_delayed ? h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp : h->G1;
+    case KC_HEAD_B: {  // eager schedule
+      if (!small || h->in_delayed) return false;
       HeadMom mom;
       mom.mu = c.momentum;
       mom.wd = c.weight_decay;
@@ -582,7 +565,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
         mom.vb1 = h->V + h->off_b1;
         mom.vb2 = h->V + h->off_b2;
       }
-      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, g1, h->y, ix, P, B, Bp,
+      launch_head_b(s, h->PL, W + h->off_W2, W + h->off_b1, W + h->off_b2, h->Dp, h->Z1, h->G1, h->y, ix, P, B, Bp,
                     C, Cp, Hp, h->hyper, mom);
       return true;
     }

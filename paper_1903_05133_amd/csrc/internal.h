@@ -268,19 +268,9 @@ struct Z1Args {
   int P, M, Mp, Hp, K1, k;
 };
 void launch_z1_delayed(hipStream_t s, const Z1Args& a);
-// Correction of the first-layer pre-activations under delayed updates: at
-// step k of a block the learner's first weight block is its block base minus
-// lr times the sum of its previous steps' G^T X, so
-//   Z1 = X Wb^T + b1 - lr * sum_{k2<k} gram[k][k2] G[k2].
-struct HeadCorr {
-  const float* gram = nullptr;  // [P][K1][K1][Bp][Bp] of the block (nullptr: none)
-  const float* gs = nullptr;    // [K1][P][Bp][Hp] hidden errors of the block's steps
-  int k = 0, K1 = 1;
-  const float* lr = nullptr;    // device scalar step size
-};
 // part_split: floats between split-K partial sums (0: P * Mp * Hp).
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
-                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr = HeadCorr(),
+                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp,
                    int64_t part_split = 0);
 // Heavy-ball step with L2 decay of the second layer and the biases in
 // k_head_b: buffers laid out like W2, b1, b2 (nullptr: no buffers).

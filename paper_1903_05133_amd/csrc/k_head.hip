@@ -224,22 +224,15 @@ constexpr int kHM = 32;  // samples per chunk
 //   PL[p][m][c][ht] = [ht == 0] b2[c] + sum_{h in slice} ReLU(Z1[m][h]) * W2[c][h]
 // (b2 is folded into slice 0's, so k_head_b never reads the b2 it updates).
 // Thread t reads 16-byte pieces (units 4*(t%8) .. +3) of row t/8 of the chunk.
-// With delayed first-layer updates (corr.gram set) the pre-activations also
-// take the correction -lr * sum_{k2<k} gram[k][k2] G[k2] of the learner's
-// earlier steps in the block (M <= 32: one chunk; the errors' slice for this
-// workgroup's units is staged in LDS, the Gram rows are read per thread).
-constexpr int kCorrMaxK = 7;  // earlier steps in a block (K1 <= 8)
+constexpr int kCorrMaxK = 7;  // earlier steps in a block (K1 <= 8) of the delayed head's corrections
 template <int KC>
 __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, int KS, const float* __restrict__ b1,
                                                 const float* __restrict__ W2, const float* __restrict__ b2,
                                                 int64_t w_pitch,
                                                 float* __restrict__ Z1, float* __restrict__ PL, int P, int M, int Mp,
-                                                int C, int Cp, int Hp, int htiles, HeadCorr corr,
-                                                int64_t split) {
+                                                int C, int Cp, int Hp, int htiles, int64_t split) {
   __shared__ float zs[kHM][kHU + 1];
   __shared__ float ws[KC][kHU + 1];
-  __shared__ __attribute__((aligned(16))) float gsl[kCorrMaxK][kHM][kHU];
-  __shared__ __attribute__((aligned(16))) float grl[kCorrMaxK][kHM][kHM + 4];
   const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
   const int tid = threadIdx.x, u4 = tid & 7, rr = tid >> 3;
   const int h4 = ht * kHU + 4 * u4;
@@ -261,44 +254,11 @@ __global__ __launch_bounds__(256) void k_head_a(const float* __restrict__ part, 
     for (int ks = 0; ks < KS; ++ks) z += *(const f32x4*)(pm + ks * split);
     return z;
   };
-  // The first chunk's partials are read before the correction operands are
-  // staged, so the two sets of loads overlap.
-  const f32x4 z_first = part_sum(0);
-  const int kc = corr.gram != nullptr ? corr.k : 0;
-  if (kc > 0) {
-    // errors of the earlier steps, this slice: gsl[k2][s][u] = G[k2][p][s][32*ht + u],
-    // and the learner's Gram rows: grl[k2][s][s2] = gram[k][k2][s][s2]
-    for (int e = tid; e < kc * kHM * (kHU / 4); e += 256) {
-      const int k2 = e / (kHM * (kHU / 4)), rem = e % (kHM * (kHU / 4));
-      const int sm = rem / (kHU / 4), c4 = rem % (kHU / 4);
-      const f32x4 v = *(const f32x4*)(corr.gs + (((int64_t)k2 * P + p) * Mp + (sm < Mp ? sm : 0)) * Hp + ht * kHU + 4 * c4);
-      *(f32x4*)&gsl[k2][sm][4 * c4] = sm < M ? v : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    const float* gk = corr.gram + (((int64_t)p * corr.K1 + corr.k) * corr.K1) * Mp * Mp;
-    for (int e = tid; e < kc * Mp * Mp; e += 256) {
-      const int k2 = e / (Mp * Mp), rem = e % (Mp * Mp);
-      grl[k2][rem / Mp][rem % Mp] = gk[(int64_t)k2 * Mp * Mp + rem];
-    }
-    __syncthreads();
-  }
   for (int m0 = 0; m0 < M; m0 += kHM) {
     const int m = m0 + rr;
     const bool mok = m < M;
-    f32x4 z = m0 == 0 ? z_first : part_sum(m0);
+    f32x4 z = part_sum(m0);
     z += bias;
-    if (kc > 0) {
-      // Rows and columns past M are zero in both staged operands, so the
-      // sum runs over the padded minibatch in fours.
-      f32x4 c = {0.f, 0.f, 0.f, 0.f};
-      for (int k2 = 0; k2 < kc; ++k2)
-#pragma unroll 2
-        for (int s2 = 0; s2 < Mp; s2 += 4) {
-          const f32x4 g = *(const f32x4*)&grl[k2][rr][s2];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) c += g[i] * *(const f32x4*)&gsl[k2][s2 + i][4 * u4];
-        }
-      z -= *corr.lr * c;
-    }
     if (mok) *(f32x4*)(Z1 + ((int64_t)p * Mp + m) * Hp + h4) = z;
     zs[rr][4 * u4 + 0] = mok ? fmaxf(z.x, 0.0f) : 0.0f;
     zs[rr][4 * u4 + 1] = mok ? fmaxf(z.y, 0.0f) : 0.0f;
@@ -788,16 +748,16 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
-                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp, HeadCorr corr,
+                   int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp,
                    int64_t part_split) {
   const int htiles = Hp / kHU;
   const int64_t split = part_split > 0 ? part_split : (int64_t)P * Mp * Hp;
   if (C <= 16)
     launch(k_head_a<16>, P * htiles, 256, 0, s, part, KS, b1, W2, b2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
-           corr, split);
+           split);
   else
     launch(k_head_a<32>, P * htiles, 256, 0, s, part, KS, b1, W2, b2, w_pitch, Z1, PL, P, M, Mp, C, Cp, Hp, htiles,
-           corr, split);
+           split);
 }
 
 void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* b2, int64_t w_pitch,
