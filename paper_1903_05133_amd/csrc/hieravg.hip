@@ -11,13 +11,20 @@
 // equal-size cluster means equal the global mean, so it changes nothing but
 // rounding.
 //
-// Where the fused step kernel applies (padded minibatch up to 64), the update
-// of the first weight block at step t also computes the first-layer forward
-// partials of step t+1 from the new weights, and at the end of a block also
-// takes the cluster mean of that block in between; a small kernel then takes
-// the cluster mean of the remaining parameters.  Only step 0 of a round runs
-// the stand-alone forward kernel, and the last step the plain update before
-// the global mean.
+// Two schedules compute this round (include/hieravg.h, update_mode):
+//  - eager: every step updates every learner's first weight block.  Where the
+//    fused step kernel applies (padded minibatch up to 64), the update at
+//    step t also computes the first-layer forward partials of step t+1 from
+//    the new weights, and at the end of a block also takes the cluster mean
+//    of that block in between; a small kernel then takes the cluster mean of
+//    the remaining parameters.  Only step 0 of a round runs the stand-alone
+//    forward kernel, and the last step the plain update before the global
+//    mean.
+//  - delayed (MLP): within a block the first weight block of every learner of
+//    a cluster is the cluster's block-start copy minus the rank-B updates of
+//    its earlier steps, so one GEMM per cluster gives the forward of all K1
+//    steps (plus Gram corrections), and one GEMM per cluster at the block end
+//    applies the K1*S learners' updates and the cluster mean together.
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
@@ -207,7 +214,10 @@ int alloc_zero(hieravg* h, void** p, size_t bytes, const char* what) {
 
 bool delayed_applies(const hieravg_config& c) {
   const bool whole_blocks = c.k_global == 0 || c.k_global % c.K1 == 0;
-  return c.kind == HIERAVG_KIND_MLP && c.B <= 32 && c.K1 <= 8 && whole_blocks &&
+  // The block update addresses dataset rows by 32-bit offsets in 64-float
+  // units (a dataset below 2^38 floats).
+  const bool rows_fit = (double)c.n_samples * (double)round_up(c.in_dim, 64) < 274877906944.0;
+  return c.kind == HIERAVG_KIND_MLP && c.B <= 32 && c.K1 <= 8 && whole_blocks && rows_fit &&
          (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows && c.momentum == 0.0f && c.weight_decay == 0.0f;
 }
 
@@ -411,9 +421,6 @@ int build(hieravg* h) {
   return HIERAVG_OK;
 }
 
-// The single kernel launch of class `kc` for step tt of the current round
-// (tt selects the step's sample indices, or the averaging workload's given
-// gradients).  Returns false for a class this workload does not launch.
 // The heavy-ball buffers and decay of an update GEMM over the parameter block
 // at offset `off` (bias at `boff`) of the replica rows.
 void with_momentum(const hieravg* h, UpdArgs& u, int64_t off, int64_t boff) {
@@ -425,6 +432,9 @@ void with_momentum(const hieravg* h, UpdArgs& u, int64_t off, int64_t boff) {
   }
 }
 
+// The single kernel launch of class `kc` for step tt of the current round
+// (tt selects the step's sample indices, or the averaging workload's given
+// gradients).  Returns false for a class this workload does not launch.
 bool launch_class(hieravg* h, int kc, int tt) {
   const hieravg_config& c = h->cfg;
   const int P = c.P, B = c.B, S = c.S;

@@ -59,6 +59,17 @@ constexpr uint64_t kTagTestNoise = 0x68762e746e6f6973ull;  // "hv.tnois"
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// n / d for 0 <= n < 2^24, d >= 1, from inv = 1.0f / d (computed once by the
+// caller): the float quotient is within one of the true one, and one
+// correction step each way makes it exact.  A few vector instructions
+// instead of the long sequence of an integer division.
+__device__ inline int qdiv_small(int n, int d, float inv) {
+  int q = (int)((float)n * inv);
+  q += (q + 1) * d <= n ? 1 : 0;
+  q -= q * d > n ? 1 : 0;
+  return q;
+}
+
 // Workgroup index -> logical tile index such that consecutive logical tiles
 // run on the same XCD (the hardware deals workgroups to the 8 XCDs round
 // robin).  Tiles that share operands then share an L2.

@@ -60,16 +60,21 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   bool aok[2], wok[2];
   int off[2];
   const float* wp = a.W + (int64_t)(g / a.wdiv) * a.w_pitch;
+  const float inv_mp = 1.0f / (float)a.Mp, inv_vs = 1.0f / (float)(a.vS > 0 ? a.vS : 1);
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int q = tid + 1024 * i;
     const int r = q >> 4, c4 = q & 15;
     off[i] = r * kLdsStride + 4 * c4;
     const int m = mbase + r;
-    const int jj = m / a.Mp, sm = m - jj * a.Mp;
+    const int jj = qdiv_small(m, a.Mp, inv_mp), sm = m - jj * a.Mp;
     aok[i] = m < GM && sm < a.M;
     const int v = aok[i] ? jj : 0;
-    const int64_t p = a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
+    int64_t p = (int64_t)g * a.SG + v;
+    if (a.vS > 0) {
+      const int k = qdiv_small(v, a.vS, inv_vs);
+      p = (int64_t)k * a.P + (int64_t)g * a.vS + (v - k * a.vS);
+    }
     arow[i] = a.A + (int64_t)a.idx[p * a.M + (aok[i] ? sm : 0)] * a.lda + 4 * c4;
     const int n = nbase + r;
     wok[i] = n < a.N;
@@ -118,14 +123,21 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   const int64_t PT = a.PT > 0 ? a.PT : a.P;
   const int col = nbase + wn + l32;
   if (col < a.N) {
+    // The lane's rows 8i + e (e < 4) share one member (Mp is a multiple of
+    // 16, GM of 16), so the row -> (member, sample) split runs once per i.
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = mbase + wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
-      if (row >= GM) continue;
-      const int v = row / a.Mp, sm = row - v * a.Mp;
-      const int64_t p =
-          a.vS > 0 ? (int64_t)(v / a.vS) * a.P + (int64_t)g * a.vS + v % a.vS : (int64_t)g * a.SG + v;
-      a.part[(((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col] = acc[r];
+    for (int i = 0; i < 4; ++i) {
+      const int row0 = mbase + wm + 8 * i + 4 * lhi;
+      if (row0 >= GM) continue;
+      const int v = qdiv_small(row0, a.Mp, inv_mp), sm = row0 - v * a.Mp;
+      int64_t p = (int64_t)g * a.SG + v;
+      if (a.vS > 0) {
+        const int k = qdiv_small(v, a.vS, inv_vs);
+        p = (int64_t)k * a.P + (int64_t)g * a.vS + (v - k * a.vS);
+      }
+      float* dst = a.part + (((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[(int64_t)e * a.N] = acc[4 * i + e];
     }
   }
 }
@@ -157,8 +169,18 @@ void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int t
 // stages ahead (two register sets) and each stage costs one barrier.  NTH/64
 // waves split the tile into 32-row x (2*kUN/NW)-column blocks of 32x32x2
 // MFMAs.
-template <int NTH>
-__global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int ntiles) {
+//
+// Address arithmetic stays out of the stage loop (a SIMD's matrix core idles
+// while it executes vector ALU instructions, so every such instruction per
+// stage costs MFMA time): the input-row offset of every contraction row is
+// tabulated in LDS once, in 64-float units, and with kAligned (B a multiple
+// of 32) a stage is 32 consecutive samples of one (step, learner), whose
+// error rows follow from scalar counters.  Input rows past the contraction
+// and columns past the block are read from valid rows and columns instead of
+// being masked: they only meet zero error rows or feed discarded outputs.
+template <int NTH, bool kAligned>
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k_block_update(BlkArgs a, int mtiles,
+                                                                                         int ntiles) {
   constexpr int NW = NTH / 64;            // waves
   constexpr int kWCn = NW / 2;            // waves across the columns (two 32-row blocks)
   constexpr int kWN = kUN / kWCn;         // columns per wave
@@ -166,7 +188,7 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
   constexpr int kStage = kSC * (kLA + kLB);
   constexpr int kLds = 2 * kStage > kUM * kLB ? 2 * kStage : kUM * kLB;
   __shared__ __attribute__((aligned(16))) float lds[kLds];
-  extern __shared__ int32_t sidx[];  // [K1*SG*B] sample index of each contraction row
+  extern __shared__ uint32_t xtb[];  // [K1*SG*B] input row offset of each contraction row, / 64
   float* Gt = lds;  // [kUM][kLB] gradient tile (after the stages)
   // Tiles that share minibatch rows (same group and columns) are neighbours.
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -188,18 +210,20 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
   const int xc4 = tid % kXP, xr0 = tid / kXP;
   const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
   const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
-  // Row r of the contraction: step k, learner g*SG + j, sample s.  The
-  // quotients come from a float reciprocal (r < 2^24) and one correction step.
+  const float* Xc = a.X + xcol;
+  // G piece i of this thread: stage row (qq >> 4), columns m .. m+3 (a row
+  // past Mrows reads row 0: its gradient row is discarded).
+  int64_t goff[kGL];
+#pragma unroll
+  for (int i = 0; i < kGL; ++i) {
+    const int qq = tid + NTH * i, m = mrow0 + 4 * (qq & 15);
+    goff[i] = (int64_t)(qq >> 4) * a.ldg + (m < a.Mrows ? m : 0);
+  }
+  // Row r of the contraction: step k, learner g*SG + j, sample s (r < 2^24).
   const float inv_sb = 1.0f / (float)SB, inv_b = 1.0f / (float)a.B;
-  auto qdiv = [](int n, int d, float inv) {
-    int q = (int)((float)n * inv);
-    q += (q + 1) * d <= n ? 1 : 0;
-    q -= q * d > n ? 1 : 0;
-    return q;
-  };
   auto gx_row = [&](int r, int64_t& grow, int64_t& irow) {
-    const int k = qdiv(r, SB, inv_sb), rem = r - k * SB;
-    const int j = qdiv(rem, a.B, inv_b), sm = rem - j * a.B;
+    const int k = qdiv_small(r, SB, inv_sb), rem = r - k * SB;
+    const int j = qdiv_small(rem, a.B, inv_b), sm = rem - j * a.B;
     const int64_t kp = (int64_t)k * a.P + (int64_t)g * a.SG + j;
     grow = kp * a.Mp + sm;
     irow = kp * a.B + sm;
@@ -208,36 +232,58 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
   // before its rows go to LDS (two blocks of MFMAs of latency hiding).
   struct StageRegs {
     f32x4 ga[kGL], xb[kXL];
-    bool gok[kGL], xok[kXL];
+    bool gok[kGL];
   };
   StageRegs RA, RB;
-  // The sample index of every contraction row, read once into LDS: the
-  // stage loads then depend on no other global load (loads complete in issue
+  // The input row of every contraction row, read once into LDS: the stage
+  // loads then depend on no other global load (loads complete in issue
   // order, so an index load in the loop would make the wait for it a wait
-  // for the stage data issued before it).
+  // for the stage data issued before it).  The launcher checks that the
+  // offsets fit 32 bits in 64-float units.
   for (int r = tid; r < R; r += NTH) {
     int64_t grow, irow;
     gx_row(r, grow, irow);
-    sidx[r] = a.idx[irow];
+    xtb[r] = (uint32_t)(((int64_t)a.idx[irow] * a.ldx) >> 6);
   }
   __syncthreads();
+  // kAligned (Mp = B): the SG learners of a step are consecutive error rows,
+  // so the next stage to load starts gb_off floats into G and the offset
+  // grows by 32 rows per stage, plus the other learners' rows at each step
+  // boundary (every SB/32 stages).  load_stage runs for st = 0, 1, 2, ... in
+  // order; past the end it reloads the last stage.
+  int64_t gb_off = (int64_t)g * a.SG * a.Mp * a.ldg;
+  int st_in_step = 0;
+  const int stages_per_step = SB / kSC;
+  const int64_t stage_step = (int64_t)kSC * a.ldg;
+  const int64_t step_jump = (int64_t)(a.P - a.SG) * a.Mp * a.ldg;
   auto load_stage = [&](int st, StageRegs& q) {
     const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
+    if constexpr (kAligned) {
+      const float* gb = a.G + gb_off;
 #pragma unroll
-    for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
-      const int qq = tid + NTH * i;
-      const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
-      q.gok[i] = r < R && m < a.Mrows;
-      int64_t grow, irow;
-      gx_row(q.gok[i] ? r : 0, grow, irow);
-      q.ga[i] = *(const f32x4*)(a.G + (q.gok[i] ? grow * a.ldg + m : 0));
+      for (int i = 0; i < kGL; ++i) q.ga[i] = *(const f32x4*)(gb + goff[i]);
+      if (st < nst - 1) {
+        gb_off += stage_step;
+        if (++st_in_step == stages_per_step) {
+          st_in_step = 0;
+          gb_off += step_jump;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
+        const int qq = tid + NTH * i;
+        const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
+        q.gok[i] = r < R;
+        int64_t grow, irow;
+        gx_row(q.gok[i] ? r : 0, grow, irow);
+        q.ga[i] = *(const f32x4*)(a.G + grow * a.ldg + (m < a.Mrows ? m : 0));
+      }
     }
 #pragma unroll
     for (int i = 0; i < kXL; ++i) {  // X rows of contraction rows s0 + xr0 + kXR*i
       const int r = s0 + xr0 + kXR * i;
-      q.xok[i] = r < R && xcol_ok;
-      const int xrow = sidx[r < R ? r : 0];
-      q.xb[i] = *(const f32x4*)(a.X + (q.xok[i] ? (int64_t)xrow * a.ldx + xcol : 0));
+      q.xb[i] = *(const f32x4*)(Xc + ((uint64_t)xtb[kAligned || r < R ? r : 0] << 6));
     }
   };
   auto store_stage = [&](int buf, const StageRegs& q) {
@@ -246,10 +292,10 @@ __global__ __launch_bounds__(NTH) void k_block_update(BlkArgs a, int mtiles, int
 #pragma unroll
     for (int i = 0; i < kGL; ++i) {
       const int qq = tid + NTH * i;
-      *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = q.gok[i] ? q.ga[i] : zero4;
+      *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = kAligned || q.gok[i] ? q.ga[i] : zero4;
     }
 #pragma unroll
-    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xok[i] ? q.xb[i] : zero4;
+    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xb[i];
   };
 
   f32x16 acc[kNA];
@@ -333,8 +379,11 @@ void launch_block_update(hipStream_t s, const BlkArgs& a) {
   const int mtiles = (a.Mrows + kUM - 1) / kUM;
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
-  const uint32_t shmem = sizeof(int32_t) * a.K1 * a.SG * a.B;
-  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
+  const uint32_t shmem = sizeof(uint32_t) * a.K1 * a.SG * a.B;
+  if (a.B % kSC == 0)
+    launch(k_block_update<HAV_BLK_THREADS, true>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
+  else
+    launch(k_block_update<HAV_BLK_THREADS, false>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
 }
 
 // ------------------------------------------------------------ Gram blocks

@@ -62,6 +62,9 @@ SMALL = {
     "mlp_group_mean_S8": cases.case("mlp", 16, 8, 2, 2, B=12, IN=200, H=70, C=5, N=300, lr=0.1, seed=13),
     # fused step with the mean of 4 learners on the softmax model; ragged last column tile
     "softmax_group_mean_S4": cases.case("softmax", 8, 4, 1, 3, B=20, IN=130, C=12, N=90, lr=0.2, seed=14),
+    # B = 32: the block update's stages are whole (step, learner) runs of
+    # samples; ragged hidden and input widths, two learners per cluster
+    "mlp_batch_32_ragged": cases.case("mlp", 6, 2, 3, 2, B=32, IN=200, H=70, C=5, N=300, lr=0.05, seed=15),
     "mlp_one_learner": cases.case("mlp", 1, 1, 3, 2, B=8, IN=96, H=33, C=5, N=64, lr=0.1, seed=7),
     "mlp_one_sample_dataset": cases.case("mlp", 4, 4, 2, 1, B=3, IN=50, H=20, C=2, N=1, lr=0.1, seed=8),
     "softmax_ragged": cases.case("softmax", 3, 3, 3, 1, B=17, IN=33, C=17, N=50, lr=0.2, seed=3),
