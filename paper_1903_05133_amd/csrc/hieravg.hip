@@ -111,6 +111,7 @@ struct hieravg {
   float* Gs = nullptr;     // [K1][P][Bp][Hp] hidden errors of the block's steps
   float* gram = nullptr;   // [KSG][K2][P][K1][K1][Bp][Bp] Gram blocks of the round
   int32_t* ylab = nullptr; // [T][P][B] labels of the drawn samples (delayed schedule)
+  uint32_t* btab = nullptr; // [2][K2][P/S][Rp] row tables of the block update (BlkTables)
   float* part2 = nullptr;  // layer-2 split-K partials of the delayed schedule with more than 32 classes
   // Evaluation (allocated at the first hieravg_evaluate).
   int eval_rows = 0;                  // chunk capacity (multiple of 16)
@@ -166,7 +167,7 @@ void run(hieravg* h, int kc, F&& fn) {
 void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
-  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper,
+  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
@@ -390,6 +391,10 @@ int build(hieravg* h) {
       if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->ylab, sizeof(int32_t) * (size_t)T * P * c.B, "sample labels"))) return rc;
+      const int64_t rp = round_up((int64_t)c.K1 * c.S * c.B, 32);
+      if ((rc = alloc_zero(h, (void**)&h->btab, 2 * sizeof(uint32_t) * (size_t)c.K2 * (P / c.S) * rp,
+                           "block update row tables")))
+        return rc;
       // more than 32 classes: the layer-2 partials of a step must not overwrite
       // the block forward's partials of the later steps
       if (h->C > kSmallC &&
@@ -461,10 +466,22 @@ bool launch_class(hieravg* h, int kc, int tt) {
   const int Bp = h->Bp, C = (int)h->C, Cp = (int)h->Cp, Hp = (int)h->Hp, INp = (int)h->INp;
   const bool mlp = c.kind == HIERAVG_KIND_MLP, small = mlp && C <= kSmallC;
   switch (kc) {
-    case KC_DRAW:
+    case KC_DRAW: {
+      BlkTables tb;
+      if (h->in_delayed) {
+        tb.Rp = (int)round_up((int64_t)c.K1 * S * B, 32);
+        tb.gtab = h->btab;
+        tb.xtab = h->btab + (int64_t)c.K2 * (P / S) * tb.Rp;
+        tb.K1 = c.K1;
+        tb.S = S;
+        tb.Mp = Bp;
+        tb.ldg = h->Hp;
+        tb.ldx = h->INp;
+      }
       launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, h->T, (uint64_t)h->N,
-                          h->key_index, h->y, h->in_delayed ? h->ylab : nullptr);
+                          h->key_index, h->y, h->in_delayed ? h->ylab : nullptr, tb);
       return true;
+    }
     case KC_FWD1: {
       FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, mlp ? Hp : Cp, INp, h->KS1,
                 h->cps1};
@@ -540,8 +557,10 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (!h->delayed) return false;
       const int b = tt / c.K1;
       const int64_t w1 = h->Hp * h->INp;
+      const int64_t rp = round_up((int64_t)c.K1 * S * B, 32), blk = (int64_t)(P / S) * rp;
       BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
-                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S};
+                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S,
+                h->btab + b * blk, h->btab + (int64_t)c.K2 * blk + b * blk};
       launch_block_update(s, a);
       return true;
     }

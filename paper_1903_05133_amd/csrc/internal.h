@@ -143,9 +143,23 @@ void launch_init_matrix(hipStream_t s, float* W, int64_t rows, int64_t cols, int
                         uint64_t layer, float scale);
 void launch_init_vector(hipStream_t s, float* w, int64_t D, uint64_t key, float std);
 void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int T, uint64_t key, float std);
+// Row tables of the block update (delayed updates): for block b, cluster g
+// and contraction row r = (k*S + j)*B + s (step k of the block, learner
+// g*S + j, sample s) at [(b*(P/S) + g)*Rp + r], the offsets in 64-float
+// units of that row's hidden-error row (row (k*P + g*S + j)*Mp + s of pitch
+// ldg) and of its sample's dataset row (pitch ldx).  Rows R..Rp-1 of each
+// table (R = K1*S*B, Rp = R rounded up to 32) stay 0.
+struct BlkTables {
+  uint32_t* gtab = nullptr;
+  uint32_t* xtab = nullptr;
+  int K1 = 1, S = 1, Mp = 0, Rp = 0;
+  int64_t ldg = 0, ldx = 0;
+};
 // ylab (optional): the label of every drawn sample, same layout as idx.
+// tables.gtab (optional): also write the block update's row tables.
 void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
-                         int T, uint64_t N, uint64_t key, const int32_t* labels = nullptr, int32_t* ylab = nullptr);
+                         int T, uint64_t N, uint64_t key, const int32_t* labels = nullptr, int32_t* ylab = nullptr,
+                         const BlkTables& tables = BlkTables());
 
 // GEMMs (k_gemm.hip).
 struct FwdArgs {
@@ -219,9 +233,10 @@ struct BlkArgs {
   int P, SG, K1, B, Mp, Mrows, Ncols;
   const float* lr;      // device scalar step size; the mean takes lr / lr_div
   float lr_div;
+  const uint32_t* gtab;  // this block's row tables (BlkTables): [P/SG][Rp] each
+  const uint32_t* xtab;
 };
-// Contraction rows (K1 * SG * B) the block update takes: their sample indices
-// live in LDS beside the 50 KB of operand stages.
+// Largest contraction (K1 * SG * B rows) of a block update.
 constexpr int kBlkMaxRows = 16384;
 void launch_block_update(hipStream_t s, const BlkArgs& a);
 

@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256) void k_gen_grads(float* __restrict__ G, int64_
 __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx, uint64_t* step_ctr,
                                                       uint32_t* done_ctr, int P, int B, int T, uint64_t N,
                                                       uint64_t key, const int32_t* __restrict__ labels,
-                                                      int32_t* __restrict__ ylab) {
+                                                      int32_t* __restrict__ ylab, BlkTables tb) {
   const uint64_t t0 = *step_ctr;
   const int64_t total = (int64_t)T * P * B;
   for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
@@ -80,6 +80,13 @@ __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx,
     const int32_t i = (int32_t)(hash64(key, ctr) % N);
     idx[e] = i;
     if (ylab) ylab[e] = labels[i];
+    if (tb.gtab) {
+      // Row r = (k*S + learner-in-cluster)*B + s of cluster j/S in block tt/K1.
+      const int64_t b = tt / tb.K1, k = tt - b * tb.K1, g = j / tb.S, jc = j - g * tb.S;
+      const int64_t o = (b * (P / tb.S) + g) * tb.Rp + (k * tb.S + jc) * B + s;
+      tb.gtab[o] = (uint32_t)((((k * P + j) * tb.Mp + s) * tb.ldg) >> 6);
+      tb.xtab[o] = (uint32_t)(((int64_t)i * tb.ldx) >> 6);
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -123,9 +130,10 @@ void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int
 }
 
 void launch_draw_indices(hipStream_t s, int32_t* idx, uint64_t* step_ctr, uint32_t* done_ctr, int P, int B,
-                         int T, uint64_t N, uint64_t key, const int32_t* labels, int32_t* ylab) {
+                         int T, uint64_t N, uint64_t key, const int32_t* labels, int32_t* ylab,
+                         const BlkTables& tables) {
   launch(k_draw_indices, grid_for((int64_t)T * P * B, 1024), 256, 0, s, idx, step_ctr, done_ctr, P, B, T, N, key,
-         labels, ylab);
+         labels, ylab, tables);
 }
 
 }  // namespace hav

@@ -163,188 +163,154 @@ void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int t
 }
 
 // ------------------------------------------------------------ delayed update
-// Tile of k_update_tn (64 rows x kUN columns of one group's W1), contracted
-// over the K1*SG*B rows (step k, learner j, sample s) of the group in stages
-// of 32 rows through two LDS buffers: each stage's loads are issued two
-// stages ahead (two register sets) and each stage costs one barrier.  NTH/64
-// waves split the tile into 32-row x (2*kUN/NW)-column blocks of 32x32x2
-// MFMAs.
+// Tile of the block update: 64 rows (hidden units m) x kUN columns (inputs n)
+// of one group's W1, contracted over the K1*SG*B rows r = (step k, learner
+// g*SG + j, sample s) of the group in stages of 32 rows through two LDS
+// buffers (one barrier per stage; each stage's loads are issued two stages
+// ahead).  Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4))
+// as one chain of 32x32x2 MFMAs.
 //
-// Address arithmetic stays out of the stage loop (a SIMD's matrix core idles
-// while it executes vector ALU instructions, so every such instruction per
-// stage costs MFMA time): the input-row offset of every contraction row is
-// tabulated in LDS once, in 64-float units, and with kAligned (B a multiple
-// of 32) a stage is 32 consecutive samples of one (step, learner), whose
-// error rows follow from scalar counters.  Input rows past the contraction
-// and columns past the block are read from valid rows and columns instead of
-// being masked: they only meet zero error rows or feed discarded outputs.
-template <int NTH, bool kAligned>
-__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k_block_update(BlkArgs a, int mtiles,
-                                                                                         int ntiles) {
-  constexpr int NW = NTH / 64;            // waves
-  constexpr int kWCn = NW / 2;            // waves across the columns (two 32-row blocks)
-  constexpr int kWN = kUN / kWCn;         // columns per wave
-  constexpr int kNA = kWN / 32;           // 32x32 accumulators per wave
-  constexpr int kStage = kSC * (kLA + kLB);
+// The stage tiles sit in LDS transposed, contraction index innermost
+// (At[m][r], Bt[n][r], 32 floats per row with no padding): lane (l, h) then
+// reads four consecutive r of its row with one 16-byte read and feeds them
+// to four MFMAs (MFMA (q, e) of a stage contracts r = 4q + e for lanes with
+// h = 0 and 16 + 4q + e for h = 1, a permutation of the stage's rows that
+// both operands share).  The 16-byte chunk c of row x is stored at chunk
+// c ^ ((x >> 1) & 7), so the 16 rows a quarter-wave reads or writes fall
+// into 16 distinct bank groups.  Wave w loads the stage's rows 4w .. 4w+3
+// (lane l: error column m = l, input columns n = l and l + 64) with 4-byte
+// loads, so each lane holds four consecutive r of one column: the
+// transposed 16-byte chunk it writes.
+//
+// No vector arithmetic runs per stage (a SIMD's matrix core idles while it
+// executes vector ALU instructions): the error-row and input-row offsets of
+// every contraction row come from tables (64-float units) that the index
+// draw writes, read with scalar loads, so each row's address is a scalar
+// base plus the lane's fixed column.  Rows past the contraction point at row
+// 0 and have their error rows zeroed; columns past the block read valid
+// columns and feed discarded outputs.
+constexpr int kBU = 32;  // LDS row length of the transposed stage tiles (= kSC)
+__device__ inline int bu_swz(int x, int c) { return (x << 5) + ((c ^ ((x >> 1) & 7)) << 2); }
+
+template <int NTH>
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k_block_update(
+    BlkArgs a, const uint32_t* __restrict__ gtab, const uint32_t* __restrict__ xtab, int mtiles, int ntiles) {
+  static_assert(NTH == 512 && kUN == 128 && kUM == 64 && kSC == 32, "block update tiling");
+  constexpr int kStage = (kUM + kUN) * kBU;  // floats per LDS stage: At then Bt
   constexpr int kLds = 2 * kStage > kUM * kLB ? 2 * kStage : kUM * kLB;
   __shared__ __attribute__((aligned(16))) float lds[kLds];
-  extern __shared__ uint32_t xtb[];  // [K1*SG*B] input row offset of each contraction row, / 64
   float* Gt = lds;  // [kUM][kLB] gradient tile (after the stages)
   // Tiles that share minibatch rows (same group and columns) are neighbours.
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int mt = bid % mtiles;
   const int nt = (bid / mtiles) % ntiles;
   const int g = bid / (ntiles * mtiles);
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar row arithmetic
   const int l32 = lane & 31, lhi = lane >> 5;
   const int mrow0 = mt * kUM, ncol0 = nt * kUN;
-  const int wn = (wave % kWCn) * kWN, wm = (wave / kWCn) * 32;
+  const int wn = (wave & 3) * 32, wm = (wave >> 2) * 32;
   const bool wave_on = ncol0 + wn < a.Ncols;
-  const int SB = a.SG * a.B;
-  const int R = a.K1 * SB;  // contraction rows
+  const int R = a.K1 * a.SG * a.B;  // contraction rows
   const int nst = (R + kSC - 1) / kSC;
-  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  const uint32_t* gt = gtab + (int64_t)g * nst * kSC;
+  const uint32_t* xt = xtab + (int64_t)g * nst * kSC;
+  // This lane's columns as byte offsets within a row.  Each row is read
+  // through a buffer resource whose range ends at the row's last valid
+  // column, so columns past the block read 0 (their outputs are discarded).
+  const int gcol = 4 * (mrow0 + lane), xcol0 = 4 * (ncol0 + lane), xcol1 = xcol0 + 256;
+  const int grow_bytes = 4 * a.Mrows, xrow_bytes = 4 * a.Ncols;
+  constexpr int kRsrcWord3 = 0x00020000;  // raw 32-bit buffer access (gfx9 family)
 
-  constexpr int kXP = kUN / 4, kXR = NTH / kXP, kXL = kSC / kXR;
-  constexpr int kGL = kSC * (kUM / 4) / NTH;  // G pieces per thread per stage
-  const int xc4 = tid % kXP, xr0 = tid / kXP;
-  const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
-  const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
-  const float* Xc = a.X + xcol;
-  // G piece i of this thread: stage row (qq >> 4), columns m .. m+3 (a row
-  // past Mrows reads row 0: its gradient row is discarded).
-  int64_t goff[kGL];
-#pragma unroll
-  for (int i = 0; i < kGL; ++i) {
-    const int qq = tid + NTH * i, m = mrow0 + 4 * (qq & 15);
-    goff[i] = (int64_t)(qq >> 4) * a.ldg + (m < a.Mrows ? m : 0);
-  }
-  // Row r of the contraction: step k, learner g*SG + j, sample s (r < 2^24).
-  const float inv_sb = 1.0f / (float)SB, inv_b = 1.0f / (float)a.B;
-  auto gx_row = [&](int r, int64_t& grow, int64_t& irow) {
-    const int k = qdiv_small(r, SB, inv_sb), rem = r - k * SB;
-    const int j = qdiv_small(rem, a.B, inv_b), sm = rem - j * a.B;
-    const int64_t kp = (int64_t)k * a.P + (int64_t)g * a.SG + j;
-    grow = kp * a.Mp + sm;
-    irow = kp * a.B + sm;
-  };
-  // Stage registers: two sets, so each stage's loads are issued two stages
-  // before its rows go to LDS (two blocks of MFMAs of latency hiding).
   struct StageRegs {
-    f32x4 ga[kGL], xb[kXL];
-    bool gok[kGL];
+    float gv[4], x0[4], x1[4];
   };
   StageRegs RA, RB;
-  // The input row of every contraction row, read once into LDS: the stage
-  // loads then depend on no other global load (loads complete in issue
-  // order, so an index load in the loop would make the wait for it a wait
-  // for the stage data issued before it).  The launcher checks that the
-  // offsets fit 32 bits in 64-float units.
-  for (int r = tid; r < R; r += NTH) {
-    int64_t grow, irow;
-    gx_row(r, grow, irow);
-    xtb[r] = (uint32_t)(((int64_t)a.idx[irow] * a.ldx) >> 6);
-  }
-  __syncthreads();
-  // kAligned (Mp = B): the SG learners of a step are consecutive error rows,
-  // so the next stage to load starts gb_off floats into G and the offset
-  // grows by 32 rows per stage, plus the other learners' rows at each step
-  // boundary (every SB/32 stages).  load_stage runs for st = 0, 1, 2, ... in
-  // order; past the end it reloads the last stage.
-  int64_t gb_off = (int64_t)g * a.SG * a.Mp * a.ldg;
-  int st_in_step = 0;
-  const int stages_per_step = SB / kSC;
-  const int64_t stage_step = (int64_t)kSC * a.ldg;
-  const int64_t step_jump = (int64_t)(a.P - a.SG) * a.Mp * a.ldg;
   auto load_stage = [&](int st, StageRegs& q) {
-    const int s0 = (st < nst ? st : nst - 1) * kSC;  // past the end: the last stage again
-    if constexpr (kAligned) {
-      const float* gb = a.G + gb_off;
+    const int r0 = (st < nst ? st : nst - 1) * kSC + 4 * wave;  // past the end: the last stage again
+    const uint4 go = *(const uint4*)(gt + r0);
+    const uint4 xo = *(const uint4*)(xt + r0);
+    const uint32_t gr[4] = {go.x, go.y, go.z, go.w}, xr[4] = {xo.x, xo.y, xo.z, xo.w};
 #pragma unroll
-      for (int i = 0; i < kGL; ++i) q.ga[i] = *(const f32x4*)(gb + goff[i]);
-      if (st < nst - 1) {
-        gb_off += stage_step;
-        if (++st_in_step == stages_per_step) {
-          st_in_step = 0;
-          gb_off += step_jump;
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < kGL; ++i) {  // G rows s0 .. s0+32, columns mrow0 .. +64
-        const int qq = tid + NTH * i;
-        const int r = s0 + (qq >> 4), m = mrow0 + 4 * (qq & 15);
-        q.gok[i] = r < R;
-        int64_t grow, irow;
-        gx_row(q.gok[i] ? r : 0, grow, irow);
-        q.ga[i] = *(const f32x4*)(a.G + grow * a.ldg + (m < a.Mrows ? m : 0));
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kXL; ++i) {  // X rows of contraction rows s0 + xr0 + kXR*i
-      const int r = s0 + xr0 + kXR * i;
-      q.xb[i] = *(const f32x4*)(Xc + ((uint64_t)xtb[kAligned || r < R ? r : 0] << 6));
+    for (int i = 0; i < 4; ++i) {
+      const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.G) + ((uint64_t)gr[i] << 6), 0, grow_bytes, kRsrcWord3);
+      const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.X) + ((uint64_t)xr[i] << 6), 0, xrow_bytes, kRsrcWord3);
+      q.gv[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(grs, gcol, 0, 0));
+      q.x0[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xrs, xcol0, 0, 0));
+      q.x1[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xrs, xcol1, 0, 0));
     }
   };
-  auto store_stage = [&](int buf, const StageRegs& q) {
-    float* As = lds + buf * kStage;
-    float* Bs = As + kSC * kLA;
+  auto store_stage = [&](int st, int buf, StageRegs& q) {
+    float* S = lds + buf * kStage;
+    const int r0 = st * kSC + 4 * wave;
+    if (r0 + 4 > R) {  // rows past the contraction: zero error rows
 #pragma unroll
-    for (int i = 0; i < kGL; ++i) {
-      const int qq = tid + NTH * i;
-      *(f32x4*)&As[(qq >> 4) * kLA + 4 * (qq & 15)] = kAligned || q.gok[i] ? q.ga[i] : zero4;
+      for (int i = 0; i < 4; ++i)
+        if (r0 + i >= R) q.gv[i] = 0.0f;
     }
-#pragma unroll
-    for (int i = 0; i < kXL; ++i) *(f32x4*)&Bs[(xr0 + kXR * i) * kLB + 4 * xc4] = q.xb[i];
+    *(f32x4*)&S[bu_swz(lane, wave)] = f32x4{q.gv[0], q.gv[1], q.gv[2], q.gv[3]};
+    float* Bt = S + kUM * kBU;
+    *(f32x4*)&Bt[bu_swz(lane, wave)] = f32x4{q.x0[0], q.x0[1], q.x0[2], q.x0[3]};
+    *(f32x4*)&Bt[bu_swz(lane + 64, wave)] = f32x4{q.x1[0], q.x1[1], q.x1[2], q.x1[3]};
   };
 
-  f32x16 acc[kNA];
+  f32x16 acc;
 #pragma unroll
-  for (int j = 0; j < kNA; ++j)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  // Operand rows of this lane and their swizzled chunk bases.
+  const int arow = wm + l32, brow = wn + l32;
+  const int aoff = arow << 5, boff = (kUM + brow) << 5;
+  const int asw = (4 * lhi) ^ ((arow >> 1) & 7), bsw = (4 * lhi) ^ ((brow >> 1) & 7);
   auto mfma_stage = [&](int buf) {
     if (!wave_on) return;
-    const float* As = lds + buf * kStage;
-    const float* Bs = As + kSC * kLA;
+    const float* S = lds + buf * kStage;
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int ss = 0; ss < kSC; ss += 2) {
-      const int sr = ss + lhi;
-      const float av = As[sr * kLA + wm + l32];
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 x = *(const f32x4*)&S[aoff + ((asw ^ q) << 2)];
+      const f32x4 y = *(const f32x4*)&S[boff + ((bsw ^ q) << 2)];
 #pragma unroll
-      for (int j = 0; j < kNA; ++j)
-        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kLB + wn + 32 * j + l32], acc[j], 0, 0, 0);
+      for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[e], y[e], acc, 0, 0, 0);
     }
     __builtin_amdgcn_s_setprio(0);
   };
 
   load_stage(0, RA);
   load_stage(1, RB);
-  store_stage(0, RA);
+  store_stage(0, 0, RA);
   __syncthreads();
-  // Iteration st: loads of stage st+2 go out, the MFMAs of stage st (LDS
-  // buffer st&1) run, stage st+1 goes to the other buffer.  Unrolled by two
-  // so each register set is named statically.
-  for (int st = 0; st < nst; st += 2) {
+  // Iteration st: loads of stage st+2 go out, the MFMAs of stage st (buffer
+  // 0) run, stage st+1 goes to buffer 1; then the same one stage later with
+  // the buffers and register sets swapped.  A single loop exit and the odd
+  // last stage after the loop keep the load waits where the data is used.
+  int st = 0;
+  for (; st + 1 < nst; st += 2) {
     load_stage(st + 2, RA);
     __builtin_amdgcn_sched_barrier(0);
     mfma_stage(0);
-    store_stage(1, RB);
+    store_stage(st + 1, 1, RB);
     __syncthreads();
-    if (st + 1 >= nst) break;
     load_stage(st + 3, RB);
     __builtin_amdgcn_sched_barrier(0);
     mfma_stage(1);
-    store_stage(0, RA);
+    store_stage(st + 2, 0, RA);
+    __syncthreads();
+  }
+  if (st < nst) {  // an odd stage count: the last stage is in buffer 0
+    mfma_stage(0);
     __syncthreads();
   }
 
-  // Base tile (16-byte pieces, thread t: column piece t%kXP of rows t/kXP +
-  // kXR*i), loaded only now so that its registers are free during the
+  // Base tile (16-byte pieces, thread t: column piece t%32 of rows t/32 +
+  // 16*i), loaded only now so that its registers are free during the
   // contraction (three workgroups per CU); its latency overlaps the
   // accumulator transfer to LDS.
-  constexpr int kWL = kUM / kXR;
+  constexpr int kXP = kUN / 4, kXR = NTH / kXP, kWL = kUM / kXR;
+  const int xc4 = tid % kXP, xr0 = tid / kXP;
+  const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
+  const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
   const float* Wb = a.Wb + (int64_t)g * a.wb_pitch;
   f32x4 wv[kWL];
 #pragma unroll
@@ -353,12 +319,10 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
     wv[i] = *(const f32x4*)(Wb + (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
   }
 #pragma unroll
-  for (int j = 0; j < kNA; ++j)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
-      Gt[row * kLB + wn + 32 * j + l32] = acc[j][r];
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+    Gt[row * kLB + wn + l32] = acc[r];
+  }
   __syncthreads();
   float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
   const float lr_eff = *a.lr / a.lr_div;
@@ -379,11 +343,7 @@ void launch_block_update(hipStream_t s, const BlkArgs& a) {
   const int mtiles = (a.Mrows + kUM - 1) / kUM;
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
-  const uint32_t shmem = sizeof(uint32_t) * a.K1 * a.SG * a.B;
-  if (a.B % kSC == 0)
-    launch(k_block_update<HAV_BLK_THREADS, true>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
-  else
-    launch(k_block_update<HAV_BLK_THREADS, false>, grid, HAV_BLK_THREADS, shmem, s, a, mtiles, ntiles);
+  launch(k_block_update<HAV_BLK_THREADS>, grid, HAV_BLK_THREADS, 0, s, a, a.gtab, a.xtab, mtiles, ntiles);
 }
 
 // ------------------------------------------------------------ Gram blocks
