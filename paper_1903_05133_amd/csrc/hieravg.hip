@@ -607,7 +607,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       const int k = kc == KC_HEAD_END ? c.K1 : tt % c.K1;
       const int blk = tt / c.K1;
       HeadStepArgs a{};
-      a.part = h->part + (int64_t)(k < c.K1 ? k : 0) * P * Bp * Hp;
+      a.part = h->part;
       a.KS = h->ks_cur;
       a.split = (int64_t)c.K1 * P * Bp * Hp;
       a.W2 = W + h->off_W2;
@@ -619,8 +619,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.pl_half = (int64_t)P * (Hp / 32) * Bp * Cp;
       a.gs = h->Gs;
       a.gram = h->gram ? h->gram + (int64_t)blk * P * c.K1 * c.K1 * Bp * Bp : nullptr;
-      // the previous step's labels (HEAD_END: this step's, the block's last)
-      a.ylab_prev = h->ylab + (int64_t)(kc == KC_HEAD_END ? tt : tt - 1) * P * B;
+      a.ylab = h->ylab + (int64_t)blk * c.K1 * P * B;
       a.lr = h->hyper;
       a.P = P;
       a.M = B;
@@ -629,8 +628,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.Cp = Cp;
       a.Hp = Hp;
       a.K1 = c.K1;
-      a.k = k;
-      launch_head_step(s, a);
+      launch_head_step(s, a, k);
       return true;
     }
     case KC_REDUCE1:

@@ -310,14 +310,15 @@ void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* 
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, const float* lr, HeadMom mom = HeadMom());
 
-// One launch per local step of the delayed schedule (C <= 32, M <= 32, K1 <= 8):
-// workgroup (p, slice of 32 hidden units) finishes step k-1's backward for its
-// units (logits from every slice's partial logits, softmax gradient, hidden
-// error into gs[k-1], SGD steps of b1, W2 and, on slice 0, b2) and runs step
-// k's forward for them (pre-activations with the Gram correction, partial
-// logits).  k = 0: forward only; k = K1: backward of the block's last step.
+// Head of the delayed schedule (C <= 32, M <= 32, K1 <= 8), step k of a
+// block: workgroup (p, slice of 32 hidden units) finishes step k-1's backward
+// for its units (logits from every slice's partial logits, softmax gradient,
+// hidden error into gs[k-1], SGD steps of b1, W2 and, on slice 0, b2) and
+// runs step k's forward for them (pre-activations with the Gram correction,
+// partial logits).  k = 0: forward only; k = K1: backward of the block's last
+// step.
 struct HeadStepArgs {
-  const float* part;      // step k's layer-1 split-K partials (split floats apart)
+  const float* part;      // the block's layer-1 split-K partials: step k at + k*P*Mp*Hp, splits `split` apart
   int KS;
   int64_t split;
   float* W2;              // replica 0's second weight block; replica p at + p*w_pitch
@@ -329,11 +330,12 @@ struct HeadStepArgs {
   int64_t pl_half;        // floats per parity
   float* gs;              // [K1][P][Mp][Hp] hidden errors of the block's steps
   const float* gram;      // [P][K1][K1][Mp][Mp] of the block
-  const int32_t* ylab_prev;  // [P][M] labels of the samples of step k-1
+  const int32_t* ylab;    // [K1][P][M] labels of the block's samples
   const float* lr;        // device scalar step size
-  int P, M, Mp, C, Cp, Hp, K1, k;
+  int P, M, Mp, C, Cp, Hp, K1;
 };
-void launch_head_step(hipStream_t s, const HeadStepArgs& a);
+// One launch for step k.
+void launch_head_step(hipStream_t s, const HeadStepArgs& a, int k);
 
 // Per-row softmax cross-entropy and first-argmax hit of an evaluation chunk
 // from split-K logit partials part[ks][m][Cp] (split floats apart) and bias.

@@ -401,7 +401,8 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 }
 
 // Fused head of the delayed schedule (HeadStepArgs).  Workgroup (p, ht) owns
-// hidden units h = 32*ht + u of learner p; M <= 32 samples, one chunk.
+// hidden units h = 32*ht + u of learner p; M <= 32 samples, one chunk.  Step k
+// of a block:
 //  (A) k > 0, the rest of step k-1: logits of every sample from the partial
 //      logits of all slices (b2 is folded into slice 0's), its softmax
 //      cross-entropy gradient G2 (mean over the minibatch; eight threads per
@@ -416,9 +417,10 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 // read and written by slice 0 only, so no workgroup depends on another
 // within a launch.  Every global load the launch needs that does not depend
 // on (A) is issued before (A) starts: step k's partials, the Gram rows and
-// the earlier steps' hidden errors of (B).
+// the earlier steps' hidden errors of (B), and this slice's W2, Z1 and b1
+// for (A).
 template <int KC>
-__global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
+__global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, int k) {
   constexpr int kG = 256 / kHU, kR = kHM / kG;
   constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
   constexpr int kGrlS = kHM + 1;                    // Gram row stride (conflict-free column reads)
@@ -444,14 +446,17 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   float* b1 = a.b1 + (int64_t)p * a.w_pitch;
   float* b2 = a.b2 + (int64_t)p * a.w_pitch;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-
-  // Step k's partial sums.
   const int u4 = tid & 7, rr = tid >> 3;
   const int h4 = ht * kHU + 4 * u4;
+  const int gsm = tid / (kHU / 4), gc4 = tid % (kHU / 4);
+  const int u = tid % kHU, g = tid / kHU, h = ht * kHU + u;
+  const int64_t step_floats = (int64_t)a.P * Mp * Hp;  // one step of the block's partials
+
+  // Step k's partial sums.
   f32x4 z = zero4;
-  const int kc = a.k < a.K1 ? a.k : 0;  // earlier steps whose correction (B) applies
-  if (a.k < a.K1) {
-    const float* pm = a.part + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+  const int kc = k < a.K1 ? k : 0;  // earlier steps whose correction (B) applies
+  if (k < a.K1) {
+    const float* pm = a.part + k * step_floats + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
 #pragma unroll 8
     for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
   }
@@ -459,40 +464,40 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   // each step's 32 x 32 slice; step k-1 comes from (A)) and the Gram rows
   // gram[k][k2] (piece tid of each Mp x Mp block).
   f32x4 gv[kCorrMaxK - 1], gr[kCorrMaxK];
-  const int gsm = tid / (kHU / 4), gc4 = tid % (kHU / 4);
 #pragma unroll
   for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2) {
     gv[k2] = zero4;
     if (k2 < kc - 1 && gsm < M)
       gv[k2] = *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + gsm) * Hp + ht * kHU + 4 * gc4);
   }
-  const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
+  const float* gk = a.gram + (((int64_t)p * a.K1 + k) * a.K1) * Mp * Mp;
 #pragma unroll
   for (int k2 = 0; k2 < kCorrMaxK; ++k2) {
     gr[k2] = zero4;
     if (k2 < kc && tid < Mp * Mp / 4) gr[k2] = *(const f32x4*)(gk + (int64_t)k2 * Mp * Mp + 4 * tid);
   }
-
-  if (a.k > 0) {  // (A): the rest of step k-1
-    const int kp = a.k - 1;
-    const int u = tid % kHU, g = tid / kHU, h = ht * kHU + u;
-    float* g2s = region;                   // [kHM][KC + 1]
-    float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
-    if (tid < kHM) ys[tid] = a.ylab_prev[(int64_t)p * M + (tid < M ? tid : 0)];
-    float wc[KC];
+  // (A)'s operands of this slice: W2[:, h], the pre-activations of step
+  // k-1 and b1[h] (all written by this workgroup only).
+  float wc[KC], zp[kR], b1h = 0.0f;
+  if (k > 0) {
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
       const float v = w2[(int64_t)(c < C ? c : 0) * Hp + h];
       wc[c] = c < C ? v : 0.0f;
     }
-    float zp[kR];
 #pragma unroll
     for (int i = 0; i < kR; ++i) {
       const int mm = g + kG * i;
       const float v = a.Z1[((int64_t)p * Mp + (mm < M ? mm : 0)) * Hp + h];
       zp[i] = mm < M ? v : 0.0f;
     }
-    const float b1h = b1[h];
+    b1h = b1[h];
+  }
+  if (k > 0) {  // (A): the rest of step k-1
+    const int kp = k - 1;
+    float* g2s = region;                   // [kHM][KC + 1]
+    float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
+    if (tid < kHM) ys[tid] = a.ylab[((int64_t)kp * a.P + p) * M + (tid < M ? tid : 0)];
     const float* plp = a.PL + (int64_t)(kp & 1) * a.pl_half;
 #pragma unroll
     for (int q = 0; q < kHM * KC / 256; ++q) {
@@ -567,7 +572,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
 #pragma unroll
         for (int c = 0; c < KC; ++c) dw2[c] += g2s[mm * (KC + 1) + c] * act;
       }
-      if (a.k < a.K1) gsl(kp, mm, u) = g1;  // for (B) (k-1 <= K1-2 < kCorrMaxK)
+      if (k < a.K1) gsl(kp, mm, u) = g1;  // for (B) (k-1 <= K1-2 < kCorrMaxK)
     }
     if (ht == 0 && tid < C)
       for (int mm = 0; mm < M; ++mm) db2 += g2s[mm * (KC + 1) + tid];
@@ -606,7 +611,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
     if (tid < kHU) bs[tid] = b1[ht * kHU + tid];
     if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2[tid] : 0.0f;
   }
-  if (a.k >= a.K1) return;
+  if (k >= a.K1) return;
 
   // (B): step k's forward for this slice.
 #pragma unroll
@@ -616,11 +621,11 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   for (int k2 = 0; k2 < kCorrMaxK; ++k2)
     if (k2 < kc && tid < Mp * Mp / 4) {
       const int rem = 4 * tid;
-      float* g = &grl[(k2 * kHM + rem / Mp) * kGrlS + rem % Mp];
-      g[0] = gr[k2].x;
-      g[1] = gr[k2].y;
-      g[2] = gr[k2].z;
-      g[3] = gr[k2].w;
+      float* gp = &grl[(k2 * kHM + rem / Mp) * kGrlS + rem % Mp];
+      gp[0] = gr[k2].x;
+      gp[1] = gr[k2].y;
+      gp[2] = gr[k2].z;
+      gp[3] = gr[k2].w;
     }
   float* zs = region;           // [kHM][kHU + 1]
   float* cbuf = region + kZs;   // [4][kHM][kHM + 1]
@@ -660,7 +665,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   zs[rr * (kHU + 1) + 4 * u4 + 2] = mok ? fmaxf(z.z, 0.0f) : 0.0f;
   zs[rr * (kHU + 1) + 4 * u4 + 3] = mok ? fmaxf(z.w, 0.0f) : 0.0f;
   __syncthreads();
-  float* plo = a.PL + (int64_t)(a.k & 1) * a.pl_half;
+  float* plo = a.PL + (int64_t)(k & 1) * a.pl_half;
 #pragma unroll
   for (int q = 0; q < kHM * KC / 256; ++q) {
     const int e = tid + 256 * q, mm = e / KC, c = e % KC;
@@ -671,12 +676,12 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles) {
   }
 }
 
-void launch_head_step(hipStream_t s, const HeadStepArgs& a) {
+void launch_head_step(hipStream_t s, const HeadStepArgs& a, int k) {
   const int htiles = a.Hp / kHU;
   if (a.C <= 16)
-    launch(k_head_step<16>, a.P * htiles, 256, 0, s, a, htiles);
+    launch(k_head_step<16>, a.P * htiles, 256, 0, s, a, htiles, k);
   else
-    launch(k_head_step<32>, a.P * htiles, 256, 0, s, a, htiles);
+    launch(k_head_step<32>, a.P * htiles, 256, 0, s, a, htiles, k);
 }
 
 // Evaluation: one wave per row m < M of a chunk.  Logits l_c = b_c + sum_ks

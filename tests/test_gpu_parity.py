@@ -268,6 +268,23 @@ def test_torch_stream_and_profile(gpu_lib):
     assert all(ms >= 0.0 for _, ms in stats.values())
 
 
+def test_delayed_head_wide_hidden_layer(gpu_lib):
+    """18 learners x 16 hidden slices (H = 480, ragged last slice) = 288 head
+    workgroups per launch, more than one per CU: one head launch per step and
+    one for the block's last backward; parity with the oracle."""
+    from paper_1903_05133_amd import HierAvg
+    c = cases.case("mlp", 18, 3, 2, 2, B=12, IN=64, H=480, C=6, N=200, lr=0.05, seed=16)
+    with HierAvg(config=cases.native_config(c, "delayed")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+        h.profile(False)
+        got = h.params()
+        idx = h.last_indices()
+    assert stats["head_step"][0] == 4 and stats["head_step_end"][0] == 2
+    _check(c, got, idx, *_oracle(c, 1))
+
+
 def test_delayed_schedule_profile(gpu_lib):
     """Delayed updates, P=6 S=3 K1=2 K2=3: per block one forward of its steps
     and one update of the cluster copies, per step one fused head kernel
