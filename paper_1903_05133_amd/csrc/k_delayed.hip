@@ -366,11 +366,14 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   const int ks = blockIdx.x % KSG;
   const int pb = blockIdx.x / KSG;  // p + P * b
   const int p = pb % P, b = pb / P;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar block bookkeeping
   const int lrow = lane & 15, lgrp = lane >> 4;
   const int rows = K1 * Bp;
   const int nch = K / kKC;
   const int c0 = (int)((int64_t)nch * ks / KSG), c1 = (int)((int64_t)nch * (ks + 1) / KSG);
+  // Bp is 16 or 32 (B <= 32): row and block indices split with shifts.
+  const int lg_bp = Bp == 32 ? 5 : 4, lg_mbs = lg_bp - 4;
   // Row r = k*Bp + s of the block: sample s of step b*K1 + k (rows past B: zero).
   const float* src[kLPT];
   bool ok[kLPT];
@@ -379,30 +382,36 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   for (int i = 0; i < kLPT; ++i) {
     const int q = tid + 256 * i;
     const int r = q >> 4, c4 = q & 15;
-    const int k = r / Bp, sm = r - k * Bp;
+    const int k = r >> lg_bp, sm = r & (Bp - 1);
     ok[i] = r < rows && sm < B;
     const int64_t e = ((int64_t)(b * K1 + (ok[i] ? k : 0)) * P + p) * B + (ok[i] ? sm : 0);
     src[i] = X + (int64_t)idx[e] * ldx + 4 * c4;
     off[i] = (r < kRows ? r : 0) * kL + 4 * c4;
   }
   // Output blocks of this wave: block e = wave + 4*t over the lower triangle
-  // (pair (k, k2), row block mb, column block nb).
-  const int mbs = Bp / 16;
+  // (pair (k, k2), row block mb, column block nb); wave-uniform.
+  const int mbs = 1 << lg_mbs;
   const int nblk = K1 * (K1 - 1) / 2 * mbs * mbs;
+  int bk[NB], bk2[NB], bmb[NB], bnb[NB];
   int arow[NB], brow[NB];
   bool bon[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
     const int e = wave + 4 * t;
     bon[t] = e < nblk;
-    int pr = (bon[t] ? e : 0) / (mbs * mbs), rem = (bon[t] ? e : 0) % (mbs * mbs);
+    const int ee = bon[t] ? e : 0;
+    const int pr = ee >> (2 * lg_mbs), rem = ee & (mbs * mbs - 1);
     int k = 1, k2 = pr;
     while (k2 >= k) {
       k2 -= k;
       ++k;
     }
-    arow[t] = (k * Bp + 16 * (rem / mbs) + lrow) * kL + 4 * lgrp;
-    brow[t] = (k2 * Bp + 16 * (rem % mbs) + lrow) * kL + 4 * lgrp;
+    bk[t] = k;
+    bk2[t] = k2;
+    bmb[t] = rem >> lg_mbs;
+    bnb[t] = rem & (mbs - 1);
+    arow[t] = (k * Bp + 16 * bmb[t] + lrow) * kL + 4 * lgrp;
+    brow[t] = (k2 * Bp + 16 * bnb[t] + lrow) * kL + 4 * lgrp;
   }
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   f32x4 acc[NB];
@@ -413,10 +422,19 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
 #pragma unroll
     for (int i = 0; i < kLPT; ++i) v[i] = *(const f32x4*)(src[i] + (int64_t)c * kKC);
   };
+  // rows is a multiple of 16, so piece i exists for all threads or none;
+  // with B == Bp every staged row is a sample.
+  const bool all_rows = B == Bp;
   auto store = [&]() {
+    if (all_rows) {
 #pragma unroll
-    for (int i = 0; i < kLPT; ++i)
-      if (tid + 256 * i < rows * (kKC / 4)) *(f32x4*)&xs[off[i]] = ok[i] ? v[i] : zero4;
+      for (int i = 0; i < kLPT; ++i)
+        if (16 * i < rows) *(f32x4*)&xs[off[i]] = v[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < kLPT; ++i)
+        if (16 * i < rows) *(f32x4*)&xs[off[i]] = ok[i] ? v[i] : zero4;
+    }
   };
   if (c0 < c1) {
     load(c0);
@@ -440,21 +458,14 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
     }
   }
   // gram[ks][b][p][k][k2][s][s2]
+  const int K2n = gridDim.x / (KSG * P);
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
     if (!bon[t]) continue;
-    const int e = wave + 4 * t;
-    const int pr = e / (mbs * mbs), rem = e % (mbs * mbs);
-    int k = 1, k2 = pr;
-    while (k2 >= k) {
-      k2 -= k;
-      ++k;
-    }
-    const int K2n = gridDim.x / (KSG * P);
-    float* out = gram + (((((int64_t)ks * K2n + b) * P + p) * K1 + k) * K1 + k2) * Bp * Bp;
+    float* out = gram + (((((int64_t)ks * K2n + b) * P + p) * K1 + bk[t]) * K1 + bk2[t]) * Bp * Bp +
+                 (16 * bmb[t] + 4 * lgrp) * Bp + 16 * bnb[t] + lrow;
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      out[(16 * (rem / mbs) + 4 * lgrp + r) * Bp + 16 * (rem % mbs) + lrow] = acc[t][r];
+    for (int r = 0; r < 4; ++r) out[r * Bp] = acc[t][r];
   }
 }
 
@@ -492,7 +503,7 @@ int gram_splits(int P, int K2, int K) {
 void launch_gram(hipStream_t s, const float* X, int64_t ldx, int K, const int32_t* idx, float* gram, int P, int K1,
                  int K2, int B, int Bp, int KSG) {
   const int nblk = K1 * (K1 - 1) / 2 * (Bp / 16) * (Bp / 16);
-  if (nblk == 0) return;
+  if (nblk == 0 || (Bp != 16 && Bp != 32)) return;  // the delayed schedule has B <= 32
   const unsigned grid = (unsigned)((int64_t)P * K2 * KSG);
   const int nb = (nblk + 3) / 4;
 #define HAV_GRAM(N_, R_) launch(k_gram<N_, R_>, grid, 256, 0, s, X, ldx, K, idx, gram, P, K1, B, Bp, KSG)
