@@ -59,10 +59,12 @@ constexpr uint64_t kTagTestNoise = 0x68762e746e6f6973ull;  // "hv.tnois"
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-// n / d for 0 <= n < 2^24, d >= 1, from inv = 1.0f / d (computed once by the
-// caller): the float quotient is within one of the true one, and one
-// correction step each way makes it exact.  A few vector instructions
-// instead of the long sequence of an integer division.
+// n / d for 0 <= n < 2^22, d >= 1, from inv = qdiv_inv(d) (1/d to within an
+// ulp, computed once by the caller): n * inv is within one of n / d, so the
+// truncated quotient is off by at most one, and one correction step each way
+// makes it exact.  A few vector instructions instead of the long sequence of
+// an integer division.
+__device__ inline float qdiv_inv(int d) { return __builtin_amdgcn_rcpf((float)d); }
 __device__ inline int qdiv_small(int n, int d, float inv) {
   int q = (int)((float)n * inv);
   q += (q + 1) * d <= n ? 1 : 0;

@@ -38,11 +38,12 @@ constexpr int kBT = 128;  // tile rows and columns
 __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mtiles) {
   __shared__ __attribute__((aligned(16))) float As[2][kBT * kLdsStride];
   __shared__ __attribute__((aligned(16))) float Ws[2][kBT * kLdsStride];
+  // Tile (nt, mt, ks, g) of this workgroup: float-reciprocal quotients (a few
+  // vector instructions each, where an integer division takes dozens).
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int nt = bid % ntiles;
-  const int mt = (bid / ntiles) % mtiles;
-  const int ks = (bid / (ntiles * mtiles)) % a.KS;
-  const int g = bid / (ntiles * mtiles * a.KS);
+  const int q1 = qdiv_small(bid, ntiles, qdiv_inv(ntiles)), nt = bid - q1 * ntiles;
+  const int q2 = qdiv_small(q1, mtiles, qdiv_inv(mtiles)), mt = q1 - q2 * mtiles;
+  const int g = qdiv_small(q2, a.KS, qdiv_inv(a.KS)), ks = q2 - g * a.KS;
   const int GM = a.SG * a.Mp;
   const int nch = a.K / kKC;
   const int c0 = ks * a.cps;
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   bool aok[2], wok[2];
   int off[2];
   const float* wp = a.W + (int64_t)(g / a.wdiv) * a.w_pitch;
-  const float inv_mp = 1.0f / (float)a.Mp, inv_vs = 1.0f / (float)(a.vS > 0 ? a.vS : 1);
+  const float inv_mp = qdiv_inv(a.Mp), inv_vs = qdiv_inv(a.vS > 0 ? a.vS : 1);
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int q = tid + 1024 * i;
@@ -124,17 +125,35 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   const int col = nbase + wn + l32;
   if (col < a.N) {
     // The lane's rows 8i + e (e < 4) share one member (Mp is a multiple of
-    // 16, GM of 16), so the row -> (member, sample) split runs once per i.
+    // 16, GM of 16).  The (member, sample) split of row 8i follows from that
+    // of row 8(i-1): 8 < Mp, so the sample wraps into the next member at
+    // most once, and the member's (step, learner) advances the same way.
+    int row0 = mbase + wm + 4 * lhi;
+    int v = qdiv_small(row0, a.Mp, inv_mp), sm = row0 - v * a.Mp;
+    int vk = 0, vj = v;  // v = vk * vS + vj
+    if (a.vS > 0) {
+      vk = qdiv_small(v, a.vS, inv_vs);
+      vj = v - vk * a.vS;
+    }
+    const int64_t gbase = a.vS > 0 ? (int64_t)g * a.vS : (int64_t)g * a.SG;
+    const int64_t kstride = a.vS > 0 ? a.P : 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row0 = mbase + wm + 8 * i + 4 * lhi;
-      if (row0 >= GM) continue;
-      const int v = qdiv_small(row0, a.Mp, inv_mp), sm = row0 - v * a.Mp;
-      int64_t p = (int64_t)g * a.SG + v;
-      if (a.vS > 0) {
-        const int k = qdiv_small(v, a.vS, inv_vs);
-        p = (int64_t)k * a.P + (int64_t)g * a.vS + (v - k * a.vS);
+      if (i > 0) {
+        row0 += 8;
+        sm += 8;
+        if (sm >= a.Mp) {
+          sm -= a.Mp;
+          if (a.vS > 0 && ++vj == a.vS) {
+            vj = 0;
+            ++vk;
+          } else if (a.vS <= 0) {
+            ++vj;
+          }
+        }
       }
+      if (row0 >= GM) break;
+      const int64_t p = vk * kstride + gbase + vj;
       float* dst = a.part + (((int64_t)ks * PT + p) * a.Mp + sm) * a.N + col;
 #pragma unroll
       for (int e = 0; e < 4; ++e) dst[(int64_t)e * a.N] = acc[4 * i + e];
