@@ -462,9 +462,10 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
       __syncthreads();
       load(c + 1 < c1 ? c + 1 : c);  // next chunk in flight (the last again at the end)
       __builtin_amdgcn_sched_barrier(0);
+      // Blocks past nblk repeat block 0 (their sums are not stored): no
+      // branch around the MFMAs, so the accumulators stay in place.
 #pragma unroll
       for (int t = 0; t < NB; ++t) {
-        if (!bon[t]) continue;
 #pragma unroll
         for (int q = 0; q < kKC / 16; ++q) {
           const f32x4 x = *(const f32x4*)&xs[arow[t] + 16 * q];
