@@ -373,14 +373,15 @@ void launch_block_update(hipStream_t s, const BlkArgs& a) {
 // owns a fixed set of the 16x16 output blocks of the lower block triangle
 // (16x16x4 MFMAs, the k permutation of k_fwd_nt).  Every minibatch row is
 // read once per split; the consumer adds the KSG partial sums.
-constexpr int kGramMaxBlocks = 28;  // 16x16 output blocks per wave (K1 <= 8, Bp <= 32)
+constexpr int kGT = 512, kGW = kGT / 64;  // threads and waves per workgroup
+constexpr int kGramMaxBlocks = 14;  // 16x16 output blocks per wave (K1 <= 8, Bp <= 32)
 template <int NB, int ROWS>
-__global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t ldx, int K,
+__global__ __launch_bounds__(kGT) void k_gram(const float* __restrict__ X, int64_t ldx, int K,
                                               const int32_t* __restrict__ idx, float* __restrict__ gram, int P,
                                               int K1, int B, int Bp, int KSG) {
   constexpr int kRows = ROWS;         // LDS capacity in rows (K1 * Bp <= ROWS)
   constexpr int kL = kKC + 4;         // LDS row length
-  constexpr int kLPT = kRows * (kKC / 4) / 256;  // 16-byte pieces per thread per chunk (at most)
+  constexpr int kLPT = kRows * (kKC / 4) / kGT;  // 16-byte pieces per thread per chunk (at most)
   __shared__ __attribute__((aligned(16))) float xs[kRows * kL];
   const int ks = blockIdx.x % KSG;
   const int pb = blockIdx.x / KSG;  // p + P * b
@@ -399,7 +400,7 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   int off[kLPT];
 #pragma unroll
   for (int i = 0; i < kLPT; ++i) {
-    const int q = tid + 256 * i;
+    const int q = tid + kGT * i;
     const int r = q >> 4, c4 = q & 15;
     const int k = r >> lg_bp, sm = r & (Bp - 1);
     ok[i] = r < rows && sm < B;
@@ -407,7 +408,7 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
     src[i] = X + (int64_t)idx[e] * ldx + 4 * c4;
     off[i] = (r < kRows ? r : 0) * kL + 4 * c4;
   }
-  // Output blocks of this wave: block e = wave + 4*t over the lower triangle
+  // Output blocks of this wave: block e = wave + kGW*t over the lower triangle
   // (pair (k, k2), row block mb, column block nb); wave-uniform.
   const int mbs = 1 << lg_mbs;
   const int nblk = K1 * (K1 - 1) / 2 * mbs * mbs;
@@ -416,7 +417,7 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   bool bon[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
-    const int e = wave + 4 * t;
+    const int e = wave + kGW * t;
     bon[t] = e < nblk;
     const int ee = bon[t] ? e : 0;
     const int pr = ee >> (2 * lg_mbs), rem = ee & (mbs * mbs - 1);
@@ -441,18 +442,18 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
 #pragma unroll
     for (int i = 0; i < kLPT; ++i) v[i] = *(const f32x4*)(src[i] + (int64_t)c * kKC);
   };
-  // rows is a multiple of 16, so piece i exists for all threads or none;
-  // with B == Bp every staged row is a sample.
+  // Piece i holds row (tid >> 4) + 32*i; with B == Bp every staged row is a
+  // sample.
   const bool all_rows = B == Bp;
   auto store = [&]() {
     if (all_rows) {
 #pragma unroll
       for (int i = 0; i < kLPT; ++i)
-        if (16 * i < rows) *(f32x4*)&xs[off[i]] = v[i];
+        if ((tid >> 4) + 32 * i < rows) *(f32x4*)&xs[off[i]] = v[i];
     } else {
 #pragma unroll
       for (int i = 0; i < kLPT; ++i)
-        if (16 * i < rows) *(f32x4*)&xs[off[i]] = ok[i] ? v[i] : zero4;
+        if ((tid >> 4) + 32 * i < rows) *(f32x4*)&xs[off[i]] = ok[i] ? v[i] : zero4;
     }
   };
   if (c0 < c1) {
@@ -525,18 +526,18 @@ void launch_gram(hipStream_t s, const float* X, int64_t ldx, int K, const int32_
   const int nblk = K1 * (K1 - 1) / 2 * (Bp / 16) * (Bp / 16);
   if (nblk == 0 || (Bp != 16 && Bp != 32)) return;  // the delayed schedule has B <= 32
   const unsigned grid = (unsigned)((int64_t)P * K2 * KSG);
-  const int nb = (nblk + 3) / 4;
-#define HAV_GRAM(N_, R_) launch(k_gram<N_, R_>, grid, 256, 0, s, X, ldx, K, idx, gram, P, K1, B, Bp, KSG)
+  const int nb = (nblk + kGW - 1) / kGW;
+#define HAV_GRAM(N_, R_) launch(k_gram<N_, R_>, grid, kGT, 0, s, X, ldx, K, idx, gram, P, K1, B, Bp, KSG)
   if (K1 * Bp <= 128) {
-    if (nb <= 2)
-      HAV_GRAM(2, 128);
-    else if (nb <= 6)
-      HAV_GRAM(6, 128);
+    if (nb <= 1)
+      HAV_GRAM(1, 128);
+    else if (nb <= 3)
+      HAV_GRAM(3, 128);
     else
-      HAV_GRAM(12, 128);
+      HAV_GRAM(6, 128);
   } else {
-    if (nb <= 12)
-      HAV_GRAM(12, 256);
+    if (nb <= 6)
+      HAV_GRAM(6, 256);
     else
       HAV_GRAM(kGramMaxBlocks, 256);
   }
