@@ -561,12 +561,18 @@ bool launch_class(hieravg* h, int kc, int tt) {
       BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
                 b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S,
                 h->btab + b * blk, h->btab + (int64_t)c.K2 * blk + b * blk};
+      if (b < c.K2 - 1 && S > 1) {  // the block-end cluster mean of b1, W2, b2 (the last block's is global)
+        a.tail = W + h->off_b1;
+        a.tail_pitch = h->Dp;
+        a.tail_len = h->Dp - h->off_b1;
+      }
       launch_block_update(s, a);
       return true;
     }
-    case KC_W1_MEAN:
+    case KC_W1_MEAN:  // with the global mean of b1, W2, b2 in the same launch
       if (!h->delayed) return false;
-      launch_mean_rows(s, W + h->off_W1, h->Wc, h->Hp * h->INp, h->Hp * h->INp, P / S);
+      launch_mean_rows(s, W + h->off_W1, h->Wc, h->Hp * h->INp, h->Hp * h->INp, P / S, P > 1 ? W + h->off_b1 : nullptr,
+                       h->Dp, h->Dp - h->off_b1, P);
       return true;
     case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, S); return true;
     case KC_GLOBAL_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, P); return true;
@@ -870,11 +876,9 @@ void enqueue_round(hieravg* h) {
         for (int k = 0; k < c.K1; ++k)
           for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2}) go(kc, b * c.K1 + k);
       }
-      go(KC_BLOCK_UPDATE, b * c.K1);
-      if (b < c.K2 - 1 && S > 1) go(KC_TAIL_MEAN, 0);
+      go(KC_BLOCK_UPDATE, b * c.K1);  // with the cluster mean of b1, W2, b2 for b < K2 - 1
     }
-    go(KC_W1_MEAN, 0);
-    if (P > 1) go(KC_TAIL_GLOBAL, 0);
+    go(KC_W1_MEAN, 0);  // with the global mean of b1, W2, b2
   } else {
     run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
     bool have_fwd = false;

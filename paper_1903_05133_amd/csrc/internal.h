@@ -237,6 +237,12 @@ struct BlkArgs {
   float lr_div;
   const uint32_t* gtab;  // this block's row tables (BlkTables): [P/SG][Rp] each
   const uint32_t* xtab;
+  // Optional (tail set): also replace the columns [0, tail_len) of each
+  // group's SG replica rows (replica 0's at tail, tail_pitch floats apart) by
+  // the group's mean: the cluster mean of the parameters after the first
+  // block, which no other part of the launch touches.
+  float* tail = nullptr;
+  int64_t tail_pitch = 0, tail_len = 0;
 };
 // Largest contraction (K1 * SG * B rows) of a block update.
 constexpr int kBlkMaxRows = 16384;
@@ -348,8 +354,11 @@ void launch_eval_rows(hipStream_t s, const float* part, int KS, int64_t split, c
 // Mean over each cluster of S rows of the columns [0, len) of W (row pitch
 // `pitch`, both multiples of 4 floats).
 void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int P, int S);
-// dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4 floats).
-void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n);
+// dst[i] = mean over r < n of src[r*pitch + i], i < len (multiples of 4
+// floats); in the same launch (W set) the columns [0, len_b) of the nb rows
+// of W (pitch_b apart) replaced by their mean.
+void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n,
+                      float* W = nullptr, int64_t pitch_b = 0, int64_t len_b = 0, int nb = 0);
 // flag = 1 if any of rows 1..n-1 of W (pitch floats apart) differs from row 0
 // in columns [0, len) (bit patterns; len a multiple of 4); flag untouched otherwise.
 void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t len, int n, int* flag);

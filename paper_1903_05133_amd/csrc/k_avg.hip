@@ -175,18 +175,35 @@ void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int 
          0.0f);
 }
 
+// Workgroups below g1: dst = mean of the n rows of src.  The others (when W
+// is set): each column of the first n4b pieces of W's nb rows replaced by the
+// rows' mean, rows added in order.
 __global__ __launch_bounds__(256) void k_mean_rows(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
-                                                   int64_t pitch4, int64_t n4, int n) {
-  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-    f32x4 sum = src[i];
-    for (int r = 1; r < n; ++r) sum += src[r * pitch4 + i];
-    dst[i] = sum / (float)n;
+                                                   int64_t pitch4, int64_t n4, int n, int g1, f32x4* __restrict__ W,
+                                                   int64_t pitchb4, int64_t n4b, int nb) {
+  if ((int)blockIdx.x < g1) {
+    for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)g1 * 256) {
+      f32x4 sum = src[i];
+      for (int r = 1; r < n; ++r) sum += src[r * pitch4 + i];
+      dst[i] = sum / (float)n;
+    }
+    return;
+  }
+  const int gb = gridDim.x - g1;
+  for (int64_t i = (blockIdx.x - g1) * 256ll + threadIdx.x; i < n4b; i += (int64_t)gb * 256) {
+    f32x4 sum = W[i];
+    for (int r = 1; r < nb; ++r) sum += W[r * pitchb4 + i];
+    const f32x4 mean = sum / (float)nb;
+    for (int r = 0; r < nb; ++r) W[r * pitchb4 + i] = mean;
   }
 }
 
-void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n) {
+void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch, int64_t len, int n, float* W,
+                      int64_t pitch_b, int64_t len_b, int nb) {
   const int64_t n4 = len / 4;
-  launch(k_mean_rows, col_runs(n4, 256, 1), 256, 0, s, (f32x4*)dst, (const f32x4*)src, pitch / 4, n4, n);
+  const unsigned g1 = col_runs(n4, 256, 1), gb = W ? col_runs(len_b / 4, 256, 1) : 0;
+  launch(k_mean_rows, g1 + gb, 256, 0, s, (f32x4*)dst, (const f32x4*)src, pitch / 4, n4, n, (int)g1, (f32x4*)W,
+         pitch_b / 4, len_b / 4, nb);
 }
 
 __global__ __launch_bounds__(256) void k_rows_differ(const int4* __restrict__ W, int64_t pitch4, int64_t n4, int n,

@@ -234,6 +234,19 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
   const int nst = (R + kSC - 1) / kSC;
   const uint32_t* gt = gtab + (int64_t)g * nst * kSC;
   const uint32_t* xt = xtab + (int64_t)g * nst * kSC;
+  if (a.tail && mt == 0) {
+    // This group's cluster mean of the parameters after the first block: the
+    // workgroups of row tile 0 take one run of columns each (rows in order).
+    f32x4* T = (f32x4*)a.tail + (int64_t)g * a.SG * (a.tail_pitch / 4);
+    const int64_t p4 = a.tail_pitch / 4, n4 = a.tail_len / 4, per = (n4 + ntiles - 1) / ntiles;
+    const int64_t i1 = min(n4, (nt + 1) * per);
+    for (int64_t i = nt * per + tid; i < i1; i += NTH) {
+      f32x4 sum = T[i];
+      for (int j = 1; j < a.SG; ++j) sum += T[j * p4 + i];
+      const f32x4 mean = sum / (float)a.SG;
+      for (int j = 0; j < a.SG; ++j) T[j * p4 + i] = mean;
+    }
+  }
   // This lane's columns as byte offsets within a row.  Each row is read
   // through a buffer resource whose range ends at the row's last valid
   // column, so columns past the block read 0 (their outputs are discarded).

@@ -303,7 +303,8 @@ def test_delayed_schedule_profile(gpu_lib):
         assert stats["fwd1_block_gemm"][0] == 3 and stats["head_step"][0] == 6 and stats["head_step_end"][0] == 3
         assert not {"head_a", "head_b"} & set(stats)
         assert stats["block_update_gemm"][0] == 3 and stats["gram"][0] == 1
-        assert stats["tail_group_mean"][0] == 2 and stats["tail_global_mean"][0] == 1
+        # the means of b1, W2, b2 ride in the block update (cluster) and the W1 mean (global)
+        assert not {"tail_group_mean", "tail_global_mean"} & set(stats)
         assert stats["w1_global_mean"][0] == 1
         assert not {"fwd1_gemm", "update1_gemm", "step1_gemm", "global_mean"} & set(stats)
         h.set_params(h.params())  # equal rows: still delayed
