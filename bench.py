@@ -49,16 +49,18 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
     f = 4
     G = P // S
     pairs = K1 * (K1 - 1) // 2
+    tail = H + C * H + C  # b1, W2, b2: their cluster (global) mean rides in the block update (W1 mean)
     return {
         # forward of block 0's K1 steps from the common W1: W1 once, the
         # K1*P minibatches, the K1*P pre-activation blocks
         "fwd1_block_gemm": (f * (H * IN + K1 * P * B * IN + K1 * P * B * H), K1 * P * 2 * B * H * IN),
         # block end: the base read once, G cluster copies written, the block's
         # hidden errors and minibatch rows read
-        "block_update_gemm": (f * (H * IN + G * H * IN + K1 * P * B * (H + IN)), K1 * P * 2 * B * H * IN),
+        "block_update_gemm": (f * (H * IN + G * H * IN + K1 * P * B * (H + IN) + 2 * P * tail),
+                              K1 * P * 2 * B * H * IN),
         # Gram blocks of the round: every minibatch row read once, blocks written
         "gram": (f * (K2 * K1 * P * B * IN + K2 * P * pairs * B * B), K2 * P * pairs * 2 * B * B * IN),
-        "w1_global_mean": (f * (G + 1) * H * IN, G * H * IN),
+        "w1_global_mean": (f * ((G + 1) * H * IN + 2 * P * tail), G * H * IN + P * tail),
         "fwd1_gemm": (P * f * (H * IN + B * IN + B * H), P * 2 * B * H * IN),
         "reduce1": (P * f * (H + B * H), P * B * H),
         "fwd2_gemm": (P * f * (C * H + B * H + B * C), P * 2 * B * C * H),
