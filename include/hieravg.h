@@ -65,10 +65,12 @@ typedef struct hieravg* hieravg_t;
  *           correction -lr * sum_{k'<k} (X_k X_k'^T) G_k' and the cluster
  *           mean at the block end is one update of the copy by the summed
  *           G^T X of the cluster's learners and steps.  Needs the MLP with
- *           B <= 32, K1 <= 8, K1*S*B <= 16384, plain SGD
+ *           B <= 32, K1 <= 8, K1*S*B <= 16384, whole blocks (k_global a
+ *           multiple of K1), a dataset under 2^38 floats, plain SGD
  *           (momentum = weight_decay = 0), and a round that starts with equal
- *           W1 in every replica (true after create and after every round;
- *           after hieravg_set_params the next round runs EAGER).
+ *           W1 in every replica (true after create, after every round, and
+ *           after hieravg_set_params with equal W1 rows; otherwise that next
+ *           round runs EAGER).
  *  AUTO:    DELAYED where it applies and its extra Gram products cost at most
  *           an eighth of the step's flops ((K1 - 1) * B <= H / 2), else EAGER.
  */
