@@ -452,74 +452,103 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   const int u = tid % kHU, g = tid / kHU, h = ht * kHU + u;
   const int64_t step_floats = (int64_t)a.P * Mp * Hp;  // one step of the block's partials
 
-  // Step k's partial sums.
-  f32x4 z = zero4;
+  // Every global load that does not depend on (A) is issued here, with no
+  // wait between them: the addresses are clamped into the buffers instead of
+  // branched around per thread, and values are masked where they are used.
+  // Step k's partials, first kPv splits (the rest, if any, are added in (B)).
+  constexpr int kPv = 4;
   const int kc = k < a.K1 ? k : 0;  // earlier steps whose correction (B) applies
+  f32x4 pv[kPv];
   if (k < a.K1) {
     const float* pm = a.part + k * step_floats + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
-#pragma unroll 8
-    for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
+#pragma unroll
+    for (int ks = 0; ks < kPv; ++ks) pv[ks] = *(const f32x4*)(pm + (ks < a.KS ? ks : a.KS - 1) * a.split);
   }
   // (B)'s operands: the hidden errors of steps k2 < k-1 (16-byte piece tid of
   // each step's 32 x 32 slice; step k-1 comes from (A)) and the Gram rows
   // gram[k][k2] (piece tid of each Mp x Mp block).
   f32x4 gv[kCorrMaxK - 1], gr[kCorrMaxK];
+  if (kc > 1) {
+    const float* gb = a.gs + ((int64_t)p * Mp + (gsm < M ? gsm : M - 1)) * Hp + ht * kHU + 4 * gc4;
 #pragma unroll
-  for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2) {
-    gv[k2] = zero4;
-    if (k2 < kc - 1 && gsm < M)
-      gv[k2] = *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + gsm) * Hp + ht * kHU + 4 * gc4);
+    for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2)
+      gv[k2] = *(const f32x4*)(gb + (int64_t)(k2 < kc - 1 ? k2 : kc - 2) * a.P * Mp * Hp);
   }
-  const float* gk = a.gram + (((int64_t)p * a.K1 + k) * a.K1) * Mp * Mp;
+  if (kc > 0) {
+    const float* gk = a.gram + (((int64_t)p * a.K1 + k) * a.K1) * Mp * Mp +
+                      4 * (tid < Mp * Mp / 4 ? tid : Mp * Mp / 4 - 1);
 #pragma unroll
-  for (int k2 = 0; k2 < kCorrMaxK; ++k2) {
-    gr[k2] = zero4;
-    if (k2 < kc && tid < Mp * Mp / 4) gr[k2] = *(const f32x4*)(gk + (int64_t)k2 * Mp * Mp + 4 * tid);
+    for (int k2 = 0; k2 < kCorrMaxK; ++k2) gr[k2] = *(const f32x4*)(gk + (int64_t)(k2 < kc ? k2 : kc - 1) * Mp * Mp);
   }
-  // (A)'s operands of this slice: W2[:, h], the pre-activations of step
-  // k-1 and b1[h] (all written by this workgroup only).
-  float wc[KC], zp[kR], b1h = 0.0f;
+  // (A)'s operands of this slice: W2[:, h] and the pre-activations of step
+  // k-1 (written by this workgroup only; classes c >= C and samples past M
+  // read row 0 and are never used), b1[h], and b2, which only slice 0 uses
+  // (and alone writes).  Step 0 takes b1 and b2 from here too.
+  float wc[KC], zp[kR];
+  const float b1h = b1[h], b2v = b2[tid < C ? tid : 0];
   if (k > 0) {
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const float v = w2[(int64_t)(c < C ? c : 0) * Hp + h];
-      wc[c] = c < C ? v : 0.0f;
-    }
+    for (int c = 0; c < KC; ++c) wc[c] = w2[(int64_t)(c < C ? c : 0) * Hp + h];
 #pragma unroll
     for (int i = 0; i < kR; ++i) {
       const int mm = g + kG * i;
-      const float v = a.Z1[((int64_t)p * Mp + (mm < M ? mm : 0)) * Hp + h];
-      zp[i] = mm < M ? v : 0.0f;
+      zp[i] = a.Z1[((int64_t)p * Mp + (mm < M ? mm : 0)) * Hp + h];
     }
-    b1h = b1[h];
   }
   if (k > 0) {  // (A): the rest of step k-1
     const int kp = k - 1;
     float* g2s = region;                   // [kHM][KC + 1]
     float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
-    if (tid < kHM) ys[tid] = a.ylab[((int64_t)kp * a.P + p) * M + (tid < M ? tid : 0)];
+    const int yv = a.ylab[((int64_t)kp * a.P + p) * M + (tid < M ? tid : 0)];
     const float* plp = a.PL + (int64_t)(kp & 1) * a.pl_half;
+    constexpr int kQ = kHM * KC / 256;
+    const float* pl[kQ];
+    bool ok[kQ];
 #pragma unroll
-    for (int q = 0; q < kHM * KC / 256; ++q) {
+    for (int q = 0; q < kQ; ++q) {
       const int e = tid + 256 * q, mm = e / KC, c = e % KC;
-      const bool ok = mm < M && c < C;
-      const float* pl = plp + (((int64_t)p * Mp + (ok ? mm : 0)) * Cp + (ok ? c : 0)) * htiles;
-      float l = 0.0f;
-      if ((htiles & 3) == 0) {  // 16-byte pieces, still added in slice order
-#pragma unroll 4
-        for (int t = 0; t < htiles; t += 4) {
-          const f32x4 v = *(const f32x4*)(pl + t);
-          l += v.x;
-          l += v.y;
-          l += v.z;
-          l += v.w;
-        }
-      } else {
-#pragma unroll 8
-        for (int t = 0; t < htiles; ++t) l += pl[t];
-      }
-      g2s[mm * (KC + 1) + c] = ok ? l : 0.0f;
+      ok[q] = mm < M && c < C;
+      pl[q] = plp + (((int64_t)p * Mp + (ok[q] ? mm : 0)) * Cp + (ok[q] ? c : 0)) * htiles;
     }
+    float l[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) l[q] = 0.0f;
+    if ((htiles & 3) == 0) {
+      // 16-byte pieces, four per logit and pass, all issued before the
+      // pass's first add (pieces past htiles re-read the last one and are
+      // not added); the slices are still added in order.
+      for (int t0 = 0; t0 < htiles; t0 += 16) {
+        f32x4 v[kQ][4];
+#pragma unroll
+        for (int q = 0; q < kQ; ++q)
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            v[q][t] = *(const f32x4*)(pl[q] + (t0 + 4 * t < htiles ? t0 + 4 * t : htiles - 4));
+        __builtin_amdgcn_sched_barrier(0);  // keep the pass's loads ahead of its adds
+#pragma unroll
+        for (int q = 0; q < kQ; ++q)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const bool in = t0 + 4 * t < htiles;
+            l[q] += in ? v[q][t].x : 0.0f;
+            l[q] += in ? v[q][t].y : 0.0f;
+            l[q] += in ? v[q][t].z : 0.0f;
+            l[q] += in ? v[q][t].w : 0.0f;
+          }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+#pragma unroll 8
+        for (int t = 0; t < htiles; ++t) l[q] += pl[q][t];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const int e = tid + 256 * q;
+      g2s[(e / KC) * (KC + 1) + e % KC] = ok[q] ? l[q] : 0.0f;
+    }
+    if (tid < kHM) ys[tid] = yv;
     __syncthreads();
     {  // softmax gradient: eight threads per sample, KC/8 classes each
       const int row = tid >> 3, l8 = tid & 7;
@@ -598,25 +627,31 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
       }
     }
     if (ht == 0 && tid < KC) {
-      const float nb2 = tid < C ? b2[tid] - lr * db2 : 0.0f;
+      const float nb2 = tid < C ? b2v - lr * db2 : 0.0f;
       if (tid < C) b2[tid] = nb2;
       b2l[tid] = nb2;
     }
-  } else {
-    for (int e = tid; e < KC * kHU; e += 256) {
-      const int c = e / kHU, hh = e % kHU;
-      const float v = w2[(int64_t)(c < C ? c : 0) * Hp + ht * kHU + hh];
-      ws[c * (kHU + 1) + hh] = c < C ? v : 0.0f;
+  } else {  // step 0: (B)'s W2 slice, b1 and b2 as they are
+    float wv[KC * kHU / 256];
+#pragma unroll
+    for (int q = 0; q < KC * kHU / 256; ++q) {
+      const int c = (tid + 256 * q) / kHU;
+      wv[q] = w2[(int64_t)(c < C ? c : 0) * Hp + ht * kHU + u];
     }
-    if (tid < kHU) bs[tid] = b1[ht * kHU + tid];
-    if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2[tid] : 0.0f;
+#pragma unroll
+    for (int q = 0; q < KC * kHU / 256; ++q) {
+      const int c = (tid + 256 * q) / kHU;
+      ws[c * (kHU + 1) + u] = c < C ? wv[q] : 0.0f;
+    }
+    if (tid < kHU) bs[tid] = b1h;
+    if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2v : 0.0f;
   }
   if (k >= a.K1) return;
 
   // (B): step k's forward for this slice.
 #pragma unroll
   for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2)
-    if (k2 < kc - 1) *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gv[k2];
+    if (k2 < kc - 1) *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gsm < M ? gv[k2] : zero4;
 #pragma unroll
   for (int k2 = 0; k2 < kCorrMaxK; ++k2)
     if (k2 < kc && tid < Mp * Mp / 4) {
@@ -629,6 +664,15 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
     }
   float* zs = region;           // [kHM][kHU + 1]
   float* cbuf = region + kZs;   // [4][kHM][kHM + 1]
+  // Step k's partial sums (splits added in order), then b1.
+  f32x4 z = zero4;
+#pragma unroll
+  for (int ks = 0; ks < kPv; ++ks)
+    if (ks < a.KS) z += pv[ks];
+  for (int ks = kPv; ks < a.KS; ++ks) {
+    const float* pm = a.part + k * step_floats + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+    z += *(const f32x4*)(pm + ks * a.split);
+  }
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
   if (kc > 0) {
