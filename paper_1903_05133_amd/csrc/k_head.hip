@@ -422,10 +422,13 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 template <int KC>
 __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, int k) {
   constexpr int kG = 256 / kHU, kR = kHM / kG;
+  static_assert(KC % kG == 0, "class tiles are whole sample groups");
   constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
   constexpr int kGrlS = kHM + 1;                    // Gram row stride (conflict-free column reads)
   constexpr int kGrl = kCorrMaxK * kHM * kGrlS;      // Gram rows of step k
-  constexpr int kPhaseA = kHM * (KC + 1) + kG * (KC + 1) * kHU;
+  constexpr int kGS = KC + 4;   // G2 row stride (16-byte rows)
+  constexpr int kRed = KC + 2;  // per-group sums: dW2[c], db1, db2
+  constexpr int kPhaseA = kHM * kGS + kG * kRed * kHU;
   constexpr int kZs = kHM * (kHU + 1);
   constexpr int kCbuf = 4 * kHM * (kHM + 1);          // per-wave partial corrections
   constexpr int kRegion = kPhaseA > kZs + kCbuf ? kPhaseA : kZs + kCbuf;
@@ -485,7 +488,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   // read row 0 and are never used), b1[h], and b2, which only slice 0 uses
   // (and alone writes).  Step 0 takes b1 and b2 from here too.
   float wc[KC], zp[kR];
-  const float b1h = b1[h], b2v = b2[tid < C ? tid : 0];
+  const float b1h = b1[h], b2v = b2[u < C ? u : 0];
   if (k > 0) {
 #pragma unroll
     for (int c = 0; c < KC; ++c) wc[c] = w2[(int64_t)(c < C ? c : 0) * Hp + h];
@@ -497,8 +500,8 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   }
   if (k > 0) {  // (A): the rest of step k-1
     const int kp = k - 1;
-    float* g2s = region;                   // [kHM][KC + 1]
-    float* red = region + kHM * (KC + 1);  // [kG][KC + 1][kHU]
+    float* g2s = region;              // [kHM][kGS]
+    float* red = region + kHM * kGS;  // [kG][kRed][kHU]
     const int yv = a.ylab[((int64_t)kp * a.P + p) * M + (tid < M ? tid : 0)];
     const float* plp = a.PL + (int64_t)(kp & 1) * a.pl_half;
     constexpr int kQ = kHM * KC / 256;
@@ -546,13 +549,13 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
 #pragma unroll
     for (int q = 0; q < kQ; ++q) {
       const int e = tid + 256 * q;
-      g2s[(e / KC) * (KC + 1) + e % KC] = ok[q] ? l[q] : 0.0f;
+      g2s[(e / KC) * kGS + e % KC] = ok[q] ? l[q] : 0.0f;
     }
     if (tid < kHM) ys[tid] = yv;
     __syncthreads();
     {  // softmax gradient: eight threads per sample, KC/8 classes each
       const int row = tid >> 3, l8 = tid & 7;
-      float* rowp = g2s + row * (KC + 1);
+      float* rowp = g2s + row * kGS;
       float v[KC / 8];
       float mx = -INFINITY;
 #pragma unroll
@@ -581,6 +584,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         }
     }
     __syncthreads();
+    // Thread (u, g) takes samples g + 8i: G1 = (G2 W2)[m][h] * [Z1 > 0]
+    // and its partial sums of the steps of W2[:, h] and b1[h] (and, in
+    // slice 0, of b2[c = u]); the eight groups' partials are then added in
+    // group order, each sum by its own thread.
     float db1 = 0.0f, db2 = 0.0f;
     float dw2[KC];
 #pragma unroll
@@ -592,44 +599,57 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
       float g1 = 0.0f;
       if (mm < M) {
         const float act = fmaxf(zp[i], 0.0f);
+        const f32x4* row4 = (const f32x4*)(g2s + mm * kGS);
+        float gr2[KC];
+#pragma unroll
+        for (int c4 = 0; c4 < KC / 4; ++c4) {
+          const f32x4 v = row4[c4];
+          gr2[4 * c4] = v.x;
+          gr2[4 * c4 + 1] = v.y;
+          gr2[4 * c4 + 2] = v.z;
+          gr2[4 * c4 + 3] = v.w;
+        }
         float da = 0.0f;
 #pragma unroll
-        for (int c = 0; c < KC; ++c) da += g2s[mm * (KC + 1) + c] * wc[c];
+        for (int c = 0; c < KC; ++c) da += gr2[c] * wc[c];
         g1 = zp[i] > 0.0f ? da : 0.0f;
         g1out[(int64_t)mm * Hp] = g1;
         db1 += g1;
 #pragma unroll
-        for (int c = 0; c < KC; ++c) dw2[c] += g2s[mm * (KC + 1) + c] * act;
+        for (int c = 0; c < KC; ++c) dw2[c] += gr2[c] * act;
+        if (ht == 0 && u < KC) db2 += g2s[mm * kGS + u];
       }
       if (k < a.K1) gsl(kp, mm, u) = g1;  // for (B) (k-1 <= K1-2 < kCorrMaxK)
     }
-    if (ht == 0 && tid < C)
-      for (int mm = 0; mm < M; ++mm) db2 += g2s[mm * (KC + 1) + tid];
-    red[(g * (KC + 1) + KC) * kHU + u] = db1;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) red[(g * (KC + 1) + c) * kHU + u] = dw2[c];
+    for (int c = 0; c < KC; ++c) red[(g * kRed + c) * kHU + u] = dw2[c];
+    red[(g * kRed + KC) * kHU + u] = db1;
+    red[(g * kRed + KC + 1) * kHU + u] = db2;
     __syncthreads();
-    if (g == 0) {
-      float sb = 0.0f;
 #pragma unroll
-      for (int q = 0; q < kG; ++q) sb += red[(q * (KC + 1) + KC) * kHU + u];
-      const float nb = b1h - lr * sb;
-      b1[h] = nb;
-      bs[u] = nb;
+    for (int j = 0; j < (kRed + kG - 1) / kG; ++j) {
+      const int c = g + kG * j;  // sum c of unit u
+      if (c < kRed) {
+        float sum = 0.0f;
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        float gsum = 0.0f;
+        for (int q = 0; q < kG; ++q) sum += red[(q * kRed + c) * kHU + u];
+        if (kG * j < KC && c < KC) {  // (KC is a multiple of kG)
+          float wo = wc[kG * j < KC ? kG * j : 0];  // W2[c][h] from this thread's registers
 #pragma unroll
-        for (int q = 0; q < kG; ++q) gsum += red[(q * (KC + 1) + c) * kHU + u];
-        const float nw = wc[c] - lr * gsum;
-        if (c < C) w2[(int64_t)c * Hp + h] = nw;
-        ws[c * (kHU + 1) + u] = c < C ? nw : 0.0f;
+          for (int q = 1; q < kG; ++q) wo = g == q ? wc[kG * j < KC ? kG * j + q : 0] : wo;
+          const float nw = wo - lr * sum;
+          if (c < C) w2[(int64_t)c * Hp + h] = nw;
+          ws[c * (kHU + 1) + u] = c < C ? nw : 0.0f;
+        } else if (c == KC) {
+          const float nb = b1h - lr * sum;
+          b1[h] = nb;
+          bs[u] = nb;
+        } else if (ht == 0 && u < KC) {  // c == KC + 1: b2[u]
+          const float nb2 = u < C ? b2v - lr * sum : 0.0f;
+          if (u < C) b2[u] = nb2;
+          b2l[u] = nb2;
+        }
       }
-    }
-    if (ht == 0 && tid < KC) {
-      const float nb2 = tid < C ? b2v - lr * db2 : 0.0f;
-      if (tid < C) b2[tid] = nb2;
-      b2l[tid] = nb2;
     }
   } else {  // step 0: (B)'s W2 slice, b1 and b2 as they are
     float wv[KC * kHU / 256];
@@ -644,7 +664,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
       ws[c * (kHU + 1) + u] = c < C ? wv[q] : 0.0f;
     }
     if (tid < kHU) bs[tid] = b1h;
-    if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2v : 0.0f;
+    if (ht == 0 && tid < KC) b2l[tid] = tid < C ? b2v : 0.0f;  // tid = u here
   }
   if (k >= a.K1) return;
 
