@@ -695,28 +695,31 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   }
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   if (kc > 0) {
     // The correction sum_{k2<k} gram[k][k2] G1[k2] of this slice is a 32 x 32
-    // product with k*Mp terms: wave w takes the steps k2 = w, w + 4 as 32x32x2
-    // MFMAs (lane (l, h): Gram row l and error row l of unit l at s2 = 2j + h);
-    // the waves' partial tiles are added in wave order.  Staged errors are
-    // zero past row M, so the sum runs over the padded minibatch.
-    const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, lhi = lane >> 5;
-    if (wave < kc) {
-      f32x16 acc;
+    // product with k*Mp terms, as 32x32x2 MFMAs (lane (l, h): Gram row l and
+    // error row l of unit l at s2 = 2j + h).  Wave w takes the pairs j of
+    // its quarter of the minibatch for every k2; the four partial tiles are
+    // added in wave order.  Staged errors are zero past row M, so the sum
+    // runs over the padded minibatch (Mp = 16 or 32).
+    const int l32 = lane & 31, lhi = lane >> 5, jq = Mp / 8;
+    f32x16 acc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-      for (int k2 = wave; k2 < kc; k2 += 4)
-        for (int j = 0; j < Mp / 2; ++j)
-          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(grl[(k2 * kHM + l32) * kGrlS + 2 * j + lhi],
-                                                     gsl(k2, 2 * j + lhi, l32), acc, 0, 0, 0);
+    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+    for (int k2 = 0; k2 < kc; ++k2)
+      for (int jj = 0; jj < jq; ++jj) {
+        const int j = wave * jq + jj;
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(grl[(k2 * kHM + l32) * kGrlS + 2 * j + lhi],
+                                                   gsl(k2, 2 * j + lhi, l32), acc, 0, 0, 0);
+      }
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        cbuf[(wave * kHM + 8 * (r >> 2) + 4 * lhi + (r & 3)) * (kHM + 1) + l32] = acc[r];
-    }
+    for (int r = 0; r < 16; ++r)
+      cbuf[(wave * kHM + 8 * (r >> 2) + 4 * lhi + (r & 3)) * (kHM + 1) + l32] = acc[r];
     __syncthreads();
     f32x4 c = zero4;
-    for (int w = 0; w < (kc < 4 ? kc : 4); ++w) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
       const float* cr = cbuf + (w * kHM + rr) * (kHM + 1) + 4 * u4;
       c += f32x4{cr[0], cr[1], cr[2], cr[3]};
     }
@@ -729,14 +732,26 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   zs[rr * (kHU + 1) + 4 * u4 + 2] = mok ? fmaxf(z.z, 0.0f) : 0.0f;
   zs[rr * (kHU + 1) + 4 * u4 + 3] = mok ? fmaxf(z.w, 0.0f) : 0.0f;
   __syncthreads();
-  float* plo = a.PL + (int64_t)(k & 1) * a.pl_half;
+  // Partial logits of this slice, relu(Z1) (32 x 32) times the W2 slice
+  // transposed, as 16x16x4 MFMAs: wave w takes samples 16 (w & 1) .. +15
+  // and classes 16 (w >> 1) .. +15 (lane (i, q): sample row i and class
+  // row i at unit 4s + q; result rows 4q .. 4q+3 of class column i).
+  if (wave < 2 * (KC / 16)) {
+    const int l16 = lane & 15, lq = lane >> 4, m0 = 16 * (wave & 1), c0 = 16 * (wave >> 1);
+    f32x4 acc = zero4;
 #pragma unroll
-  for (int q = 0; q < kHM * KC / 256; ++q) {
-    const int e = tid + 256 * q, mm = e / KC, c = e % KC;
-    float acc = ht == 0 ? b2l[c] : 0.0f;
+    for (int s4 = 0; s4 < kHU / 4; ++s4)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(zs[(m0 + l16) * (kHU + 1) + 4 * s4 + lq],
+                                                 ws[(c0 + l16) * (kHU + 1) + 4 * s4 + lq], acc, 0, 0, 0);
+    float* plo = a.PL + (int64_t)(k & 1) * a.pl_half;
+    const int c = c0 + l16;
+    const float bb = ht == 0 ? b2l[c] : 0.0f;  // slice 0 adds b2
+    const float accs[4] = {acc.x, acc.y, acc.z, acc.w};
 #pragma unroll
-    for (int hh = 0; hh < kHU; ++hh) acc += zs[mm * (kHU + 1) + hh] * ws[c * (kHU + 1) + hh];
-    if (mm < M && c < C) plo[(((int64_t)p * Mp + mm) * Cp + c) * htiles + ht] = acc;
+    for (int r = 0; r < 4; ++r) {
+      const int mm = m0 + 4 * lq + r;
+      if (mm < M && c < C) plo[(((int64_t)p * Mp + mm) * Cp + c) * htiles + ht] = accs[r] + bb;
+    }
   }
 }
 

@@ -65,6 +65,10 @@ SMALL = {
     # B = 32: the block update's stages are whole (step, learner) runs of
     # samples; ragged hidden and input widths, two learners per cluster
     "mlp_batch_32_ragged": cases.case("mlp", 6, 2, 3, 2, B=32, IN=200, H=70, C=5, N=300, lr=0.05, seed=15),
+    # 17..32 classes (the delayed head's 32-class tiles) with 32- and 16-row
+    # padded minibatches, both ragged
+    "mlp_c24_batch_24": cases.case("mlp", 4, 2, 3, 2, B=24, IN=150, H=70, C=24, N=300, lr=0.05, seed=17),
+    "mlp_c20_batch_10": cases.case("mlp", 4, 4, 4, 1, B=10, IN=90, H=100, C=20, N=200, lr=0.1, seed=18),
     "mlp_one_learner": cases.case("mlp", 1, 1, 3, 2, B=8, IN=96, H=33, C=5, N=64, lr=0.1, seed=7),
     "mlp_one_sample_dataset": cases.case("mlp", 4, 4, 2, 1, B=3, IN=50, H=20, C=2, N=1, lr=0.1, seed=8),
     "softmax_ragged": cases.case("softmax", 3, 3, 3, 1, B=17, IN=33, C=17, N=50, lr=0.2, seed=3),
