@@ -426,9 +426,8 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
   constexpr int kGrlS = kHM + 1;                    // Gram row stride (conflict-free column reads)
   constexpr int kGrl = kCorrMaxK * kHM * kGrlS;      // Gram rows of step k
-  constexpr int kGS = KC + 4;   // G2 row stride (16-byte rows)
-  constexpr int kRed = KC + 2;  // per-group sums: dW2[c], db1, db2
-  constexpr int kPhaseA = kHM * kGS + kG * kRed * kHU;
+  constexpr int kGS = KC + 4;  // G2 row stride (16-byte rows)
+  constexpr int kPhaseA = kHM * kGS + (KC + kHM) * (kHU + 1);
   constexpr int kZs = kHM * (kHU + 1);
   constexpr int kCbuf = 4 * kHM * (kHM + 1);          // per-wave partial corrections
   constexpr int kRegion = kPhaseA > kZs + kCbuf ? kPhaseA : kZs + kCbuf;
@@ -483,25 +482,32 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
 #pragma unroll
     for (int k2 = 0; k2 < kCorrMaxK; ++k2) gr[k2] = *(const f32x4*)(gk + (int64_t)(k2 < kc ? k2 : kc - 1) * Mp * Mp);
   }
-  // (A)'s operands of this slice: W2[:, h] and the pre-activations of step
-  // k-1 (written by this workgroup only; classes c >= C and samples past M
-  // read row 0 and are never used), b1[h], and b2, which only slice 0 uses
-  // (and alone writes).  Step 0 takes b1 and b2 from here too.
-  float wc[KC], zp[kR];
+  // (A)'s operands of this slice: W2[c][h] for c = g + 8q (classes past C
+  // read row 0) and the pre-activations of step k-1
+  // at samples g + 8i (past M: row 0, never used), all written by this
+  // workgroup only; b1[h], and b2, which only slice 0 uses (and alone
+  // writes).  Step 0 stages the same W2 values for (B).
+  constexpr int kWq = KC * kHU / 256;
+  float wv[kWq], zp[kR];
   const float b1h = b1[h], b2v = b2[u < C ? u : 0];
-  if (k > 0) {
 #pragma unroll
-    for (int c = 0; c < KC; ++c) wc[c] = w2[(int64_t)(c < C ? c : 0) * Hp + h];
+  for (int q = 0; q < kWq; ++q) {
+    const int c = g + kG * q;
+    wv[q] = w2[(int64_t)(c < C ? c : 0) * Hp + h];
+  }
+  if (k > 0) {
 #pragma unroll
     for (int i = 0; i < kR; ++i) {
       const int mm = g + kG * i;
       zp[i] = a.Z1[((int64_t)p * Mp + (mm < M ? mm : 0)) * Hp + h];
     }
   }
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   if (k > 0) {  // (A): the rest of step k-1
     const int kp = k - 1;
-    float* g2s = region;              // [kHM][kGS]
-    float* red = region + kHM * kGS;  // [kG][kRed][kHU]
+    float* g2s = region;                 // [kHM][kGS] G2
+    float* wold = g2s + kHM * kGS;       // [KC][kHU + 1] the W2 slice before the step
+    float* z1p = wold + KC * (kHU + 1);  // [kHM][kHU + 1] Z1 of step k-1
     const int yv = a.ylab[((int64_t)kp * a.P + p) * M + (tid < M ? tid : 0)];
     const float* plp = a.PL + (int64_t)(kp & 1) * a.pl_half;
     constexpr int kQ = kHM * KC / 256;
@@ -553,6 +559,12 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
     }
     if (tid < kHM) ys[tid] = yv;
     __syncthreads();
+    // Staged here, not before the barrier above, so that these loads may
+    // still be in flight while the logits are summed.
+#pragma unroll
+    for (int q = 0; q < kWq; ++q) wold[(g + kG * q) * (kHU + 1) + u] = wv[q];  // rows c >= C: row 0, met by zero G2
+#pragma unroll
+    for (int i = 0; i < kR; ++i) z1p[(g + kG * i) * (kHU + 1) + u] = zp[i];
     {  // softmax gradient: eight threads per sample, KC/8 classes each
       const int row = tid >> 3, l8 = tid & 7;
       float* rowp = g2s + row * kGS;
@@ -584,83 +596,82 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         }
     }
     __syncthreads();
-    // Thread (u, g) takes samples g + 8i: G1 = (G2 W2)[m][h] * [Z1 > 0]
-    // and its partial sums of the steps of W2[:, h] and b1[h] (and, in
-    // slice 0, of b2[c = u]); the eight groups' partials are then added in
-    // group order, each sum by its own thread.
-    float db1 = 0.0f, db2 = 0.0f;
-    float dw2[KC];
+    if (wave == 0) {
+      // G1 = (G2 W2)[m][h] * [Z1 > 0] as 32x32x2 MFMAs over the classes
+      // (lane (l, hi): G2 row l and W2 row 2j + hi of unit l; acc[r] is row
+      // 8(r/4) + 4hi + r%4 of unit l); its column sums step b1.  Rows past M
+      // are zero (their G2 rows are).
+      const int l32 = lane & 31, lhi = lane >> 5;
+      f32x16 acc;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) dw2[c] = 0.0f;
-    float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + h;
+      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kR; ++i) {
-      const int mm = g + kG * i;
-      float g1 = 0.0f;
-      if (mm < M) {
-        const float act = fmaxf(zp[i], 0.0f);
-        const f32x4* row4 = (const f32x4*)(g2s + mm * kGS);
-        float gr2[KC];
+      for (int j = 0; j < KC / 2; ++j)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(g2s[l32 * kGS + 2 * j + lhi], wold[(2 * j + lhi) * (kHU + 1) + l32],
+                                                   acc, 0, 0, 0);
+      // The 16 Z1 values are read before any is used, and the stores sit
+      // after all of them, so no wait separates the rows.
+      float g1[16];
 #pragma unroll
-        for (int c4 = 0; c4 < KC / 4; ++c4) {
-          const f32x4 v = row4[c4];
-          gr2[4 * c4] = v.x;
-          gr2[4 * c4 + 1] = v.y;
-          gr2[4 * c4 + 2] = v.z;
-          gr2[4 * c4 + 3] = v.w;
-        }
-        float da = 0.0f;
+      for (int r = 0; r < 16; ++r) g1[r] = z1p[(8 * (r >> 2) + 4 * lhi + (r & 3)) * (kHU + 1) + l32];
+      __builtin_amdgcn_sched_barrier(0);
+      float db1 = 0.0f;
 #pragma unroll
-        for (int c = 0; c < KC; ++c) da += gr2[c] * wc[c];
-        g1 = zp[i] > 0.0f ? da : 0.0f;
-        g1out[(int64_t)mm * Hp] = g1;
-        db1 += g1;
-#pragma unroll
-        for (int c = 0; c < KC; ++c) dw2[c] += gr2[c] * act;
-        if (ht == 0 && u < KC) db2 += g2s[mm * kGS + u];
+      for (int r = 0; r < 16; ++r) {
+        g1[r] = g1[r] > 0.0f ? acc[r] : 0.0f;
+        db1 += g1[r];
       }
-      if (k < a.K1) gsl(kp, mm, u) = g1;  // for (B) (k-1 <= K1-2 < kCorrMaxK)
-    }
+      if (k < a.K1)  // for (B) (k-1 <= K1-2 < kCorrMaxK)
 #pragma unroll
-    for (int c = 0; c < KC; ++c) red[(g * kRed + c) * kHU + u] = dw2[c];
-    red[(g * kRed + KC) * kHU + u] = db1;
-    red[(g * kRed + KC + 1) * kHU + u] = db2;
-    __syncthreads();
+        for (int r = 0; r < 16; ++r) gsl(kp, 8 * (r >> 2) + 4 * lhi + (r & 3), l32) = g1[r];
+      float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + ht * kHU + l32;
 #pragma unroll
-    for (int j = 0; j < (kRed + kG - 1) / kG; ++j) {
-      const int c = g + kG * j;  // sum c of unit u
-      if (c < kRed) {
-        float sum = 0.0f;
+      for (int r = 0; r < 16; ++r) {
+        const int mm = 8 * (r >> 2) + 4 * lhi + (r & 3);
+        if (mm < M) g1out[(int64_t)mm * Hp] = g1[r];
+      }
+      db1 += __shfl_xor(db1, 32);
+      if (lhi == 0) {  // lane l32 = u: h of this thread
+        const float nb = b1h - lr * db1;
+        b1[h] = nb;
+        bs[u] = nb;
+      }
+    } else if (wave < 3) {
+      // dW2[c][h] = sum_m G2[m][c] relu(Z1)[m][h] as 16x16x4 MFMAs over the
+      // samples, 16 x 16 tiles (c0, u0) split over waves 1 and 2 (lane
+      // (i, q): class c0 + i and unit u0 + i at sample 4s + q; acc[r] is
+      // class c0 + 4q + r of unit u0 + i); W2 takes its step.
+      const int l16 = lane & 15, lq = lane >> 4;
+      for (int t = wave - 1; t < 2 * (KC / 16); t += 2) {
+        const int c0 = 16 * (t >> 1), u0 = 16 * (t & 1);
+        f32x4 acc = zero4;
 #pragma unroll
-        for (int q = 0; q < kG; ++q) sum += red[(q * kRed + c) * kHU + u];
-        if (kG * j < KC && c < KC) {  // (KC is a multiple of kG)
-          float wo = wc[kG * j < KC ? kG * j : 0];  // W2[c][h] from this thread's registers
+        for (int s4 = 0; s4 < kHM / 4; ++s4) {
+          const int mm = 4 * s4 + lq;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(g2s[mm * kGS + c0 + l16],
+                                                     fmaxf(z1p[mm * (kHU + 1) + u0 + l16], 0.0f), acc, 0, 0, 0);
+        }
+        const float accs[4] = {acc.x, acc.y, acc.z, acc.w};
+        const int uu = u0 + l16;
 #pragma unroll
-          for (int q = 1; q < kG; ++q) wo = g == q ? wc[kG * j < KC ? kG * j + q : 0] : wo;
-          const float nw = wo - lr * sum;
-          if (c < C) w2[(int64_t)c * Hp + h] = nw;
-          ws[c * (kHU + 1) + u] = c < C ? nw : 0.0f;
-        } else if (c == KC) {
-          const float nb = b1h - lr * sum;
-          b1[h] = nb;
-          bs[u] = nb;
-        } else if (ht == 0 && u < KC) {  // c == KC + 1: b2[u]
-          const float nb2 = u < C ? b2v - lr * sum : 0.0f;
-          if (u < C) b2[u] = nb2;
-          b2l[u] = nb2;
+        for (int r = 0; r < 4; ++r) {
+          const int c = c0 + 4 * lq + r;
+          const float nw = wold[c * (kHU + 1) + uu] - lr * accs[r];
+          if (c < C) w2[(int64_t)c * Hp + ht * kHU + uu] = nw;
+          ws[c * (kHU + 1) + uu] = c < C ? nw : 0.0f;
         }
       }
+    } else if (ht == 0 && lane < KC) {  // wave 3 of slice 0: b2[c = lane] (= u)
+      float sb = 0.0f;
+      for (int mm = 0; mm < M; ++mm) sb += g2s[mm * kGS + lane];
+      const float nb2 = lane < C ? b2v - lr * sb : 0.0f;
+      if (lane < C) b2[lane] = nb2;
+      b2l[lane] = nb2;
     }
   } else {  // step 0: (B)'s W2 slice, b1 and b2 as they are
-    float wv[KC * kHU / 256];
 #pragma unroll
-    for (int q = 0; q < KC * kHU / 256; ++q) {
-      const int c = (tid + 256 * q) / kHU;
-      wv[q] = w2[(int64_t)(c < C ? c : 0) * Hp + ht * kHU + u];
-    }
-#pragma unroll
-    for (int q = 0; q < KC * kHU / 256; ++q) {
-      const int c = (tid + 256 * q) / kHU;
+    for (int q = 0; q < kWq; ++q) {
+      const int c = g + kG * q;
       ws[c * (kHU + 1) + u] = c < C ? wv[q] : 0.0f;
     }
     if (tid < kHU) bs[tid] = b1h;
@@ -695,7 +706,6 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   }
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   if (kc > 0) {
     // The correction sum_{k2<k} gram[k][k2] G1[k2] of this slice is a 32 x 32
     // product with k*Mp terms, as 32x32x2 MFMAs (lane (l, h): Gram row l and
