@@ -181,19 +181,29 @@ void launch_group_mean(hipStream_t s, float* W, int64_t pitch, int64_t len, int 
 __global__ __launch_bounds__(256) void k_mean_rows(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
                                                    int64_t pitch4, int64_t n4, int n, int g1, f32x4* __restrict__ W,
                                                    int64_t pitchb4, int64_t n4b, int nb) {
-  if ((int)blockIdx.x < g1) {
-    for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)g1 * 256) {
-      f32x4 sum = src[i];
-      for (int r = 1; r < n; ++r) sum += src[r * pitch4 + i];
-      dst[i] = sum / (float)n;
+  // Rows are read eight at a time, all loads of a group issued before its
+  // adds (a row past the last re-reads the last one and is not added), and
+  // added in row order.
+  auto row_sum = [](const f32x4* __restrict__ base, int64_t pitch, int rows) {
+    f32x4 sum = base[0];
+    for (int r0 = 1; r0 < rows; r0 += 8) {
+      f32x4 v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = base[(int64_t)(r0 + j < rows ? r0 + j : rows - 1) * pitch];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (r0 + j < rows) sum += v[j];
     }
+    return sum;
+  };
+  if ((int)blockIdx.x < g1) {
+    for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)g1 * 256)
+      dst[i] = row_sum(src + i, pitch4, n) / (float)n;
     return;
   }
   const int gb = gridDim.x - g1;
   for (int64_t i = (blockIdx.x - g1) * 256ll + threadIdx.x; i < n4b; i += (int64_t)gb * 256) {
-    f32x4 sum = W[i];
-    for (int r = 1; r < nb; ++r) sum += W[r * pitchb4 + i];
-    const f32x4 mean = sum / (float)nb;
+    const f32x4 mean = row_sum(W + i, pitchb4, nb) / (float)nb;
     for (int r = 0; r < nb; ++r) W[r * pitchb4 + i] = mean;
   }
 }
