@@ -596,53 +596,58 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         }
     }
     __syncthreads();
-    if (wave == 0) {
-      // G1 = (G2 W2)[m][h] * [Z1 > 0] as 32x32x2 MFMAs over the classes
-      // (lane (l, hi): G2 row l and W2 row 2j + hi of unit l; acc[r] is row
-      // 8(r/4) + 4hi + r%4 of unit l); its column sums step b1.  Rows past M
+    const int l16 = lane & 15, lq = lane >> 4;
+    if (wave < 2) {
+      // G1 = (G2 W2)[m][h] * [Z1 > 0] for units u0 = 16 w .. +15 as 16x16x4
+      // MFMAs over the classes, two 16-sample tiles (lane (i, q): G2 row
+      // m0 + i and W2 row 4s + q of unit u0 + i; acc[t][r] is sample
+      // m0 + 4q + r of unit u0 + i); its column sums step b1.  Rows past M
       // are zero (their G2 rows are).
-      const int l32 = lane & 31, lhi = lane >> 5;
-      f32x16 acc;
+      const int u0 = 16 * wave, uu = u0 + l16;
+      f32x4 acc[2] = {zero4, zero4};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+      for (int s4 = 0; s4 < KC / 4; ++s4) {
+        const float b = wold[(4 * s4 + lq) * (kHU + 1) + uu];
 #pragma unroll
-      for (int j = 0; j < KC / 2; ++j)
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(g2s[l32 * kGS + 2 * j + lhi], wold[(2 * j + lhi) * (kHU + 1) + l32],
-                                                   acc, 0, 0, 0);
-      // The 16 Z1 values are read before any is used, and the stores sit
+        for (int t = 0; t < 2; ++t)
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(g2s[(16 * t + l16) * kGS + 4 * s4 + lq], b, acc[t], 0, 0, 0);
+      }
+      // The eight Z1 values are read before any is used, and the stores sit
       // after all of them, so no wait separates the rows.
-      float g1[16];
+      float g1[8];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) g1[r] = z1p[(8 * (r >> 2) + 4 * lhi + (r & 3)) * (kHU + 1) + l32];
+      for (int e = 0; e < 8; ++e) g1[e] = z1p[(16 * (e >> 2) + 4 * lq + (e & 3)) * (kHU + 1) + uu];
       __builtin_amdgcn_sched_barrier(0);
       float db1 = 0.0f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        g1[r] = g1[r] > 0.0f ? acc[r] : 0.0f;
-        db1 += g1[r];
+      for (int e = 0; e < 8; ++e) {
+        const f32x4 av = acc[e >> 2];
+        const float v = (e & 3) == 0 ? av.x : (e & 3) == 1 ? av.y : (e & 3) == 2 ? av.z : av.w;
+        g1[e] = g1[e] > 0.0f ? v : 0.0f;
+        db1 += g1[e];
       }
       if (k < a.K1)  // for (B) (k-1 <= K1-2 < kCorrMaxK)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) gsl(kp, 8 * (r >> 2) + 4 * lhi + (r & 3), l32) = g1[r];
-      float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + ht * kHU + l32;
+        for (int e = 0; e < 8; ++e) gsl(kp, 16 * (e >> 2) + 4 * lq + (e & 3), uu) = g1[e];
+      float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + ht * kHU + uu;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int mm = 8 * (r >> 2) + 4 * lhi + (r & 3);
-        if (mm < M) g1out[(int64_t)mm * Hp] = g1[r];
+      for (int e = 0; e < 8; ++e) {
+        const int mm = 16 * (e >> 2) + 4 * lq + (e & 3);
+        if (mm < M) g1out[(int64_t)mm * Hp] = g1[e];
       }
+      db1 += __shfl_xor(db1, 16);
       db1 += __shfl_xor(db1, 32);
-      if (lhi == 0) {  // lane l32 = u: h of this thread
+      if (lq == wave) {  // this thread's unit u is uu (tid % 32 = 16 w + i)
         const float nb = b1h - lr * db1;
         b1[h] = nb;
         bs[u] = nb;
       }
-    } else if (wave < 3) {
+    } else {
       // dW2[c][h] = sum_m G2[m][c] relu(Z1)[m][h] as 16x16x4 MFMAs over the
-      // samples, 16 x 16 tiles (c0, u0) split over waves 1 and 2 (lane
+      // samples, 16 x 16 tiles (c0, u0) split over waves 2 and 3 (lane
       // (i, q): class c0 + i and unit u0 + i at sample 4s + q; acc[r] is
       // class c0 + 4q + r of unit u0 + i); W2 takes its step.
-      const int l16 = lane & 15, lq = lane >> 4;
-      for (int t = wave - 1; t < 2 * (KC / 16); t += 2) {
+      for (int t = wave - 2; t < 2 * (KC / 16); t += 2) {
         const int c0 = 16 * (t >> 1), u0 = 16 * (t & 1);
         f32x4 acc = zero4;
 #pragma unroll
@@ -661,7 +666,8 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
           ws[c * (kHU + 1) + uu] = c < C ? nw : 0.0f;
         }
       }
-    } else if (ht == 0 && lane < KC) {  // wave 3 of slice 0: b2[c = lane] (= u)
+    }
+    if (ht == 0 && wave == 3 && lane < KC) {  // slice 0: b2[c = lane] (= u)
       float sb = 0.0f;
       for (int mm = 0; mm < M; ++mm) sb += g2s[mm * kGS + lane];
       const float nb2 = lane < C ? b2v - lr * sb : 0.0f;
