@@ -419,13 +419,14 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 // on (A) is issued before (A) starts: step k's partials, the Gram rows and
 // the earlier steps' hidden errors of (B), and this slice's W2, Z1 and b1
 // for (A).
-template <int KC>
+// NK: slots for the earlier steps of a block (K1 - 1 <= NK).
+template <int KC, int NK>
 __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, int k) {
   constexpr int kG = 256 / kHU, kR = kHM / kG;
   static_assert(KC % kG == 0, "class tiles are whole sample groups");
-  constexpr int kGsl = kCorrMaxK * kHM * kHU;        // G1 slices of the block's steps
+  constexpr int kGsl = NK * kHM * kHU;     // G1 slices of the block's steps
   constexpr int kGrlS = kHM + 1;                    // Gram row stride (conflict-free column reads)
-  constexpr int kGrl = kCorrMaxK * kHM * kGrlS;      // Gram rows of step k
+  constexpr int kGrl = NK * kHM * kGrlS;   // Gram rows of step k
   constexpr int kGS = KC + 4;  // G2 row stride (16-byte rows)
   constexpr int kPhaseA = kHM * kGS + (KC + kHM) * (kHU + 1);
   constexpr int kZs = kHM * (kHU + 1);
@@ -434,7 +435,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   __shared__ __attribute__((aligned(16))) float lds[kGsl + kGrl + kRegion + KC * (kHU + 1) + kHU + KC];
   __shared__ int ys[kHM];
   auto gsl = [&](int k2, int s, int u) -> float& { return lds[(k2 * kHM + s) * kHU + u]; };
-  float* grl = lds + kGsl;          // [kCorrMaxK][kHM][kGrlS]
+  float* grl = lds + kGsl;          // [NK][kHM][kGrlS]
   float* region = grl + kGrl;
   float* ws = region + kRegion;     // [KC][kHU + 1] W2 slice (after (A))
   float* bs = ws + KC * (kHU + 1);  // [kHU] b1 slice (after (A))
@@ -469,18 +470,18 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   // (B)'s operands: the hidden errors of steps k2 < k-1 (16-byte piece tid of
   // each step's 32 x 32 slice; step k-1 comes from (A)) and the Gram rows
   // gram[k][k2] (piece tid of each Mp x Mp block).
-  f32x4 gv[kCorrMaxK - 1], gr[kCorrMaxK];
+  f32x4 gv[NK - 1], gr[NK];
   if (kc > 1) {
     const float* gb = a.gs + ((int64_t)p * Mp + (gsm < M ? gsm : M - 1)) * Hp + ht * kHU + 4 * gc4;
 #pragma unroll
-    for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2)
+    for (int k2 = 0; k2 < NK - 1; ++k2)
       gv[k2] = *(const f32x4*)(gb + (int64_t)(k2 < kc - 1 ? k2 : kc - 2) * a.P * Mp * Hp);
   }
   if (kc > 0) {
     const float* gk = a.gram + (((int64_t)p * a.K1 + k) * a.K1) * Mp * Mp +
                       4 * (tid < Mp * Mp / 4 ? tid : Mp * Mp / 4 - 1);
 #pragma unroll
-    for (int k2 = 0; k2 < kCorrMaxK; ++k2) gr[k2] = *(const f32x4*)(gk + (int64_t)(k2 < kc ? k2 : kc - 1) * Mp * Mp);
+    for (int k2 = 0; k2 < NK; ++k2) gr[k2] = *(const f32x4*)(gk + (int64_t)(k2 < kc ? k2 : kc - 1) * Mp * Mp);
   }
   // (A)'s operands of this slice: W2[c][h] for c = g + 8q (classes past C
   // read row 0) and the pre-activations of step k-1
@@ -626,7 +627,7 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         g1[e] = g1[e] > 0.0f ? v : 0.0f;
         db1 += g1[e];
       }
-      if (k < a.K1)  // for (B) (k-1 <= K1-2 < kCorrMaxK)
+      if (k < a.K1)  // for (B) (k-1 <= K1-2 < NK)
 #pragma unroll
         for (int e = 0; e < 8; ++e) gsl(kp, 16 * (e >> 2) + 4 * lq + (e & 3), uu) = g1[e];
       float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + ht * kHU + uu;
@@ -687,10 +688,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
 
   // (B): step k's forward for this slice.
 #pragma unroll
-  for (int k2 = 0; k2 < kCorrMaxK - 1; ++k2)
+  for (int k2 = 0; k2 < NK - 1; ++k2)
     if (k2 < kc - 1) *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gsm < M ? gv[k2] : zero4;
 #pragma unroll
-  for (int k2 = 0; k2 < kCorrMaxK; ++k2)
+  for (int k2 = 0; k2 < NK; ++k2)
     if (k2 < kc && tid < Mp * Mp / 4) {
       const int rem = 4 * tid;
       float* gp = &grl[(k2 * kHM + rem / Mp) * kGrlS + rem % Mp];
@@ -773,10 +774,18 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
 
 void launch_head_step(hipStream_t s, const HeadStepArgs& a, int k) {
   const int htiles = a.Hp / kHU;
-  if (a.C <= 16)
-    launch(k_head_step<16>, a.P * htiles, 256, 0, s, a, htiles, k);
-  else
-    launch(k_head_step<32>, a.P * htiles, 256, 0, s, a, htiles, k);
+  // Blocks of up to 4 steps take the 3-slot variant (fewer idle prefetches).
+  if (a.C <= 16) {
+    if (a.K1 <= 4)
+      launch(k_head_step<16, 3>, a.P * htiles, 256, 0, s, a, htiles, k);
+    else
+      launch(k_head_step<16, kCorrMaxK>, a.P * htiles, 256, 0, s, a, htiles, k);
+  } else {
+    if (a.K1 <= 4)
+      launch(k_head_step<32, 3>, a.P * htiles, 256, 0, s, a, htiles, k);
+    else
+      launch(k_head_step<32, kCorrMaxK>, a.P * htiles, 256, 0, s, a, htiles, k);
+  }
 }
 
 // Evaluation: one wave per row m < M of a chunk.  Logits l_c = b_c + sum_ks

@@ -125,10 +125,11 @@ def test_large_class_delayed_updates_match_oracle(name, gpu_lib):
     _check(c, got, idx, *_oracle(c, 2))
 
 
-def test_delayed_updates_long_block(gpu_lib):
-    """K1 = 8 earlier-step corrections (the largest block the delayed path
-    takes), B = 32, S = 2, three blocks."""
-    c = cases.case("mlp", 4, 2, 8, 3, B=32, IN=130, H=96, C=7, N=400, sigma=0.5, lr=0.05, seed=15)
+@pytest.mark.parametrize("K1,C", [(8, 7), (6, 20)])
+def test_delayed_updates_long_block(K1, C, gpu_lib):
+    """Blocks of more than four steps (K1 = 8 is the largest the delayed path
+    takes), with 16- and 32-class head tiles; B = 32, S = 2, three blocks."""
+    c = cases.case("mlp", 4, 2, K1, 3, B=32, IN=130, H=96, C=C, N=400, sigma=0.5, lr=0.05, seed=15)
     got, idx, _ = _run_gpu(c, rounds=1, mode="delayed")
     _check(c, got, idx, *_oracle(c, 1))
 
