@@ -406,19 +406,20 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
 //  (A) k > 0, the rest of step k-1: logits of every sample from the partial
 //      logits of all slices (b2 is folded into slice 0's), its softmax
 //      cross-entropy gradient G2 (mean over the minibatch; eight threads per
-//      sample), then for this slice, with thread (u = t%32, g = t/32) taking
-//      samples g + 8i: G1 = (G2 W2)[m][h] * [Z1 > 0] into gs[k-1] and into LDS
-//      for (B); the eight sample groups' sums give the steps of b1[h] and
-//      W2[:, h] (the new values stay in LDS for (B)); slice 0 steps b2.
+//      sample), then for this slice, on the matrix cores: G1 = (G2 W2)[m][h]
+//      * [Z1 > 0] into gs[k-1] and into LDS for (B), with its column sums
+//      stepping b1[h] (waves 0 and 1, 16 units each), and the step of
+//      W2[:, h] from G2^T relu(Z1) (waves 2 and 3); the new values stay in
+//      LDS for (B); slice 0 steps b2.
 //  (B) k < K1, step k: Z1 = b1 + sum of the split-K partials
 //      - lr * sum_{k2<k} gram[k][k2] G1[k2] for this slice, its ReLU, and the
 //      slice's partial logits into PL[k&1] (slice 0 adds b2).
 // (A) reads PL[(k-1)&1] of every slice while (B) writes PL[k&1], and b2 is
 // read and written by slice 0 only, so no workgroup depends on another
-// within a launch.  Every global load the launch needs that does not depend
-// on (A) is issued before (A) starts: step k's partials, the Gram rows and
-// the earlier steps' hidden errors of (B), and this slice's W2, Z1 and b1
-// for (A).
+// within a launch.  Every global load the launch needs is issued before the
+// first wait: step k's partials, the Gram rows and the earlier steps' hidden
+// errors of (B), this slice's W2, Z1, b1 (and b2) and the partial logits
+// and labels of (A).
 // NK: slots for the earlier steps of a block (K1 - 1 <= NK).
 template <int KC, int NK>
 __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, int k) {
