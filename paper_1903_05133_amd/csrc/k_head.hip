@@ -400,6 +400,14 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
     step(b2 + po + tid, mom.vb2 ? mom.vb2 + po + tid : nullptr, b2[po + tid], db2);
 }
 
+// Value of another lane in the same group of eight by a DPP move: control
+// 0xB1 (quad_perm 1,0,3,2) takes lane i^1, 0x4E (quad_perm 2,3,0,1) lane
+// i^2, 0x141 (row_half_mirror) lane 7-i of the eight.
+template <int kCtrl>
+__device__ inline float dpp8(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), kCtrl, 0xF, 0xF, false));
+}
+
 // Fused head of the delayed schedule (HeadStepArgs).  Workgroup (p, ht) owns
 // hidden units h = 32*ht + u of learner p; M <= 32 samples, one chunk.  Step k
 // of a block:
@@ -578,16 +586,18 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         v[j] = rowp[c];
         if (c < C) mx = fmaxf(mx, v[j]);
       }
-#pragma unroll
-      for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 8));
+      mx = fmaxf(mx, dpp8<0xB1>(mx));  // the eight lanes of a sample by DPP moves:
+      mx = fmaxf(mx, dpp8<0x4E>(mx));  // partner lane i^1, then i^2, then the
+      mx = fmaxf(mx, dpp8<0x141>(mx)); // mirror 7-i (a lane of the other quad)
       float sum = 0.0f;
 #pragma unroll
       for (int j = 0; j < KC / 8; ++j) {
         v[j] = l8 + 8 * j < C ? expf(v[j] - mx) : 0.0f;
         sum += v[j];
       }
-#pragma unroll
-      for (int o = 1; o < 8; o <<= 1) sum += __shfl_xor(sum, o, 8);
+      sum += dpp8<0xB1>(sum);
+      sum += dpp8<0x4E>(sum);
+      sum += dpp8<0x141>(sum);
       const int y = ys[row];
       const float invB = 1.0f / (float)M;
       if (row < M)
