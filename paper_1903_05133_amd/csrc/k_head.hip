@@ -450,7 +450,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   float* bs = ws + KC * (kHU + 1);  // [kHU] b1 slice (after (A))
   float* b2l = bs + kHU;            // [KC] b2 (slice 0, after (A))
 
-  const int p = blockIdx.x / htiles, ht = blockIdx.x % htiles;
+  // The slices of a learner run on one XCD (consecutive ids after the
+  // remap), so the partial logits they exchange stay within one L2.
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int p = bid / htiles, ht = bid % htiles;
   const int tid = threadIdx.x;
   const int M = a.M, C = a.C, Cp = a.Cp, Hp = a.Hp, Mp = a.Mp;
   const float lr = *a.lr;
