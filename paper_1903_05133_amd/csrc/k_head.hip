@@ -496,10 +496,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
     for (int k2 = 0; k2 < NK; ++k2) gr[k2] = *(const f32x4*)(gk + (int64_t)(k2 < kc ? k2 : kc - 1) * Mp * Mp);
   }
   // (A)'s operands of this slice: W2[c][h] for c = g + 8q (classes past C
-  // read row 0) and the pre-activations of step k-1
-  // at samples g + 8i (past M: row 0, never used), all written by this
-  // workgroup only; b1[h], and b2, which only slice 0 uses (and alone
-  // writes).  Step 0 stages the same W2 values for (B).
+  // read row 0) and the pre-activations of step k-1 at samples g + 8i (past
+  // M: row 0, never used), all written by this workgroup only; b1[h], and
+  // b2, which only slice 0 uses (and alone writes).  Step 0 stages the same
+  // W2 values for (B).
   constexpr int kWq = KC * kHU / 256;
   float wv[kWq], zp[kR];
   const float b1h = b1[h], b2v = b2[u < C ? u : 0];
