@@ -210,6 +210,29 @@ int hieravg_set_lr(hieravg_t h, float lr);
 int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
                      int64_t* correct);
 
+/*
+ * hieravg_evaluate for callers that cannot allocate device memory (code that
+ * must not call hipMalloc or hipFree: tight serving or evaluation loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * hieravg_evaluate; it allocates nothing.  Its chunk buffers (row list,
+ * split-K partials, activations, per-row losses and hits) live in one
+ * file-scope device array of HIERAVG_EVAL_SCRATCH_BYTES bytes that exists
+ * once on every GPU the library runs on and is held until the process ends;
+ * the chunk is the largest of 4096, 2048, ..., 16 rows whose buffers fit.
+ * Every call on a GPU shares that GPU's array (nothing in it needs to start
+ * at zero), so calls that overlap on one GPU, from any handles or threads,
+ * race and must be serialised by the caller.  Split 1 evaluates held-out
+ * rows that an earlier hieravg_evaluate call of the handle generated
+ * (n_rows above that count: HIERAVG_ESIZE).  A model whose 16-row chunk does
+ * not fit the array (2*hidden + classes above about 262000 for the MLP,
+ * classes above that for softmax regression) gets HIERAVG_ESIZE with the
+ * size it would need.  Runs on the handle's stream,
+ * on the handle's device, and synchronises.
+ */
+#define HIERAVG_EVAL_SCRATCH_BYTES ((size_t)16 << 20)
+int hieravg_evaluate_noalloc(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
+                             int64_t* correct);
+
 /* Release every resource of the handle.  NULL-safe. */
 void hieravg_destroy(hieravg_t h);
 

@@ -29,6 +29,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -115,6 +116,7 @@ struct hieravg {
   float* part2 = nullptr;  // layer-2 split-K partials of the delayed schedule with more than 32 classes
   // Evaluation (allocated at the first hieravg_evaluate).
   int eval_rows = 0;                  // chunk capacity (multiple of 16)
+  int64_t eval_part_cap = 0, eval_part2_cap = 0;  // floats in eval_part, eval_part2
   int32_t* eval_iota = nullptr;       // [eval_rows] 0, 1, 2, ...
   float *eval_part = nullptr, *eval_part2 = nullptr, *eval_Z1 = nullptr, *eval_loss = nullptr;
   int32_t* eval_hit = nullptr;
@@ -123,6 +125,7 @@ struct hieravg {
   int32_t* ytest = nullptr;           // [n_test]
   int KSG = 1;             // feature splits of the Gram blocks
   hipStream_t own_stream = nullptr, stream = nullptr;
+  int device = 0;  // the device current at create (every buffer lives there)
   int64_t steps = 0;
   int T = 1;  // SGD steps per round
   // One round's kernels, captured on first use and replayed for every round
@@ -307,6 +310,7 @@ int64_t plan(hieravg* h, int B) {
 
 int build(hieravg* h) {
   const hieravg_config& c = h->cfg;
+  HAV_CHECK(hipGetDevice(&h->device));
   HAV_CHECK(hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking));
   h->stream = h->own_stream;
   {
@@ -888,6 +892,184 @@ void enqueue_round(hieravg* h) {
   }
 }
 
+// ------------------------------------------------------------ evaluation
+constexpr int kEvalMaxChunk = 4096;  // rows per evaluation chunk
+
+// Device buffers of one evaluation: a chunk of `rows` rows at a time.
+struct EvalBufs {
+  int rows = 0;
+  int32_t* iota = nullptr;   // [rows] 0, 1, 2, ...
+  float* part = nullptr;     // first-layer split-K partials, capacity part_cap floats
+  int64_t part_cap = 0;
+  float* Z1 = nullptr;       // [rows][Hp] (MLP)
+  float* part2 = nullptr;    // logit split-K partials (MLP), capacity part2_cap floats
+  int64_t part2_cap = 0;
+  float* loss = nullptr;     // [rows]
+  int32_t* hit = nullptr;    // [rows]
+};
+
+int eval_check(hieravg* h, int32_t replica, int32_t split, int64_t n_rows, const double* mean_loss,
+               const int64_t* correct) {
+  if (!h || !mean_loss || !correct) {
+    set_error("NULL handle or output");
+    return HIERAVG_EINVAL;
+  }
+  if (h->cfg.kind == HIERAVG_KIND_AVERAGING) {
+    set_error("the averaging-only workload has no model to evaluate");
+    return HIERAVG_EINVAL;
+  }
+  if (replica < 0 || replica >= h->cfg.P || (split != 0 && split != 1) || n_rows < 1 ||
+      (split == 0 && n_rows > h->N) || n_rows > (int64_t(1) << 31)) {
+    set_error("bad replica, split or row count (split 0 takes at most N rows)");
+    return HIERAVG_EINVAL;
+  }
+  return HIERAVG_OK;
+}
+
+// Split count of a forward over one row group of Mp rows whose partials must
+// fit in `cap` floats (cap >= Mp * N).
+void split_within(int Mp, int N, int K, int64_t cap, int* KS, int* cps) {
+  plan_split(1, Mp, N, K, KS, cps);
+  const int nch = K / 64;
+  const int64_t ks_max = std::max<int64_t>(1, cap / ((int64_t)Mp * N));
+  if (*KS > ks_max) {
+    const int c = (int)((nch + ks_max - 1) / ks_max);
+    *cps = c;
+    *KS = (nch + c - 1) / c;
+  }
+}
+
+// Loss and hits of rows 0 .. n_rows-1 of a split, chunk by chunk: the forward
+// kernels of the round (first layer from the dataset rows, split-K partials),
+// then per row the softmax cross-entropy at the label and the first argmax;
+// the host adds the per-row values in double.
+int eval_chunks(hieravg* h, const EvalBufs& b, int replica, int split, int64_t n_rows, double* mean_loss,
+                int64_t* correct) {
+  const bool mlp = h->cfg.kind == HIERAVG_KIND_MLP;
+  const int Hp = (int)h->Hp, Cp = (int)h->Cp, INp = (int)h->INp, C = (int)h->C;
+  const int n1 = mlp ? Hp : Cp;
+  hipStream_t s = h->stream;
+  const float* Xs = split == 0 ? h->X : h->Xtest;
+  const int32_t* ys = split == 0 ? h->y : h->ytest;
+  // Replica `replica`; its first weight block lives in replica 0 while the
+  // learners share it under delayed updates.
+  const float* Wr = h->W + (int64_t)replica * h->Dp;
+  const float* W1r = (h->rows_stale ? h->W : Wr) + h->off_W1;
+  double total = 0.0;
+  int64_t hits = 0;
+  float lh[kEvalMaxChunk];
+  int32_t hh[kEvalMaxChunk];
+  for (int64_t r0 = 0; r0 < n_rows; r0 += b.rows) {
+    const int M = (int)std::min<int64_t>(b.rows, n_rows - r0);
+    const int Mp = (int)round_up(M, 16);
+    int KS1, cps1;
+    split_within(Mp, n1, INp, b.part_cap, &KS1, &cps1);
+    FwdArgs f{Xs + r0 * h->INp, b.iota, h->INp, W1r, 0, h->INp, b.part, 1, M, Mp, n1, INp, KS1, cps1};
+    launch_fwd(s, f, A_GATHER);
+    if (mlp) {
+      launch_reduce_bias(s, b.part, KS1, Wr + h->off_b1, 0, b.Z1, 1, M, Mp, Hp);
+      int KS2, cps2;
+      split_within(Mp, Cp, Hp, b.part2_cap, &KS2, &cps2);
+      FwdArgs f2{b.Z1, nullptr, h->Hp, Wr + h->off_W2, 0, h->Hp, b.part2, 1, M, Mp, Cp, Hp, KS2, cps2};
+      launch_fwd(s, f2, A_RELU);
+      launch_eval_rows(s, b.part2, KS2, (int64_t)Mp * Cp, Wr + h->off_b2, ys + r0, M, Cp, C, b.loss, b.hit);
+    } else {
+      launch_eval_rows(s, b.part, KS1, (int64_t)Mp * Cp, Wr + h->off_b1, ys + r0, M, Cp, C, b.loss, b.hit);
+    }
+    HAV_CHECK(hipGetLastError());
+    HAV_CHECK(hipMemcpyAsync(lh, b.loss, sizeof(float) * M, hipMemcpyDeviceToHost, s));
+    HAV_CHECK(hipMemcpyAsync(hh, b.hit, sizeof(int32_t) * M, hipMemcpyDeviceToHost, s));
+    HAV_CHECK(hipStreamSynchronize(s));
+    for (int i = 0; i < M; ++i) {
+      total += lh[i];
+      hits += hh[i];
+    }
+  }
+  *mean_loss = total / (double)n_rows;
+  *correct = hits;
+  return HIERAVG_OK;
+}
+
+// The device scratch array of hieravg_evaluate_noalloc: one per GPU (a
+// file-scope device array exists once on every device the library runs on),
+// kept until the process ends.  Host code never passes `scratch` itself to a
+// kernel (on the host it names a stand-in, not device memory): it looks up
+// the array's device address once per device and uses that.
+constexpr int64_t kScratchFloats = HIERAVG_EVAL_SCRATCH_BYTES / sizeof(float);
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on device `dev` (the current device).
+int scratch_on_device(int dev, float** out) {
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("device id out of the range of the scratch table");
+    return HIERAVG_EINVAL;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_error(std::string("hipGetSymbolAddress of the evaluation scratch failed: ") + hipGetErrorString(e));
+      return HIERAVG_EHIP;
+    }
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HIERAVG_OK;
+}
+
+// Makes `dev` current for a scope and restores the caller's device.
+struct DeviceGuard {
+  int prev = -1;
+  int enter(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) {
+      prev = -1;
+      set_error("hipGetDevice failed");
+      return HIERAVG_EHIP;
+    }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) {
+      set_error("hipSetDevice to the handle's device failed");
+      return HIERAVG_EHIP;
+    }
+    return HIERAVG_OK;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+// Largest chunk (rows, a multiple of 16 up to kEvalMaxChunk) whose buffers fit
+// in the scratch array with one split each, and the partial capacities.
+int eval_scratch_plan(const hieravg* h, int* rows, int64_t* part_cap, int64_t* part2_cap) {
+  const bool mlp = h->cfg.kind == HIERAVG_KIND_MLP;
+  const int64_t n1 = mlp ? h->Hp : h->Cp;
+  for (int r = kEvalMaxChunk; r >= 16; r /= 2) {
+    const int64_t fixed = 3 * round_up(r, 64) + (mlp ? round_up((int64_t)r * h->Hp, 64) : 0);
+    int64_t p2 = 0;
+    if (mlp) {
+      int KS2, cps2;
+      plan_split(1, r, (int)h->Cp, (int)h->Hp, &KS2, &cps2);
+      p2 = round_up((int64_t)KS2 * r * h->Cp, 64);
+      if (fixed + p2 + r * n1 > kScratchFloats) p2 = round_up((int64_t)r * h->Cp, 64);
+    }
+    const int64_t left = kScratchFloats - fixed - p2;
+    if (left >= r * n1) {
+      *rows = r;
+      *part_cap = left;
+      *part2_cap = p2;
+      return HIERAVG_OK;
+    }
+  }
+  const int64_t need = 4 * (3 * 64 + 16 * n1 + (mlp ? 16 * (h->Hp + h->Cp) : 0));
+  set_error("hieravg_evaluate_noalloc: a 16-row chunk of this model needs " + std::to_string(need) +
+            " bytes of scratch, more than its " + std::to_string((long long)HIERAVG_EVAL_SCRATCH_BYTES));
+  return HIERAVG_ESIZE;
+}
+
 }  // namespace
 
 extern "C" {
@@ -977,29 +1159,20 @@ int hieravg_set_lr(hieravg_t h, float lr) {
 
 int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
                      int64_t* correct) {
-  if (!h || !mean_loss || !correct) {
-    set_error("NULL handle or output");
-    return HIERAVG_EINVAL;
-  }
+  int rc = eval_check(h, replica, split, n_rows, mean_loss, correct);
+  if (rc != HIERAVG_OK) return rc;
   const hieravg_config& c = h->cfg;
-  if (c.kind == HIERAVG_KIND_AVERAGING) {
-    set_error("the averaging-only workload has no model to evaluate");
-    return HIERAVG_EINVAL;
-  }
-  if (replica < 0 || replica >= c.P || (split != 0 && split != 1) || n_rows < 1 ||
-      (split == 0 && n_rows > h->N) || n_rows > (int64_t(1) << 31)) {
-    set_error("bad replica, split or row count (split 0 takes at most N rows)");
-    return HIERAVG_EINVAL;
-  }
   const bool mlp = c.kind == HIERAVG_KIND_MLP;
   const int Hp = (int)h->Hp, Cp = (int)h->Cp, INp = (int)h->INp, C = (int)h->C;
   hipStream_t s = h->stream;
   HAV_CHECK(hipStreamSynchronize(s));
-  // Buffers for chunks of up to 4096 rows.
-  const int chunk = (int)std::min<int64_t>(4096, round_up(n_rows, 16));
-  int KS1e, cps1e, KS2e = 1, cps2e = 1;
-  plan_split(1, chunk, mlp ? Hp : Cp, INp, &KS1e, &cps1e);
-  if (mlp) plan_split(1, chunk, Cp, Hp, &KS2e, &cps2e);
+  // Buffers for chunks of up to kEvalMaxChunk rows.
+  const int chunk = (int)std::min<int64_t>(kEvalMaxChunk, round_up(n_rows, 16));
+  // Partials for the split counts of a full chunk (a shorter last chunk
+  // takes at most as many floats: split_within caps its splits).
+  int ks1, ks2 = 1, cps;
+  plan_split(1, chunk, mlp ? Hp : Cp, INp, &ks1, &cps);
+  if (mlp) plan_split(1, chunk, Cp, Hp, &ks2, &cps);
   if (chunk > h->eval_rows) {
     void* old[] = {h->eval_iota, h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit};
     for (void* b : old)
@@ -1008,9 +1181,6 @@ int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows
     h->eval_part = h->eval_part2 = h->eval_Z1 = h->eval_loss = nullptr;
     h->eval_hit = nullptr;
     h->eval_rows = 0;
-    int rc;
-    // KS for a chunk is at most the number of 64-wide K chunks.
-    const int64_t ks1 = std::max<int64_t>(KS1e, INp / 64), ks2 = mlp ? std::max<int64_t>(KS2e, Hp / 64) : 1;
     if ((rc = alloc_zero(h, (void**)&h->eval_iota, sizeof(int32_t) * chunk, "evaluation rows")) ||
         (rc = alloc_zero(h, (void**)&h->eval_part, sizeof(float) * ks1 * chunk * (mlp ? Hp : Cp), "evaluation partials")) ||
         (rc = alloc_zero(h, (void**)&h->eval_loss, sizeof(float) * chunk, "evaluation losses")) ||
@@ -1019,11 +1189,12 @@ int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows
     if (mlp && ((rc = alloc_zero(h, (void**)&h->eval_part2, sizeof(float) * ks2 * chunk * Cp, "evaluation logits")) ||
                 (rc = alloc_zero(h, (void**)&h->eval_Z1, sizeof(float) * chunk * Hp, "evaluation activations"))))
       return rc;
-    std::vector<int32_t> iota(chunk);
-    for (int i = 0; i < chunk; ++i) iota[i] = i;
-    HAV_CHECK(hipMemcpyAsync(h->eval_iota, iota.data(), sizeof(int32_t) * chunk, hipMemcpyHostToDevice, s));
+    launch_iota(s, h->eval_iota, chunk);
+    HAV_CHECK(hipGetLastError());
     HAV_CHECK(hipStreamSynchronize(s));
     h->eval_rows = chunk;
+    h->eval_part_cap = (int64_t)ks1 * chunk * (mlp ? Hp : Cp);
+    h->eval_part2_cap = mlp ? (int64_t)ks2 * chunk * Cp : 0;
   }
   // Held-out rows: the dataset recipe with its own label and noise streams.
   if (split == 1 && n_rows > h->n_test) {
@@ -1032,7 +1203,6 @@ int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows
     h->Xtest = nullptr;
     h->ytest = nullptr;
     h->n_test = 0;
-    int rc;
     if ((rc = alloc_zero(h, (void**)&h->Xtest, sizeof(float) * n_rows * h->INp, "held-out rows")) ||
         (rc = alloc_zero(h, (void**)&h->ytest, sizeof(int32_t) * n_rows, "held-out labels")))
       return rc;
@@ -1042,48 +1212,53 @@ int hieravg_evaluate(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows
     HAV_CHECK(hipGetLastError());
     h->n_test = n_rows;
   }
-  const float* Xs = split == 0 ? h->X : h->Xtest;
-  const int32_t* ys = split == 0 ? h->y : h->ytest;
-  // Replica `replica`; its first weight block lives in replica 0 while the
-  // learners share it under delayed updates.
-  const float* Wr = h->W + (int64_t)replica * h->Dp;
-  const float* W1r = (h->rows_stale ? h->W : Wr) + h->off_W1;
-  double total = 0.0;
-  int64_t hits = 0;
-  std::vector<float> lh(chunk);
-  std::vector<int32_t> hh(chunk);
-  for (int64_t r0 = 0; r0 < n_rows; r0 += chunk) {
-    const int M = (int)std::min<int64_t>(chunk, n_rows - r0);
-    const int Mp = (int)round_up(M, 16);
-    int KS1, cps1;
-    plan_split(1, Mp, mlp ? Hp : Cp, INp, &KS1, &cps1);
-    FwdArgs f{Xs + r0 * h->INp, h->eval_iota, h->INp, W1r, 0, h->INp, h->eval_part, 1, M, Mp, mlp ? Hp : Cp, INp,
-              KS1, cps1};
-    launch_fwd(s, f, A_GATHER);
-    if (mlp) {
-      launch_reduce_bias(s, h->eval_part, KS1, Wr + h->off_b1, 0, h->eval_Z1, 1, M, Mp, Hp);
-      int KS2, cps2;
-      plan_split(1, Mp, Cp, Hp, &KS2, &cps2);
-      FwdArgs f2{h->eval_Z1, nullptr, h->Hp, Wr + h->off_W2, 0, h->Hp, h->eval_part2, 1, M, Mp, Cp, Hp, KS2, cps2};
-      launch_fwd(s, f2, A_RELU);
-      launch_eval_rows(s, h->eval_part2, KS2, (int64_t)Mp * Cp, Wr + h->off_b2, ys + r0, M, Cp, C, h->eval_loss,
-                       h->eval_hit);
-    } else {
-      launch_eval_rows(s, h->eval_part, KS1, (int64_t)Mp * Cp, Wr + h->off_b1, ys + r0, M, Cp, C, h->eval_loss,
-                       h->eval_hit);
-    }
-    HAV_CHECK(hipGetLastError());
-    HAV_CHECK(hipMemcpyAsync(lh.data(), h->eval_loss, sizeof(float) * M, hipMemcpyDeviceToHost, s));
-    HAV_CHECK(hipMemcpyAsync(hh.data(), h->eval_hit, sizeof(int32_t) * M, hipMemcpyDeviceToHost, s));
-    HAV_CHECK(hipStreamSynchronize(s));
-    for (int i = 0; i < M; ++i) {
-      total += lh[i];
-      hits += hh[i];
-    }
+  EvalBufs b;
+  b.rows = chunk;
+  b.iota = h->eval_iota;
+  b.part = h->eval_part;
+  b.part_cap = h->eval_part_cap;
+  b.Z1 = h->eval_Z1;
+  b.part2 = h->eval_part2;
+  b.part2_cap = h->eval_part2_cap;
+  b.loss = h->eval_loss;
+  b.hit = h->eval_hit;
+  return eval_chunks(h, b, replica, split, n_rows, mean_loss, correct);
+}
+
+int hieravg_evaluate_noalloc(hieravg_t h, int32_t replica, int32_t split, int64_t n_rows, double* mean_loss,
+                             int64_t* correct) {
+  int rc = eval_check(h, replica, split, n_rows, mean_loss, correct);
+  if (rc != HIERAVG_OK) return rc;
+  if (split == 1 && n_rows > h->n_test) {
+    set_error("hieravg_evaluate_noalloc: the held-out rows are generated (and allocated) by hieravg_evaluate; " +
+              std::to_string(h->n_test) + " exist, " + std::to_string(n_rows) + " requested");
+    return HIERAVG_ESIZE;
   }
-  *mean_loss = total / (double)n_rows;
-  *correct = hits;
-  return HIERAVG_OK;
+  EvalBufs b;
+  if ((rc = eval_scratch_plan(h, &b.rows, &b.part_cap, &b.part2_cap)) != HIERAVG_OK) return rc;
+  DeviceGuard dg;
+  if ((rc = dg.enter(h->device)) != HIERAVG_OK) return rc;
+  float* base = nullptr;
+  if ((rc = scratch_on_device(h->device, &base)) != HIERAVG_OK) return rc;
+  // Regions of the scratch array (offsets in floats, each a multiple of 64).
+  const bool mlp = h->cfg.kind == HIERAVG_KIND_MLP;
+  const int64_t rows64 = round_up(b.rows, 64);
+  int64_t off = 0;
+  b.iota = (int32_t*)(base + off);
+  off += rows64;
+  b.loss = base + off;
+  off += rows64;
+  b.hit = (int32_t*)(base + off);
+  off += rows64;
+  b.Z1 = mlp ? base + off : nullptr;
+  off += mlp ? round_up((int64_t)b.rows * h->Hp, 64) : 0;
+  b.part2 = mlp ? base + off : nullptr;
+  off += mlp ? round_up(b.part2_cap, 64) : 0;
+  b.part = base + off;
+  HAV_CHECK(hipStreamSynchronize(h->stream));
+  launch_iota(h->stream, b.iota, b.rows);
+  HAV_CHECK(hipGetLastError());
+  return eval_chunks(h, b, replica, split, n_rows, mean_loss, correct);
 }
 
 int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {

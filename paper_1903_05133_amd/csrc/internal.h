@@ -145,6 +145,8 @@ void launch_init_matrix(hipStream_t s, float* W, int64_t rows, int64_t cols, int
                         uint64_t layer, float scale);
 void launch_init_vector(hipStream_t s, float* w, int64_t D, uint64_t key, float std);
 void launch_gen_grads(hipStream_t s, float* G, int64_t D, int64_t Dp, int P, int T, uint64_t key, float std);
+// dst[i] = i, i < n (n >= 1).
+void launch_iota(hipStream_t s, int32_t* dst, int n);
 // Row tables of the block update (delayed updates): for block b, cluster g
 // and contraction row r = (k*S + j)*B + s (step k of the block, learner
 // g*S + j, sample s) at [(b*(P/S) + g)*Rp + r], the offsets in 64-float

@@ -100,11 +100,19 @@ __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx,
   }
 }
 
+// dst[i] = i for i < n (the row list of an evaluation chunk).
+__global__ __launch_bounds__(256) void k_iota(int32_t* __restrict__ dst, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = i;
+}
+
 static int grid_for(int64_t n, int cap = 8192) {
   int64_t g = (n + 255) / 256;
   if (g < 1) g = 1;
   return (int)(g < cap ? g : cap);
 }
+
+void launch_iota(hipStream_t s, int32_t* dst, int n) { launch(k_iota, (n + 255) / 256, 256, 0, s, dst, n); }
 
 void launch_gen_labels(hipStream_t s, int32_t* y, int64_t N, uint64_t key, uint64_t C) {
   launch(k_gen_labels, grid_for(N), 256, 0, s, y, N, key, C);

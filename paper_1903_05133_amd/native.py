@@ -46,6 +46,8 @@ SIGNATURES = {
     "hieravg_set_momentum": (ctypes.c_int, [_H, ctypes.c_void_p, ctypes.c_size_t]),
     "hieravg_evaluate": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
+    "hieravg_evaluate_noalloc": (ctypes.c_int, [_H, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "hieravg_last_error": (ctypes.c_char_p, []),
     "hieravg_dim": (ctypes.c_int64, [_H]),
     "hieravg_step_count": (ctypes.c_int64, [_H]),

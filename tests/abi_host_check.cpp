@@ -26,6 +26,9 @@ int main() {
   expect(hieravg_params(nullptr, nullptr, 0) == HIERAVG_EINVAL, "params null");
   expect(hieravg_check_finite(nullptr) == HIERAVG_EINVAL, "finite null");
   expect(hieravg_set_step_count(nullptr, 1) == HIERAVG_EINVAL, "step null");
+  double loss = 0.0;
+  int64_t hits = 0;
+  expect(hieravg_evaluate_noalloc(nullptr, 0, 0, 1, &loss, &hits) == HIERAVG_EINVAL, "evaluate_noalloc null");
   expect(std::strcmp(hieravg_kernel_class_name(-1), "") == 0, "class -1");
   expect(std::strcmp(hieravg_kernel_class_name(hieravg_kernel_classes()), "") == 0, "class n");
   hieravg_destroy(nullptr);
