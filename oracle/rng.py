@@ -150,10 +150,13 @@ def init_uniform(seed: int, layer: int, rows: int, cols: int):
     """Initial weight matrix [rows, cols] of layer `layer`: (2u - 1) * s with
     u = (H >> 40) * 2^-24 and s = fp32(1 / sqrt(cols)) (fan-in scaling)."""
     key = stream_key(seed, TAG_INIT)
-    e = (np.uint64(layer) << np.uint64(48)) + np.arange(rows * cols, dtype=np.uint64)
-    u = (h(key, e) >> np.uint64(40)).astype(np.float64) * 2.0 ** -24
     s = float(np.float32(1.0 / np.sqrt(float(cols))))
-    w = ((2.0 * u - 1.0) * s).astype(np.float32).astype(np.float64)
+    w = np.empty(rows * cols, dtype=np.float64)
+    step = 1 << 20  # elements per piece (the values do not depend on it)
+    for a in range(0, rows * cols, step):
+        e = (np.uint64(layer) << np.uint64(48)) + np.arange(a, min(a + step, rows * cols), dtype=np.uint64)
+        u = (h(key, e) >> np.uint64(40)).astype(np.float64) * 2.0 ** -24
+        w[a:a + len(e)] = ((2.0 * u - 1.0) * s).astype(np.float32)
     return w.reshape(rows, cols)
 
 

@@ -460,3 +460,86 @@ def test_averaged_buffers_with_one_group_per_step_are_large_batch_momentum():
         torch_loss(p, prm, np.concatenate(Xs), np.concatenate(ys)).backward()
         opt.step()
     assert relerr(st.W[0], flatten(p, prm)) < 1e-12
+
+
+# ------------------------------------------------------- ReLU decisions at a kink
+def _kink_problem():
+    return M.Problem(M.MLP, 1, 1, 1, 1, 2, IN=2, H=2, C=2, N=4)
+
+
+def test_kink_monitor_margins_by_hand():
+    """Two samples, two units.  z1 = X W1^T + b1 and the margins
+    |z1| / (sum_k |x_k W1[h,k]| + |b1[h]|), written out:
+      sample 0: unit 0  1*2 + 2*(-1) + 0   = 0     over 2 + 2 + 0      = 4     -> 0
+                unit 1  1*.5 + 2*.25 - .5  = 0.5   over .5 + .5 + .5   = 1.5   -> 1/3
+      sample 1: unit 0  3*2 + (-1)*(-1) + 0 = 7    over 6 + 1 + 0      = 7     -> 1
+                unit 1  3*.5 - .25 - .5    = 0.75  over 1.5 + .25 + .5 = 2.25  -> 1/3"""
+    X = np.array([[1.0, 2.0], [3.0, -1.0]])
+    W1 = np.array([[2.0, -1.0], [0.5, 0.25]])
+    b1 = np.array([0.0, -0.5])
+    mon = M.KinkMonitor(2)
+    mon.observe(X @ W1.T + b1, X, W1, b1, t=5, j=3)
+    assert np.allclose(mon.min_margin, [0.0, 1.0 / 3.0], rtol=0, atol=1e-15)
+    assert mon.decisions == [(5, 3, 0, 0, 0.0)]
+    # a planted pre-activation just off zero: b1[0] = 2^-30 gives z1 = 2^-30
+    # over 4 + 2^-30; b1[0] = 2^-12 gives a margin of about 2^-14, above the
+    # default threshold 2^-16
+    for b, flagged in ((2.0 ** -30, True), (2.0 ** -12, False)):
+        mon = M.KinkMonitor(2)
+        bb = np.array([b, -0.5])
+        mon.observe(X @ W1.T + bb, X, W1, bb, t=0, j=0)
+        want = b / (4.0 + b)
+        assert abs(mon.min_margin[0] - want) <= 1e-15 * want
+        assert [d[:4] for d in mon.decisions] == ([(0, 0, 0, 0)] if flagged else [])
+    # the monitor sees every learner step of a run, labelled by step and learner
+    p = M.Problem(M.MLP, 4, 2, 2, 1, 8, IN=20, H=12, C=5, N=64, sigma=0.5, lr=0.1, seed=3)
+    mon = M.KinkMonitor(p.H, threshold=1.0)   # every decision
+    M.run(p, 1, monitor=mon)
+    assert len(mon.decisions) == p.T * p.P * p.B * p.H
+    assert {(d[0], d[1]) for d in mon.decisions} == {(t, j) for t in range(p.T) for j in range(p.P)}
+
+
+def test_flipped_decision_is_the_other_relu_derivative():
+    """With z1[s, h] exactly 0 the activation is 0 on both branches, so taking
+    the decision the other way only changes the derivative [z1 > 0] there:
+    the gradient equals autograd's with d ReLU/dz = 1 at that one entry
+    (relu(z) + (z - z.detach()) at (s, h): same value, derivative + 1)."""
+    p = _kink_problem()
+    row = np.zeros(M.param_count(p))
+    blk = M.unpack(p, row)
+    blk["W1"][:] = [[2.0, -1.0], [0.5, 0.25]]
+    blk["b1"][:] = [0.0, -0.5]
+    blk["W2"][:] = [[0.3, -0.7], [-0.2, 0.4]]
+    blk["b2"][:] = [0.1, -0.1]
+    X = np.array([[1.0, 2.0], [3.0, -1.0]])
+    y = np.array([1, 0])
+    plain = M.minibatch_gradient(p, row, X, y)
+    flipped = M.minibatch_gradient(p, row, X, y, flips=[(0, 0)])
+
+    def autograd(extra):
+        prm = torch_params(p, row)
+        z1 = torch.tensor(X) @ prm["W1"].T + prm["b1"]
+        e = torch.zeros(2, 2)
+        e[0, 0] = extra
+        a1 = torch.relu(z1) + (z1 - z1.detach()) * e
+        z2 = a1 @ prm["W2"].T + prm["b2"]
+        torch.nn.functional.cross_entropy(z2, torch.tensor(y)).backward()
+        return flatten_grad(p, prm)
+
+    assert relerr(plain, autograd(0.0)) < 1e-14
+    assert relerr(flipped, autograd(1.0)) < 1e-14
+    d = M.unpack(p, flipped - plain)
+    assert np.any(d["W1"][0] != 0) and np.all(d["W1"][1] == 0) and np.all(d["W2"] == 0)
+
+
+def flatten_grad(p, prm):
+    return np.concatenate([prm[name].grad.numpy().reshape(-1) for name, _ in M.segments(p)])
+
+
+def test_flips_touch_only_their_learner_and_step():
+    p = M.Problem(M.MLP, 2, 2, 2, 1, 4, IN=10, H=6, C=3, N=20, sigma=0.5, lr=0.1, seed=5)
+    base = M.run(p, 1)
+    same = M.run(p, 1, flips=frozenset([(7, 0, 0, 0)]))  # a step outside the round
+    assert np.array_equal(base.W, same.W)
+    moved = M.run(p, 1, flips=frozenset([(1, 1, 2, 3)]))
+    assert not np.array_equal(base.W, moved.W)

@@ -1,6 +1,9 @@
-"""The parity gate used by the GPU tests rejects planted mistakes (planted in
-oracle output on the CPU) and accepts only deviations it can attribute to a
-ReLU decision within float32 rounding."""
+"""The parity gate used by the GPU tests, checked both ways on the CPU.
+
+It must reject planted mistakes (planted in oracle output) and accept a
+deviation only when it is exactly the other correct branch of a ReLU decision
+at a kink: the oracle re-run with that near-zero decision taken the other way
+must then match every parameter to the strict tolerance."""
 
 import numpy as np
 import pytest
@@ -8,14 +11,23 @@ import pytest
 import cases
 from oracle import method as M
 
+CASE = cases.case("mlp", 4, 2, 2, 2, B=8, IN=40, H=128, C=5, N=64, sigma=0.5, lr=0.1, seed=3)
+
 
 @pytest.fixture(scope="module")
 def mlp_run():
-    c = cases.case("mlp", 4, 2, 2, 2, B=8, IN=40, H=128, C=5, N=64, sigma=0.5, lr=0.1, seed=3)
-    prob = cases.oracle_problem(c)
+    prob = cases.oracle_problem(CASE)
     mon = M.KinkMonitor(prob.H)
     st = M.run(prob, 1, monitor=mon)
-    return prob, st, mon
+    # a monitor with a wide threshold: decisions close to (not at) a kink,
+    # whose flip changes the result far beyond rounding
+    wide = M.KinkMonitor(prob.H, threshold=0.05)
+    M.run(prob, 1, monitor=wide)
+    return prob, st, mon, wide
+
+
+def _rerun(prob):
+    return lambda flips: M.run(prob, 1, flips=flips).W
 
 
 def _perturb_unit(prob, W, h, rel):
@@ -25,58 +37,89 @@ def _perturb_unit(prob, W, h, rel):
     return out
 
 
+def _monitor_with(prob, decisions):
+    mon = M.KinkMonitor(prob.H)
+    mon.decisions = list(decisions)
+    return mon
+
+
+def _flip_that_matters(prob, st, wide, k=0):
+    """The k-th wide-threshold decision whose flip moves the result beyond the
+    gate (so the plain gate rejects that run)."""
+    found = []
+    for d in sorted(wide.decisions, key=lambda d: d[4]):
+        W = M.run(prob, 1, flips=frozenset([d[:4]])).W
+        if not cases.parity_report(prob, W.astype(np.float32), st.W)[0]:
+            found.append((d, W))
+            if len(found) > k:
+                return found[k]
+    pytest.fail("no decision whose flip matters")
+
+
 def test_exact_copy_passes(mlp_run):
-    prob, st, mon = mlp_run
-    ok, det = cases.parity_report(prob, st.W.astype(np.float32), st.W, mon)
-    assert ok and det["worst"][1] < 1e-6
+    prob, st, mon, _ = mlp_run
+    ok, det = cases.branch_parity(prob, st.W.astype(np.float32), st.W, mon, _rerun(prob))
+    assert ok and det["worst"][1] < 1e-6 and "flipped" not in det
 
 
 def test_unexplained_unit_deviation_fails(mlp_run):
-    prob, st, mon = mlp_run
-    h = int(np.argmax(mon.min_margin))          # the unit farthest from any kink
-    ok, det = cases.parity_report(prob, _perturb_unit(prob, st.W, h, 1e-3), st.W, mon)
+    prob, st, mon, wide = mlp_run
+    h = wide.decisions[0][3]                    # even a unit with candidate decisions
+    got = _perturb_unit(prob, st.W, h, 1e-3)
+    ok, det = cases.parity_report(prob, got, st.W)
+    assert not ok and h in det["units"]
+    ok, det = cases.branch_parity(prob, got, st.W, wide, _rerun(prob))
+    assert not ok and det["candidates"]         # flips were tried, none explains it
+
+
+def test_other_branch_of_a_flagged_decision_passes(mlp_run):
+    prob, st, _, wide = mlp_run
+    d, W = _flip_that_matters(prob, st, wide)
+    got = W.astype(np.float32)
+    assert not cases.parity_report(prob, got, st.W)[0]
+    ok, det = cases.branch_parity(prob, got, st.W, _monitor_with(prob, [d]), _rerun(prob))
+    assert ok and det["flipped"] == [d]
+    # the same run is rejected when the decision was not flagged as near a kink
+    ok, _ = cases.branch_parity(prob, got, st.W, _monitor_with(prob, []), _rerun(prob))
+    assert not ok
+    ok, _ = cases.branch_parity(prob, got, st.W, None, _rerun(prob))
     assert not ok
 
 
-def test_kink_explained_unit_deviation_passes_only_when_small(mlp_run):
-    prob, st, mon = mlp_run
-    h = 7
-    mon2 = M.KinkMonitor(prob.H)
-    mon2.min_margin = mon.min_margin.copy()
-    mon2.min_margin[h] = 1e-9                   # as if unit h had a near-zero pre-activation
-    ok, det = cases.parity_report(prob, _perturb_unit(prob, st.W, h, 1e-3), st.W, mon2)
-    assert ok and det["exempt_units"] == [h]
-    ok, _ = cases.parity_report(prob, _perturb_unit(prob, st.W, h, 0.1), st.W, mon2)
-    assert not ok                                # beyond the validity bound
-    ok, _ = cases.parity_report(prob, _perturb_unit(prob, st.W, h, 1e-3), st.W, None)
-    assert not ok                                # no kink evidence: strict gate
+def test_two_flipped_decisions_are_found(mlp_run):
+    prob, st, _, wide = mlp_run
+    d1, _ = _flip_that_matters(prob, st, wide, 0)
+    d2, _ = _flip_that_matters(prob, st, wide, 1)
+    got = M.run(prob, 1, flips=frozenset([d1[:4], d2[:4]])).W.astype(np.float32)
+    ok, det = cases.branch_parity(prob, got, st.W, _monitor_with(prob, [d1, d2]), _rerun(prob))
+    assert ok and sorted(det["flipped"]) == sorted([d1, d2])
 
 
-def test_too_many_exempt_units_fail(mlp_run):
-    prob, st, mon = mlp_run
-    mon2 = M.KinkMonitor(prob.H)
-    mon2.min_margin = np.full(prob.H, 1e-9)
-    W = st.W.astype(np.float32).copy()
-    for h in range(10):
-        W = _perturb_unit(prob, W.astype(np.float64), h, 1e-3)
-    ok, det = cases.parity_report(prob, W, st.W, mon2)
+def test_flip_plus_a_mistake_fails(mlp_run):
+    prob, st, _, wide = mlp_run
+    d, W = _flip_that_matters(prob, st, wide)
+    got = W.astype(np.float32).copy()
+    blk = M.unpack(prob, got[2])
+    blk["b2"][0] += 1e-3 * np.abs(blk["b2"]).max()
+    ok, _ = cases.branch_parity(prob, got, st.W, _monitor_with(prob, [d]), _rerun(prob))
     assert not ok
 
 
-@pytest.mark.parametrize("block", ["b2", "W2"])
+@pytest.mark.parametrize("block", ["b2", "W2", "b1"])
 def test_other_blocks_stay_strict(mlp_run, block):
-    prob, st, mon = mlp_run
+    prob, st, mon, wide = mlp_run
     W = st.W.astype(np.float32).copy()
     blk = M.unpack(prob, W[1])
     blk[block].reshape(-1)[0] += 1e-3 * np.abs(blk[block]).max()
-    ok, _ = cases.parity_report(prob, W, st.W, mon)
+    ok, _ = cases.branch_parity(prob, W, st.W, wide, _rerun(prob))
     assert not ok
 
 
-def test_softmax_has_no_exception():
+def test_softmax_gate_is_strict():
     c = cases.case("softmax", 2, 1, 1, 1, B=4, IN=10, C=3, N=20, lr=0.1)
     prob = cases.oracle_problem(c)
     st = M.run(prob, 1)
     W = st.W.astype(np.float32).copy()
     W[0, 3] += 1e-3 * np.abs(st.W).max()
-    assert not cases.parity_report(prob, W, st.W, None)[0]
+    assert not cases.branch_parity(prob, W, st.W, None, _rerun(prob))[0]
+    assert cases.branch_parity(prob, st.W.astype(np.float32), st.W, None, _rerun(prob))[0]
