@@ -1,26 +1,37 @@
 """Benchmark of the Hier-AVG hot path on one MI355X.
 
-One bench "step" is one Hier-AVG round (K2 blocks of K1 local SGD steps of
-all P learners, the cluster means and the global mean) of the MLP
-3072 -> 512 -> 10 workload with P=16, S=4, K1=4, K2=4, B=32, lr=0.05 on
-synthetic data (N=50000 rows: class-mean pattern + N(0, 0.5) noise).
-`value` is learner-SGD-steps per second (P*K1*K2 per round) with the dataset
-and replicas resident in HBM.
+One bench "step" is one Hier-AVG round (Algorithm 1, Sec. 3.1: K2 blocks of
+K1 local SGD steps of all P learners, the cluster means and the global mean)
+of the headline workload: the 3-layer MLP 150528 -> 1024 ReLU -> 1000 with
+softmax cross-entropy (155.2M parameters per replica), P=16, S=4, K1=4,
+K2=2, B=32, lr=0.02, on synthetic ImageNet-shaped data (N=100000 rows of
+224*224*3 features: class-mean pattern ~N(0,1) + N(0,1) noise, 1000
+classes).  This is the largest single-GPU workload.  `value` is
+learner-SGD-steps per second (P*K1*K2 per round) with the dataset (60.2 GB)
+and the replicas (9.9 GB) resident in HBM.
 
 Also reported, on the same JSON line:
-  roofline      the dominant kernel of the round (largest launches x duration):
-                algorithmic bytes (or flops) per launch over its mean duration,
-                timed with HIP events on the handle's stream around 200
-                back-to-back launches of it after the timed rounds
-  averaging     the averaging-only workload (P=32 replicas of 11.7M floats,
-                S=4, K1=1, K2=4, heavy-ball momentum 0.9, lr 0.1): HBM GB/s of
-                the fused update + cluster mean and update + global mean
-                kernels as a fraction of the 8 TB/s peak
-  cpu_baseline  the CPU oracle (float64 numpy) on one round of the same
-                workload, on this host's cores
+  roofline      the dominant kernel of the headline round (largest launches x
+                duration): algorithmic flops (or bytes) per launch over its
+                mean duration, timed with HIP events on the handle's stream
+                around a graph of back-to-back launches of it; `traffic` is the
+                HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
+                counters (profiles/traffic.json) while the kernel's source is
+                unchanged since they were taken
+  configs       the other workloads, each timed the same way: softmax
+                3072 -> 10 (P=4, launch-bound: us per round, launches per
+                step), MLP 3072-512-10 at P=16 and at P=64 (B=64, MFMA-bound),
+                and the averaging-only workload (P=32 replicas of 11.7M floats,
+                heavy-ball momentum, cluster mean every step, global mean
+                every 4): HBM GB/s of the averaging kernels as a fraction of
+                8 TB/s
+  cpu_baseline  the CPU oracle (float64 numpy) on a sample of the headline
+                workload: one SGD step of all 16 learners, on this host's
+                cores, and one learner's step on one thread
 """
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -32,6 +43,17 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
+F = 4                          # bytes per float
+
+HEADLINE = "mlp_150528_1024_1000"
+# name -> (named workload, P, S, K1, K2, B, lr, rounds timed)
+WORKLOADS = {
+    "softmax_3072_10": ("softmax_3072_10", 4, 2, 2, 2, 8, 0.05, 400),
+    "mlp_3072_512_10": ("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, 200),
+    "mlp_3072_512_10_p64": ("mlp_3072_512_10", 64, 8, 8, 4, 64, 0.1, 20),
+    "averaging_11_7M": ("averaging_11_7M", 32, 4, 1, 4, 1, 0.1, 20),
+    HEADLINE: ("mlp_150528_1024_1000", 16, 4, 4, 2, 32, 0.02, None),
+}
 
 
 def log(*a):
@@ -39,246 +61,255 @@ def log(*a):
 
 
 # ---------------------------------------------------------------- algorithmic work
+def step_work(c):
+    """Algorithmic flops and bytes of one learner's SGD step: the forward and
+    weight-gradient products (no input gradient), every parameter read and
+    written once, the sampled rows and labels read once."""
+    B, IN, H, C = c["B"], c["IN"], c["H"], c["C"]
+    if c["kind"] == "softmax":
+        D = C * IN + C
+        return 4 * B * IN * C, 8 * D + 4 * B * IN + 4 * B
+    D = H * IN + H + C * H + C
+    return 4 * B * IN * H + 6 * B * H * C, 8 * D + 4 * B * IN + 4 * B
+
+
 def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
-    """Algorithmic bytes and flops per launch of each kernel class of one MLP
-    step (all P learners): every operand the step needs read once and every
-    result written once, at its logical (unpadded) size.  Split-K partial
-    sums are an implementation choice and are not counted.  The delayed-update
-    kernels are counted for the launch that is timed (step 0 of block 0,
-    where every learner reads replica 0's W1)."""
-    f = 4
+    """Algorithmic (bytes, flops) per launch of each kernel class of an MLP
+    round: every operand a launch needs read once and every result written
+    once, at its logical (unpadded) size.  Split-K partial sums are an
+    implementation choice and are not counted.  The delayed-update block
+    kernels differ between the first block (every cluster reads replica 0's
+    W1) and the others (each cluster reads its own copy); their bytes are the
+    mean over the K2 blocks of a round."""
     G = P // S
     pairs = K1 * (K1 - 1) // 2
     tail = H + C * H + C  # b1, W2, b2: their cluster (global) mean rides in the block update (W1 mean)
+    bases = (1 + (K2 - 1) * G) / K2          # W1 bases read per block, mean over the blocks
+    tail_means = (K2 - 1) / K2 if S > 1 else 0.0  # blocks whose update also takes the tail's cluster mean
+    k_avg = (K1 - 1) / 2.0                   # earlier steps corrected per step, mean over a block
     return {
-        # forward of block 0's K1 steps from the common W1: W1 once, the
-        # K1*P minibatches, the K1*P pre-activation blocks
-        "fwd1_block_gemm": (f * (H * IN + K1 * P * B * IN + K1 * P * B * H), K1 * P * 2 * B * H * IN),
-        # block end: the base read once, G cluster copies written, the block's
-        # hidden errors and minibatch rows read
-        "block_update_gemm": (f * (H * IN + G * H * IN + K1 * P * B * (H + IN) + 2 * P * tail),
+        # forward of a block's K1 steps from the block-start bases: the bases,
+        # the K1*P minibatches, the K1*P pre-activation blocks
+        "fwd1_block_gemm": (F * (bases * H * IN + K1 * P * B * IN + K1 * P * B * H), K1 * P * 2 * B * H * IN),
+        # block end: the bases read once, G cluster copies written, the
+        # block's hidden errors and minibatch rows read, the tail's mean
+        "block_update_gemm": (F * (bases * H * IN + G * H * IN + K1 * P * B * (H + IN) + tail_means * 2 * P * tail),
                               K1 * P * 2 * B * H * IN),
         # Gram blocks of the round: every minibatch row read once, blocks written
-        "gram": (f * (K2 * K1 * P * B * IN + K2 * P * pairs * B * B), K2 * P * pairs * 2 * B * B * IN),
-        "w1_global_mean": (f * ((G + 1) * H * IN + 2 * P * tail), G * H * IN + P * tail),
-        "fwd1_gemm": (P * f * (H * IN + B * IN + B * H), P * 2 * B * H * IN),
-        "reduce1": (P * f * (H + B * H), P * B * H),
-        "fwd2_gemm": (P * f * (C * H + B * H + B * C), P * 2 * B * C * H),
-        "softmax_grad": (P * f * (C + 2 * B * C) + P * B * 8, P * B * C * 4),
-        "bwd_hidden": (P * f * (B * C + C * H + 2 * B * H), P * 2 * B * C * H),
-        "update2_gemm": (P * f * (2 * C * H + B * C + B * H + 2 * C), P * 2 * B * C * H),
-        "update1_gemm": (P * f * (2 * H * IN + B * H + B * IN + 2 * H), P * 2 * B * H * IN),
+        "gram": (F * (K2 * K1 * P * B * IN + K2 * P * pairs * B * B), K2 * P * pairs * 2 * B * B * IN),
+        "w1_global_mean": (F * ((G + 1) * H * IN + 2 * P * tail), G * H * IN + P * tail),
+        # pre-activations of one step with the Gram correction of the earlier
+        # steps (more than 32 classes)
+        "z1_delayed": (F * P * (B * H + H + k_avg * (B * H + B * B) + B * H), P * 2 * B * B * H * k_avg),
+        "fwd1_gemm": (P * F * (H * IN + B * IN + B * H), P * 2 * B * H * IN),
+        "reduce1": (P * F * (H + B * H), P * B * H),
+        "fwd2_gemm": (P * F * (C * H + B * H + B * C), P * 2 * B * C * H),
+        "softmax_grad": (P * F * (C + 2 * B * C) + P * B * 8, P * B * C * 4),
+        "bwd_hidden": (P * F * (B * C + C * H + 2 * B * H), P * 2 * B * C * H),
+        "update2_gemm": (P * F * (2 * C * H + B * C + B * H + 2 * C), P * 2 * B * C * H),
+        "update1_gemm": (P * F * (2 * H * IN + B * H + B * IN + 2 * H), P * 2 * B * H * IN),
         # update of W1 at step t and forward of step t+1: W1 read and written
         # once, G1 and the two minibatches read, the next pre-activations
-        # written once; the group-mean variant moves the same bytes
-        "step1_gemm": (P * f * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
-        "step1_gemm_group_mean": (P * f * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
+        # written once; the cluster-mean variant moves the same bytes
+        "step1_gemm": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
+        "step1_gemm_group_mean": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
     }
 
 
-def mean_bytes(P, D):
-    return 2 * 4 * P * D
+def kernel_work(c):
+    P, S, K1, K2 = c["P"], c["S"], c["K1"], c["K2"]
+    if c["kind"] == "averaging":
+        D = c["IN"]
+        return {
+            # read w, v, g and write w, v of every learner
+            "momentum": (20 * P * D, 0), "momentum_group_mean": (20 * P * D, 0),
+            # every learner's w read from the stored global mean once; v, g read and v, w written per learner
+            "momentum_first_step": (16 * P * D + 4 * D, 0),
+            # w, v, g read and v written per learner; the common mean written once
+            "momentum_global_mean": (16 * P * D + 4 * D, 0),
+        }
+    if c["kind"] == "softmax":
+        B, IN, C = c["B"], c["IN"], c["C"]
+        D = C * IN + C
+        return {"fwd1_gemm": (P * F * (C * IN + B * IN + B * C), P * 2 * B * C * IN),
+                "update1_gemm": (P * F * (2 * D + B * C + B * IN), P * 2 * B * C * IN),
+                "step1_gemm": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
+                "step1_gemm_group_mean": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
+                "global_mean": (2 * F * P * D, P * D)}
+    w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"])
+    D = c["H"] * c["IN"] + c["H"] + c["C"] * c["H"] + c["C"]
+    tail = D - c["H"] * c["IN"]
+    w["group_mean"] = (2 * F * P * D, P * D)
+    w["global_mean"] = (2 * F * P * D, P * D)
+    w["tail_group_mean"] = (2 * F * P * tail, P * tail)
+    w["tail_global_mean"] = (2 * F * P * tail, P * tail)
+    return w
 
 
-def counter_mfma_util(kernel_class):
-    """MfmaUtil (fraction) of `kernel_class` from the committed counter summary
-    (profiles/mfma.json), or None when the kernel's source has changed since."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "mfma.json")
+def source_record(path, workload, kernel_class):
+    """The committed counter record of `kernel_class` in `workload`
+    (profiles/<path>), or None when the kernel's source has changed since the
+    counters were taken."""
     try:
-        rec = json.load(open(path))["kernels"][kernel_class]
+        rec = json.load(open(os.path.join(ROOT, "profiles", path)))["workloads"][workload]["kernels"][kernel_class]
         cur = hashlib.sha256(open(os.path.join(ROOT, rec["source"]), "rb").read()).hexdigest()
     except (OSError, KeyError, ValueError):
         return None
-    return rec["mfma_util"] if cur == rec["source_sha256"] else None
+    return rec if cur == rec["source_sha256"] else None
 
 
-def counter_traffic(kernel_class):
-    """HBM bytes per launch of `kernel_class` from the committed counter
-    summary (profiles/traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled by
-    a calibration stream), or None when the kernel's source has changed since
-    the counters were taken."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    try:
-        rec = json.load(open(path))["kernels"][kernel_class]
-        cur = hashlib.sha256(open(os.path.join(ROOT, rec["source"]), "rb").read()).hexdigest()
-    except (OSError, KeyError, ValueError):
-        return None
-    return rec["bytes"] if cur == rec["source_sha256"] else None
-
-
-# ---------------------------------------------------------------- main workload
-def bench_mlp(args):
+# ---------------------------------------------------------------- one workload
+def run_workload(name, rounds, warmup, reps=None):
+    """Create the workload's handle, run `warmup` rounds, time `rounds` rounds
+    with HIP events on the handle's stream, then profile one more pass
+    (launch counts per kernel class) and time every kernel class over a graph
+    of back-to-back launches of it."""
     import torch
     import cases
     from paper_1903_05133_amd import HierAvg
 
-    c = cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0)
-    P, K1, K2, B = c["P"], c["K1"], c["K2"], c["B"]
-    IN, H, C = c["IN"], c["H"], c["C"]
+    wl, P, S, K1, K2, B, lr, _ = WORKLOADS[name]
+    c = cases.named(wl, P, S, K1, K2, B, lr, seed=0)
     h = HierAvg(config=cases.native_config(c))
     stream = torch.cuda.Stream()
     h.set_stream(stream)
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         h.round()
     h.sync()
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(rounds):
         h.round()
     end.record(stream)
     h.sync()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = start.elapsed_time(end)
-    log(f"[bench] mlp: {args.steps} rounds in {ms:.3f} ms (host wall {wall * 1e3:.3f} ms)")
-
-    # Second timed pass with HIP events around every launch.
+    log(f"[bench] {name}: {rounds} rounds in {ms:.3f} ms (host wall {wall * 1e3:.3f} ms)")
+    # One more pass with HIP events around every launch: launch counts and
+    # time shares per kernel class.
     h.profile(True)
-    start.record(stream)
-    for _ in range(args.steps):
-        h.round()
-    end.record(stream)
+    h.round()
     stats = h.profile_read()
     h.profile(False)
-    torch.cuda.synchronize()
-    ms_prof = start.elapsed_time(end)
-    # Per-launch durations: every kernel class of the round timed over 200
-    # back-to-back launches between two HIP events on the handle's stream (the
-    # event pair adds a few microseconds to a single launch; here it is spread
-    # over 200).  This changes the replicas, so it comes last.
-    dur_ms = {name: h.time_kernel(name, 200) for name in stats if name != "draw_indices"}
+    h.sync()
+    # Per-launch durations: each kernel class over a graph of back-to-back
+    # launches between two HIP events on the handle's stream (spreads the
+    # events' own cost).  This changes the replicas, so it comes last.
+    if reps is None:
+        reps = 200 if ms / rounds < 5.0 else 20
+    dur_ms = {k: h.time_kernel(k, reps) for k in stats if k != "draw_indices"}
     h.close()
+    torch.cuda.empty_cache()
+    return c, ms / rounds, stats, dur_ms
 
-    work = mlp_kernel_work(P, c["S"], K1, K2, B, IN, H, C)
-    D = H * IN + H + C * H + C
-    work["group_mean"] = (mean_bytes(P, D), P * D)
-    work["global_mean"] = (mean_bytes(P, D), P * D)
-    work["tail_group_mean"] = (mean_bytes(P, D - H * IN), P * (D - H * IN))
-    work["tail_global_mean"] = (mean_bytes(P, D - H * IN), P * (D - H * IN))
+
+def summarize(name, c, ms_round, stats, dur_ms):
+    """Per-config record: round time, learner-steps/s, launches, the
+    method's algorithmic flops and bytes per round as fractions of the peaks,
+    and every kernel class with its measured duration and roofline."""
+    P, K1, K2 = c["P"], c["K1"], c["K2"]
+    work = kernel_work(c)
     kernels = {}
-    for name, (n, tot) in stats.items():
-        avg = dur_ms.get(name, tot / n)
-        b, fl = work.get(name, (0, 0))
-        kernels[name] = {"launches": n, "avg_us": round(avg * 1e3, 3), "share": None, "GBps": round(b / (avg * 1e-3) / 1e9, 1) if b else None,
-                         "TFLOPs": round(fl / (avg * 1e-3) / 1e12, 2) if fl else None}
     total = sum(t for _, t in stats.values())
-    for name, (n, tot) in stats.items():
-        kernels[name]["share"] = round(tot / total, 4)
-    # the dominant kernel among those with a stated algorithmic work
-    dom = max((k for k in dur_ms if k in work), key=lambda k: dur_ms[k] * stats[k][0])
+    for k, (n, tot) in stats.items():
+        avg = dur_ms.get(k, tot / n)
+        b, fl = work.get(k, (0, 0))
+        kernels[k] = {"launches": n, "avg_us": round(avg * 1e3, 3), "share": round(tot / total, 4),
+                      "GBps": round(b / (avg * 1e-3) / 1e9, 1) if b else None,
+                      "TFLOPs": round(fl / (avg * 1e-3) / 1e12, 2) if fl else None,
+                      "mfma_frac": round(fl / (avg * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4) if fl else None,
+                      "hbm_frac": round(b / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if b else None}
+    launches = sum(n for n, _ in stats.values())
+    out = {"workload": name, "P": P, "S": c["S"], "K1": K1, "K2": K2, "ms_per_round": round(ms_round, 5),
+           "us_per_round": round(ms_round * 1e3, 2), "launches_per_round": launches,
+           "launches_per_step": round(launches / (K1 * K2), 2), "kernels": kernels}
+    if c["kind"] == "averaging":
+        round_bytes = sum(n * work.get(k, (0, 0))[0] for k, (n, _) in stats.items())
+        out.update({"D": c["IN"], "momentum": c["momentum"], "lr": c["lr"], "alg_bytes_per_round": round_bytes,
+                    "round_GBps": round(round_bytes / (ms_round * 1e-3) / 1e9, 1)})
+        out["round_frac"] = round(out["round_GBps"] / HBM_PEAK_GBS, 4)
+        return out
+    fl, by = step_work(c)
+    steps = P * K1 * K2
+    out.update({"B": c["B"], "lr": c["lr"], "N": c["N"], "learner_steps_per_round": steps,
+                "learner_steps_per_s": round(steps / (ms_round * 1e-3), 1),
+                "schedule": "delayed" if "fwd1_block_gemm" in stats else "eager",
+                "round_mfma_frac": round(steps * fl / (ms_round * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
+                "round_alg_bytes_frac": round(steps * by / (ms_round * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+    return out
+
+
+def roofline(c, stats, dur_ms):
+    """The dominant kernel (largest launches x duration among the kernels
+    with a stated algorithmic work) against the peak of the resource whose
+    ideal time for that work is longer."""
+    work = kernel_work(c)
+    dom = max((k for k in dur_ms if work.get(k, (0, 0))[1] or work.get(k, (0, 0))[0]),
+              key=lambda k: dur_ms[k] * stats[k][0])
     avg_s = dur_ms[dom] * 1e-3
     b, fl = work[dom]
-    traffic = counter_traffic(dom)
-    # The bound is the resource whose ideal time for the kernel's algorithmic
-    # work is longer: HBM bytes at 8 TB/s or fp32 MFMA flops at 157.3 TFLOP/s.
-    mfma_bound = fl / (FP32_MFMA_PEAK_TFLOPS * 1e12) > b / (HBM_PEAK_GBS * 1e9)
-    if mfma_bound:
+    if fl / (FP32_MFMA_PEAK_TFLOPS * 1e12) > b / (HBM_PEAK_GBS * 1e9):
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(fl / avg_s / 1e12, 2),
                 "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(fl / avg_s / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)}
     else:
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(b / avg_s / 1e9, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(b / avg_s / 1e9 / HBM_PEAK_GBS, 4)}
-    roof.update({"traffic": None if traffic is None else round(traffic),
-                 "alg_bytes_per_launch": b, "alg_flops_per_launch": fl, "avg_us": round(avg_s * 1e6, 3),
+    tr = source_record("traffic.json", HEADLINE, dom)
+    mu = source_record("mfma.json", HEADLINE, dom)
+    roof.update({"traffic": None if tr is None else round(tr["bytes"]),
+                 "alg_bytes_per_launch": round(b), "alg_flops_per_launch": fl, "avg_us": round(avg_s * 1e6, 3),
                  "hbm_frac": round(b / avg_s / 1e9 / HBM_PEAK_GBS, 4),
-                 "mfma_frac": round(fl / avg_s / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4) if fl else None})
-    mu = counter_mfma_util(dom)
-    roof["mfma_util_counter"] = None if mu is None else round(mu, 4)
-    steps_per_round = P * K1 * K2
-    return {
-        "value": steps_per_round * args.steps / (ms * 1e-3),
-        "ms_per_step": ms / args.steps,
-        "profiled_ms_per_step": ms_prof / args.steps,
-        "config": {"workload": "mlp_3072_512_10", "P": P, "S": c["S"], "K1": K1, "K2": K2, "B": B, "lr": c["lr"],
-                   "N": c["N"], "seed": c["seed"], "learner_steps_per_round": steps_per_round},
-        "roofline": roof,
-        "kernels": kernels,
-    }
-
-
-# ---------------------------------------------------------------- averaging-only
-def bench_averaging(args):
-    import torch
-    import cases
-    from paper_1903_05133_amd import HierAvg
-
-    c = cases.named("averaging_11_7M", 32, 4, 1, 4, 1, 0.1, seed=0)
-    P, D = c["P"], c["IN"]
-    h = HierAvg(config=cases.native_config(c))
-    stream = torch.cuda.Stream()
-    h.set_stream(stream)
-    for _ in range(2):
-        h.round()
-    h.sync()
-    rounds = args.avg_rounds
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(rounds):
-        h.round()
-    end.record(stream)
-    h.sync()
-    ms = start.elapsed_time(end)
-    h.profile(True)
-    for _ in range(rounds):
-        h.round()
-    stats = h.profile_read()
-    h.profile(False)
-    dur_ms = {name: h.time_kernel(name, 20) for name in stats}
-    h.close()
-    per_launch = 20 * P * D  # read w, v, g; write w, v
-    out = {"config": {"workload": "averaging_11_7M", "P": P, "S": c["S"], "K1": c["K1"], "K2": c["K2"], "D": D,
-                      "momentum": c["momentum"], "lr": c["lr"]},
-           "ms_per_round": ms / rounds, "alg_bytes_per_launch": per_launch, "kernels": {}}
-    for name, (n, tot) in stats.items():
-        avg_s = dur_ms[name] * 1e-3
-        gbs = per_launch / avg_s / 1e9
-        out["kernels"][name] = {"launches": n, "avg_us": round(avg_s * 1e6, 2), "GBps": round(gbs, 1),
-                                "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    round_bytes = per_launch * c["K1"] * c["K2"]
-    out["round_GBps"] = round(round_bytes / (ms / rounds * 1e-3) / 1e9, 1)
-    out["round_frac"] = round(out["round_GBps"] / HBM_PEAK_GBS, 4)
-    return out
+                 "mfma_frac": round(fl / avg_s / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4) if fl else None,
+                 "mfma_util_counter": None if mu is None else round(mu["mfma_util"], 4)})
+    return roof
 
 
 # ---------------------------------------------------------------- CPU oracle
 def cpu_baseline():
+    """The oracle (float64 numpy, as it stands) on a sample of the headline
+    workload: the first SGD step of all 16 learners (16 learner-steps; the
+    state and data generator set up untimed), with numpy's BLAS on every core
+    of this process's affinity set, then one learner's next step with BLAS
+    limited to one thread."""
     import cases
     from oracle import method as M
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    c = cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0)
+    from threadpoolctl import threadpool_info, threadpool_limits
+    cores = len(os.sched_getaffinity(0))
+    blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    wl, P, S, K1, K2, B, lr, _ = WORKLOADS[HEADLINE]
+    c = cases.named(wl, P, S, K1, K2, B, lr, seed=0)
     prob = cases.oracle_problem(c)
-    # whole rounds of the timed workload until about 10 s of CPU work (at most 8)
     st = M.create(prob)
     data = M.Dataset(prob)
-    rounds = 0
     t0 = time.perf_counter()
-    while rounds < 8 and (rounds == 0 or time.perf_counter() - t0 < 10.0):
-        M.hieravg_round(prob, st, data)
-        rounds += 1
+    M.sgd_step_all(prob, data, st)
     dt = time.perf_counter() - t0
-    steps = rounds * c["P"] * c["K1"] * c["K2"]
-    return {"value": round(steps / dt, 2), "unit": "learner-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{rounds} round{'s' if rounds > 1 else ''} of mlp_3072_512_10 (P=16 S=4 K1=4 K2=4 B=32): {steps} learner-steps "
-                      f"in {dt:.2f} s, float64 numpy"}
+    with threadpool_limits(1):
+        t1 = time.perf_counter()
+        M.learner_step(prob, data, st, 0)
+        dt1 = time.perf_counter() - t1
+    return {"value": round(P / dt, 3), "unit": "learner-steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"first SGD step of all {P} learners of {HEADLINE} (P=16 S=4 K1=4 K2=2 B=32): {P} "
+                      f"learner-steps in {dt:.2f} s, float64 numpy, BLAS threads {blas}; the cluster and global "
+                      f"means are not in the sample",
+            "blas_threads": blas,
+            "value_1thread": round(1.0 / dt1, 4),
+            "sample_1thread": f"learner 0's second SGD step, BLAS limited to 1 thread: {dt1:.2f} s"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--avg-rounds", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=20, help="timed rounds of the headline workload")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--only", default=None, help="time only these workloads, comma-separated (profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-averaging", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first copy a 1 GiB tensor 3 times (a plain copy kernel of known bytes for counter runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Hier-AVG learners are rows of one replica array on a single "
@@ -287,34 +318,58 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
 
-    res = bench_mlp(args)
-    log(f"[bench] mlp done: {res['value']:.0f} learner-steps/s, {res['ms_per_step']:.4f} ms/round")
-    avg = None if args.no_averaging else bench_averaging(args)
-    if avg:
-        log(f"[bench] averaging done: {avg['round_GBps']} GB/s per round")
-    cpu = None if args.no_cpu_baseline else cpu_baseline()
+    configs = {}
+    head = None
+    for name, spec in WORKLOADS.items():
+        if args.only and name not in args.only.split(","):
+            continue
+        if name == HEADLINE:
+            c, ms, stats, dur = run_workload(name, args.steps, args.warmup)
+            head = (c, ms, stats, dur)
+        else:
+            c, ms, stats, dur = run_workload(name, spec[7], 5)
+            configs[name] = summarize(name, c, ms, stats, dur)
+        log(f"[bench] {name} done: {ms:.4f} ms/round")
+    cpu = None if (args.no_cpu_baseline or args.only) else cpu_baseline()
     if cpu:
-        log(f"[bench] cpu baseline done: {cpu['value']} learner-steps/s on {cpu['cores']} threads")
+        log(f"[bench] cpu baseline done: {cpu['value']} learner-steps/s on {cpu['cores']} cores")
+    if head is None:
+        print(json.dumps({"configs": configs}), flush=True)
+        return
+    c, ms, stats, dur = head
+    summ = summarize(HEADLINE, c, ms, stats, dur)
     line = {
         "metric": "learner-SGD-steps/sec and averaging HBM GB/s (frac of peak), 1 MI355X",
-        "value": round(res["value"], 1),
+        "value": summ["learner_steps_per_s"],
         "unit": "learner-steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(res["ms_per_step"], 5),
+        "ms_per_step": round(ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": res["config"],
-        "roofline": res["roofline"],
+        "config": {"workload": HEADLINE, "P": c["P"], "S": c["S"], "K1": c["K1"], "K2": c["K2"], "B": c["B"],
+                   "lr": c["lr"], "N": c["N"], "seed": c["seed"], "learner_steps_per_round": summ["learner_steps_per_round"],
+                   "schedule": summ["schedule"]},
+        "roofline": roofline(c, stats, dur),
         "cpu_baseline": cpu,
-        "averaging": avg,
-        "profiled_ms_per_step": round(res["profiled_ms_per_step"], 5),
-        "kernels": res["kernels"],
+        "round_mfma_frac": summ["round_mfma_frac"],
+        "round_alg_bytes_frac": summ["round_alg_bytes_frac"],
+        "launches_per_round": summ["launches_per_round"],
+        "kernels": summ["kernels"],
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
 

@@ -53,7 +53,7 @@ const char* kClassNames[KC_COUNT] = {
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
-    "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean"};
+    "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -82,6 +82,7 @@ struct hieravg {
   float* W = nullptr;    // [P][Dp] replicas
   float* V = nullptr;    // [P][Dp] momentum buffers (momentum > 0, or the averaging kind)
   float* Gr = nullptr;   // [K1*K2][P][Dp] given gradients (averaging kind)
+  float* Wm = nullptr;   // [Dp] averaging kind: every learner's parameters after a global mean
   float* X = nullptr;    // [N][INp] dataset
   int32_t* y = nullptr;  // [N] labels
   int32_t* idx = nullptr;  // [K2][K1][P][B] indices of the current round
@@ -98,7 +99,9 @@ struct hieravg {
   uint64_t key_index = 0;
   int KS1 = 1, cps1 = 1, KS2 = 1, cps2 = 1;
   int Bmax = 0;             // minibatch size at create: the buffers' capacity
-  bool rows_stale = false;  // replicas 1..P-1 hold an old W1 (after a delayed round)
+  bool rows_stale = false;  // replicas 1..P-1 hold an old W1 (after a delayed round);
+                            // averaging kind: every row is old, Wm holds the parameters
+  bool in_shared = false;   // averaging kind: the round being enqueued starts from Wm
   bool fused = false;       // the fused step kernel applies (SG = 1)
   bool fused_mean = false;  // ... and also with the cluster mean (SG = S)
   int KS_step = 1, KS_mean = 1;  // forward splits written by the fused kernel
@@ -170,7 +173,7 @@ void run(hieravg* h, int kc, F&& fn) {
 void release(hieravg* h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
-  void* bufs[] = {h->W,  h->V,  h->Gr, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
+  void* bufs[] = {h->W,  h->V,  h->Gr, h->Wm, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
@@ -330,8 +333,11 @@ int build(hieravg* h) {
     if ((rc = alloc_zero(h, (void**)&h->V, sizeof(float) * P * h->Dp, "momentum buffers"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->Gr, sizeof(float) * (size_t)T * P * h->Dp, "given gradients"))) return rc;
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
+    if ((rc = alloc_zero(h, (void**)&h->Wm, sizeof(float) * h->Dp, "common parameters"))) return rc;
     launch_init_vector(h->stream, h->W, h->D, hash64(seed, kTagInit), c.init_std);
     launch_gen_grads(h->stream, h->Gr, h->D, h->Dp, P, T, hash64(seed, kTagGrad), c.grad_std);
+    // Every learner starts from w~_1: the first round reads it from Wm.
+    HAV_CHECK(hipMemcpyAsync(h->Wm, h->W, sizeof(float) * h->Dp, hipMemcpyDeviceToDevice, h->stream));
   } else {
     const bool mlp = c.kind == HIERAVG_KIND_MLP;
     h->IN = c.in_dim;
@@ -441,6 +447,17 @@ void with_momentum(const hieravg* h, UpdArgs& u, int64_t off, int64_t boff) {
   }
 }
 
+// Averaging kind: the launch class of step tt of a round (the heavy-ball step
+// alone, with the cluster mean at the end of a block, or with the global mean
+// at the end of the round).
+int avg_step_mean(const hieravg* h, int tt) {
+  const hieravg_config& c = h->cfg;
+  const bool end_round = tt == h->T - 1, end_block = (tt + 1) % c.K1 == 0;
+  if (end_round && c.P > 1) return KC_MOMENTUM_GLOBAL;
+  if (end_block && !end_round && c.S > 1) return KC_MOMENTUM_GROUP;
+  return KC_MOMENTUM;
+}
+
 // The single kernel launch of class `kc` for step tt of the current round
 // (tt selects the step's sample indices, or the averaging workload's given
 // gradients).  Returns false for a class this workload does not launch.
@@ -458,9 +475,17 @@ bool launch_class(hieravg* h, int kc, int tt) {
       case KC_MOMENTUM_GROUP:
         launch_momentum_step(s, W, h->V, g, h->Dp, P, S, true, h->hyper, c.momentum, c.weight_decay);
         return true;
-      case KC_MOMENTUM_GLOBAL:
-        launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, h->hyper, c.momentum, c.weight_decay);
+      case KC_MOMENTUM_GLOBAL:  // every learner shares the result: it goes to Wm once
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, P, true, h->hyper, c.momentum, c.weight_decay, nullptr,
+                             h->Wm);
         return true;
+      case KC_MOMENTUM_FIRST: {  // the round's first step, every learner starting from Wm
+        if (!h->in_shared) return false;
+        const int v = avg_step_mean(h, 0);
+        launch_momentum_step(s, W, h->V, g, h->Dp, P, v == KC_MOMENTUM_GLOBAL ? P : S, v != KC_MOMENTUM, h->hyper,
+                             c.momentum, c.weight_decay, h->Wm, h->Wm);
+        return true;
+      }
       case KC_VMEAN_GROUP:
       case KC_VMEAN_GLOBAL: launch_group_mean(s, h->V, h->Dp, h->Dp, P, kc == KC_VMEAN_GROUP ? S : P); return true;
       default: return false;
@@ -845,14 +870,12 @@ void enqueue_round(hieravg* h) {
   const int T = h->T;
   const int P = c.P, S = c.S;
   if (c.kind == HIERAVG_KIND_AVERAGING) {
+    // The first step reads every learner's parameters from Wm when the round
+    // starts from a common value; the global mean writes Wm.
     for (int tt = 0; tt < T; ++tt) {
-      const bool end_round = tt == T - 1, end_block = (tt + 1) % c.K1 == 0;
-      int kc = KC_MOMENTUM;
-      if (end_round && P > 1)
-        kc = KC_MOMENTUM_GLOBAL;
-      else if (end_block && !end_round && S > 1)
-        kc = KC_MOMENTUM_GROUP;
-      run(h, kc, [&] { launch_class(h, kc, tt); });
+      const int kc = avg_step_mean(h, tt);
+      const int lk = tt == 0 && h->in_shared ? KC_MOMENTUM_FIRST : kc;
+      run(h, lk, [&] { launch_class(h, lk, tt); });
       if (c.avg_momentum && kc != KC_MOMENTUM) {
         const int vk = kc == KC_MOMENTUM_GLOBAL ? KC_VMEAN_GLOBAL : KC_VMEAN_GROUP;
         run(h, vk, [&] { launch_class(h, vk, tt); });
@@ -1079,9 +1102,12 @@ int hieravg_round(hieravg_t h) {
     set_error("NULL handle");
     return HIERAVG_EINVAL;
   }
-  // Delayed updates need every learner to start the round from replica 0's W1.
+  const bool avg = h->cfg.kind == HIERAVG_KIND_AVERAGING;
+  // Delayed updates need every learner to start the round from replica 0's
+  // W1; the averaging kind starts from Wm when the learners share it.
   h->in_delayed = h->delayed && h->w1_shared;
-  if (!h->in_delayed && h->rows_stale) {
+  h->in_shared = avg && h->w1_shared;
+  if (!avg && !h->in_delayed && h->rows_stale) {
     // An eager round reads every replica's W1: copy replica 0's to the others.
     const size_t w1 = sizeof(float) * h->Hp * h->INp;
     for (int p = 1; p < h->cfg.P; ++p)
@@ -1092,7 +1118,7 @@ int hieravg_round(hieravg_t h) {
   if (h->profiling) {
     enqueue_round(h);
   } else {
-    hipGraphExec_t& exec = h->round_exec[h->in_delayed ? 1 : 0];
+    hipGraphExec_t& exec = h->round_exec[h->in_delayed || h->in_shared ? 1 : 0];
     if (!exec) {
       HAV_CHECK(hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
       enqueue_round(h);
@@ -1110,7 +1136,13 @@ int hieravg_round(hieravg_t h) {
   }
   HAV_CHECK(hipGetLastError());
   // After the global mean every learner holds replica 0's W1 (under delayed
-  // updates only replica 0's copy is written).
+  // updates only replica 0's copy is written); averaging kind: Wm holds every
+  // learner's parameters (with P = 1 the round's last step writes row 0).
+  if (avg && h->cfg.P > 1) {
+    h->rows_stale = true;
+  } else if (avg) {
+    HAV_CHECK(hipMemcpyAsync(h->Wm, h->W, sizeof(float) * h->Dp, hipMemcpyDeviceToDevice, h->stream));
+  }
   h->w1_shared = true;
   if (h->in_delayed) h->rows_stale = true;
   h->steps += h->T;
@@ -1277,11 +1309,13 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {
   for (int p = 0; p < P; ++p)
     for (size_t i = 0; i < segs.size(); ++i) {
       const Segment& g = segs[i];
-      // After delayed updates only replica 0 holds the (common) W1.
-      const int64_t src_row = (i == 0 && h->rows_stale) ? 0 : p;
-      HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols,
-                                 h->W + src_row * h->Dp + g.src_off, sizeof(float) * g.src_ld,
-                                 sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
+      // After delayed updates only replica 0 holds the (common) W1; after an
+      // averaging-kind round Wm holds every learner's parameters.
+      const float* src = h->W + (int64_t)p * h->Dp;
+      if (i == 0 && h->rows_stale) src = h->cfg.kind == HIERAVG_KIND_AVERAGING ? h->Wm : h->W;
+      HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols, src + g.src_off,
+                                 sizeof(float) * g.src_ld, sizeof(float) * g.cols, g.rows, hipMemcpyDefault,
+                                 h->stream));
     }
   HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
@@ -1305,15 +1339,20 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
   h->w1_shared = false;  // unless every row's W1 equals row 0's (a round-boundary checkpoint)
   h->rows_stale = false;
-  if (h->cfg.kind == HIERAVG_KIND_MLP) {
+  const bool avg = h->cfg.kind == HIERAVG_KIND_AVERAGING;
+  if (h->cfg.kind == HIERAVG_KIND_MLP || avg) {
+    // MLP: equal W1 rows allow delayed updates; averaging kind: equal rows
+    // let the next round start from Wm.
     if (!h->flag) HAV_CHECK(hipMalloc((void**)&h->flag, sizeof(int)));
     HAV_CHECK(hipMemsetAsync(h->flag, 0, sizeof(int), h->stream));
-    launch_rows_differ(h->stream, h->W + h->off_W1, h->Dp, h->Hp * h->INp, P, h->flag);
+    launch_rows_differ(h->stream, h->W + h->off_W1, h->Dp, avg ? h->Dp : h->Hp * h->INp, P, h->flag);
     HAV_CHECK(hipGetLastError());
     int differ = 0;
     HAV_CHECK(hipMemcpyAsync(&differ, h->flag, sizeof(int), hipMemcpyDeviceToHost, h->stream));
     HAV_CHECK(hipStreamSynchronize(h->stream));
     h->w1_shared = differ == 0;
+    if (avg && h->w1_shared)
+      HAV_CHECK(hipMemcpyAsync(h->Wm, h->W, sizeof(float) * h->Dp, hipMemcpyDeviceToDevice, h->stream));
   }
   HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;
@@ -1384,7 +1423,12 @@ int hieravg_check_finite(hieravg_t h) {
   }
   if (!h->flag) HAV_CHECK(hipMalloc((void**)&h->flag, sizeof(int)));
   HAV_CHECK(hipMemsetAsync(h->flag, 0, sizeof(int), h->stream));
-  launch_any_nonfinite(h->stream, h->W, (int64_t)h->cfg.P * h->Dp, h->flag);
+  // After a round every learner's parameters are replica 0's (Wm for the
+  // averaging kind); the other rows may hold older values.
+  if (h->rows_stale)
+    launch_any_nonfinite(h->stream, h->cfg.kind == HIERAVG_KIND_AVERAGING ? h->Wm : h->W, h->Dp, h->flag);
+  else
+    launch_any_nonfinite(h->stream, h->W, (int64_t)h->cfg.P * h->Dp, h->flag);
   HAV_CHECK(hipGetLastError());
   int bad = 0;
   HAV_CHECK(hipMemcpyAsync(&bad, h->flag, sizeof(int), hipMemcpyDeviceToHost, h->stream));

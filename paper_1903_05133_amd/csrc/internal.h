@@ -113,6 +113,7 @@ enum KernelClass {
   KC_Z1_DELAYED,     // delayed updates, more than 32 classes: pre-activations with the Gram correction
   KC_VMEAN_GROUP,    // averaged momentum buffers: cluster mean of v
   KC_VMEAN_GLOBAL,   // averaged momentum buffers: global mean of v
+  KC_MOMENTUM_FIRST, // averaging kind: a round's first step, from the stored global mean
   KC_COUNT
 };
 
@@ -366,7 +367,14 @@ void launch_mean_rows(hipStream_t s, float* dst, const float* src, int64_t pitch
 void launch_rows_differ(hipStream_t s, const float* W, int64_t pitch, int64_t len, int n, int* flag);
 // flag = 1 if any of the n floats at W is inf or NaN (n a multiple of 4).
 void launch_any_nonfinite(hipStream_t s, const float* W, int64_t n, int* flag);
+// Heavy-ball step of every learner on its given gradient, optionally followed
+// by the mean over each cluster of S rows (average).  shared_in (optional,
+// Dp floats): every learner's parameters are read from this vector instead of
+// its row (after a global mean they are the same); mean_out (optional, Dp
+// floats, S = P): the global mean goes there instead of to the P rows.  The
+// two never alias the rows.
 void launch_momentum_step(hipStream_t s, float* W, float* V, const float* Gr, int64_t Dp, int P, int S,
-                          bool average, const float* lr, float mu, float wd);
+                          bool average, const float* lr, float mu, float wd, const float* shared_in = nullptr,
+                          float* mean_out = nullptr);
 
 }  // namespace hav

@@ -128,6 +128,7 @@ def branch_parity(prob, got, want, monitor, rerun, max_runs=MAX_BRANCH_RUNS):
             ok2, det2 = parity_report(prob, got, rerun(frozenset(d[:4] for d in subset)))
             if ok2:
                 det2["flipped"] = list(subset)
+                det2["candidates"] = cands
                 det2["unflipped_worst"] = det["worst"]
                 return True, det2
     return False, det

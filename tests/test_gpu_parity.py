@@ -200,6 +200,41 @@ def test_named_averaging_workload_sampled(gpu_lib):
     assert err <= TOL
 
 
+def test_averaging_stored_mean_and_rows_that_differ(gpu_lib):
+    """Averaging kind: the global mean is stored once and the next round's
+    first step reads it (profile: momentum_first_step); after set_params with
+    rows that differ the first step reads every row (no first-step class),
+    with equal rows it reads the stored value again.  Parameters and buffers
+    against the oracle continuing from the same state, round by round."""
+    from paper_1903_05133_amd import HierAvg
+    c = cases.case("averaging", 8, 4, 1, 3, IN=1003, lr=0.1, momentum=0.9, seed=37)
+    prob = cases.oracle_problem(c)
+    st = M.create(prob)
+    with HierAvg(config=cases.native_config(c)) as h:
+        for r, edit in enumerate([None, "differ", "equal", None]):
+            if edit is not None:
+                w = h.params()
+                if edit == "differ":
+                    w[3] += np.float32(0.25)
+                else:
+                    w[:] = w[5]
+                h.set_params(w)
+                st.W = w.astype(np.float64)
+            h.profile(True)
+            h.round()
+            stats = h.profile_read()
+            h.profile(False)
+            M.hieravg_round(prob, st)
+            got, vgot = h.params(), h.momentum()
+            first = "momentum_first_step" in stats
+            assert first == (edit != "differ"), (r, edit, stats)
+            assert stats["momentum_global_mean"][0] == 1 and h.finite()
+            for arr, want in ((got, st.W), (vgot, st.V)):
+                ok, det = cases.parity_report(prob, arr, want)
+                print(f"[gpu case] averaging round {r} ({edit}) worst {det['worst']}", flush=True)
+                assert ok, det
+
+
 @pytest.mark.slow
 def test_named_large_mlp_workload(gpu_lib):
     """MLP 150528 -> 1024 -> 1000, N = 100000, at its full dimensions on the
