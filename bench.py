@@ -83,18 +83,24 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
     mean over the K2 blocks of a round."""
     G = P // S
     pairs = K1 * (K1 - 1) // 2
-    tail = H + C * H + C  # b1, W2, b2: their cluster (global) mean rides in the block update (W1 mean)
+    tail = H + C * H + C  # b1, W2, b2: their cluster (global) mean rides in the block update
     bases = (1 + (K2 - 1) * G) / K2          # W1 bases read per block, mean over the blocks
-    tail_means = (K2 - 1) / K2 if S > 1 else 0.0  # blocks whose update also takes the tail's cluster mean
     k_avg = (K1 - 1) / 2.0                   # earlier steps corrected per step, mean over a block
+    # block update, per block b: its bases read (replica 0's W1 for b = 0, the
+    # G cluster copies after), its result written (G copies; the last block:
+    # the global mean, once), the block's errors and minibatch rows read, and
+    # the cluster (last block: global) mean of b1, W2, b2 read and written
+    upd = 0.0
+    for b in range(K2):
+        last = b == K2 - 1
+        upd += (1 if b == 0 else G) * H * IN + (1 if last else G) * H * IN + K1 * P * B * (H + IN)
+        upd += 2 * P * tail if (P > 1 if last else S > 1) else 0
+    upd /= K2
     return {
         # forward of a block's K1 steps from the block-start bases: the bases,
         # the K1*P minibatches, the K1*P pre-activation blocks
         "fwd1_block_gemm": (F * (bases * H * IN + K1 * P * B * IN + K1 * P * B * H), K1 * P * 2 * B * H * IN),
-        # block end: the bases read once, G cluster copies written, the
-        # block's hidden errors and minibatch rows read, the tail's mean
-        "block_update_gemm": (F * (bases * H * IN + G * H * IN + K1 * P * B * (H + IN) + tail_means * 2 * P * tail),
-                              K1 * P * 2 * B * H * IN),
+        "block_update_gemm": (F * upd, K1 * P * 2 * B * H * IN),
         # Gram blocks of the round: every minibatch row read once, blocks written
         "gram": (F * (K2 * K1 * P * B * IN + K2 * P * pairs * B * B), K2 * P * pairs * 2 * B * B * IN),
         "w1_global_mean": (F * ((G + 1) * H * IN + 2 * P * tail), G * H * IN + P * tail),

@@ -108,6 +108,7 @@ struct hieravg {
   int ks_cur = 1;                // splits of the partials currently in `part`
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
+  bool global_last = false; // the last block's update takes the global mean (K1*P*B rows fit)
   bool w1_shared = true;   // every learner's W1 equals replica 0's (other rows may be stale)
   bool in_delayed = false; // the round being enqueued uses them
   int KS_b = 1, cps_b = 1; // splits of the block-wide forward
@@ -301,6 +302,10 @@ int64_t plan(hieravg* h, int B) {
     const bool cheap = (int64_t)(c.K1 - 1) * h->Bp * 2 <= h->Hp;
     h->delayed = c.update_mode == HIERAVG_UPDATE_DELAYED || (c.update_mode == HIERAVG_UPDATE_AUTO && cheap);
   }
+  // The last block's update over all P learners has one group of output
+  // tiles (64 x 128); with fewer than two per CU the G cluster updates and a
+  // separate mean of the copies fill the GPU better.
+  h->global_last = h->delayed && (int64_t)c.K1 * P * B <= kBlkMaxRows && (h->Hp / 64) * (h->INp / 128) >= 512;
   if (h->delayed) {
     // One GEMM per cluster and block: the K1*S minibatches against the copy.
     plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
@@ -506,6 +511,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
         tb.Mp = Bp;
         tb.ldg = h->Hp;
         tb.ldx = h->INp;
+        tb.K2 = c.K2;
+        tb.global_last = h->global_last;
       }
       launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, h->T, (uint64_t)h->N,
                           h->key_index, h->y, h->in_delayed ? h->ylab : nullptr, tb);
@@ -590,7 +597,22 @@ bool launch_class(hieravg* h, int kc, int tt) {
       BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
                 b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S,
                 h->btab + b * blk, h->btab + (int64_t)c.K2 * blk + b * blk};
-      if (b < c.K2 - 1 && S > 1) {  // the block-end cluster mean of b1, W2, b2 (the last block's is global)
+      if (b == c.K2 - 1 && h->global_last) {
+        // The last block: one update over all P learners from the mean of the
+        // cluster copies (the global mean of Algorithm 1, which skips the
+        // cluster mean before it), into replica 0's W1, and the global mean
+        // of b1, W2, b2.
+        a.SG = P;
+        a.lr_div = (float)P;
+        a.nbase = b == 0 ? 1 : P / S;
+        a.Wo = W + h->off_W1;
+        a.wo_pitch = 0;
+        if (P > 1) {
+          a.tail = W + h->off_b1;
+          a.tail_pitch = h->Dp;
+          a.tail_len = h->Dp - h->off_b1;
+        }
+      } else if (b < c.K2 - 1 && S > 1) {  // the block-end cluster mean of b1, W2, b2
         a.tail = W + h->off_b1;
         a.tail_pitch = h->Dp;
         a.tail_len = h->Dp - h->off_b1;
@@ -868,7 +890,7 @@ namespace {
 void enqueue_round(hieravg* h) {
   const hieravg_config& c = h->cfg;
   const int T = h->T;
-  const int P = c.P, S = c.S;
+  const int P = c.P;
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     // The first step reads every learner's parameters from Wm when the round
     // starts from a common value; the global mean writes Wm.
@@ -903,9 +925,11 @@ void enqueue_round(hieravg* h) {
         for (int k = 0; k < c.K1; ++k)
           for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2}) go(kc, b * c.K1 + k);
       }
-      go(KC_BLOCK_UPDATE, b * c.K1);  // with the cluster mean of b1, W2, b2 for b < K2 - 1
+      // with the cluster mean of b1, W2, b2 for b < K2 - 1; the last block's
+      // update takes the global mean of every block
+      go(KC_BLOCK_UPDATE, b * c.K1);
     }
-    go(KC_W1_MEAN, 0);  // with the global mean of b1, W2, b2
+    if (!h->global_last) go(KC_W1_MEAN, 0);  // with the global mean of b1, W2, b2
   } else {
     run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
     bool have_fwd = false;

@@ -154,11 +154,16 @@ void launch_iota(hipStream_t s, int32_t* dst, int n);
 // units of that row's hidden-error row (row (k*P + g*S + j)*Mp + s of pitch
 // ldg) and of its sample's dataset row (pitch ldx).  Rows R..Rp-1 of each
 // table (R = K1*S*B, Rp = R rounded up to 32) stay 0.
+// With global_last, the last block (b = K2-1) instead holds one table over
+// all P learners, row r = (k*P + j)*B + s at [(b*(P/S))*Rp + r], for the
+// block update that takes the global mean in the same launch.
 struct BlkTables {
   uint32_t* gtab = nullptr;
   uint32_t* xtab = nullptr;
   int K1 = 1, S = 1, Mp = 0, Rp = 0;
   int64_t ldg = 0, ldx = 0;
+  int K2 = 0;
+  bool global_last = false;
 };
 // ylab (optional): the label of every drawn sample, same layout as idx.
 // tables.gtab (optional): also write the block update's row tables.
@@ -246,6 +251,10 @@ struct BlkArgs {
   // block, which no other part of the launch touches.
   float* tail = nullptr;
   int64_t tail_pitch = 0, tail_len = 0;
+  // The base of a group is the mean of nbase blocks wb_pitch apart (added in
+  // order): the global update of the last block starts from the mean of the
+  // cluster copies.
+  int nbase = 1;
 };
 // Largest contraction (K1 * SG * B rows) of a block update.
 constexpr int kBlkMaxRows = 16384;

@@ -81,9 +81,11 @@ __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx,
     idx[e] = i;
     if (ylab) ylab[e] = labels[i];
     if (tb.gtab) {
-      // Row r = (k*S + learner-in-cluster)*B + s of cluster j/S in block tt/K1.
+      // Row r = (k*S + learner-in-cluster)*B + s of cluster j/S in block tt/K1
+      // (the last block with global_last: row (k*P + j)*B + s of one table).
       const int64_t b = tt / tb.K1, k = tt - b * tb.K1, g = j / tb.S, jc = j - g * tb.S;
-      const int64_t o = (b * (P / tb.S) + g) * tb.Rp + (k * tb.S + jc) * B + s;
+      const int64_t o = tb.global_last && b == tb.K2 - 1 ? b * (P / tb.S) * tb.Rp + (k * P + j) * B + s
+                                                         : (b * (P / tb.S) + g) * tb.Rp + (k * tb.S + jc) * B + s;
       tb.gtab[o] = (uint32_t)((((k * P + j) * tb.Mp + s) * tb.ldg) >> 6);
       tb.xtab[o] = (uint32_t)(((int64_t)i * tb.ldx) >> 6);
     }

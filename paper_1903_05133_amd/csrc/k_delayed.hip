@@ -343,12 +343,27 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
   const int xc4 = tid % kXP, xr0 = tid / kXP;
   const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
   const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
-  const float* Wb = a.Wb + (int64_t)g * a.wb_pitch;
+  const float* Wb = a.Wb + (int64_t)g * a.nbase * a.wb_pitch;
   f32x4 wv[kWL];
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {
     const int row = mrow0 + xr0 + kXR * i;
     wv[i] = *(const f32x4*)(Wb + (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
+  }
+  if (a.nbase > 1) {  // the mean of the bases, added in order
+    for (int c = 1; c < a.nbase; ++c) {
+      f32x4 v[kWL];
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) {
+        const int row = mrow0 + xr0 + kXR * i;
+        v[i] = *(const f32x4*)(Wb + (int64_t)c * a.wb_pitch +
+                               (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
+      }
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) wv[i] += v[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) wv[i] = wv[i] / (float)a.nbase;
   }
 #pragma unroll
   for (int r = 0; r < 16; ++r) {

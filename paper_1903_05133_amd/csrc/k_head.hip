@@ -153,6 +153,133 @@ __global__ __launch_bounds__(256) void k_bwd_hidden(const float* __restrict__ G2
   }
 }
 
+// The same product on the matrix cores: G1[p][m][h] = [Z1 > 0] * sum_c
+// G2[p][m][c] W2[p][c][h].  Workgroup (learner p, 32 samples, 32 hidden
+// units): wave w takes classes [16w, 16w + 16) of each 64-class chunk with
+// 32x32x2 MFMAs into its own 32x32 accumulator block.  Chunks are staged in
+// LDS (G2 transposed, class-major, so a wave's operand reads are consecutive
+// words), double-buffered, with two register sets so that the loads of chunk
+// c + 2 are in flight while chunk c is multiplied; the four partial blocks
+// are added in wave order through LDS.  Rows past M and classes past Cp read
+// as zero.  b1 (M <= 32 only): also the step b1[h] -= lr * sum_m G1[m][h].
+constexpr int kBhM = 32, kBhN = 32, kBhC = 64;
+constexpr int kBhLG = kBhM + 1, kBhLW = kBhN + 4;  // odd G2 stride: the transposing stores spread over the banks
+constexpr int kBhLds = 2 * kBhC * (kBhLG + kBhLW);
+__global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict__ G2, const float* __restrict__ W2,
+                                                         int64_t w_pitch, const float* __restrict__ Z1,
+                                                         float* __restrict__ G1, int M, int Mp, int Cp, int Hp,
+                                                         int htiles, int mtiles, float* __restrict__ b1,
+                                                         const float* __restrict__ lr_ptr) {
+  __shared__ __attribute__((aligned(16))) float lds[kBhLds];
+  // buffer b: G2 chunk [class][sample] at gsb(b), W2 chunk [class][unit] at wsb(b)
+  auto gsb = [&](int b) { return lds + b * (kBhC * kBhLG); };
+  auto wsb = [&](int b) { return lds + 2 * kBhC * kBhLG + b * (kBhC * kBhLW); };
+  const int ht = blockIdx.x % htiles;
+  const int mt = (blockIdx.x / htiles) % mtiles;
+  const int p = blockIdx.x / (htiles * mtiles);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int m0 = mt * kBhM, h0 = ht * kBhN;
+  const float* g2 = G2 + (int64_t)p * Mp * Cp;
+  const float* w2 = W2 + (int64_t)p * w_pitch;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  const int nch = (Cp + kBhC - 1) / kBhC;
+
+  // G2 pieces: q = tid + 256*i, sample q >> 4, classes 4*(q & 15) .. +3.
+  // W2 pieces: q = tid + 256*i, class q >> 3, units 4*(q & 7) .. +3.
+  f32x4 ga[2][2], wa[2][2];
+  auto load = [&](int c0, f32x4 (&g)[2], f32x4 (&w)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i, r = q >> 4, c = c0 + 4 * (q & 15);
+      const bool ok = m0 + r < M && c < Cp;
+      const f32x4 v = *(const f32x4*)(g2 + (ok ? (int64_t)(m0 + r) * Cp + c : 0));
+      g[i] = ok ? v : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i, c = c0 + (q >> 3);
+      const bool ok = c < Cp;
+      const f32x4 v = *(const f32x4*)(w2 + (ok ? (int64_t)c * Hp + h0 + 4 * (q & 7) : 0));
+      w[i] = ok ? v : zero4;
+    }
+  };
+  auto store = [&](int buf, const f32x4 (&g)[2], const f32x4 (&w)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i, r = q >> 4, c4 = 4 * (q & 15);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gsb(buf)[(c4 + j) * kBhLG + r] = g[i][j];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      *(f32x4*)&wsb(buf)[(q >> 3) * kBhLW + 4 * (q & 7)] = w[i];
+    }
+  };
+
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  load(0, ga[0], wa[0]);
+  if (nch > 1) load(kBhC, ga[1], wa[1]);
+  store(0, ga[0], wa[0]);
+  __syncthreads();
+  // Chunk ch sits in LDS buffer ch & 1; chunk ch + 1 is in register set
+  // (ch + 1) & 1 (loaded one iteration earlier); chunk ch + 2 goes into the
+  // register set that chunk ch used.
+  for (int ch = 0; ch < nch; ++ch) {
+    const int buf = ch & 1;
+    if (ch + 2 < nch) {
+      if (buf == 0)
+        load((ch + 2) * kBhC, ga[0], wa[0]);
+      else
+        load((ch + 2) * kBhC, ga[1], wa[1]);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // those loads go out before the MFMAs
+    const float* gb = gsb(buf);
+    const float* wb = wsb(buf);
+#pragma unroll
+    for (int ss = 0; ss < kBhC / 4; ss += 2) {
+      const int k = wave * (kBhC / 4) + ss + lhi;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(gb[k * kBhLG + l32], wb[k * kBhLW + l32], acc, 0, 0, 0);
+    }
+    if (ch + 1 < nch) {
+      if (buf == 0)
+        store(1, ga[1], wa[1]);
+      else
+        store(0, ga[0], wa[0]);
+    }
+    __syncthreads();
+  }
+  // Waves 1-3 hand their blocks to wave 0 through LDS ([3][32][33]).
+  if (wave > 0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      lds[((wave - 1) * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3)) * 33 + l32] = acc[r];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int h = h0 + l32;
+    float db = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 8 * (r >> 2) + 4 * lhi + (r & 3), m = m0 + row;
+      const float g = ((acc[r] + lds[row * 33 + l32]) + lds[(32 + row) * 33 + l32]) + lds[(64 + row) * 33 + l32];
+      if (m < M) {
+        const int64_t o = ((int64_t)p * Mp + m) * Hp + h;
+        const float g1 = Z1[o] > 0.0f ? g : 0.0f;
+        G1[o] = g1;
+        db += g1;
+      }
+    }
+    if (b1) {  // rows 0-3, 8-11, ... of lanes 0-31, then the other rows of lanes 32-63
+      const float other = __shfl_xor(db, 32, 64);
+      if (lhi == 0) b1[(int64_t)p * w_pitch + h] -= *lr_ptr * (db + other);
+    }
+  }
+}
+
 // Delayed-update pre-activations for the head with more than 32 classes
 // (Z1Args): workgroup (p, slice of 32 hidden units); the Gram correction as in
 // k_head_step (32x32x2 MFMAs over the earlier steps, split over the waves).
@@ -866,8 +993,14 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
 
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr) {
-  const int htiles = (Hp + 63) / 64;
-  launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles, b1, lr);
+  if (b1 && M > kBhM) {  // the b1 step needs every sample in one workgroup
+    const int htiles = (Hp + 63) / 64;
+    launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles, b1, lr);
+    return;
+  }
+  const int htiles = Hp / kBhN, mtiles = (M + kBhM - 1) / kBhM;
+  launch(k_bwd_hidden_mfma, (unsigned)((int64_t)P * mtiles * htiles), 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, Cp,
+         Hp, htiles, mtiles, b1, lr);
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,

@@ -385,7 +385,8 @@ def test_delayed_schedule_profile(gpu_lib):
         assert stats["fwd1_block_gemm"][0] == 3 and stats["head_step"][0] == 6 and stats["head_step_end"][0] == 3
         assert not {"head_a", "head_b"} & set(stats)
         assert stats["block_update_gemm"][0] == 3 and stats["gram"][0] == 1
-        # the means of b1, W2, b2 ride in the block update (cluster) and the W1 mean (global)
+        # the cluster means of b1, W2, b2 ride in the block updates, their
+        # global mean in the launch that averages the cluster copies of W1
         assert not {"tail_group_mean", "tail_global_mean"} & set(stats)
         assert stats["w1_global_mean"][0] == 1
         assert not {"fwd1_gemm", "update1_gemm", "step1_gemm", "global_mean"} & set(stats)
@@ -404,6 +405,34 @@ def test_delayed_schedule_profile(gpu_lib):
         h.profile(True)
         h.round()
         assert "fwd1_block_gemm" in h.profile_read() and "fwd1_gemm" not in h.profile_read()
+
+
+@pytest.mark.parametrize("name", ["fused_wide", "fused_one_block", "separate_many_rows"])
+def test_delayed_last_block_global_mean(name, gpu_lib):
+    """The last block's update over all P learners from the mean of the
+    cluster copies (the global mean of W1, b1, W2, b2 in the same launch)
+    where W1 has at least 512 output tiles (8192 inputs x 512 units; also
+    with one block per round, whose base is replica 0's W1, updated in
+    place); with more rows than one update takes (K1*P*B = 8*72*32 > 16384)
+    the last block updates the cluster copies and a separate launch averages
+    them."""
+    from paper_1903_05133_amd import HierAvg
+    c = {"fused_wide": cases.case("mlp", 4, 2, 2, 3, B=16, IN=8192, H=512, C=6, N=200, sigma=0.5, lr=0.05, seed=19),
+         "fused_one_block": cases.case("mlp", 4, 2, 3, 1, B=12, IN=8200, H=500, C=20, N=200, sigma=0.5, lr=0.05,
+                                       seed=20),
+         "separate_many_rows": cases.case("mlp", 72, 8, 8, 2, B=32, IN=64, H=64, C=5, N=500, sigma=0.5, lr=0.05,
+                                          seed=21)}[name]
+    with HierAvg(config=cases.native_config(c, "delayed")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+        h.profile(False)
+        h.round()
+        got = h.params()
+        idx = h.last_indices()
+    assert stats["block_update_gemm"][0] == c["K2"]
+    assert ("w1_global_mean" in stats) == (name == "separate_many_rows")
+    _check(c, got, idx, *_oracle(c, 2), mode="delayed")
 
 
 def test_unfused_schedule_profile(gpu_lib):
