@@ -316,6 +316,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB tensor 3 times (a plain copy kernel of known bytes for counter runs)")
+    ap.add_argument("--quick", action="store_true",
+                    help="counter runs: every workload times --steps rounds and 3 launches per kernel class")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Hier-AVG learners are rows of one replica array on a single "
@@ -338,11 +340,13 @@ def main():
     for name, spec in WORKLOADS.items():
         if args.only and name not in args.only.split(","):
             continue
+        reps = 3 if args.quick else None
         if name == HEADLINE:
-            c, ms, stats, dur = run_workload(name, args.steps, args.warmup)
+            c, ms, stats, dur = run_workload(name, args.steps, args.warmup, reps)
             head = (c, ms, stats, dur)
         else:
-            c, ms, stats, dur = run_workload(name, spec[7], 5)
+            c, ms, stats, dur = run_workload(name, args.steps if args.quick else spec[7], args.warmup if args.quick else 5,
+                                             reps)
             configs[name] = summarize(name, c, ms, stats, dur)
         log(f"[bench] {name} done: {ms:.4f} ms/round")
     cpu = None if (args.no_cpu_baseline or args.only) else cpu_baseline()
