@@ -66,11 +66,15 @@ typedef struct hieravg* hieravg_t;
  *           mean at the block end is one update of the copy by the summed
  *           G^T X of the cluster's learners and steps.  Needs the MLP with
  *           B <= 32, K1 <= 8, K1*S*B <= 16384, whole blocks (k_global a
- *           multiple of K1), a dataset under 2^38 floats, plain SGD
- *           (momentum = weight_decay = 0), and a round that starts with equal
- *           W1 in every replica (true after create, after every round, and
- *           after hieravg_set_params with equal W1 rows; otherwise that next
- *           round runs EAGER).
+ *           multiple of K1), a dataset under 2^38 floats, momentum buffers
+ *           that the means leave alone (avg_momentum = 0), and a round that
+ *           starts with equal W1 in every replica (true after create, after
+ *           every round, and after hieravg_set_params with equal W1 rows;
+ *           otherwise that next round runs EAGER).  With momentum or weight
+ *           decay the K1 heavy-ball steps of a block are linear in (W1, V1):
+ *           W1 and its buffer at step n are fixed multiples of the block-start
+ *           pair plus weighted sums of the step gradients, and the block end
+ *           applies those weights in the same cluster GEMM.
  *  AUTO:    DELAYED where it applies and its extra Gram products cost at most
  *           an eighth of the step's flops ((K1 - 1) * B <= H / 2), else EAGER.
  */

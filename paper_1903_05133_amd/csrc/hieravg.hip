@@ -53,7 +53,8 @@ const char* kClassNames[KC_COUNT] = {
     "momentum",     "momentum_group_mean",          "momentum_global_mean",        "step1_gemm",
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
-    "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step"};
+    "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step",
+    "fwd1_block_gemm_v", "scale_errors", "buffer_update_gemm"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -94,7 +95,8 @@ struct hieravg {
   uint64_t* ctr = nullptr;  // [0]: global step counter; [1]: workgroup counter of the draw
   int* flag = nullptr;       // result word of device-side checks
   int n_allocs = 0, fail_alloc = 0;  // allocation count of create; the forced failure (debug)
-  float* hyper = nullptr;   // [0]: step size lr read by the kernels (hieravg_set_lr)
+  float* hyper = nullptr;   // [0]: step size lr read by the kernels (hieravg_set_lr); the heavy-ball
+                            // coefficient table of the delayed schedule (internal.h)
 
   uint64_t key_index = 0;
   int KS1 = 1, cps1 = 1, KS2 = 1, cps2 = 1;
@@ -109,6 +111,14 @@ struct hieravg {
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
   bool global_last = false; // the last block's update takes the global mean (K1*P*B rows fit)
+  bool hb = false;          // delayed updates with momentum or weight decay (heavy-ball blocks)
+  int KSv = 1, cpsv = 1;    // splits of the block-wide forward from the learners' buffers
+  float* partv = nullptr;   // [KSv][K1][P][Bp][Hp] partials of X_k V^T (momentum > 0)
+  float* Gu = nullptr;      // [K1][P][Bp][Hp] errors scaled for the block-end parameter update
+  float* Gt = nullptr;      // [K1][P][Bp][Hp] errors scaled for the buffer update (momentum > 0)
+  float* Wc2 = nullptr;     // second set of cluster copies (heavy-ball: the block-start copies stay
+                            // intact for the buffer update)
+  uint32_t* btab1 = nullptr;  // per-learner row tables of the buffer update
   bool w1_shared = true;   // every learner's W1 equals replica 0's (other rows may be stale)
   bool in_delayed = false; // the round being enqueued uses them
   int KS_b = 1, cps_b = 1; // splits of the block-wide forward
@@ -176,6 +186,7 @@ void release(hieravg* h) {
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->Wm, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
+                  h->partv, h->Gu, h->Gt, h->Wc2, h->btab1,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -226,7 +237,30 @@ bool delayed_applies(const hieravg_config& c) {
   // units (a dataset below 2^38 floats).
   const bool rows_fit = (double)c.n_samples * (double)round_up(c.in_dim, 64) < 274877906944.0;
   return c.kind == HIERAVG_KIND_MLP && c.B <= 32 && c.K1 <= 8 && whole_blocks && rows_fit &&
-         (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows && c.momentum == 0.0f && c.weight_decay == 0.0f;
+         (int64_t)c.K1 * c.S * c.B <= kBlkMaxRows && c.avg_momentum == 0;
+}
+
+// Heavy-ball coefficient table (see internal.h) for step size lr, momentum
+// mu and decay wd over blocks of up to K1 steps: A^n and A^n e in double,
+// stored as float.
+void hb_table(float lr, float mu, float wd, int K1, float* hyper) {
+  const double g = lr, m = mu, l = wd;
+  double a00 = 1.0, a01 = 0.0, a10 = 0.0, a11 = 1.0;  // A^0
+  for (int n = 0; n <= K1 && n < kHbStride; ++n) {
+    hyper[hb_index(HB_P, n)] = (float)a00;
+    hyper[hb_index(HB_Q, n)] = (float)a01;
+    hyper[hb_index(HB_R, n)] = (float)a10;
+    hyper[hb_index(HB_S, n)] = (float)a11;
+    hyper[hb_index(HB_U, n)] = (float)(-g * a00 + a01);
+    hyper[hb_index(HB_T, n)] = (float)(-g * a10 + a11);
+    // A^(n+1) = A A^n with A = [[1 - g l, -g m], [l, m]]
+    const double b00 = (1.0 - g * l) * a00 - g * m * a10, b01 = (1.0 - g * l) * a01 - g * m * a11;
+    const double b10 = l * a00 + m * a10, b11 = l * a01 + m * a11;
+    a00 = b00;
+    a01 = b01;
+    a10 = b10;
+    a11 = b11;
+  }
 }
 
 int validate(const hieravg_config& c) {
@@ -250,8 +284,8 @@ int validate(const hieravg_config& c) {
   if (!std::isfinite(c.weight_decay) || c.weight_decay < 0.0f) return bad("weight_decay must be finite and >= 0");
   if (c.avg_momentum != 0 && c.avg_momentum != 1) return bad("avg_momentum must be 0 or 1");
   if (c.update_mode == HIERAVG_UPDATE_DELAYED && !delayed_applies(c))
-    return bad("delayed updates need the MLP with B <= 32, K1 <= 8, K1*S*B <= 16384, whole blocks and plain SGD "
-               "(no momentum or weight decay)");
+    return bad("delayed updates need the MLP with B <= 32, K1 <= 8, K1*S*B <= 16384, whole blocks and momentum "
+               "buffers that are not averaged (avg_momentum = 0)");
   if (c.kind == HIERAVG_KIND_AVERAGING) {
     if (c.in_dim < 1 || c.in_dim > (int64_t(1) << 36)) return bad("averaging: D must be in [1, 2^36]");
     if (!std::isfinite(c.init_std) || !std::isfinite(c.grad_std)) return bad("averaging: stds must be finite");
@@ -304,16 +338,34 @@ int64_t plan(hieravg* h, int B) {
   }
   // The last block's update over all P learners has one group of output
   // tiles (64 x 128); with fewer than two per CU the G cluster updates and a
-  // separate mean of the copies fill the GPU better.
-  h->global_last = h->delayed && (int64_t)c.K1 * P * B <= kBlkMaxRows && (h->Hp / 64) * (h->INp / 128) >= 512;
+  // separate mean of the copies fill the GPU better.  Heavy-ball blocks with
+  // one block per round keep the cluster updates: the buffers' update needs
+  // the block-start parameters, which the global update would overwrite.
+  h->hb = h->delayed && (c.momentum > 0.0f || c.weight_decay > 0.0f);
+  h->global_last = h->delayed && (int64_t)c.K1 * P * B <= kBlkMaxRows && (h->Hp / 64) * (h->INp / 128) >= 512 &&
+                   !(h->hb && c.K2 < 2);
   if (h->delayed) {
     // One GEMM per cluster and block: the K1*S minibatches against the copy.
     plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
                    HAV_FWD_BLOCK_TARGET);
     ks_max = std::max<int64_t>(ks_max, (int64_t)h->KS_b * c.K1);
+    // Heavy-ball with momentum: one more per learner, its K1 minibatches
+    // against its own buffer.
+    if (h->hb && c.momentum > 0.0f)
+      plan_split_blk(P, c.K1 * h->Bp, (int)h->Hp, (int)h->INp, &h->KSv, &h->cpsv, HAV_FWD_BLOCK_TARGET);
   }
   h->ks_cur = h->KS1;
   return std::max<int64_t>(ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);
+}
+
+// The step size and the heavy-ball coefficient table, to the device.
+hipError_t write_hyper(hieravg* h) {
+  float hyper[kHyperFloats] = {};
+  hyper[0] = h->cfg.lr;
+  hb_table(h->cfg.lr, h->cfg.momentum, h->cfg.weight_decay, std::min(h->cfg.K1, kHbStride - 1), hyper);
+  const hipError_t e = hipMemcpyAsync(h->hyper, hyper, sizeof(hyper), hipMemcpyHostToDevice, h->stream);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(h->stream);
 }
 
 int build(hieravg* h) {
@@ -323,8 +375,8 @@ int build(hieravg* h) {
   h->stream = h->own_stream;
   {
     int rc;
-    if ((rc = alloc_zero(h, (void**)&h->hyper, 4 * sizeof(float), "hyperparameters"))) return rc;
-    HAV_CHECK(hipMemcpyAsync(h->hyper, &c.lr, sizeof(float), hipMemcpyHostToDevice, h->stream));
+    if ((rc = alloc_zero(h, (void**)&h->hyper, kHyperFloats * sizeof(float), "hyperparameters"))) return rc;
+    HAV_CHECK(write_hyper(h));
   }
   const int P = c.P;
   const uint64_t seed = c.seed;
@@ -369,16 +421,18 @@ int build(hieravg* h) {
     // Buffers hold the largest launch plan over every batch size up to the
     // create-time B (hieravg_set_batch may lower it).
     h->Bmax = c.B;
-    int64_t part_floats = 0, part2_floats = 0;
-    bool any_delayed = false;
+    int64_t part_floats = 0, part2_floats = 0, partv_floats = 0;
+    bool any_delayed = false, any_hb = false;
     int Bp_del = 0;
     for (int b = 16; b <= round_up(c.B, 16); b += 16) {
       const int64_t pf = plan(h, std::min(b, c.B));
       part_floats = std::max(part_floats, pf);
       if (h->delayed) {
         any_delayed = true;
+        any_hb = any_hb || h->hb;
         Bp_del = std::max(Bp_del, h->Bp);
         part2_floats = std::max<int64_t>(part2_floats, (int64_t)h->KS2 * P * h->Bp * h->Cp);
+        if (h->hb) partv_floats = std::max<int64_t>(partv_floats, (int64_t)h->KSv * c.K1 * P * h->Bp * h->Hp);
       }
     }
     plan(h, c.B);
@@ -405,6 +459,19 @@ int build(hieravg* h) {
       const int64_t w1 = h->Hp * h->INp;
       if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
+      if (any_hb) {
+        if ((rc = alloc_zero(h, (void**)&h->Wc2, sizeof(float) * (P / c.S) * w1, "second cluster copies of W1")) ||
+            (rc = alloc_zero(h, (void**)&h->Gu, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "scaled block errors")))
+          return rc;
+        if (c.momentum > 0.0f) {
+          const int64_t rp1 = round_up((int64_t)c.K1 * c.B, 32);
+          if ((rc = alloc_zero(h, (void**)&h->Gt, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "buffer block errors")) ||
+              (rc = alloc_zero(h, (void**)&h->partv, sizeof(float) * partv_floats, "buffer partials")) ||
+              (rc = alloc_zero(h, (void**)&h->btab1, 2 * sizeof(uint32_t) * (size_t)c.K2 * P * rp1,
+                               "buffer update row tables")))
+            return rc;
+        }
+      }
       if ((rc = alloc_zero(h, (void**)&h->ylab, sizeof(int32_t) * (size_t)T * P * c.B, "sample labels"))) return rc;
       const int64_t rp = round_up((int64_t)c.K1 * c.S * c.B, 32);
       if ((rc = alloc_zero(h, (void**)&h->btab, 2 * sizeof(uint32_t) * (size_t)c.K2 * (P / c.S) * rp,
@@ -451,6 +518,11 @@ void with_momentum(const hieravg* h, UpdArgs& u, int64_t off, int64_t boff) {
     u.vbias = u.bias ? h->V + boff : nullptr;
   }
 }
+
+// Cluster copies written by the update of block b (read by block b + 1):
+// one set, updated in place, for plain SGD; heavy-ball blocks alternate two
+// sets so that the buffer update still reads the block-start copies.
+float* wc_buf(const hieravg* h, int b) { return h->hb && (b & 1) ? h->Wc2 : h->Wc; }
 
 // Averaging kind: the launch class of step tt of a round (the heavy-ball step
 // alone, with the cluster mean at the end of a block, or with the global mean
@@ -513,6 +585,11 @@ bool launch_class(hieravg* h, int kc, int tt) {
         tb.ldx = h->INp;
         tb.K2 = c.K2;
         tb.global_last = h->global_last;
+        if (h->hb && h->V) {
+          tb.Rp1 = (int)round_up((int64_t)c.K1 * B, 32);
+          tb.gtab1 = h->btab1;
+          tb.xtab1 = h->btab1 + (int64_t)c.K2 * P * tb.Rp1;
+        }
       }
       launch_draw_indices(s, h->idx, h->ctr, (uint32_t*)(h->ctr + 1), P, B, h->T, (uint64_t)h->N,
                           h->key_index, h->y, h->in_delayed ? h->ylab : nullptr, tb);
@@ -580,7 +657,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       // (the round-start W1 in replica 0 for b = 0, else the cluster's copy);
       // partials go to part[ks][k][P][Bp][Hp].
       const int b = tt / c.K1;
-      FwdArgs f{h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
+      FwdArgs f{h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : wc_buf(h, b - 1),
                 b == 0 ? 0 : h->Hp * h->INp, h->INp, h->part, P, B, Bp, Hp, INp, h->KS_b, h->cps_b};
       f.SG = c.K1 * S;
       f.vS = S;
@@ -589,14 +666,61 @@ bool launch_class(hieravg* h, int kc, int tt) {
       h->ks_cur = h->KS_b;
       return true;
     }
+    case KC_FWD1_BLOCK_V: {
+      // Heavy-ball with momentum: X_k V^T of learner j's K1 steps from its own
+      // buffer (groups of K1 members, the block's steps of one learner).
+      if (!h->delayed || !h->hb || !h->V) return false;
+      const int b = tt / c.K1;
+      FwdArgs f{h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, h->V + h->off_W1, h->Dp, h->INp, h->partv, P, B,
+                Bp, Hp, INp, h->KSv, h->cpsv};
+      f.SG = c.K1;
+      f.vS = 1;
+      f.PT = c.K1 * P;
+      launch_fwd_blk(s, f);
+      return true;
+    }
+    case KC_SCALE_ERRORS:
+      if (!h->delayed || !h->hb) return false;
+      launch_scale_errors(s, h->Gs, h->Gu, h->V ? h->Gt : nullptr, h->hyper, c.K1, (int64_t)P * Bp * Hp);
+      return true;
+    case KC_BUF_UPDATE: {
+      // Heavy-ball with momentum, block end: each learner's buffer of W1,
+      // v = r_K W_b + s_K v + sum_k t_{K-1-k} G_k^T X_k (its own rows).
+      if (!h->delayed || !h->hb || !h->V) return false;
+      const int b = tt / c.K1;
+      const int64_t w1 = h->Hp * h->INp;
+      const int64_t rp1 = round_up((int64_t)c.K1 * B, 32), blk1 = (int64_t)P * rp1;
+      BlkArgs a{h->Gt, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp,
+                b == 0 ? W + h->off_W1 : wc_buf(h, b - 1), b == 0 ? 0 : w1, h->V + h->off_W1, h->Dp, h->INp, P, 1,
+                c.K1, B, Bp, Hp, INp, h->hyper, 1.0f, h->btab1 + b * blk1, h->btab1 + (int64_t)c.K2 * blk1 + b * blk1};
+      a.base_div = S;
+      a.hb = h->hyper;
+      a.hb_c1 = hb_index(HB_R, c.K1);
+      a.hb_c2 = hb_index(HB_S, c.K1);
+      a.B2 = h->V + h->off_W1;
+      a.b2_pitch = h->Dp;
+      a.b2_rows = 1;
+      launch_block_update(s, a);
+      return true;
+    }
     case KC_BLOCK_UPDATE: {
       if (!h->delayed) return false;
       const int b = tt / c.K1;
       const int64_t w1 = h->Hp * h->INp;
       const int64_t rp = round_up((int64_t)c.K1 * S * B, 32), blk = (int64_t)(P / S) * rp;
-      BlkArgs a{h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp, b == 0 ? W + h->off_W1 : h->Wc,
-                b == 0 ? 0 : w1, h->Wc, w1, h->INp, P, S, c.K1, B, Bp, Hp, INp, h->hyper, (float)S,
-                h->btab + b * blk, h->btab + (int64_t)c.K2 * blk + b * blk};
+      BlkArgs a{h->hb ? h->Gu : h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp,
+                b == 0 ? W + h->off_W1 : wc_buf(h, b - 1), b == 0 ? 0 : w1, wc_buf(h, b), w1, h->INp, P, S, c.K1, B,
+                Bp, Hp, INp, h->hyper, (float)S, h->btab + b * blk, h->btab + (int64_t)c.K2 * blk + b * blk};
+      if (h->hb) {  // p_K W_b + q_K mean_j V_j + the errors scaled by u / S
+        a.hb = h->hyper;
+        a.hb_c1 = hb_index(HB_P, c.K1);
+        a.hb_c2 = hb_index(HB_Q, c.K1);
+        if (h->V) {
+          a.B2 = h->V + h->off_W1;
+          a.b2_pitch = h->Dp;
+          a.b2_rows = S;
+        }
+      }
       if (b == c.K2 - 1 && h->global_last) {
         // The last block: one update over all P learners from the mean of the
         // cluster copies (the global mean of Algorithm 1, which skips the
@@ -605,6 +729,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
         a.SG = P;
         a.lr_div = (float)P;
         a.nbase = b == 0 ? 1 : P / S;
+        if (a.B2) a.b2_rows = P;
         a.Wo = W + h->off_W1;
         a.wo_pitch = 0;
         if (P > 1) {
@@ -622,7 +747,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
     }
     case KC_W1_MEAN:  // with the global mean of b1, W2, b2 in the same launch
       if (!h->delayed) return false;
-      launch_mean_rows(s, W + h->off_W1, h->Wc, h->Hp * h->INp, h->Hp * h->INp, P / S, P > 1 ? W + h->off_b1 : nullptr,
+      launch_mean_rows(s, W + h->off_W1, wc_buf(h, c.K2 - 1), h->Hp * h->INp, h->Hp * h->INp, P / S,
+                       P > 1 ? W + h->off_b1 : nullptr,
                        h->Dp, h->Dp - h->off_b1, P);
       return true;
     case KC_GROUP_MEAN: launch_group_mean(s, W, h->Dp, h->Dp, P, S); return true;
@@ -685,6 +811,19 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.Cp = Cp;
       a.Hp = Hp;
       a.K1 = c.K1;
+      if (h->hb) {  // heavy-ball blocks: coefficients, buffer partials, head buffers
+        a.hb = h->hyper;
+        a.partv = h->partv;
+        a.KSv = h->KSv;
+        a.splitv = (int64_t)c.K1 * P * Bp * Hp;
+        a.mu = c.momentum;
+        a.wd = c.weight_decay;
+        if (h->V) {
+          a.vw2 = h->V + h->off_W2;
+          a.vb1 = h->V + h->off_b1;
+          a.vb2 = h->V + h->off_b2;
+        }
+      }
       launch_head_step(s, a, k);
       return true;
     }
@@ -703,7 +842,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (small) return false;
       if (h->in_delayed)  // the hidden errors are kept for the block end; b1 takes its step here
         launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp, P, B,
-                          Bp, C, Cp, Hp, W + h->off_b1, h->hyper);
+                          Bp, C, Cp, Hp, W + h->off_b1, h->hyper, h->hb && h->V ? h->V + h->off_b1 : nullptr,
+                          h->hb ? c.momentum : 0.0f, h->hb ? c.weight_decay : 0.0f);
       else
         launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp);
       return true;
@@ -726,6 +866,14 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.Hp = Hp;
       a.K1 = c.K1;
       a.k = k;
+      if (h->hb) {
+        a.hb = h->hyper;
+        if (h->V) {
+          a.partv = h->partv + (int64_t)k * P * Bp * Hp;
+          a.KSv = h->KSv;
+          a.splitv = (int64_t)c.K1 * P * Bp * Hp;
+        }
+      }
       launch_z1_delayed(s, a);
       return true;
     }
@@ -918,6 +1066,7 @@ void enqueue_round(hieravg* h) {
     }
     for (int b = 0; b < c.K2; ++b) {
       go(KC_FWD1_BLOCK, b * c.K1);
+      if (h->hb && h->V) go(KC_FWD1_BLOCK_V, b * c.K1);  // heavy-ball: X_k V^T of every learner
       if (h->C <= kSmallC) {
         for (int k = 0; k < c.K1; ++k) go(KC_HEAD_STEP, b * c.K1 + k);
         go(KC_HEAD_END, b * c.K1 + c.K1 - 1);
@@ -925,9 +1074,13 @@ void enqueue_round(hieravg* h) {
         for (int k = 0; k < c.K1; ++k)
           for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2}) go(kc, b * c.K1 + k);
       }
+      if (h->hb) go(KC_SCALE_ERRORS, b * c.K1);
       // with the cluster mean of b1, W2, b2 for b < K2 - 1; the last block's
       // update takes the global mean of every block
       go(KC_BLOCK_UPDATE, b * c.K1);
+      // heavy-ball with momentum: each learner's buffer, from the block-start
+      // copies the update above left intact
+      if (h->hb && h->V) go(KC_BUF_UPDATE, b * c.K1);
     }
     if (!h->global_last) go(KC_W1_MEAN, 0);  // with the global mean of b1, W2, b2
   } else {
@@ -1208,8 +1361,8 @@ int hieravg_set_lr(hieravg_t h, float lr) {
     return HIERAVG_EINVAL;
   }
   h->cfg.lr = lr;
-  HAV_CHECK(hipMemcpyAsync(h->hyper, &h->cfg.lr, sizeof(float), hipMemcpyHostToDevice, h->stream));
   HAV_CHECK(hipStreamSynchronize(h->stream));
+  HAV_CHECK(write_hyper(h));  // the step size and the heavy-ball coefficients
   return HIERAVG_OK;
 }
 

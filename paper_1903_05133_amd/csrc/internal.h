@@ -114,11 +114,29 @@ enum KernelClass {
   KC_VMEAN_GROUP,    // averaged momentum buffers: cluster mean of v
   KC_VMEAN_GLOBAL,   // averaged momentum buffers: global mean of v
   KC_MOMENTUM_FIRST, // averaging kind: a round's first step, from the stored global mean
+  KC_FWD1_BLOCK_V,   // heavy-ball delayed updates: X_k V^T of a block's steps from each learner's buffer
+  KC_SCALE_ERRORS,   // heavy-ball delayed updates: the block's errors scaled for the block-end updates
+  KC_BUF_UPDATE,     // heavy-ball delayed updates: block-end update of each learner's first-layer buffer
   KC_COUNT
 };
 
 // Largest class count handled by the fused small-C head kernels.
 constexpr int kSmallC = 32;
+
+// ------------------------------------------------------------ heavy-ball blocks
+// Heavy-ball SGD with L2 decay (d = g + wd*w; v <- mu*v + d; w <- w - lr*v)
+// over the steps of a block is linear in the block-start (w, v) and the
+// steps' gradients g_m: with A = [[1 - lr*wd, -lr*mu], [wd, mu]] acting on
+// (w, v) and e = (-lr, 1), after n steps
+//   w_n = p_n w + q_n v + sum_{m<n} u_{n-1-m} g_m,
+//   v_n = r_n w + s_n v + sum_{m<n} t_{n-1-m} g_m,
+// where A^n = [[p_n, q_n], [r_n, s_n]], u_n = (A^n e)_w, t_n = (A^n e)_v.
+// The device table (after the step size in the handle's hyperparameters)
+// holds p, q, r, s, u, t for n = 0..K1, kHbStride floats apart.
+constexpr int kHbOff = 16, kHbStride = 16;
+enum HbCoef { HB_P = 0, HB_Q, HB_R, HB_S, HB_U, HB_T, HB_COUNT };
+__host__ __device__ inline int hb_index(int which, int n) { return kHbOff + which * kHbStride + n; }
+constexpr int kHyperFloats = kHbOff + HB_COUNT * kHbStride;
 
 // ------------------------------------------------------------ launching
 // Events that time the next launch on this thread (both null: not timing).
@@ -157,6 +175,8 @@ void launch_iota(hipStream_t s, int32_t* dst, int n);
 // With global_last, the last block (b = K2-1) instead holds one table over
 // all P learners, row r = (k*P + j)*B + s at [(b*(P/S))*Rp + r], for the
 // block update that takes the global mean in the same launch.
+// gtab1 (optional): the same rows per learner, row r = k*B + s of learner j
+// in block b at [(b*P + j)*Rp1 + r] (the heavy-ball buffer updates).
 struct BlkTables {
   uint32_t* gtab = nullptr;
   uint32_t* xtab = nullptr;
@@ -164,6 +184,9 @@ struct BlkTables {
   int64_t ldg = 0, ldx = 0;
   int K2 = 0;
   bool global_last = false;
+  uint32_t* gtab1 = nullptr;
+  uint32_t* xtab1 = nullptr;
+  int Rp1 = 0;
 };
 // ylab (optional): the label of every drawn sample, same layout as idx.
 // tables.gtab (optional): also write the block update's row tables.
@@ -253,8 +276,20 @@ struct BlkArgs {
   int64_t tail_pitch = 0, tail_len = 0;
   // The base of a group is the mean of nbase blocks wb_pitch apart (added in
   // order): the global update of the last block starts from the mean of the
-  // cluster copies.
-  int nbase = 1;
+  // cluster copies.  Group g reads base g / base_div (its cluster's copy for
+  // a per-learner update).
+  int nbase = 1, base_div = 1;
+  // Heavy-ball block end (hb set, the coefficient table): the result is
+  //   hb[c1] * base + hb[c2] * (mean of the group's b2_rows rows of B2)
+  //   + sum / lr_div
+  // with the contraction's error rows already scaled by their step's
+  // coefficient (G = the scaled errors); group g's rows of B2 are
+  // g*b2_rows .. +b2_rows-1, b2_pitch floats apart.
+  const float* hb = nullptr;
+  int hb_c1 = 0, hb_c2 = 0;
+  const float* B2 = nullptr;
+  int64_t b2_pitch = 0;
+  int b2_rows = 0;
 };
 // Largest contraction (K1 * SG * B rows) of a block update.
 constexpr int kBlkMaxRows = 16384;
@@ -295,9 +330,15 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp);
 // b1 (optional, replica 0's; replica p at + p*w_pitch): also take the SGD step
 // b1[h] -= lr * sum_m G1[m][h] (delayed updates, where no update GEMM steps b1).
+// vb1 (optional, with b1): heavy-ball buffer of b1 (laid out like it) for the
+// step with momentum mu and decay wd (d = sum + wd*b1; v <- mu*v + d).
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
                        float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1 = nullptr,
-                       const float* lr = nullptr);
+                       const float* lr = nullptr, float* vb1 = nullptr, float mu = 0.0f, float wd = 0.0f);
+// Heavy-ball delayed updates, after a block's last step: Gu[k] = u_{K1-1-k}
+// Gs[k] and (Gt set) Gt[k] = t_{K1-1-k} Gs[k] for k < K1, n floats per step
+// (n a multiple of 4).
+void launch_scale_errors(hipStream_t s, const float* Gs, float* Gu, float* Gt, const float* hb, int K1, int64_t n);
 // Pre-activations of step k of a block under delayed updates for the head
 // with more than 32 classes: Z1 = b1 + sum of the split-K partials
 // - lr * sum_{k2<k} gram[k][k2] G1[k2] (M <= 32, K1 <= 8).
@@ -312,6 +353,12 @@ struct Z1Args {
   float* Z1;              // [P][Mp][Hp]
   const float* lr;
   int P, M, Mp, Hp, K1, k;
+  // Heavy-ball delayed updates (hb set): Z1 = p_k (partials) + q_k (partv
+  // partials, if set) + b1 + sum_{k2<k} u_{k-1-k2} gram[k][k2] G1[k2].
+  const float* hb = nullptr;
+  const float* partv = nullptr;  // step k's partials of X_k V^T, splits splitv apart
+  int KSv = 0;
+  int64_t splitv = 0;
 };
 void launch_z1_delayed(hipStream_t s, const Z1Args& a);
 // part_split: floats between split-K partial sums (0: P * Mp * Hp).
@@ -353,6 +400,18 @@ struct HeadStepArgs {
   const int32_t* ylab;    // [K1][P][M] labels of the block's samples
   const float* lr;        // device scalar step size
   int P, M, Mp, C, Cp, Hp, K1;
+  // Heavy-ball delayed updates (hb set: the coefficient table): the forward
+  // of step k is p_k (part) + q_k (partv, if set) + b1 + sum_{k2<k}
+  // u_{k-1-k2} gram[k][k2] G1[k2], and b1, W2, b2 take heavy-ball steps with
+  // decay (buffers vb1, vw2, vb2 laid out like b1, W2, b2; null when mu = 0).
+  const float* hb = nullptr;
+  const float* partv = nullptr;
+  int KSv = 0;
+  int64_t splitv = 0;
+  float* vw2 = nullptr;
+  float* vb1 = nullptr;
+  float* vb2 = nullptr;
+  float mu = 0.0f, wd = 0.0f;
 };
 // One launch for step k.
 void launch_head_step(hipStream_t s, const HeadStepArgs& a, int k);

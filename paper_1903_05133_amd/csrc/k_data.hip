@@ -86,8 +86,15 @@ __global__ __launch_bounds__(256) void k_draw_indices(int32_t* __restrict__ idx,
       const int64_t b = tt / tb.K1, k = tt - b * tb.K1, g = j / tb.S, jc = j - g * tb.S;
       const int64_t o = tb.global_last && b == tb.K2 - 1 ? b * (P / tb.S) * tb.Rp + (k * P + j) * B + s
                                                          : (b * (P / tb.S) + g) * tb.Rp + (k * tb.S + jc) * B + s;
-      tb.gtab[o] = (uint32_t)((((k * P + j) * tb.Mp + s) * tb.ldg) >> 6);
-      tb.xtab[o] = (uint32_t)(((int64_t)i * tb.ldx) >> 6);
+      const uint32_t go = (uint32_t)((((k * P + j) * tb.Mp + s) * tb.ldg) >> 6);
+      const uint32_t xo = (uint32_t)(((int64_t)i * tb.ldx) >> 6);
+      tb.gtab[o] = go;
+      tb.xtab[o] = xo;
+      if (tb.gtab1) {  // learner j's own rows, r = k*B + s
+        const int64_t o1 = (b * P + j) * tb.Rp1 + k * B + s;
+        tb.gtab1[o1] = go;
+        tb.xtab1[o1] = xo;
+      }
     }
   }
   __syncthreads();

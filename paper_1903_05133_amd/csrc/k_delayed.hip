@@ -343,7 +343,7 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
   const int xc4 = tid % kXP, xr0 = tid / kXP;
   const bool xcol_ok = ncol0 + 4 * xc4 < a.Ncols;
   const int xcol = xcol_ok ? ncol0 + 4 * xc4 : 0;
-  const float* Wb = a.Wb + (int64_t)g * a.nbase * a.wb_pitch;
+  const float* Wb = a.Wb + (int64_t)(g / a.base_div) * a.nbase * a.wb_pitch;
   f32x4 wv[kWL];
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {
@@ -372,6 +372,36 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
   }
   __syncthreads();
   float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
+  if (a.hb) {
+    // Heavy-ball block end: hb[c1] * base + hb[c2] * (mean of the group's
+    // rows of B2) + sum / lr_div, the errors already scaled per step.
+    const float c1 = a.hb[a.hb_c1], c2 = a.hb[a.hb_c2], c3 = 1.0f / a.lr_div;
+    f32x4 bm[kWL];
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) bm[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (a.B2) {
+      const float* b2 = a.B2 + (int64_t)g * a.b2_rows * a.b2_pitch;
+      for (int j = 0; j < a.b2_rows; ++j) {
+#pragma unroll
+        for (int i = 0; i < kWL; ++i) {
+          const int row = mrow0 + xr0 + kXR * i;
+          bm[i] += *(const f32x4*)(b2 + (int64_t)j * a.b2_pitch +
+                                   (row < a.Mrows && xcol_ok ? (int64_t)row * a.ldw + xcol : 0));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) bm[i] = bm[i] / (float)a.b2_rows;
+    }
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) {
+      const int rl = xr0 + kXR * i, row = mrow0 + rl;
+      if (xcol_ok && row < a.Mrows) {
+        const f32x4 gsum = *(const f32x4*)&Gt[rl * kLB + 4 * xc4];
+        *(f32x4*)(Wo + (int64_t)row * a.ldw + xcol) = c1 * wv[i] + c2 * bm[i] + c3 * gsum;
+      }
+    }
+    return;
+  }
   const float lr_eff = *a.lr / a.lr_div;
 #pragma unroll
   for (int i = 0; i < kWL; ++i) {

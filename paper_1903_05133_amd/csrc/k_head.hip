@@ -169,7 +169,8 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
                                                          int64_t w_pitch, const float* __restrict__ Z1,
                                                          float* __restrict__ G1, int M, int Mp, int Cp, int Hp,
                                                          int htiles, int mtiles, float* __restrict__ b1,
-                                                         const float* __restrict__ lr_ptr) {
+                                                         const float* __restrict__ lr_ptr, float* __restrict__ vb1,
+                                                         float mu, float wd) {
   __shared__ __attribute__((aligned(16))) float lds[kBhLds];
   // buffer b: G2 chunk [class][sample] at gsb(b), W2 chunk [class][unit] at wsb(b)
   auto gsb = [&](int b) { return lds + b * (kBhC * kBhLG); };
@@ -275,8 +276,36 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
     }
     if (b1) {  // rows 0-3, 8-11, ... of lanes 0-31, then the other rows of lanes 32-63
       const float other = __shfl_xor(db, 32, 64);
-      if (lhi == 0) b1[(int64_t)p * w_pitch + h] -= *lr_ptr * (db + other);
+      if (lhi == 0) {
+        float* bp = b1 + (int64_t)p * w_pitch + h;
+        if (mu == 0.0f && wd == 0.0f) {
+          *bp -= *lr_ptr * (db + other);
+        } else {  // heavy-ball step with decay: d = g + wd*b; v <- mu*v + d; b <- b - lr*v
+          float d = (db + other) + wd * *bp;
+          if (vb1) {
+            float* vp = vb1 + (int64_t)p * w_pitch + h;
+            d = mu * *vp + d;
+            *vp = d;
+          }
+          *bp -= *lr_ptr * d;
+        }
+      }
     }
+  }
+}
+
+// Heavy-ball delayed updates: the block's hidden errors scaled by their
+// step's block-end coefficients, Gu[k] = u_{K1-1-k} Gs[k] (for the update of
+// the parameters) and Gt[k] = t_{K1-1-k} Gs[k] (for the buffers).
+__global__ __launch_bounds__(256) void k_scale_errors(const f32x4* __restrict__ Gs, f32x4* __restrict__ Gu,
+                                                      f32x4* __restrict__ Gt, const float* __restrict__ hb, int K1,
+                                                      int64_t n4) {
+  const int k = blockIdx.y;
+  const float cu = hb[hb_index(HB_U, K1 - 1 - k)], ct = hb[hb_index(HB_T, K1 - 1 - k)];
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const f32x4 g = Gs[k * n4 + i];
+    Gu[k * n4 + i] = cu * g;
+    if (Gt) Gt[k * n4 + i] = ct * g;
   }
 }
 
@@ -297,12 +326,23 @@ __global__ __launch_bounds__(256) void k_z1_delayed(Z1Args a, int htiles) {
   const float* pm = a.part + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
 #pragma unroll 8
   for (int ks = 0; ks < a.KS; ++ks) z += *(const f32x4*)(pm + ks * a.split);
+  if (a.hb) {  // heavy-ball block: p_k X_k W^T + q_k X_k V^T
+    z = a.hb[hb_index(HB_P, kc)] * z;
+    if (a.partv && kc > 0) {
+      const float* pv = a.partv + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+      f32x4 zv = zero4;
+#pragma unroll 8
+      for (int ks = 0; ks < a.KSv; ++ks) zv += *(const f32x4*)(pv + ks * a.splitv);
+      z += a.hb[hb_index(HB_Q, kc)] * zv;
+    }
+  }
   z += *(const f32x4*)(a.b1 + (int64_t)p * a.w_pitch + h4);
   if (kc > 0) {
     const int gsm = tid / (kHS / 4), gc4 = tid % (kHS / 4);
     for (int k2 = 0; k2 < kc; ++k2) {
-      const f32x4 v =
+      f32x4 v =
           *(const f32x4*)(a.gs + (((int64_t)k2 * a.P + p) * Mp + (gsm < M ? gsm : 0)) * Hp + ht * kHS + 4 * gc4);
+      if (a.hb) v = a.hb[hb_index(HB_U, kc - 1 - k2)] * v;  // the step's own coefficient
       *(f32x4*)&gsl[k2][gsm][4 * gc4] = gsm < M ? v : zero4;
     }
     const float* gk = a.gram + (((int64_t)p * a.K1 + a.k) * a.K1) * Mp * Mp;
@@ -327,7 +367,10 @@ __global__ __launch_bounds__(256) void k_z1_delayed(Z1Args a, int htiles) {
     f32x4 c = zero4;
     for (int w = 0; w < (kc < 4 ? kc : 4); ++w)
       c += f32x4{cbuf[w][rr][4 * u4], cbuf[w][rr][4 * u4 + 1], cbuf[w][rr][4 * u4 + 2], cbuf[w][rr][4 * u4 + 3]};
-    z -= *a.lr * c;
+    if (a.hb)
+      z += c;  // the coefficients (u_n, which carry -lr) are in the staged errors
+    else
+      z -= *a.lr * c;
   }
   if (rr < M) *(f32x4*)(a.Z1 + ((int64_t)p * Mp + rr) * Hp + h4) = z;
 }
@@ -768,9 +811,11 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
         g1[e] = g1[e] > 0.0f ? v : 0.0f;
         db1 += g1[e];
       }
-      if (k < a.K1)  // for (B) (k-1 <= K1-2 < NK)
+      if (k < a.K1) {  // for (B) (k-1 <= K1-2 < NK); heavy-ball: scaled by u_0
+        const float cu = a.hb ? a.hb[hb_index(HB_U, 0)] : 1.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) gsl(kp, 16 * (e >> 2) + 4 * lq + (e & 3), uu) = g1[e];
+        for (int e = 0; e < 8; ++e) gsl(kp, 16 * (e >> 2) + 4 * lq + (e & 3), uu) = a.hb ? cu * g1[e] : g1[e];
+      }
       float* g1out = a.gs + ((int64_t)kp * a.P + p) * Mp * Hp + ht * kHU + uu;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -780,7 +825,18 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
       db1 += __shfl_xor(db1, 16);
       db1 += __shfl_xor(db1, 32);
       if (lq == wave) {  // this thread's unit u is uu (tid % 32 = 16 w + i)
-        const float nb = b1h - lr * db1;
+        float nb;
+        if (a.hb) {  // heavy-ball step with decay
+          float d = db1 + a.wd * b1h;
+          if (a.vb1) {
+            float* vp = a.vb1 + (int64_t)p * a.w_pitch + h;
+            d = a.mu * *vp + d;
+            *vp = d;
+          }
+          nb = b1h - lr * d;
+        } else {
+          nb = b1h - lr * db1;
+        }
         b1[h] = nb;
         bs[u] = nb;
       }
@@ -803,7 +859,19 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int c = c0 + 4 * lq + r;
-          const float nw = wold[c * (kHU + 1) + uu] - lr * accs[r];
+          const float wo = wold[c * (kHU + 1) + uu];
+          float nw;
+          if (a.hb) {  // heavy-ball step with decay
+            float d = accs[r] + a.wd * wo;
+            if (a.vw2 && c < C) {
+              float* vp = a.vw2 + (int64_t)p * a.w_pitch + (int64_t)c * Hp + ht * kHU + uu;
+              d = a.mu * *vp + d;
+              *vp = d;
+            }
+            nw = wo - lr * d;
+          } else {
+            nw = wo - lr * accs[r];
+          }
           if (c < C) w2[(int64_t)c * Hp + ht * kHU + uu] = nw;
           ws[c * (kHU + 1) + uu] = c < C ? nw : 0.0f;
         }
@@ -812,6 +880,14 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
     if (ht == 0 && wave == 3 && lane < KC) {  // slice 0: b2[c = lane] (= u)
       float sb = 0.0f;
       for (int mm = 0; mm < M; ++mm) sb += g2s[mm * kGS + lane];
+      if (a.hb && lane < C) {  // heavy-ball step with decay
+        sb += a.wd * b2v;
+        if (a.vb2) {
+          float* vp = a.vb2 + (int64_t)p * a.w_pitch + lane;
+          sb = a.mu * *vp + sb;
+          *vp = sb;
+        }
+      }
       const float nb2 = lane < C ? b2v - lr * sb : 0.0f;
       if (lane < C) b2[lane] = nb2;
       b2l[lane] = nb2;
@@ -830,7 +906,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   // (B): step k's forward for this slice.
 #pragma unroll
   for (int k2 = 0; k2 < NK - 1; ++k2)
-    if (k2 < kc - 1) *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gsm < M ? gv[k2] : zero4;
+    if (k2 < kc - 1) {
+      const f32x4 v = a.hb ? a.hb[hb_index(HB_U, kc - 1 - k2)] * gv[k2] : gv[k2];  // heavy-ball: u_{k-1-k2}
+      *(f32x4*)&gsl(k2, gsm, 4 * gc4) = gsm < M ? v : zero4;
+    }
 #pragma unroll
   for (int k2 = 0; k2 < NK; ++k2)
     if (k2 < kc && tid < Mp * Mp / 4) {
@@ -851,6 +930,15 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
   for (int ks = kPv; ks < a.KS; ++ks) {
     const float* pm = a.part + k * step_floats + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
     z += *(const f32x4*)(pm + ks * a.split);
+  }
+  if (a.hb) {  // heavy-ball block: p_k X_k W^T + q_k X_k V^T
+    z = a.hb[hb_index(HB_P, k)] * z;
+    if (a.partv && k > 0) {
+      const float* pv = a.partv + k * step_floats + ((int64_t)p * Mp + (rr < M ? rr : 0)) * Hp + h4;
+      f32x4 zv = zero4;
+      for (int ks = 0; ks < a.KSv; ++ks) zv += *(const f32x4*)(pv + ks * a.splitv);
+      z += a.hb[hb_index(HB_Q, k)] * zv;
+    }
   }
   __syncthreads();
   z += f32x4{bs[4 * u4], bs[4 * u4 + 1], bs[4 * u4 + 2], bs[4 * u4 + 3]};
@@ -881,7 +969,10 @@ __global__ __launch_bounds__(256) void k_head_step(HeadStepArgs a, int htiles, i
       const float* cr = cbuf + (w * kHM + rr) * (kHM + 1) + 4 * u4;
       c += f32x4{cr[0], cr[1], cr[2], cr[3]};
     }
-    z -= lr * c;
+    if (a.hb)
+      z += c;  // the coefficients (u_n, which carry -lr) are in the staged errors
+    else
+      z -= lr * c;
   }
   const bool mok = rr < M;
   if (mok) *(f32x4*)(a.Z1 + ((int64_t)p * Mp + rr) * Hp + h4) = z;
@@ -991,8 +1082,17 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
   launch(k_softmax_grad, (rows + 3) / 4, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
 }
 
+void launch_scale_errors(hipStream_t s, const float* Gs, float* Gu, float* Gt, const float* hb, int K1, int64_t n) {
+  const int64_t n4 = n / 4;
+  int64_t gx = (n4 + 255) / 256;
+  if (gx > 2048) gx = 2048;
+  launch(k_scale_errors, dim3((unsigned)gx, (unsigned)K1), 256, 0, s, (const f32x4*)Gs, (f32x4*)Gu, (f32x4*)Gt, hb, K1,
+         n4);
+}
+
 void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
-                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr) {
+                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr, float* vb1,
+                       float mu, float wd) {
   if (b1 && M > kBhM) {  // the b1 step needs every sample in one workgroup
     const int htiles = (Hp + 63) / 64;
     launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles, b1, lr);
@@ -1000,7 +1100,7 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t 
   }
   const int htiles = Hp / kBhN, mtiles = (M + kBhM - 1) / kBhM;
   launch(k_bwd_hidden_mfma, (unsigned)((int64_t)P * mtiles * htiles), 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, Cp,
-         Hp, htiles, mtiles, b1, lr);
+         Hp, htiles, mtiles, b1, lr, vb1, mu, wd);
 }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,

@@ -74,16 +74,26 @@ def test_invalid_config_rejected():
         assert "delayed" in L.hieravg_last_error().decode()
     c = config(0, 4, 2, 1, 1, B=8, in_dim=10, classes=3, n_samples=10, update_mode=2)
     assert not L.hieravg_create_config(ctypes.byref(c))
-    # the optimizer fields, for every kind; delayed updates take plain SGD only
+    # the optimizer fields, for every kind; delayed updates leave the momentum buffers out of the means
     for kw, msg in ((dict(momentum=-0.1), "momentum"), (dict(momentum=1.0), "momentum"),
                     (dict(weight_decay=-1.0), "weight_decay"), (dict(weight_decay=float("inf")), "weight_decay"),
-                    (dict(avg_momentum=2), "avg_momentum"), (dict(momentum=0.9, update_mode=2), "delayed"),
-                    (dict(weight_decay=0.1, update_mode=2), "delayed")):
+                    (dict(avg_momentum=2), "avg_momentum"),
+                    (dict(momentum=0.9, weight_decay=0.1, update_mode=2, avg_momentum=1), "delayed")):
+        kw = dict(kw)
+        avg_momentum = kw.pop("avg_momentum", None)
         c = config(1, 4, 2, 2, 1, B=8, in_dim=10, hidden=5, classes=3, n_samples=10, **kw)
-        if "avg_momentum" in kw:
-            c.avg_momentum = kw["avg_momentum"]
+        if avg_momentum is not None:
+            c.avg_momentum = avg_momentum
         assert not L.hieravg_create_config(ctypes.byref(c))
         assert msg in L.hieravg_last_error().decode()
+    # momentum and weight decay with unaveraged buffers pass validation in delayed mode
+    c = config(1, 4, 2, 2, 1, B=8, in_dim=10, hidden=5, classes=3, n_samples=10, momentum=0.9, weight_decay=0.1,
+               update_mode=2)
+    h = L.hieravg_create_config(ctypes.byref(c))
+    if h:
+        L.hieravg_destroy(h)
+    else:
+        assert "delayed" not in L.hieravg_last_error().decode()
 
 
 def test_kernel_class_names():

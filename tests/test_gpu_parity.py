@@ -621,35 +621,91 @@ MOMENTUM_CASES = {
 }
 
 
-@pytest.mark.parametrize("name", sorted(MOMENTUM_CASES))
-def test_momentum_and_weight_decay_match_oracle(name, gpu_lib):
-    """Heavy-ball buffers and L2 decay in every update kernel: parameters and
-    buffers after two rounds against the oracle (AUTO mode: these run eager)."""
+# MLP cases the delayed schedule takes (plain buffers, B <= 32): heavy-ball blocks
+HB_DELAYED = {
+    "mlp_head_mom_wd": MOMENTUM_CASES["mlp_head_mom_wd"],
+    "mlp_large_c_mom": MOMENTUM_CASES["mlp_large_c_mom"],
+    # decay without momentum (no buffers): scalar block coefficients only
+    "mlp_decay_only": cases.case("mlp", 4, 2, 3, 2, B=10, IN=90, H=70, C=5, N=100, sigma=0.5, lr=0.1,
+                                 weight_decay=0.02, seed=37),
+    # one block per round: the cluster updates and the separate mean of the copies
+    "mlp_mom_one_block": cases.case("mlp", 6, 3, 3, 1, B=8, IN=64, H=40, C=4, N=80, sigma=0.5, lr=0.05,
+                                    momentum=0.9, seed=38),
+    # W1 with 512 output tiles: the last block's global update from the mean of the copies and buffers
+    "mlp_wide_mom": cases.case("mlp", 4, 2, 2, 2, B=16, IN=8192, H=512, C=6, N=200, sigma=0.5, lr=0.02,
+                               momentum=0.9, weight_decay=0.001, seed=39),
+    # K1 = 5: four earlier steps' corrections per block, 20 to 32 classes
+    "mlp_mom_long_block": cases.case("mlp", 4, 2, 5, 2, B=12, IN=100, H=96, C=20, N=150, sigma=0.5, lr=0.05,
+                                     momentum=0.5, weight_decay=0.005, seed=40),
+}
+
+
+def _momentum_run(c, mode, rounds=2):
     from paper_1903_05133_amd import HierAvg
-    c = MOMENTUM_CASES[name]
-    print(f"[gpu case] momentum {name} {c}", flush=True)
-    with HierAvg(config=cases.native_config(c)) as h:
+    print(f"[gpu case] momentum {mode} {c}", flush=True)
+    with HierAvg(config=cases.native_config(c, mode)) as h:
         h.profile(True)
-        h.round()
-        h.round()
+        for _ in range(rounds):
+            h.round()
         stats = h.profile_read()
         got = h.params()
         vgot = h.momentum() if c["momentum"] > 0 or c["kind"] == "averaging" else None
         idx = h.last_indices() if c["kind"] != "averaging" else None
-    assert "fwd1_block_gemm" not in stats and "step1_gemm" not in stats
-    if c["avg_momentum"] and c["momentum"] > 0:
-        assert "momentum_buffer_global_mean" in stats
-    st, mon, rerun = _oracle(c, 2)
-    det = _check(c, got, idx, st, mon, rerun)
+    return got, vgot, idx, stats
+
+
+def _momentum_check(c, got, vgot, idx, mode, rounds=2):
+    st, mon, rerun = _oracle(c, rounds)
+    det = _check(c, got, idx, st, mon, rerun, mode=mode)
     if vgot is not None:
         prob = cases.oracle_problem(c)
         if det.get("flipped"):  # the buffers of the run whose branch the parameters matched
-            st = M.run(prob, 2, flips=frozenset(d[:4] for d in det["flipped"]))
+            st = M.run(prob, rounds, flips=frozenset(d[:4] for d in det["flipped"]))
         ok, det = cases.parity_report(prob, vgot, st.V)
         print(f"[gpu case] buffers: worst block error {det['worst']}", flush=True)
         assert ok, det
         if c["avg_momentum"]:
             assert np.array_equal(vgot, np.repeat(vgot[:1], vgot.shape[0], axis=0))
+
+
+@pytest.mark.parametrize("name", sorted(MOMENTUM_CASES))
+def test_momentum_and_weight_decay_match_oracle(name, gpu_lib):
+    """Heavy-ball buffers and L2 decay in every update kernel, EAGER: parameters
+    and buffers after two rounds against the oracle."""
+    c = MOMENTUM_CASES[name]
+    got, vgot, idx, stats = _momentum_run(c, "eager")
+    assert "fwd1_block_gemm" not in stats and "step1_gemm" not in stats
+    if c["avg_momentum"] and c["momentum"] > 0:
+        assert "momentum_buffer_global_mean" in stats
+    _momentum_check(c, got, vgot, idx, "eager")
+
+
+@pytest.mark.parametrize("name", sorted(HB_DELAYED))
+def test_momentum_and_weight_decay_delayed(name, gpu_lib):
+    """Heavy-ball blocks: the first layer of every learner after k steps of
+    heavy-ball SGD with decay is p_k W + q_k V + sum u G^T X (scalars from the
+    recurrence), so the block forward, the Gram corrections and the block-end
+    updates of the parameters and of every learner's buffer keep their GEMM
+    form.  AUTO takes this schedule; parameters and buffers after two rounds
+    against the oracle."""
+    c = HB_DELAYED[name]
+    got, vgot, idx, stats = _momentum_run(c, "auto")
+    assert "fwd1_block_gemm" in stats and "scale_errors" in stats
+    assert ("buffer_update_gemm" in stats) == (c["momentum"] > 0)
+    assert ("fwd1_block_gemm_v" in stats) == (c["momentum"] > 0)
+    _momentum_check(c, got, vgot, idx, "delayed")
+
+
+@pytest.mark.parametrize("mode", ["delayed", "eager"])
+def test_named_mlp_workload_momentum(mode, gpu_lib):
+    """MLP 3072 -> 512 -> 10, P=16 S=4 K1=4 K2=4 B=32, lr 0.05 with momentum
+    0.9 and weight decay 5e-4 (buffers per learner), one full round in both
+    schedules: parameters and buffers against the oracle."""
+    c = cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0)
+    c.update(momentum=0.9, weight_decay=5e-4)
+    got, vgot, idx, stats = _momentum_run(c, mode, rounds=1)
+    assert ("buffer_update_gemm" in stats) == (mode == "delayed")
+    _momentum_check(c, got, vgot, idx, mode, rounds=1)
 
 
 def test_momentum_checkpoint_resume(gpu_lib):
