@@ -27,7 +27,11 @@ constexpr int kLB = kUN + 4;    // LDS row length of the input stage and of the 
 // Large-tile variant for the block-wide forward of delayed updates (many rows
 // per weight copy): 1024 threads, output tile 128 rows x 128 columns, both
 // operands staged through LDS (double-buffered, one barrier per 64-wide K
-// chunk, the next chunk's loads in flight during the current chunk's MFMAs).
+// chunk).  The global loads run two chunks ahead in two register sets: the
+// set that goes to LDS after a chunk's MFMAs was loaded a whole chunk
+// earlier, so no wave waits on memory in the middle of its MFMA chain (with
+// loads one chunk ahead, the four waves of a SIMD all stalled on the same
+// fresh loads early in every chunk).
 // Wave w owns the 32 x 32 block (rows 32*(w/4), columns 32*(w%4)) as one
 // chain of 32x32x2 MFMAs (one accumulator chain per wave keeps the matrix
 // pipe fuller than four interleaved 16x16x4 chains), so each SIMD
@@ -109,15 +113,40 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
       for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[e], y[e], acc, 0, 0, 0);
     }
   };
+  // Two register sets: the loads of chunk c + 2 go out while chunk c is
+  // contracted and chunk c + 1 (loaded one chunk earlier) goes to LDS.
+  f32x4 av2[2], wv2[2];
+  auto load2 = [&](int c) {
+    const int64_t o = (int64_t)c * kKC;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      av2[i] = *(const f32x4*)(arow[i] + o);
+      wv2[i] = *(const f32x4*)(wrow[i] + o);
+    }
+  };
+  auto store2 = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *(f32x4*)&As[buf][off[i]] = aok[i] ? av2[i] : zero4;
+      *(f32x4*)&Ws[buf][off[i]] = wok[i] ? wv2[i] : zero4;
+    }
+  };
   if (c0 < c1) {
     load(c0);
+    load2(c0 + 1 < c1 ? c0 + 1 : c0);
     store(0);
     __syncthreads();
-    for (int c = c0; c < c1; ++c) {
-      load(c + 1 < c1 ? c + 1 : c);  // the last chunk again at the end: in range, unused
+    for (int c = c0; c < c1; c += 2) {
+      load(c + 2 < c1 ? c + 2 : c1 - 1);  // clamped: in range, unused past the end
       __builtin_amdgcn_sched_barrier(0);
-      compute((c - c0) & 1);
-      store((c - c0 + 1) & 1);
+      compute(0);
+      store2(1);
+      __syncthreads();
+      if (c + 1 >= c1) break;
+      load2(c + 3 < c1 ? c + 3 : c1 - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      store(0);
       __syncthreads();
     }
   }
