@@ -637,6 +637,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.idx_next = ix + (int64_t)P * B;
       a.part = h->part;
       a.SG = mean ? S : 1;
+      a.x_rows = h->N;
       launch_step_w1(s, a);
       h->ks_cur = mean ? h->KS_mean : h->KS_step;
       return true;

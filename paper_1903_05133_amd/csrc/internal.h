@@ -315,6 +315,7 @@ struct StepArgs {
   float* part;              // [KS][P][Mp][Mrows] forward partials of the next step
   int SG;                   // learners averaged per group (1: no mean); SG | P
   int NT;                   // set by the launcher: 128-column tiles per workgroup
+  int64_t x_rows = 0;       // rows of the dataset u.Bsrc (0: unknown)
 };
 // Whether the fused kernel handles this shape (Mp a multiple of 16 up to 64,
 // SG in {1, 2, 4, 8}, SG * Mp / 16 <= 16).

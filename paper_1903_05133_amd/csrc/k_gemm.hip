@@ -725,6 +725,200 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
   }
 }
 
+// Full-tile form of k_step_w1 for SG = 1: every sample, row and column of
+// the launch in range (B a multiple of 32, Mrows of 64, Ncols of kSN) and the
+// dataset, the learner's error rows and its weight block each below 4 GiB.
+// Every global access is a buffer access: a per-lane 32-bit byte offset that
+// stays fixed for the whole kernel (the gathered rows' offsets are read from
+// LDS once) plus a wave-uniform offset in a scalar register (the tile's
+// column, the piece's row group).  Nothing is selected or bounds-checked per
+// tile, so the tile loop runs the MFMAs, the update itself and the LDS
+// traffic and next to no other vector instruction (on gfx950 those stall
+// the SIMD's matrix core).  The second 32-sample stage of a tile is loaded
+// while the first is contracted.  Same tiles, operand layouts, k order and
+// outputs as k_step_w1.
+// The base address and size pass through readfirstlane: the resource then
+// sits in scalar registers (the caller's values are uniform), and no access
+// turns into a per-lane loop over resource values.
+__device__ inline __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint64_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b), hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)(bytes < 0xffffffffull ? bytes : 0xffffffffull));
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n, 0x00020000);
+}
+__device__ inline f32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ inline void buf_st16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff, f32x4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
+}
+
+template <int MBF>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_step_w1_full(
+    StepArgs a, int mtiles, int ntiles, int nchunks) {
+  constexpr int MP = MBF * 16;   // samples of a step (= Kb = Mp)
+  constexpr int NST = MP / kSC;  // 32-sample stages per tile
+  constexpr int kWL = kUM / kRP;
+  constexpr int kXL = kSC / kRP;
+  constexpr int kXN = MP / kRP;
+  static_assert(MP % kSC == 0 && kXL * kRP == kSC && kXN * kRP == MP, "full-tile step shapes");
+  __shared__ __attribute__((aligned(16))) float lds[kSU + MP * kSL];
+  __shared__ uint32_t roff_t[MP], roff_n[MP];
+  float* As = lds;
+  float* Bs = lds + kSC * kLA;
+  float* Wt = lds;
+  float* Xs = lds + kSU;
+  const UpdArgs& u = a.u;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = bid % mtiles;
+  const int chunk = (bid / mtiles) % nchunks;
+  const int p = bid / (mtiles * nchunks);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int mrow0 = mt * kUM;
+  const int wn = (wave & 1) * (kSN / 2), wm = (wave >> 1) * 32;
+  const int pc4 = tid % kSP, pr0 = tid / kSP;
+  const float lr = *u.lr;
+
+  // Byte offsets of this learner's gathered rows (this step and the next).
+  for (int e = tid; e < MP; e += 256) {
+    roff_t[e] = (uint32_t)((uint64_t)u.idx[(int64_t)p * MP + e] * (uint64_t)u.ldb * 4u);
+    roff_n[e] = (uint32_t)((uint64_t)a.idx_next[(int64_t)p * MP + e] * (uint64_t)u.ldb * 4u);
+  }
+  __syncthreads();
+  uint32_t xo_t[NST][kXL], xo_n[kXN];
+#pragma unroll
+  for (int st = 0; st < NST; ++st)
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) xo_t[st][i] = roff_t[kSC * st + pr0 + kRP * i] + 16u * pc4;
+#pragma unroll
+  for (int i = 0; i < kXN; ++i) xo_n[i] = roff_n[pr0 + kRP * i] + 16u * pc4;
+  // G[s][mrow0 + 4pc4] at vo_g + s*ldg*4 (s = pr0 + 16i + 32st); W[mrow0 + r][c]
+  // at vo_w + (r - pr0)*ldw*4 + 4c (r = pr0 + 16i).
+  const uint32_t vo_g = (uint32_t)(pr0 * u.ldg + 4 * pc4) * 4u;
+  const uint32_t vo_w = (uint32_t)(pr0 * u.ldw + 4 * pc4) * 4u;
+  const __amdgpu_buffer_rsrc_t rG =
+      buf_rsrc(u.G + (int64_t)p * u.Mp * u.ldg + mrow0, (uint64_t)u.Mp * u.ldg * 4);
+  const __amdgpu_buffer_rsrc_t rW =
+      buf_rsrc(u.W + (int64_t)p * u.w_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
+  const __amdgpu_buffer_rsrc_t rX = buf_rsrc(u.Bsrc, (uint64_t)a.x_rows * u.ldb * 4);
+  const int g16 = kRP * (int)u.ldg * 4, w16 = kRP * (int)u.ldw * 4;
+
+  f32x4 ga[kXL], xb[kXL], wv[kWL], xn[kXN];
+  auto load_stage = [&](int n, int st) {
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {
+      ga[i] = buf_ld16(rG, vo_g, (kSC * st * (int)u.ldg) * 4 + i * g16);
+      xb[i] = buf_ld16(rX, xo_t[st][i], n * kSN * 4);
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {
+      *(f32x4*)&As[(pr0 + kRP * i) * kLA + 4 * pc4] = ga[i];
+      *(f32x4*)&Bs[(pr0 + kRP * i) * kSL + 4 * pc4] = xb[i];
+    }
+  };
+  auto load_w = [&](int n) {
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) wv[i] = buf_ld16(rW, vo_w, n * kSN * 4 + i * w16);
+  };
+  auto load_next = [&](int n) {
+#pragma unroll
+    for (int i = 0; i < kXN; ++i) xn[i] = buf_ld16(rX, xo_n[i], n * kSN * 4);
+  };
+
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 accf[MBF];
+#pragma unroll
+  for (int b = 0; b < MBF; ++b) accf[b] = zero4;
+  f32x16 acc[kNA];
+
+  const int n_begin = chunk * a.NT, n_end = min(ntiles, n_begin + a.NT);
+  load_stage(n_begin, 0);
+  load_w(n_begin);
+  load_next(n_begin);
+  for (int n = n_begin; n < n_end; ++n) {
+    const int nn = n + 1 < n_end ? n + 1 : n;  // the last tile loads itself again: in range, unused
+#pragma unroll
+    for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[jj][r] = 0.0f;
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      store_stage();
+      if (st + 1 < NST)
+        load_stage(n, st + 1);
+      else
+        load_stage(nn, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+#pragma unroll HAV_STEP_UNROLL_U
+      for (int ss = 0; ss < kSC; ss += 2) {
+        const int sr = ss + lhi;
+        const float av = As[sr * kLA + wm + l32];
+#pragma unroll
+        for (int jj = 0; jj < kNA; ++jj)
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kSL + wn + 32 * jj + l32], acc[jj], 0, 0, 0);
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+        Wt[row * kSL + wn + 32 * jj + l32] = acc[jj][r];
+      }
+    __syncthreads();
+    // New tile: each thread overwrites its own gradient pieces with the new
+    // values and stores them.
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) {
+      f32x4* t = (f32x4*)&Wt[(pr0 + kRP * i) * kSL + 4 * pc4];
+      const f32x4 wnew = wv[i] - lr * *t;
+      buf_st16(rW, vo_w, n * kSN * 4 + i * w16, wnew);
+      *t = wnew;
+    }
+    load_w(nn);
+#pragma unroll
+    for (int i = 0; i < kXN; ++i) *(f32x4*)&Xs[(pr0 + kRP * i) * kSL + 4 * pc4] = xn[i];
+    load_next(nn);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+#pragma unroll(MBF > 2 ? 1 : HAV_STEP_UNROLL_F)
+    for (int q = 0; q < kSN / 16; ++q) {
+      const f32x4 b = *(const f32x4*)&Wt[(16 * wave + lrow) * kSL + 16 * q + 4 * lgrp];
+      f32x4 af[MBF];
+#pragma unroll
+      for (int m = 0; m < MBF; ++m) af[m] = *(const f32x4*)&Xs[(16 * m + lrow) * kSL + 16 * q + 4 * lgrp];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int m = 0; m < MBF; ++m) accf[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[m][i], b[i], accf[m], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  {
+    const int h = mrow0 + 16 * wave + lrow;
+    float* part = a.part + ((int64_t)chunk * u.P + p) * u.Mp * u.Mrows;
+#pragma unroll
+    for (int m = 0; m < MBF; ++m)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) part[(int64_t)(16 * m + 4 * lgrp + r) * u.Mrows + h] = accf[m][r];
+  }
+  if (chunk == 0 && u.bias != nullptr && tid < kUM) {
+    const int m = mrow0 + tid;
+    const float* Gp = u.G + (int64_t)p * u.Mp * u.ldg;
+    float sum = 0.0f;
+    for (int s = 0; s < MP; ++s) sum += Gp[(int64_t)s * u.ldg + m];
+    u.bias[(int64_t)p * u.w_pitch + m] -= lr * sum;
+  }
+}
+
 bool step_w1_supported(int Mp, int SG) {
   if (Mp < 1 || Mp > kStepMaxB || Mp % 16 != 0) return false;
   if (SG != 1 && SG != 2 && SG != 4 && SG != 8) return false;
@@ -750,6 +944,17 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
   step_plan(a.u.P, a.SG, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
+  const uint64_t lim = 0xffffffffull;
+  const bool full = a.SG == 1 && a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mrows % kUM == 0 &&
+                    a.u.Ncols % kSN == 0 && a.x_rows > 0 && (uint64_t)a.x_rows * a.u.ldb * 4 < lim &&
+                    (uint64_t)a.u.Mp * a.u.ldg * 4 < lim && (uint64_t)kUM * a.u.ldw * 4 < lim;
+  if (full) {
+    if (a.u.Mp == 32)
+      launch(k_step_w1_full<2>, grid, 256, 0, s, a, mtiles, ntiles, nchunks);
+    else
+      launch(k_step_w1_full<4>, grid, 256, 0, s, a, mtiles, ntiles, nchunks);
+    return;
+  }
 #define HAV_STEP(SG_, MBF_) launch(k_step_w1<SG_, MBF_>, grid, 256, 0, s, a, mtiles, ntiles, nchunks)
 #define HAV_STEP_MBF(SG_)           \
   switch (a.u.Mp / 16) {            \
