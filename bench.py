@@ -310,7 +310,7 @@ def cpu_baseline():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20, help="timed rounds of the headline workload")
+    ap.add_argument("--steps", type=int, default=50, help="timed rounds of the headline workload (50: about 1 s)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--only", default=None, help="time only these workloads, comma-separated (profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -322,11 +322,11 @@ int64_t plan(hieravg* h, int B) {
   h->fused_mean = h->fused && c.S > 1 && step_w1_supported(h->Bp, c.S);
   int64_t ks_max = h->KS1;
   if (h->fused) {
-    h->KS_step = step_w1_splits(P, 1, (int)n1, (int)h->INp);
+    h->KS_step = step_w1_splits(P, 1, h->Bp, (int)n1, (int)h->INp);
     ks_max = std::max<int64_t>(ks_max, h->KS_step);
   }
   if (h->fused_mean) {
-    h->KS_mean = step_w1_splits(P, c.S, (int)n1, (int)h->INp);
+    h->KS_mean = step_w1_splits(P, c.S, h->Bp, (int)n1, (int)h->INp);
     ks_max = std::max<int64_t>(ks_max, h->KS_mean);
   }
   h->delayed = false;

@@ -321,7 +321,7 @@ struct StepArgs {
 // SG in {1, 2, 4, 8}, SG * Mp / 16 <= 16).
 bool step_w1_supported(int Mp, int SG);
 // Number of forward splits KS the fused kernel writes for this shape.
-int step_w1_splits(int P, int SG, int Mrows, int Ncols);
+int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols);
 void launch_step_w1(hipStream_t s, StepArgs a);
 
 // Head of the network (k_head.hip).

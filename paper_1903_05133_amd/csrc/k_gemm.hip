@@ -734,9 +734,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
 // column, the piece's row group).  Nothing is selected or bounds-checked per
 // tile, so the tile loop runs the MFMAs, the update itself and the LDS
 // traffic and next to no other vector instruction (on gfx950 those stall
-// the SIMD's matrix core).  The second 32-sample stage of a tile is loaded
-// while the first is contracted.  Same tiles, operand layouts, k order and
-// outputs as k_step_w1.
+// the SIMD's matrix core).  The whole input tile of the step is loaded one
+// tile ahead.  The step's error rows of the row tile sit
+// in LDS for the whole workgroup (they do not depend on the column tile), and
+// the waves raise their priority over the MFMA loops so that the SIMD keeps
+// issuing MFMAs while other workgroups stage data.  Same tiles, operand
+// layouts, k order and outputs as k_step_w1.
 // The base address and size pass through readfirstlane: the resource then
 // sits in scalar registers (the caller's values are uniform), and no access
 // turns into a per-lane loop over resource values.
@@ -754,21 +757,26 @@ __device__ inline void buf_st16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int sof
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
 }
 
+#ifndef HAV_STEP_GP
+#define HAV_STEP_GP 1
+#endif
 template <int MBF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_step_w1_full(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 && HAV_STEP_GP ? 3 : 4))) void k_step_w1_full(
     StepArgs a, int mtiles, int ntiles, int nchunks) {
   constexpr int MP = MBF * 16;   // samples of a step (= Kb = Mp)
-  constexpr int NST = MP / kSC;  // 32-sample stages per tile
   constexpr int kWL = kUM / kRP;
-  constexpr int kXL = kSC / kRP;
-  constexpr int kXN = MP / kRP;
-  static_assert(MP % kSC == 0 && kXL * kRP == kSC && kXN * kRP == MP, "full-tile step shapes");
-  __shared__ __attribute__((aligned(16))) float lds[kSU + MP * kSL];
+  constexpr int kXN = MP / kRP;  // pieces per thread of a 64-column tile of MP rows
+  constexpr int kGL = MP * 16 / 256;  // pieces per thread of the G tile (MP rows x 64 units)
+  constexpr int kBR = MP > kUM ? MP : kUM;
+  static_assert(MP % kSC == 0 && kXN * kRP == MP, "full-tile step shapes");
+  // Gs: the step's errors of this row tile (constant over the column tiles);
+  // Bs: the tile's input rows, then (aliased) the gradient / new tile Wt;
+  // Xs: the next step's input rows of the tile.
+  __shared__ __attribute__((aligned(16))) float Gs[MP * kLA];
+  __shared__ __attribute__((aligned(16))) float Bs[kBR * kSL];
+  __shared__ __attribute__((aligned(16))) float Xs[MP * kSL];
   __shared__ uint32_t roff_t[MP], roff_n[MP];
-  float* As = lds;
-  float* Bs = lds + kSC * kLA;
-  float* Wt = lds;
-  float* Xs = lds + kSU;
+  float* Wt = Bs;
   const UpdArgs& u = a.u;
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int mt = bid % mtiles;
@@ -787,39 +795,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     roff_t[e] = (uint32_t)((uint64_t)u.idx[(int64_t)p * MP + e] * (uint64_t)u.ldb * 4u);
     roff_n[e] = (uint32_t)((uint64_t)a.idx_next[(int64_t)p * MP + e] * (uint64_t)u.ldb * 4u);
   }
-  __syncthreads();
-  uint32_t xo_t[NST][kXL], xo_n[kXN];
-#pragma unroll
-  for (int st = 0; st < NST; ++st)
-#pragma unroll
-    for (int i = 0; i < kXL; ++i) xo_t[st][i] = roff_t[kSC * st + pr0 + kRP * i] + 16u * pc4;
-#pragma unroll
-  for (int i = 0; i < kXN; ++i) xo_n[i] = roff_n[pr0 + kRP * i] + 16u * pc4;
-  // G[s][mrow0 + 4pc4] at vo_g + s*ldg*4 (s = pr0 + 16i + 32st); W[mrow0 + r][c]
-  // at vo_w + (r - pr0)*ldw*4 + 4c (r = pr0 + 16i).
-  const uint32_t vo_g = (uint32_t)(pr0 * u.ldg + 4 * pc4) * 4u;
-  const uint32_t vo_w = (uint32_t)(pr0 * u.ldw + 4 * pc4) * 4u;
   const __amdgpu_buffer_rsrc_t rG =
       buf_rsrc(u.G + (int64_t)p * u.Mp * u.ldg + mrow0, (uint64_t)u.Mp * u.ldg * 4);
   const __amdgpu_buffer_rsrc_t rW =
       buf_rsrc(u.W + (int64_t)p * u.w_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
   const __amdgpu_buffer_rsrc_t rX = buf_rsrc(u.Bsrc, (uint64_t)a.x_rows * u.ldb * 4);
-  const int g16 = kRP * (int)u.ldg * 4, w16 = kRP * (int)u.ldw * 4;
+  {
+    // G[s][mrow0 + 4pc4], s = pr0 + 16i, once for the whole workgroup.
+    const uint32_t vo_g = (uint32_t)(pr0 * u.ldg + 4 * pc4) * 4u;
+    f32x4 g[kGL];
+#pragma unroll
+    for (int i = 0; i < kGL; ++i) g[i] = buf_ld16(rG, vo_g, i * kRP * (int)u.ldg * 4);
+#pragma unroll
+    for (int i = 0; i < kGL; ++i) *(f32x4*)&Gs[(pr0 + kRP * i) * kLA + 4 * pc4] = g[i];
+  }
+  __syncthreads();
+  uint32_t xo_t[kXN], xo_n[kXN];
+#pragma unroll
+  for (int i = 0; i < kXN; ++i) {
+    xo_t[i] = roff_t[pr0 + kRP * i] + 16u * pc4;
+    xo_n[i] = roff_n[pr0 + kRP * i] + 16u * pc4;
+  }
+  const uint32_t vo_w = (uint32_t)(pr0 * u.ldw + 4 * pc4) * 4u;  // W[mrow0 + pr0 + 16i][n*kSN + 4pc4]
+  const int w16 = kRP * (int)u.ldw * 4;
 
-  f32x4 ga[kXL], xb[kXL], wv[kWL], xn[kXN];
-  auto load_stage = [&](int n, int st) {
+  f32x4 xb[kXN], wv[kWL], xn[kXN];
+  auto load_x = [&](int n) {
 #pragma unroll
-    for (int i = 0; i < kXL; ++i) {
-      ga[i] = buf_ld16(rG, vo_g, (kSC * st * (int)u.ldg) * 4 + i * g16);
-      xb[i] = buf_ld16(rX, xo_t[st][i], n * kSN * 4);
-    }
-  };
-  auto store_stage = [&]() {
-#pragma unroll
-    for (int i = 0; i < kXL; ++i) {
-      *(f32x4*)&As[(pr0 + kRP * i) * kLA + 4 * pc4] = ga[i];
-      *(f32x4*)&Bs[(pr0 + kRP * i) * kSL + 4 * pc4] = xb[i];
-    }
+    for (int i = 0; i < kXN; ++i) xb[i] = buf_ld16(rX, xo_t[i], n * kSN * 4);
   };
   auto load_w = [&](int n) {
 #pragma unroll
@@ -837,34 +840,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   f32x16 acc[kNA];
 
   const int n_begin = chunk * a.NT, n_end = min(ntiles, n_begin + a.NT);
-  load_stage(n_begin, 0);
+  load_x(n_begin);
   load_w(n_begin);
   load_next(n_begin);
   for (int n = n_begin; n < n_end; ++n) {
     const int nn = n + 1 < n_end ? n + 1 : n;  // the last tile loads itself again: in range, unused
 #pragma unroll
+    for (int i = 0; i < kXN; ++i) *(f32x4*)&Bs[(pr0 + kRP * i) * kSL + 4 * pc4] = xb[i];
+    load_x(nn);
+#pragma unroll
     for (int jj = 0; jj < kNA; ++jj)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[jj][r] = 0.0f;
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      store_stage();
-      if (st + 1 < NST)
-        load_stage(n, st + 1);
-      else
-        load_stage(nn, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll HAV_STEP_UNROLL_U
-      for (int ss = 0; ss < kSC; ss += 2) {
-        const int sr = ss + lhi;
-        const float av = As[sr * kLA + wm + l32];
+    for (int ss = 0; ss < MP; ss += 2) {
+      const int sr = ss + lhi;
+      const float av = Gs[sr * kLA + wm + l32];
 #pragma unroll
-        for (int jj = 0; jj < kNA; ++jj)
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kSL + wn + 32 * jj + l32], acc[jj], 0, 0, 0);
-      }
-      __syncthreads();
+      for (int jj = 0; jj < kNA; ++jj)
+        acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kSL + wn + 32 * jj + l32], acc[jj], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
+    __syncthreads();
 #pragma unroll
     for (int jj = 0; jj < kNA; ++jj)
 #pragma unroll
@@ -888,6 +888,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     load_next(nn);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll(MBF > 2 ? 1 : HAV_STEP_UNROLL_F)
     for (int q = 0; q < kSN / 16; ++q) {
       const f32x4 b = *(const f32x4*)&Wt[(16 * wave + lrow) * kSL + 16 * q + 4 * lgrp];
@@ -899,6 +900,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
 #pragma unroll
         for (int m = 0; m < MBF; ++m) accf[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[m][i], b[i], accf[m], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   }
 
@@ -925,24 +927,33 @@ bool step_w1_supported(int Mp, int SG) {
   return SG * (Mp / 16) <= 16;
 }
 
-static void step_plan(int P, int SG, int Mrows, int Ncols, int* mtiles, int* ntiles, int* nchunks, int* NT) {
+#ifndef HAV_STEP_TARGET_WG64
+#define HAV_STEP_TARGET_WG64 1536
+#endif
+// Workgroups a step launch aims for: about four per CU, or two waves of three
+// per CU for 64-sample steps of one learner (the full-tile kernel's LDS
+// allows three workgroups per CU there).
+static int step_target(int SG, int Mp) { return SG == 1 && Mp == 64 ? HAV_STEP_TARGET_WG64 : kStepTargetWG; }
+
+static void step_plan(int P, int SG, int Mp, int Mrows, int Ncols, int* mtiles, int* ntiles, int* nchunks, int* NT) {
   *mtiles = (Mrows + kUM - 1) / kUM;
   *ntiles = (Ncols + kSN - 1) / kSN;
   const int64_t base = (int64_t)(P / SG) * *mtiles;
-  int nc = (int)std::min<int64_t>(*ntiles, std::max<int64_t>(1, (kStepTargetWG + base - 1) / base));
+  const int target = step_target(SG, Mp);
+  int nc = (int)std::min<int64_t>(*ntiles, std::max<int64_t>(1, (target + base - 1) / base));
   *NT = (*ntiles + nc - 1) / nc;
   *nchunks = (*ntiles + *NT - 1) / *NT;
 }
 
-int step_w1_splits(int P, int SG, int Mrows, int Ncols) {
+int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols) {
   int mt, ntl, nc, NT;
-  step_plan(P, SG, Mrows, Ncols, &mt, &ntl, &nc, &NT);
+  step_plan(P, SG, Mp, Mrows, Ncols, &mt, &ntl, &nc, &NT);
   return nc;
 }
 
 void launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
-  step_plan(a.u.P, a.SG, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
+  step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
   const uint64_t lim = 0xffffffffull;
   const bool full = a.SG == 1 && a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mrows % kUM == 0 &&
