@@ -119,6 +119,14 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
         # written once; the cluster-mean variant moves the same bytes
         "step1_gemm": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
         "step1_gemm_group_mean": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
+        # update of every learner's W1 with the cluster (or global) mean
+        # written to every row: W1 read and written once per learner, G1 and
+        # the minibatch read
+        "update1_gemm_group_mean": (P * F * (2 * H * IN + B * H + B * IN), P * 2 * B * H * IN),
+        "update1_gemm_global_mean": (P * F * (2 * H * IN + B * H + B * IN), P * 2 * B * H * IN),
+        # next step's forward from each cluster's common W1: one copy per
+        # cluster, the minibatches, the pre-activations
+        "fwd1_group_gemm": (F * (G * H * IN + P * B * IN + P * B * H), P * 2 * B * H * IN),
     }
 
 

@@ -54,7 +54,8 @@ const char* kClassNames[KC_COUNT] = {
     "step1_gemm_group_mean",     "tail_group_mean", "gram", "fwd1_block_gemm", "block_update_gemm",
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
     "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step",
-    "fwd1_block_gemm_v", "scale_errors", "buffer_update_gemm"};
+    "fwd1_block_gemm_v", "scale_errors", "buffer_update_gemm", "update1_gemm_group_mean", "fwd1_group_gemm",
+    "update1_gemm_global_mean"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -107,6 +108,12 @@ struct hieravg {
   bool fused = false;       // the fused step kernel applies (SG = 1)
   bool fused_mean = false;  // ... and also with the cluster mean (SG = S)
   int KS_step = 1, KS_mean = 1;  // forward splits written by the fused kernel
+  // Block ends the fused mean step cannot take (S * B too large for its
+  // forward registers): the update with the cluster mean, then the next
+  // step's forward as one GEMM per cluster from the common first layer.
+  bool upd_mean = false;
+  int KS_g = 1, cps_g = 1;
+  bool upd_global = false;  // the round's last step: update with the global mean (SG = P)
   int ks_cur = 1;                // splits of the partials currently in `part`
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
@@ -324,6 +331,12 @@ int64_t plan(hieravg* h, int B) {
   if (h->fused) {
     h->KS_step = step_w1_splits(P, 1, h->Bp, (int)n1, (int)h->INp);
     ks_max = std::max<int64_t>(ks_max, h->KS_step);
+  }
+  h->upd_mean = mlp && h->fused && c.S > 1 && !h->fused_mean && step_w1_mean_supported(h->Bp, c.S);
+  h->upd_global = mlp && h->fused && step_w1_mean_supported(h->Bp, P);
+  if (h->upd_mean) {
+    plan_split_blk(P / c.S, c.S * h->Bp, (int)n1, (int)h->INp, &h->KS_g, &h->cps_g, HAV_FWD_BLOCK_TARGET);
+    ks_max = std::max<int64_t>(ks_max, h->KS_g);
   }
   if (h->fused_mean) {
     h->KS_mean = step_w1_splits(P, c.S, h->Bp, (int)n1, (int)h->INp);
@@ -642,6 +655,30 @@ bool launch_class(hieravg* h, int kc, int tt) {
       h->ks_cur = mean ? h->KS_mean : h->KS_step;
       return true;
     }
+    case KC_UPD1_MEAN:
+    case KC_UPD1_GLOBAL: {
+      const bool global = kc == KC_UPD1_GLOBAL;
+      if (global ? !h->upd_global : !h->upd_mean || tt + 1 >= h->T) return false;
+      StepArgs a{};
+      a.u = UpdArgs{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
+                    small ? nullptr : W + h->off_b1, P, B, Hp, INp, h->hyper};
+      a.SG = global ? P : S;
+      a.no_fwd = true;
+      a.x_rows = h->N;
+      launch_step_w1(s, a);
+      return true;
+    }
+    case KC_FWD1_GROUP: {
+      // Step tt's forward from each cluster's common first layer (every row of
+      // the cluster holds it; row g*S is read): SG = S learners per GEMM.
+      if (!h->upd_mean) return false;
+      FwdArgs f{h->X, ix, h->INp, W + h->off_W1, (int64_t)S * h->Dp, h->INp, h->part, P, B, Bp, Hp, INp,
+                h->KS_g, h->cps_g};
+      f.SG = S;
+      launch_fwd_blk(s, f);
+      h->ks_cur = h->KS_g;
+      return true;
+    }
     case KC_TAIL_MEAN: launch_group_mean(s, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P, S); return true;
     case KC_TAIL_GLOBAL: launch_group_mean(s, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P, P); return true;
     case KC_GRAM:
@@ -920,13 +957,21 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   const bool last = tt == T - 1;
   const bool mean = !last && (tt + 1) % c.K1 == 0 && c.S > 1;
   have_fwd = false;
-  if (last || !h->fused || (mean && !h->fused_mean)) {
+  if (last && h->upd_global) {  // with the global mean of every block
+    go(KC_UPD1_GLOBAL);
+    go(KC_TAIL_GLOBAL);
+  } else if (last || !h->fused || (mean && !h->fused_mean && !h->upd_mean)) {
     go(KC_UPDATE1);
     if (mean) go(KC_GROUP_MEAN);
     if (mean && h->cfg.avg_momentum && h->V) go(KC_VMEAN_GROUP);
-  } else if (mean) {
+  } else if (mean && h->fused_mean) {
     go(KC_STEP1_MEAN);
     go(KC_TAIL_MEAN);
+    have_fwd = true;
+  } else if (mean) {
+    go(KC_UPD1_MEAN);
+    go(KC_TAIL_MEAN);
+    run(h, KC_FWD1_GROUP, [&] { launch_class(h, KC_FWD1_GROUP, tt + 1); });
     have_fwd = true;
   } else {
     go(KC_STEP1);
@@ -1088,7 +1133,7 @@ void enqueue_round(hieravg* h) {
     run(h, KC_DRAW, [&] { launch_class(h, KC_DRAW, 0); });
     bool have_fwd = false;
     for (int tt = 0; tt < T; ++tt) enqueue_step(h, tt, have_fwd);
-    if (P > 1) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
+    if (P > 1 && !h->upd_global) run(h, KC_GLOBAL_MEAN, [&] { launch_class(h, KC_GLOBAL_MEAN, 0); });
     if (P > 1 && c.avg_momentum && h->V) run(h, KC_VMEAN_GLOBAL, [&] { launch_class(h, KC_VMEAN_GLOBAL, 0); });
   }
 }

@@ -117,6 +117,9 @@ enum KernelClass {
   KC_FWD1_BLOCK_V,   // heavy-ball delayed updates: X_k V^T of a block's steps from each learner's buffer
   KC_SCALE_ERRORS,   // heavy-ball delayed updates: the block's errors scaled for the block-end updates
   KC_BUF_UPDATE,     // heavy-ball delayed updates: block-end update of each learner's first-layer buffer
+  KC_UPD1_MEAN,      // layer-1 update of every learner with the local mean, no forward
+  KC_FWD1_GROUP,     // layer-1 forward of a step from each cluster's common first layer (one GEMM per cluster)
+  KC_UPD1_GLOBAL,    // layer-1 update of every learner with the global mean (a round's last step)
   KC_COUNT
 };
 
@@ -316,10 +319,14 @@ struct StepArgs {
   int SG;                   // learners averaged per group (1: no mean); SG | P
   int NT;                   // set by the launcher: 128-column tiles per workgroup
   int64_t x_rows = 0;       // rows of the dataset u.Bsrc (0: unknown)
+  bool no_fwd = false;      // SG > 1: the update and the group mean only (no partials)
 };
 // Whether the fused kernel handles this shape (Mp a multiple of 16 up to 64,
 // SG in {1, 2, 4, 8}, SG * Mp / 16 <= 16).
 bool step_w1_supported(int Mp, int SG);
+// Whether the update-and-group-mean form without the forward (no_fwd) takes
+// this shape: Mp a multiple of 16 up to 64, SG a power of two in [2, 64].
+bool step_w1_mean_supported(int Mp, int SG);
 // Number of forward splits KS the fused kernel writes for this shape.
 int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols);
 void launch_step_w1(hipStream_t s, StepArgs a);

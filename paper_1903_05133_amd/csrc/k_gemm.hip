@@ -482,15 +482,18 @@ constexpr int kStepMaxB = 64;  // largest minibatch of the fused step
 // Occupancy: at least four waves per SIMD for a single learner per group
 // (its prefetch registers then fit in 128 VGPRs), three with the group mean
 // of up to 8 x 16 forward rows (larger groups would spill).
-template <int SG, int MBF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4 : SG * MBF <= 8 ? 3 : 1))) void k_step_w1(
+// FWD = false: the update and the group mean only (no forward of the next
+// step, no partials); the next step's forward then runs as one GEMM per
+// group from the common result.
+template <int SG, int MBF, bool FWD = true>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(!FWD || SG == 1 ? 4 : SG * MBF <= 8 ? 3 : 1))) void k_step_w1(
     StepArgs a, int mtiles, int ntiles, int nchunks) {
   constexpr int MP = MBF * 16;        // rows of the next-step forward (padded minibatch)
   constexpr int kWL = kUM / kRP;      // W pieces per thread
   constexpr int kXL = kSC / kRP;      // stage input pieces per thread
   constexpr int kXN = (MP + kRP - 1) / kRP;  // next-step input pieces per thread
-  __shared__ __attribute__((aligned(16))) float lds[kSU + MP * kSL];
-  __shared__ int32_t rows_t[SG][kStepMaxB], rows_n[SG][kStepMaxB];
+  __shared__ __attribute__((aligned(16))) float lds[kSU + (FWD ? MP * kSL : 0)];
+  __shared__ int32_t rows_t[SG][kStepMaxB], rows_n[FWD ? SG : 1][FWD ? kStepMaxB : 1];
   float* As = lds;               // [kSC][kLA] error rows of a stage
   float* Bs = lds + kSC * kLA;   // [kSC][kSL] input rows of a stage
   float* Wt = lds;               // [kUM][kSL] gradient tile, then the new tile
@@ -514,7 +517,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
   for (int e = tid; e < SG * Kb; e += 256) {
     const int64_t g = (int64_t)pg * SG * Kb + e;
     rows_t[e / Kb][e % Kb] = u.idx[g];
-    rows_n[e / Kb][e % Kb] = a.idx_next[g];
+    if constexpr (FWD) rows_n[e / Kb][e % Kb] = a.idx_next[g];
   }
   __syncthreads();
 
@@ -561,6 +564,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
     }
   };
   auto load_next = [&](int n, int j) {  // X'[s][tile columns], s = pr0 + kRP*i
+    if constexpr (!FWD) return;
     const int col = n * kSN + 4 * pc4;
     const bool cok = col < u.Ncols;
 #pragma unroll
@@ -593,7 +597,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
   const int n_begin = chunk * a.NT, n_end = min(ntiles, n_begin + a.NT);
   load_stage(n_begin, 0, 0);
   load_w(n_begin, 0);
-  load_next(n_begin, 0);
+  if constexpr (FWD) load_next(n_begin, 0);
   f32x4 msum[kWL];
   for (int n = n_begin; n < n_end; ++n) {
     const int ncol0 = n * kSN;
@@ -645,7 +649,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
         const f32x4 wnew = wv[i] - lr * *t;
         if (SG == 1) {
           if (ok) *(f32x4*)(Wp + (int64_t)row * u.ldw + col) = wnew;
-          *t = ok ? wnew : zero4;
+          if constexpr (FWD) *t = ok ? wnew : zero4;
         } else {
           msum[i] = j == 0 ? wnew : msum[i] + wnew;
         }
@@ -665,8 +669,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
         if (ok)
           for (int j = 0; j < SG; ++j)
             *(f32x4*)(u.W + (int64_t)(pg * SG + j) * u.w_pitch + (int64_t)row * u.ldw + col) = mean;
-        *(f32x4*)&Wt[rl * kSL + 4 * pc4] = ok ? mean : zero4;
+        if constexpr (FWD) *(f32x4*)&Wt[rl * kSL + 4 * pc4] = ok ? mean : zero4;
       }
+    }
+    if constexpr (!FWD) {
+      __syncthreads();  // the next tile's stage overwrites the gradient tile
+      continue;
     }
 
     // Forward partials of the next step for every learner of the group.
@@ -697,7 +705,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SG == 1 ? 4
     }
   }
 
-  if (fwd_on) {
+  if (FWD && fwd_on) {
     const int h = mrow0 + 16 * wave + lrow;
 #pragma unroll
     for (int j = 0; j < SG; ++j) {
@@ -757,11 +765,8 @@ __device__ inline void buf_st16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int sof
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
 }
 
-#ifndef HAV_STEP_GP
-#define HAV_STEP_GP 1
-#endif
 template <int MBF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 && HAV_STEP_GP ? 3 : 4))) void k_step_w1_full(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3 : 4))) void k_step_w1_full(
     StepArgs a, int mtiles, int ntiles, int nchunks) {
   constexpr int MP = MBF * 16;   // samples of a step (= Kb = Mp)
   constexpr int kWL = kUM / kRP;
@@ -927,6 +932,10 @@ bool step_w1_supported(int Mp, int SG) {
   return SG * (Mp / 16) <= 16;
 }
 
+bool step_w1_mean_supported(int Mp, int SG) {
+  return Mp >= 1 && Mp <= kStepMaxB && Mp % 16 == 0 && SG >= 2 && SG <= 64 && (SG & (SG - 1)) == 0;
+}
+
 #ifndef HAV_STEP_TARGET_WG64
 #define HAV_STEP_TARGET_WG64 1536
 #endif
@@ -955,6 +964,17 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
   step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
+  if (a.no_fwd) {
+    switch (a.SG) {
+      case 2: launch(k_step_w1<2, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 4: launch(k_step_w1<4, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 8: launch(k_step_w1<8, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 16: launch(k_step_w1<16, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 32: launch(k_step_w1<32, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      default: launch(k_step_w1<64, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+    }
+    return;
+  }
   const uint64_t lim = 0xffffffffull;
   const bool full = a.SG == 1 && a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mrows % kUM == 0 &&
                     a.u.Ncols % kSN == 0 && a.x_rows > 0 && (uint64_t)a.x_rows * a.u.ldb * 4 < lim &&

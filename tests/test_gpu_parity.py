@@ -76,6 +76,13 @@ SMALL = {
     "mlp_batch_150": cases.case("mlp", 2, 2, 1, 1, B=150, IN=200, H=130, C=7, N=300, lr=0.05, seed=6),
     # fused step kernel with the cluster mean of 8 learners, one 16-row batch tile
     "mlp_group_mean_S8": cases.case("mlp", 16, 8, 2, 2, B=12, IN=200, H=70, C=5, N=300, lr=0.1, seed=13),
+    # block ends beyond the fused mean step (S * padded B over 256 rows): the
+    # update with the cluster mean, then one forward GEMM per cluster; ragged
+    # samples, rows and columns, and the more-than-32-class head (b1 stepped
+    # in the update kernel)
+    "mlp_update_mean_S8_B40": cases.case("mlp", 16, 8, 2, 2, B=40, IN=200, H=70, C=5, N=300, lr=0.1, seed=19),
+    "mlp_update_mean_S16_c40": cases.case("mlp", 16, 16, 2, 2, B=20, IN=130, H=90, C=40, N=200, sigma=0.5,
+                                          lr=0.05, seed=20),
     # fused step with the mean of 4 learners on the softmax model; ragged last column tile
     "softmax_group_mean_S4": cases.case("softmax", 8, 4, 1, 3, B=20, IN=130, C=12, N=90, lr=0.2, seed=14),
     # B = 32: the block update's stages are whole (step, learner) runs of
@@ -102,6 +109,20 @@ def test_small_cases_match_oracle(name, gpu_lib):
     got, idx, steps = _run_gpu(c, rounds=2, mode="eager")
     assert steps == 2 * c["K1"] * c["K2"]
     _check(c, got, idx, *_oracle(c, 2), mode="eager")
+
+
+@pytest.mark.parametrize("name", ["mlp_update_mean_S8_B40", "mlp_update_mean_S16_c40"])
+def test_update_mean_block_end_kernels(name, gpu_lib):
+    """Eager block ends of S * B too large for the fused mean step take the
+    update-with-mean kernel and the per-cluster forward GEMM."""
+    from paper_1903_05133_amd import HierAvg
+    c = SMALL[name]
+    with HierAvg(config=cases.native_config(c, "eager")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+    assert "update1_gemm_group_mean" in stats and "fwd1_group_gemm" in stats, stats
+    assert "step1_gemm_group_mean" not in stats and "group_mean" not in stats, stats
 
 
 # MLP cases within the delayed-update limits (at most 32 classes, B <= 32, K1 <= 8)
@@ -342,11 +363,13 @@ def test_torch_stream_and_profile(gpu_lib):
         assert np.array_equal(h.params(), ref)
     # P=4 S=2 K1=2 K2=2, padded batch 48: the stand-alone forward at step 0,
     # the fused step (with the cluster mean at the end of block 0) at steps
-    # 0-2, the plain update at the last step, then the global mean.
-    assert stats["fwd1_gemm"][0] == 1 and stats["update1_gemm"][0] == 1
+    # 0-2, the last step's update with the global mean of W1, then that of
+    # the other blocks.
+    assert stats["fwd1_gemm"][0] == 1 and "update1_gemm" not in stats
     assert stats["step1_gemm"][0] == 2 and stats["step1_gemm_group_mean"][0] == 1
     assert stats["tail_group_mean"][0] == 1 and "group_mean" not in stats
-    assert stats["draw_indices"][0] == 1 and stats["global_mean"][0] == 1
+    assert stats["update1_gemm_global_mean"][0] == 1 and stats["tail_global_mean"][0] == 1
+    assert stats["draw_indices"][0] == 1 and "global_mean" not in stats
     assert all(ms >= 0.0 for _, ms in stats.values())
 
 
