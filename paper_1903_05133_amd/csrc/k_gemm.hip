@@ -772,6 +772,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
   constexpr int kWL = kUM / kRP;
   constexpr int kXN = MP / kRP;  // pieces per thread of a 64-column tile of MP rows
   constexpr int kGL = MP * 16 / 256;  // pieces per thread of the G tile (MP rows x 64 units)
+  constexpr int kUF = MBF > 2 ? 1 : HAV_STEP_UNROLL_F;  // forward unroll (64 samples: register pressure)
   constexpr int kBR = MP > kUM ? MP : kUM;
   static_assert(MP % kSC == 0 && kXN * kRP == MP, "full-tile step shapes");
   // Gs: the step's errors of this row tile (constant over the column tiles);
@@ -894,7 +895,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
     __builtin_amdgcn_s_setprio(1);
-#pragma unroll(MBF > 2 ? 1 : HAV_STEP_UNROLL_F)
+#pragma unroll kUF
     for (int q = 0; q < kSN / 16; ++q) {
       const f32x4 b = *(const f32x4*)&Wt[(16 * wave + lrow) * kSL + 16 * q + 4 * lgrp];
       f32x4 af[MBF];
