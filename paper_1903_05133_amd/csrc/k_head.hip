@@ -85,6 +85,60 @@ __global__ __launch_bounds__(256) void k_softmax_grad(const float* __restrict__ 
   for (int c = lane; c < C; c += 64) g[c] = (g[c] / sum - (c == y ? 1.0f : 0.0f)) * invB;
 }
 
+// The same for C <= 64 * NPL with the logits in registers (lane: classes
+// lane + 64j): one pass over the partials, no logits written and read back,
+// the label issued first.  Same arithmetic in the same order as
+// k_softmax_grad.
+template <int NPL>
+__global__ __launch_bounds__(256) void k_softmax_grad_reg(const float* __restrict__ part, int KS,
+                                                          const float* __restrict__ bias, int64_t w_pitch,
+                                                          const int32_t* __restrict__ labels,
+                                                          const int32_t* __restrict__ idx, float* __restrict__ G,
+                                                          int P, int M, int Mp, int C, int Cp) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= P * M) return;
+  const int p = row / M, m = row % M;
+  const int y = labels[idx[(int64_t)p * M + m]];
+  const int64_t stride = (int64_t)P * Mp * Cp;
+  const int64_t base = ((int64_t)p * Mp + m) * Cp;
+  const float* b = bias + (int64_t)p * w_pitch;
+  float v[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int c = lane + 64 * j;
+    const float bv = b[c < C ? c : C - 1];
+    v[j] = c < C ? bv : -INFINITY;
+  }
+  for (int ks = 0; ks < KS; ++ks) {
+    const float* pk = part + ks * stride + base;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int c = lane + 64 * j;
+      const float pv = pk[c < C ? c : C - 1];
+      v[j] += c < C ? pv : 0.0f;
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) mx = fmaxf(mx, v[j]);
+  mx = wave_max(mx);
+  float sum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    v[j] = lane + 64 * j < C ? expf(v[j] - mx) : 0.0f;
+    sum += v[j];
+  }
+  sum = wave_sum(sum);
+  const float invB = 1.0f / (float)M;
+  float* g = G + base;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int c = lane + 64 * j;
+    if (c < C) g[c] = (v[j] / sum - (c == y ? 1.0f : 0.0f)) * invB;
+  }
+}
+
 // G1[p][m][h] = (sum_{c<C} G2[p][m][c] * W2_p[c][h]) * [Z1[p][m][h] > 0] for
 // m < M.  Workgroup (p, 64 hidden units): lane = unit, wave w = a quarter of
 // each 64-class chunk of G2 (staged in LDS, 16 samples at a time); the four
@@ -1079,7 +1133,20 @@ void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* b
 void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch,
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp) {
   const int rows = P * M;
-  launch(k_softmax_grad, (rows + 3) / 4, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  const unsigned grid = (unsigned)((rows + 3) / 4);
+  const int npl = (C + 63) / 64;
+  if (npl <= 1)
+    launch(k_softmax_grad_reg<1>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  else if (npl <= 2)
+    launch(k_softmax_grad_reg<2>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  else if (npl <= 4)
+    launch(k_softmax_grad_reg<4>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  else if (npl <= 8)
+    launch(k_softmax_grad_reg<8>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  else if (npl <= 16)
+    launch(k_softmax_grad_reg<16>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+  else
+    launch(k_softmax_grad, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
 }
 
 void launch_scale_errors(hipStream_t s, const float* Gs, float* Gu, float* Gt, const float* hb, int K1, int64_t n) {
