@@ -130,7 +130,10 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
     }
 
 
-def kernel_work(c):
+def kernel_work(c, classes=None):
+    """Algorithmic (bytes, flops) per launch of each kernel class; `classes`
+    (the classes a round launched) tells whether the hidden-error kernel also
+    took the second layer's step (no update2_gemm in the round)."""
     P, S, K1, K2 = c["P"], c["S"], c["K1"], c["K2"]
     if c["kind"] == "averaging":
         D = c["IN"]
@@ -151,6 +154,10 @@ def kernel_work(c):
                 "step1_gemm_group_mean": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
                 "global_mean": (2 * F * P * D, P * D)}
     w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"])
+    if classes is not None and "bwd_hidden" in classes and "update2_gemm" not in classes:
+        # hidden error and the W2 step in one pass: G2, W2, Z1 read, G1 and W2 written
+        B, H, C = c["B"], c["H"], c["C"]
+        w["bwd_hidden"] = (P * F * (B * C + 2 * C * H + 2 * B * H + C), P * 4 * B * C * H)
     D = c["H"] * c["IN"] + c["H"] + c["C"] * c["H"] + c["C"]
     tail = D - c["H"] * c["IN"]
     w["group_mean"] = (2 * F * P * D, P * D)
@@ -225,7 +232,7 @@ def summarize(name, c, ms_round, stats, dur_ms):
     method's algorithmic flops and bytes per round as fractions of the peaks,
     and every kernel class with its measured duration and roofline."""
     P, K1, K2 = c["P"], c["K1"], c["K2"]
-    work = kernel_work(c)
+    work = kernel_work(c, stats)
     kernels = {}
     total = sum(t for _, t in stats.values())
     for k, (n, tot) in stats.items():
@@ -260,7 +267,7 @@ def roofline(c, stats, dur_ms):
     """The dominant kernel (largest launches x duration among the kernels
     with a stated algorithmic work) against the peak of the resource whose
     ideal time for that work is longer."""
-    work = kernel_work(c)
+    work = kernel_work(c, stats)
     dom = max((k for k in dur_ms if work.get(k, (0, 0))[1] or work.get(k, (0, 0))[0]),
               key=lambda k: dur_ms[k] * stats[k][0])
     avg_s = dur_ms[dom] * 1e-3

@@ -114,6 +114,9 @@ struct hieravg {
   bool upd_mean = false;
   int KS_g = 1, cps_g = 1;
   bool upd_global = false;  // the round's last step: update with the global mean (SG = P)
+  // More than 32 classes, B <= 32, plain SGD: the hidden-error kernel also
+  // steps W2 and b2 (no update GEMM for the second layer).
+  bool w2_fused = false;
   int ks_cur = 1;                // splits of the partials currently in `part`
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
@@ -334,6 +337,8 @@ int64_t plan(hieravg* h, int B) {
   }
   h->upd_mean = mlp && h->fused && c.S > 1 && !h->fused_mean && step_w1_mean_supported(h->Bp, c.S);
   h->upd_global = mlp && h->fused && step_w1_mean_supported(h->Bp, P);
+  h->w2_fused = mlp && c.classes > kSmallC && bwd_hidden_update_supported(B) && c.momentum == 0.0f &&
+                c.weight_decay == 0.0f;
   if (h->upd_mean) {
     plan_split_blk(P / c.S, c.S * h->Bp, (int)n1, (int)h->INp, &h->KS_g, &h->cps_g, HAV_FWD_BLOCK_TARGET);
     ks_max = std::max<int64_t>(ks_max, h->KS_g);
@@ -881,7 +886,11 @@ bool launch_class(hieravg* h, int kc, int tt) {
       if (h->in_delayed)  // the hidden errors are kept for the block end; b1 takes its step here
         launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->Gs + (int64_t)(tt % c.K1) * P * Bp * Hp, P, B,
                           Bp, C, Cp, Hp, W + h->off_b1, h->hyper, h->hb && h->V ? h->V + h->off_b1 : nullptr,
-                          h->hb ? c.momentum : 0.0f, h->hb ? c.weight_decay : 0.0f);
+                          h->hb ? c.momentum : 0.0f, h->hb ? c.weight_decay : 0.0f,
+                          h->w2_fused ? W + h->off_b2 : nullptr);
+      else if (h->w2_fused)
+        launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp, nullptr, h->hyper,
+                          nullptr, 0.0f, 0.0f, W + h->off_b2);
       else
         launch_bwd_hidden(s, h->G2, W + h->off_W2, h->Dp, h->Z1, h->G1, P, B, Bp, C, Cp, Hp);
       return true;
@@ -916,7 +925,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     }
     case KC_UPDATE2: {
-      if (small) return false;
+      if (small || h->w2_fused) return false;
       UpdArgs u{h->G2, h->Cp, Bp, h->Z1, nullptr, h->Hp, W + h->off_W2, h->Dp, h->Hp, W + h->off_b2, P, B, Cp, Hp,
                 h->hyper};
       with_momentum(h, u, h->off_W2, h->off_b2);
@@ -948,7 +957,7 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
     n = 2;
   } else {
     seq = kLarge;
-    n = 5;
+    n = h->w2_fused ? 4 : 5;  // KC_UPDATE2 last: the hidden-error kernel steps W2 and b2
   }
   auto go = [&](int kc) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
   if (!have_fwd) go(KC_FWD1);
@@ -1118,7 +1127,8 @@ void enqueue_round(hieravg* h) {
         go(KC_HEAD_END, b * c.K1 + c.K1 - 1);
       } else {  // more than 32 classes: the layer-2 GEMMs of the eager head, per step
         for (int k = 0; k < c.K1; ++k)
-          for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2}) go(kc, b * c.K1 + k);
+          for (int kc : {KC_Z1_DELAYED, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2})
+            if (kc != KC_UPDATE2 || !h->w2_fused) go(kc, b * c.K1 + k);
       }
       if (h->hb) go(KC_SCALE_ERRORS, b * c.K1);
       // with the cluster mean of b1, W2, b2 for b < K2 - 1; the last block's

@@ -340,9 +340,14 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
 // b1[h] -= lr * sum_m G1[m][h] (delayed updates, where no update GEMM steps b1).
 // vb1 (optional, with b1): heavy-ball buffer of b1 (laid out like it) for the
 // step with momentum mu and decay wd (d = sum + wd*b1; v <- mu*v + d).
-void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
-                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1 = nullptr,
-                       const float* lr = nullptr, float* vb1 = nullptr, float mu = 0.0f, float wd = 0.0f);
+// b2 (M <= 32, plain SGD; lr required): also the second layer's step,
+// W2 -= lr * G2^T relu(Z1) and b2 -= lr * column sums of G2, in the same pass
+// over W2 (no update GEMM for this layer).
+void launch_bwd_hidden(hipStream_t s, const float* G2, float* W2, int64_t w_pitch, const float* Z1, float* G1, int P,
+                       int M, int Mp, int C, int Cp, int Hp, float* b1 = nullptr, const float* lr = nullptr,
+                       float* vb1 = nullptr, float mu = 0.0f, float wd = 0.0f, float* b2 = nullptr);
+// Whether launch_bwd_hidden takes the second layer's step for M samples.
+bool bwd_hidden_update_supported(int M);
 // Heavy-ball delayed updates, after a block's last step: Gu[k] = u_{K1-1-k}
 // Gs[k] and (Gt set) Gt[k] = t_{K1-1-k} Gs[k] for k < K1, n floats per step
 // (n a multiple of 4).

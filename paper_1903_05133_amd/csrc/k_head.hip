@@ -216,16 +216,27 @@ __global__ __launch_bounds__(256) void k_bwd_hidden(const float* __restrict__ G2
 // c + 2 are in flight while chunk c is multiplied; the four partial blocks
 // are added in wave order through LDS.  Rows past M and classes past Cp read
 // as zero.  b1 (M <= 32 only): also the step b1[h] -= lr * sum_m G1[m][h].
+//
+// UPD (one sample tile, plain SGD): the workgroup also takes the second
+// layer's SGD step on its slab W2[:, h0 .. h0+32) while each chunk is in LDS:
+// dW2 = G2^T relu(Z1) for the chunk's classes on 16x16x4 MFMAs (wave w:
+// classes 16w .. 16w+15 of the chunk, both 16-unit halves; k = the 32
+// samples), the new values written once from the old ones in LDS after
+// they fed the hidden error.  The workgroup of slice 0 also steps b2.  No
+// other workgroup reads or writes these columns of W2, so the update-GEMM's
+// separate pass over W2 is not needed.
 constexpr int kBhM = 32, kBhN = 32, kBhC = 64;
 constexpr int kBhLG = kBhM + 1, kBhLW = kBhN + 4;  // odd G2 stride: the transposing stores spread over the banks
 constexpr int kBhLds = 2 * kBhC * (kBhLG + kBhLW);
-__global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict__ G2, const float* __restrict__ W2,
+template <bool UPD>
+__global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict__ G2, float* __restrict__ W2,
                                                          int64_t w_pitch, const float* __restrict__ Z1,
                                                          float* __restrict__ G1, int M, int Mp, int Cp, int Hp,
                                                          int htiles, int mtiles, float* __restrict__ b1,
                                                          const float* __restrict__ lr_ptr, float* __restrict__ vb1,
-                                                         float mu, float wd) {
+                                                         float mu, float wd, float* __restrict__ b2) {
   __shared__ __attribute__((aligned(16))) float lds[kBhLds];
+  __shared__ float a1s[UPD ? kBhM : 1][kBhN + 1];  // relu(Z1) of the tile (UPD)
   // buffer b: G2 chunk [class][sample] at gsb(b), W2 chunk [class][unit] at wsb(b)
   auto gsb = [&](int b) { return lds + b * (kBhC * kBhLG); };
   auto wsb = [&](int b) { return lds + 2 * kBhC * kBhLG + b * (kBhC * kBhLW); };
@@ -236,9 +247,18 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
   const int l32 = lane & 31, lhi = lane >> 5;
   const int m0 = mt * kBhM, h0 = ht * kBhN;
   const float* g2 = G2 + (int64_t)p * Mp * Cp;
-  const float* w2 = W2 + (int64_t)p * w_pitch;
+  float* w2 = W2 + (int64_t)p * w_pitch;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   const int nch = (Cp + kBhC - 1) / kBhC;
+  const float lr = lr_ptr ? *lr_ptr : 0.0f;  // the eager form without steps passes no step size
+  if constexpr (UPD) {  // relu(Z1)[m][h0 + 4(t%8) ..] of the tile; rows past M are zero
+    const int m = tid >> 3, hq = 4 * (tid & 7);
+    const f32x4 z = *(const f32x4*)(Z1 + ((int64_t)p * Mp + (m < M ? m : 0)) * Hp + h0 + hq);
+    a1s[m][hq + 0] = m < M ? fmaxf(z.x, 0.0f) : 0.0f;
+    a1s[m][hq + 1] = m < M ? fmaxf(z.y, 0.0f) : 0.0f;
+    a1s[m][hq + 2] = m < M ? fmaxf(z.z, 0.0f) : 0.0f;
+    a1s[m][hq + 3] = m < M ? fmaxf(z.w, 0.0f) : 0.0f;
+  }
 
   // G2 pieces: q = tid + 256*i, sample q >> 4, classes 4*(q & 15) .. +3.
   // W2 pieces: q = tid + 256*i, class q >> 3, units 4*(q & 7) .. +3.
@@ -299,6 +319,33 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
       const int k = wave * (kBhC / 4) + ss + lhi;
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(gb[k * kBhLG + l32], wb[k * kBhLW + l32], acc, 0, 0, 0);
     }
+    if constexpr (UPD) {
+      // dW2 of classes 16w + i (i = lane%16 for A, rows 4(lane/16) + r of the
+      // result) and units j = lane%16 of each half, over the 32 samples.
+      const int i16 = lane & 15, k16 = lane >> 4;
+      f32x4 d0 = zero4, d1 = zero4;
+#pragma unroll
+      for (int kk = 0; kk < kBhM / 4; ++kk) {
+        const int m = 4 * kk + k16;
+        const float av = gb[(16 * wave + i16) * kBhLG + m];
+        d0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, a1s[m][i16], d0, 0, 0, 0);
+        d1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, a1s[m][16 + i16], d1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int cl = 16 * wave + 4 * k16 + r, c = ch * kBhC + cl;
+        if (c < Cp) {
+          w2[(int64_t)c * Hp + h0 + i16] = wb[cl * kBhLW + i16] - lr * d0[r];
+          w2[(int64_t)c * Hp + h0 + 16 + i16] = wb[cl * kBhLW + 16 + i16] - lr * d1[r];
+        }
+      }
+      if (ht == 0 && tid < kBhC && ch * kBhC + tid < Cp) {  // b2: column sums of G2 over the samples
+        float sb = 0.0f;
+#pragma unroll 8
+        for (int m = 0; m < kBhM; ++m) sb += gb[tid * kBhLG + m];
+        b2[(int64_t)p * w_pitch + ch * kBhC + tid] -= lr * sb;
+      }
+    }
     if (ch + 1 < nch) {
       if (buf == 0)
         store(1, ga[1], wa[1]);
@@ -333,7 +380,7 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
       if (lhi == 0) {
         float* bp = b1 + (int64_t)p * w_pitch + h;
         if (mu == 0.0f && wd == 0.0f) {
-          *bp -= *lr_ptr * (db + other);
+          *bp -= lr * (db + other);
         } else {  // heavy-ball step with decay: d = g + wd*b; v <- mu*v + d; b <- b - lr*v
           float d = (db + other) + wd * *bp;
           if (vb1) {
@@ -341,7 +388,7 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
             d = mu * *vp + d;
             *vp = d;
           }
-          *bp -= *lr_ptr * d;
+          *bp -= lr * d;
         }
       }
     }
@@ -1157,18 +1204,25 @@ void launch_scale_errors(hipStream_t s, const float* Gs, float* Gu, float* Gt, c
          n4);
 }
 
-void launch_bwd_hidden(hipStream_t s, const float* G2, const float* W2, int64_t w_pitch, const float* Z1,
-                       float* G1, int P, int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr, float* vb1,
-                       float mu, float wd) {
+void launch_bwd_hidden(hipStream_t s, const float* G2, float* W2, int64_t w_pitch, const float* Z1, float* G1, int P,
+                       int M, int Mp, int C, int Cp, int Hp, float* b1, const float* lr, float* vb1, float mu, float wd,
+                       float* b2) {
   if (b1 && M > kBhM) {  // the b1 step needs every sample in one workgroup
     const int htiles = (Hp + 63) / 64;
     launch(k_bwd_hidden, P * htiles, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, C, Cp, Hp, htiles, b1, lr);
     return;
   }
   const int htiles = Hp / kBhN, mtiles = (M + kBhM - 1) / kBhM;
-  launch(k_bwd_hidden_mfma, (unsigned)((int64_t)P * mtiles * htiles), 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, Cp,
-         Hp, htiles, mtiles, b1, lr, vb1, mu, wd);
+  const unsigned grid = (unsigned)((int64_t)P * mtiles * htiles);
+  if (b2)
+    launch(k_bwd_hidden_mfma<true>, grid, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, Cp, Hp, htiles, mtiles, b1, lr, vb1,
+           mu, wd, b2);
+  else
+    launch(k_bwd_hidden_mfma<false>, grid, 256, 0, s, G2, W2, w_pitch, Z1, G1, M, Mp, Cp, Hp, htiles, mtiles, b1, lr,
+           vb1, mu, wd, (float*)nullptr);
 }
+
+bool bwd_hidden_update_supported(int M) { return M <= kBhM; }
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
                    int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp,

@@ -164,6 +164,8 @@ def test_large_class_delayed_updates_match_oracle(name, gpu_lib):
         got = h.params()
         idx = h.last_indices()
     assert "block_update_gemm" in stats and "z1_delayed" in stats and "head_step" not in stats
+    # plain SGD, B <= 32: the hidden-error kernel also steps W2 and b2
+    assert "bwd_hidden" in stats and "update2_gemm" not in stats
     if c["IN"] >= 1024:
         assert "gram_reduce" in stats
     _check(c, got, idx, *_oracle(c, 2), mode="delayed")
@@ -280,6 +282,7 @@ def test_named_large_mlp_workload(gpu_lib):
         idx = h.last_indices()
     assert {"gram", "gram_reduce", "fwd1_block_gemm", "z1_delayed", "block_update_gemm"} <= set(stats)
     assert stats["block_update_gemm"][0] == 2 and stats["z1_delayed"][0] == 8
+    assert stats["bwd_hidden"][0] == 8 and "update2_gemm" not in stats
     st, mon, rerun = _oracle(c)
     prob = cases.oracle_problem(c)
     assert np.array_equal(idx.astype(np.int64), st.last_indices), "minibatch indices differ"
