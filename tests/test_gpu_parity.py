@@ -171,11 +171,12 @@ def test_large_class_delayed_updates_match_oracle(name, gpu_lib):
     _check(c, got, idx, *_oracle(c, 2), mode="delayed")
 
 
-@pytest.mark.parametrize("K1,C", [(8, 7), (6, 20)])
-def test_delayed_updates_long_block(K1, C, gpu_lib):
-    """Blocks of more than four steps (K1 = 8 is the largest the delayed path
-    takes), with 16- and 32-class head tiles; B = 32, S = 2, three blocks."""
-    c = cases.case("mlp", 4, 2, K1, 3, B=32, IN=130, H=96, C=C, N=400, sigma=0.5, lr=0.05, seed=15)
+@pytest.mark.parametrize("K1,C,B", [(8, 7, 32), (6, 20, 32), (7, 12, 32), (5, 7, 20), (2, 5, 17)])
+def test_delayed_updates_long_block(K1, C, B, gpu_lib):
+    """Blocks of two to eight steps (K1 = 8 is the largest the delayed path
+    takes) with 32-sample Gram blocks (full and ragged minibatches), 16- and
+    32-class head tiles; S = 2, three blocks."""
+    c = cases.case("mlp", 4, 2, K1, 3, B=B, IN=130, H=96, C=C, N=400, sigma=0.5, lr=0.05, seed=15)
     got, idx, _ = _run_gpu(c, rounds=1, mode="delayed")
     _check(c, got, idx, *_oracle(c, 1), mode="delayed")
 
