@@ -927,6 +927,141 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
   }
 }
 
+// Full-tile update with the group mean (no forward) for groups of SG
+// learners: per 64-column tile, each learner's new tile W_j - lr * G_j^T X_j
+// (the update of k_step_w1_full), added in learner order and scaled by 1/SG
+// (SG a power of two: exact), the mean written to every learner's row.  Per
+// learner the errors and input rows of the tile are staged through LDS while
+// the next learner's are loaded; every global access is a buffer access with
+// a fixed per-lane offset (the gathered rows' byte offsets from LDS) and a
+// scalar offset.  Same launch conditions as k_step_w1_full.
+template <int SG>
+__global__ __launch_bounds__(256) void k_step_mean_full(StepArgs a, int mtiles, int ntiles, int nchunks) {
+  constexpr int MP = 64;            // largest minibatch of the full-tile forms
+  constexpr int kWL = kUM / kRP;    // W pieces per thread (4)
+  constexpr int kXL = MP / kRP;     // G and X pieces per thread (4 each, 64 rows)
+  __shared__ __attribute__((aligned(16))) float Gs[MP * kLA];  // then the gradient tile Wt
+  __shared__ __attribute__((aligned(16))) float Bs[MP * kSL];
+  __shared__ uint32_t roff[SG][MP];
+  float* Wt = Gs;
+  static_assert(kUM * kSL <= MP * kLA, "gradient tile fits in the error stage");
+  const UpdArgs& u = a.u;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = bid % mtiles;
+  const int chunk = (bid / mtiles) % nchunks;
+  const int pg = bid / (mtiles * nchunks);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int mrow0 = mt * kUM;
+  const int wn = (wave & 1) * (kSN / 2), wm = (wave >> 1) * 32;
+  const int pc4 = tid % kSP, pr0 = tid / kSP;
+  const float lr = *u.lr;
+  const int Kb = u.Kb;  // = u.Mp, a multiple of 32 up to MP
+  for (int e = tid; e < SG * Kb; e += 256)
+    roff[e / Kb][e % Kb] = (uint32_t)((uint64_t)u.idx[(int64_t)pg * SG * Kb + e] * (uint64_t)u.ldb * 4u);
+  __syncthreads();
+  const uint32_t vo_g = (uint32_t)(pr0 * u.ldg + 4 * pc4) * 4u;
+  const uint32_t vo_w = (uint32_t)(pr0 * u.ldw + 4 * pc4) * 4u;
+  const int g16 = kRP * (int)u.ldg * 4, w16 = kRP * (int)u.ldw * 4;
+  const __amdgpu_buffer_rsrc_t rX = buf_rsrc(u.Bsrc, (uint64_t)a.x_rows * u.ldb * 4);
+  auto rG = [&](int j) {
+    return buf_rsrc(u.G + (int64_t)(pg * SG + j) * u.Mp * u.ldg + mrow0, (uint64_t)u.Mp * u.ldg * 4);
+  };
+  auto rW = [&](int j) {
+    return buf_rsrc(u.W + (int64_t)(pg * SG + j) * u.w_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
+  };
+  const int nst = Kb / kRP;  // 16-row passes of the minibatch (2 or 4)
+
+  f32x4 ga[kXL], xb[kXL], wv[kWL], msum[kWL];
+  auto load_item = [&](int n, int j) {  // errors and input rows of learner j, tile n
+    const __amdgpu_buffer_rsrc_t r = rG(j);
+#pragma unroll
+    for (int i = 0; i < kXL; ++i) {
+      const int ii = i < nst ? i : 0;  // passes past the minibatch repeat pass 0 (not stored)
+      ga[i] = buf_ld16(r, vo_g, ii * g16);
+      xb[i] = buf_ld16(rX, roff[j][pr0 + kRP * ii] + 16u * pc4, n * kSN * 4);
+    }
+  };
+  auto load_w = [&](int n, int j) {
+    const __amdgpu_buffer_rsrc_t r = rW(j);
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) wv[i] = buf_ld16(r, vo_w, n * kSN * 4 + i * w16);
+  };
+  f32x16 acc[kNA];
+
+  const int n_begin = chunk * a.NT, n_end = min(ntiles, n_begin + a.NT);
+  load_item(n_begin, 0);
+  load_w(n_begin, 0);
+  for (int n = n_begin; n < n_end; ++n) {
+#pragma unroll 1
+    for (int j = 0; j < SG; ++j) {
+      // next item: the next learner, else the next tile, else this item again
+      const bool more = j + 1 < SG || n + 1 < n_end;
+      const int jn = j + 1 < SG ? j + 1 : more ? 0 : j;
+      const int nn = j + 1 < SG ? n : more ? n + 1 : n;
+#pragma unroll
+      for (int i = 0; i < kXL; ++i)
+        if (i < nst) {
+          *(f32x4*)&Gs[(pr0 + kRP * i) * kLA + 4 * pc4] = ga[i];
+          *(f32x4*)&Bs[(pr0 + kRP * i) * kSL + 4 * pc4] = xb[i];
+        }
+      load_item(nn, jn);
+#pragma unroll
+      for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[jj][r] = 0.0f;
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      __builtin_amdgcn_s_setprio(1);
+      for (int s0 = 0; s0 < Kb; s0 += kSC) {  // 32-sample stages, each fully unrolled
+#pragma unroll
+        for (int ss = 0; ss < kSC; ss += 2) {
+          const int sr = s0 + ss + lhi;
+          const float av = Gs[sr * kLA + wm + l32];
+#pragma unroll
+          for (int jj = 0; jj < kNA; ++jj)
+            acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, Bs[sr * kSL + wn + 32 * jj + l32], acc[jj], 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_s_setprio(0);
+      __syncthreads();
+#pragma unroll
+      for (int jj = 0; jj < kNA; ++jj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+          Wt[row * kSL + wn + 32 * jj + l32] = acc[jj][r];
+        }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) {
+        const f32x4 wnew = wv[i] - lr * *(const f32x4*)&Wt[(pr0 + kRP * i) * kSL + 4 * pc4];
+        msum[i] = j == 0 ? wnew : msum[i] + wnew;
+      }
+      load_w(nn, jn);
+      __syncthreads();  // the next item's stage overwrites the gradient tile
+    }
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) msum[i] = msum[i] * (1.0f / (float)SG);
+    for (int j = 0; j < SG; ++j) {
+      const __amdgpu_buffer_rsrc_t r = rW(j);
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) buf_st16(r, vo_w, n * kSN * 4 + i * w16, msum[i]);
+    }
+  }
+  // Bias step (more than 32 classes), once per learner and row tile.
+  if (chunk == 0 && u.bias != nullptr && tid < kUM) {
+    const int m = mrow0 + tid;
+    for (int j = 0; j < SG; ++j) {
+      const int p = pg * SG + j;
+      const float* Gp = u.G + (int64_t)p * u.Mp * u.ldg;
+      float sum = 0.0f;
+      for (int s = 0; s < Kb; ++s) sum += Gp[(int64_t)s * u.ldg + m];
+      u.bias[(int64_t)p * u.w_pitch + m] -= lr * sum;
+    }
+  }
+}
+
 bool step_w1_supported(int Mp, int SG) {
   if (Mp < 1 || Mp > kStepMaxB || Mp % 16 != 0) return false;
   if (SG != 1 && SG != 2 && SG != 4 && SG != 8) return false;
@@ -965,6 +1100,21 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
   step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
+  const uint64_t lim = 0xffffffffull;
+  const bool full = a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mp <= kStepMaxB && a.u.Mrows % kUM == 0 &&
+                    a.u.Ncols % kSN == 0 && a.x_rows > 0 && (uint64_t)a.x_rows * a.u.ldb * 4 < lim &&
+                    (uint64_t)a.u.Mp * a.u.ldg * 4 < lim && (uint64_t)kUM * a.u.ldw * 4 < lim;
+  if (a.no_fwd && full) {
+    switch (a.SG) {
+      case 2: launch(k_step_mean_full<2>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 4: launch(k_step_mean_full<4>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 8: launch(k_step_mean_full<8>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 16: launch(k_step_mean_full<16>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      case 32: launch(k_step_mean_full<32>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+      default: launch(k_step_mean_full<64>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
+    }
+    return;
+  }
   if (a.no_fwd) {
     switch (a.SG) {
       case 2: launch(k_step_w1<2, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
@@ -976,11 +1126,7 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
     }
     return;
   }
-  const uint64_t lim = 0xffffffffull;
-  const bool full = a.SG == 1 && a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mrows % kUM == 0 &&
-                    a.u.Ncols % kSN == 0 && a.x_rows > 0 && (uint64_t)a.x_rows * a.u.ldb * 4 < lim &&
-                    (uint64_t)a.u.Mp * a.u.ldg * 4 < lim && (uint64_t)kUM * a.u.ldw * 4 < lim;
-  if (full) {
+  if (full && a.SG == 1) {
     if (a.u.Mp == 32)
       launch(k_step_w1_full<2>, grid, 256, 0, s, a, mtiles, ntiles, nchunks);
     else
