@@ -190,19 +190,175 @@ __global__ __launch_bounds__(1024) void k_fwd_blk(FwdArgs a, int ntiles, int mti
   }
 }
 
+// Large-tile form for full tiles and long splits: 256 x 256 output tile,
+// 32-wide K chunks in two LDS buffers (147 KB: one workgroup per CU), the
+// next chunk's loads in flight during the current chunk's MFMAs (a second
+// register set for loads two chunks ahead does not fit beside the four
+// accumulators).  No row is out of range, so no load feeds a select.  Wave w owns rows 64*(w/4) and
+// columns 64*(w%4) as four 32x32x2 chains (2 x 2 blocks), so a chunk's 64
+// MFMAs per wave share one barrier and every 16-byte operand read feeds
+// eight MFMAs instead of four.  Same k permutation and output layout as
+// k_fwd_blk.
+constexpr int kBT2 = 256;
+constexpr int kKC2 = 32;
+constexpr int kL2 = kKC2 + 4;
+__global__ __launch_bounds__(1024) void k_fwd_blk256(FwdArgs a, int ntiles, int mtiles) {
+  __shared__ __attribute__((aligned(16))) float As[2][kBT2 * kL2];
+  __shared__ __attribute__((aligned(16))) float Ws[2][kBT2 * kL2];
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int q1 = qdiv_small(bid, ntiles, qdiv_inv(ntiles)), nt = bid - q1 * ntiles;
+  const int q2 = qdiv_small(q1, mtiles, qdiv_inv(mtiles)), mt = q1 - q2 * mtiles;
+  const int g = qdiv_small(q2, a.KS, qdiv_inv(a.KS)), ks = q2 - g * a.KS;
+  const int nch = a.K / kKC;
+  const int c0 = 2 * (ks * a.cps);
+  const int c1 = 2 * min(nch, ks * a.cps + a.cps);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int wm = (wave >> 2) * 64, wn = (wave & 3) * 64;
+  const int mbase = mt * kBT2, nbase = nt * kBT2;
+
+  // Thread t stages pieces t and t + 1024 of each 256 x 32 chunk: row q/8,
+  // 16-byte column piece q%8.  Every row is in range (full tiles).
+  const float* arow[2];
+  const float* wrow[2];
+  int off[2];
+  const float* wp = a.W + (int64_t)(g / a.wdiv) * a.w_pitch;
+  const float inv_mp = qdiv_inv(a.Mp), inv_vs = qdiv_inv(a.vS > 0 ? a.vS : 1);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = tid + 1024 * i;
+    const int r = q >> 3, c4 = q & 7;
+    off[i] = r * kL2 + 4 * c4;
+    const int m = mbase + r;
+    const int jj = qdiv_small(m, a.Mp, inv_mp), sm = m - jj * a.Mp;
+    int64_t p = (int64_t)g * a.SG + jj;
+    if (a.vS > 0) {
+      const int k = qdiv_small(jj, a.vS, inv_vs);
+      p = (int64_t)k * a.P + (int64_t)g * a.vS + (jj - k * a.vS);
+    }
+    arow[i] = a.A + (int64_t)a.idx[p * a.M + sm] * a.lda + 4 * c4;
+    wrow[i] = wp + (int64_t)(nbase + r) * a.ldw + 4 * c4;
+  }
+  f32x4 av[2], wv[2];
+  auto load = [&](int c) {
+    const int64_t o = (int64_t)c * kKC2;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      av[i] = *(const f32x4*)(arow[i] + o);
+      wv[i] = *(const f32x4*)(wrow[i] + o);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *(f32x4*)&As[buf][off[i]] = av[i];
+      *(f32x4*)&Ws[buf][off[i]] = wv[i];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.0f;
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < kKC2 / 8; ++q) {
+      f32x4 xa[2], yb[2];
+#pragma unroll
+      for (int x = 0; x < 2; ++x) xa[x] = *(const f32x4*)&As[buf][(wm + 32 * x + l32) * kL2 + 8 * q + 4 * lhi];
+#pragma unroll
+      for (int y = 0; y < 2; ++y) yb[y] = *(const f32x4*)&Ws[buf][(wn + 32 * y + l32) * kL2 + 8 * q + 4 * lhi];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int y = 0; y < 2; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(xa[x][e], yb[y][e], acc[x][y], 0, 0, 0);
+    }
+  };
+  if (c0 < c1) {
+    load(c0);
+    store(0);
+    __syncthreads();
+    for (int c = c0; c < c1; ++c) {
+      load(c + 1 < c1 ? c + 1 : c);  // the last chunk again at the end: in range, unused
+      __builtin_amdgcn_sched_barrier(0);
+      compute((c - c0) & 1);
+      store((c - c0 + 1) & 1);
+      __syncthreads();
+    }
+  }
+  const int64_t PT = a.PT > 0 ? a.PT : a.P;
+  const int64_t gbase = a.vS > 0 ? (int64_t)g * a.vS : (int64_t)g * a.SG;
+  const int64_t kstride = a.vS > 0 ? a.P : 0;
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    // Rows 8i + e of block x share one member (as in k_fwd_blk).
+    int row0 = mbase + wm + 32 * x + 4 * lhi;
+    int v = qdiv_small(row0, a.Mp, inv_mp), sm = row0 - v * a.Mp;
+    int vk = 0, vj = v;
+    if (a.vS > 0) {
+      vk = qdiv_small(v, a.vS, inv_vs);
+      vj = v - vk * a.vS;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (i > 0) {
+        row0 += 8;
+        sm += 8;
+        if (sm >= a.Mp) {
+          sm -= a.Mp;
+          if (a.vS > 0 && ++vj == a.vS) {
+            vj = 0;
+            ++vk;
+          } else if (a.vS <= 0) {
+            ++vj;
+          }
+        }
+      }
+      const int64_t p = vk * kstride + gbase + vj;
+      float* dst = a.part + (((int64_t)ks * PT + p) * a.Mp + sm) * a.N + nbase + wn + l32;
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[(int64_t)e * a.N + 32 * y] = acc[x][y][4 * i + e];
+    }
+  }
+}
+
+// The large tile where it applies: every tile full, M = Mp, and at least
+// 64 32-wide chunks per split (the pipeline start is then a small share).
+static bool fwd_blk256_applies(const FwdArgs& a) {
+  const int GM = a.SG * a.Mp;
+  return GM % kBT2 == 0 && a.N % kBT2 == 0 && a.M == a.Mp && 2 * a.cps >= 64 && a.Mp % 8 == 0;
+}
+
 void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
   const int GM = a.SG * a.Mp;
   const int mtiles = (GM + kBT - 1) / kBT;
   const int ntiles = (a.N + kBT - 1) / kBT;
   const int groups = a.vS > 0 ? a.P / a.vS : a.P / a.SG;
   const unsigned grid = (unsigned)((int64_t)groups * a.KS * mtiles * ntiles);
+  if (fwd_blk256_applies(a)) {
+    const int mt2 = GM / kBT2, nt2 = a.N / kBT2;
+    launch(k_fwd_blk256, (unsigned)((int64_t)groups * a.KS * mt2 * nt2), 1024, 0, s, a, nt2, mt2);
+    return;
+  }
   launch(k_fwd_blk, grid, 1024, 0, s, a, ntiles, mtiles);
 }
 
 // Split count of k_fwd_blk: about target_wg workgroups, no empty split.
 void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg) {
-  const int64_t tiles = (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
+  int64_t tiles = (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
   const int nch = K / kKC;
+  if (rows % kBT2 == 0 && N % kBT2 == 0) {  // the 256 x 256 tile if its splits stay long
+    const int64_t t2 = (int64_t)groups * (rows / kBT2) * (N / kBT2);
+    const int64_t ks2 = std::min<int64_t>(nch, std::max<int64_t>(1, (target_wg + t2 - 1) / t2));
+    if (2 * ((nch + ks2 - 1) / ks2) >= 64) tiles = t2;
+  }
   int ks = (int)std::max<int64_t>(1, (target_wg + tiles - 1) / tiles);
   ks = std::min(ks, nch);
   const int c = (nch + ks - 1) / ks;
