@@ -598,10 +598,191 @@ __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(6))) void k
   }
 }
 
+// Two-chain form of the block update for full tiles and large grids (plain
+// SGD): 128 x 128 tile of W1 per workgroup, 8 waves, wave w owns rows
+// 32*(w%4) and columns 64*(w/4) as two 32x32x2 chains, so a 32-row stage's
+// 32 MFMAs per wave share one barrier (16 in k_block_update) and each
+// error-operand read feeds eight MFMAs; two workgroups per CU.  Stage loads
+// (wave w: rows 4w .. 4w+3 of the stage, every column of both operands),
+// row tables, transposed swizzled LDS tiles and the k order are those of
+// k_block_update.
+constexpr int kUM3 = 128, kUN3 = 128, kLB3 = kUN3 + 4;
+__global__ __launch_bounds__(512) void k_block_update2(BlkArgs a, const uint32_t* __restrict__ gtab,
+                                                        const uint32_t* __restrict__ xtab, int mtiles, int ntiles) {
+  constexpr int NTH = 512;
+  constexpr int kStage = (kUM3 + kUN3) * kBU;
+  constexpr int kLds = 2 * kStage > kUM3 * kLB3 ? 2 * kStage : kUM3 * kLB3;
+  __shared__ __attribute__((aligned(16))) float lds[kLds];
+  float* Gt = lds;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int mt = bid % mtiles;
+  const int nt = (bid / mtiles) % ntiles;
+  const int g = bid / (ntiles * mtiles);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int mrow0 = mt * kUM3, ncol0 = nt * kUN3;
+  const int wm = (wave & 3) * 32, wn = (wave >> 2) * 64;
+  const int R = a.K1 * a.SG * a.B;
+  const int nst = (R + kSC - 1) / kSC;
+  const uint32_t* gt = gtab + (int64_t)g * nst * kSC;
+  const uint32_t* xt = xtab + (int64_t)g * nst * kSC;
+  if (a.tail && mt == 0) {
+    f32x4* T = (f32x4*)a.tail + (int64_t)g * a.SG * (a.tail_pitch / 4);
+    const int64_t p4 = a.tail_pitch / 4, n4 = a.tail_len / 4, per = (n4 + ntiles - 1) / ntiles;
+    const int64_t i1 = min(n4, (nt + 1) * per);
+    for (int64_t i = nt * per + tid; i < i1; i += NTH) {
+      f32x4 sum = T[i];
+      for (int j = 1; j < a.SG; ++j) sum += T[j * p4 + i];
+      const f32x4 mean = sum / (float)a.SG;
+      for (int j = 0; j < a.SG; ++j) T[j * p4 + i] = mean;
+    }
+  }
+  const int gcol0 = 4 * (mrow0 + lane), gcol1 = gcol0 + 256, xcol0 = 4 * (ncol0 + lane), xcol1 = xcol0 + 256;
+  const int grow_bytes = 4 * a.Mrows, xrow_bytes = 4 * a.Ncols;
+  constexpr int kRsrcWord3 = 0x00020000;
+
+  struct StageRegs {
+    float g0[4], g1[4], x0[4], x1[4];
+  };
+  StageRegs RA, RB;
+  auto load_stage = [&](int st, StageRegs& q) {
+    const int r0 = (st < nst ? st : nst - 1) * kSC + 4 * wave;
+    const uint4 go = *(const uint4*)(gt + r0);
+    const uint4 xo = *(const uint4*)(xt + r0);
+    const uint32_t gr[4] = {go.x, go.y, go.z, go.w}, xr[4] = {xo.x, xo.y, xo.z, xo.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.G) + ((uint64_t)gr[i] << 6), 0, grow_bytes, kRsrcWord3);
+      const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.X) + ((uint64_t)xr[i] << 6), 0, xrow_bytes, kRsrcWord3);
+      q.g0[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(grs, gcol0, 0, 0));
+      q.g1[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(grs, gcol1, 0, 0));
+      q.x0[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xrs, xcol0, 0, 0));
+      q.x1[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xrs, xcol1, 0, 0));
+    }
+  };
+  auto store_stage = [&](int st, int buf, StageRegs& q) {
+    float* S = lds + buf * kStage;
+    const int r0 = st * kSC + 4 * wave;
+    if (r0 + 4 > R) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (r0 + i >= R) q.g0[i] = q.g1[i] = 0.0f;
+    }
+    *(f32x4*)&S[bu_swz(lane, wave)] = f32x4{q.g0[0], q.g0[1], q.g0[2], q.g0[3]};
+    *(f32x4*)&S[bu_swz(lane + 64, wave)] = f32x4{q.g1[0], q.g1[1], q.g1[2], q.g1[3]};
+    float* Bt = S + kUM3 * kBU;
+    *(f32x4*)&Bt[bu_swz(lane, wave)] = f32x4{q.x0[0], q.x0[1], q.x0[2], q.x0[3]};
+    *(f32x4*)&Bt[bu_swz(lane + 64, wave)] = f32x4{q.x1[0], q.x1[1], q.x1[2], q.x1[3]};
+  };
+
+  f32x16 acc[2];
+#pragma unroll
+  for (int y = 0; y < 2; ++y)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[y][r] = 0.0f;
+  const int arow = wm + l32;
+  const int aoff = arow << 5, asw = (4 * lhi) ^ ((arow >> 1) & 7);
+  int boff[2], bsw[2];
+#pragma unroll
+  for (int y = 0; y < 2; ++y) {
+    const int brow = wn + 32 * y + l32;
+    boff[y] = (kUM3 + brow) << 5;
+    bsw[y] = (4 * lhi) ^ ((brow >> 1) & 7);
+  }
+  auto mfma_stage = [&](int buf) {
+    const float* S = lds + buf * kStage;
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 x = *(const f32x4*)&S[aoff + ((asw ^ q) << 2)];
+      const f32x4 y0 = *(const f32x4*)&S[boff[0] + ((bsw[0] ^ q) << 2)];
+      const f32x4 y1 = *(const f32x4*)&S[boff[1] + ((bsw[1] ^ q) << 2)];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(x[e], y0[e], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(x[e], y1[e], acc[1], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  load_stage(0, RA);
+  load_stage(1, RB);
+  store_stage(0, 0, RA);
+  __syncthreads();
+  int st = 0;
+  for (; st + 1 < nst; st += 2) {
+    load_stage(st + 2, RA);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(0);
+    store_stage(st + 1, 1, RB);
+    __syncthreads();
+    load_stage(st + 3, RB);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_stage(1);
+    store_stage(st + 2, 0, RA);
+    __syncthreads();
+  }
+  if (st < nst) {
+    mfma_stage(0);
+    __syncthreads();
+  }
+  // The gradient tile to LDS first (its registers are then free for the
+  // base tile and the mean of the bases).
+#pragma unroll
+  for (int y = 0; y < 2; ++y)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = wm + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      Gt[row * kLB3 + wn + 32 * y + l32] = acc[y][r];
+    }
+  // Base tile: thread t takes column piece t%32 of rows t/32 + 16*i.
+  constexpr int kXP = kUN3 / 4, kXR = NTH / kXP, kWL = kUM3 / kXR;
+  const int xc4 = tid % kXP, xr0 = tid / kXP;
+  const int xcol = ncol0 + 4 * xc4;
+  const float* Wb = a.Wb + (int64_t)(g / a.base_div) * a.nbase * a.wb_pitch;
+  f32x4 wv[kWL];
+#pragma unroll
+  for (int i = 0; i < kWL; ++i) wv[i] = *(const f32x4*)(Wb + (int64_t)(mrow0 + xr0 + kXR * i) * a.ldw + xcol);
+  if (a.nbase > 1) {  // the mean of the bases, added in order
+    for (int c = 1; c < a.nbase; ++c) {
+      f32x4 v[kWL];
+#pragma unroll
+      for (int i = 0; i < kWL; ++i)
+        v[i] = *(const f32x4*)(Wb + (int64_t)c * a.wb_pitch + (int64_t)(mrow0 + xr0 + kXR * i) * a.ldw + xcol);
+#pragma unroll
+      for (int i = 0; i < kWL; ++i) wv[i] += v[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kWL; ++i) wv[i] = wv[i] / (float)a.nbase;
+  }
+  __syncthreads();
+  float* Wo = a.Wo + (int64_t)g * a.wo_pitch;
+  const float lr_eff = *a.lr / a.lr_div;
+#pragma unroll
+  for (int i = 0; i < kWL; ++i) {
+    const int rl = xr0 + kXR * i;
+    const f32x4 gsum = *(const f32x4*)&Gt[rl * kLB3 + 4 * xc4];
+    *(f32x4*)(Wo + (int64_t)(mrow0 + rl) * a.ldw + xcol) = wv[i] - lr_eff * gsum;
+  }
+}
+
 #ifndef HAV_BLK_THREADS
 #define HAV_BLK_THREADS 512
 #endif
 void launch_block_update(hipStream_t s, const BlkArgs& a) {
+  {  // the two-chain tile where every tile is full and the grid has at least eight per CU
+    const int groups = a.P / a.SG;
+    if (!a.hb && a.Mrows % kUM3 == 0 && a.Ncols % kUN3 == 0 &&
+        (int64_t)groups * (a.Mrows / kUM3) * (a.Ncols / kUN3) >= 2048) {
+      const int mt2 = a.Mrows / kUM3, nt2 = a.Ncols / kUN3;
+      launch(k_block_update2, (unsigned)((int64_t)groups * mt2 * nt2), 512, 0, s, a, a.gtab, a.xtab, mt2, nt2);
+      return;
+    }
+  }
   const int mtiles = (a.Mrows + kUM - 1) / kUM;
   const int ntiles = (a.Ncols + kUN - 1) / kUN;
   const unsigned grid = (unsigned)((int64_t)(a.P / a.SG) * mtiles * ntiles);
