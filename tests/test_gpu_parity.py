@@ -434,6 +434,16 @@ def test_delayed_schedule_profile(gpu_lib):
         assert "fwd1_block_gemm" in h.profile_read() and "fwd1_gemm" not in h.profile_read()
 
 
+def test_delayed_block_update_large_grid(gpu_lib):
+    """Cluster updates with at least eight full 128 x 128 tiles per CU (8
+    clusters x 4 x 64 tiles: the two-chain block-update tile) and the tail
+    means of b1, W2, b2 in the same launch: P=16 S=2 K1=4 K2=2 B=32, a
+    8192-512-10 MLP, two rounds against the oracle."""
+    c = cases.case("mlp", 16, 2, 4, 2, B=32, IN=8192, H=512, C=10, N=300, sigma=0.5, lr=0.02, seed=44)
+    got, idx, _ = _run_gpu(c, rounds=2, mode="delayed")
+    _check(c, got, idx, *_oracle(c, 2), mode="delayed")
+
+
 @pytest.mark.parametrize("name", ["fused_wide", "fused_one_block", "separate_many_rows"])
 def test_delayed_last_block_global_mean(name, gpu_lib):
     """The last block's update over all P learners from the mean of the
