@@ -17,6 +17,7 @@ import pytest
 
 import cases
 from oracle import method as M
+from oracle import rng as R
 
 pytestmark = pytest.mark.gpu
 
@@ -269,7 +270,9 @@ def test_named_large_mlp_workload(gpu_lib):
     update's cluster mean of b1, W2, b2 runs between them) -- against the
     oracle: indices bit-exact, every block within the gate.  The full
     configuration (P=16, S=4, K1=4, K2=2, B=32) is then checked for what holds
-    at any size: finite values and identical replicas after the global mean."""
+    at any size (finite values, identical replicas after the global mean) and
+    for what the oracle computes without the model: every learner's
+    minibatch indices of the round, bit for bit."""
     import torch
     from paper_1903_05133_amd import HierAvg
     c = cases.named("mlp_150528_1024_1000", 4, 2, 4, 2, 32, 0.02, seed=0)
@@ -301,6 +304,10 @@ def test_named_large_mlp_workload(gpu_lib):
         assert bool((w == w[:1]).all())
         del w
         torch.cuda.empty_cache()
+        # the round's minibatches, bit for bit: learner j's draw at step t
+        want = np.array([[R.draw_indices(full["seed"], j, t, full["B"], full["N"]) for j in range(full["P"])]
+                         for t in range(full["K1"] * full["K2"])], dtype=np.int64)
+        assert np.array_equal(h.last_indices().astype(np.int64), want.reshape(full["K2"], full["K1"], full["P"], -1))
 
 
 def test_determinism_two_handles(gpu_lib):
