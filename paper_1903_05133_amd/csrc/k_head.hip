@@ -1181,9 +1181,12 @@ void launch_softmax_grad(hipStream_t s, const float* part, int KS, const float* 
                          const int32_t* labels, const int32_t* idx, float* G, int P, int M, int Mp, int C, int Cp) {
   const int rows = P * M;
   const unsigned grid = (unsigned)((rows + 3) / 4);
+  // Up to 64 classes the plain kernel (measured faster there: 4.1 against
+  // 7.0 us at 10 classes); the register form from 65 to 1024 classes (6.9
+  // against 18.7 us at 1000).
   const int npl = (C + 63) / 64;
   if (npl <= 1)
-    launch(k_softmax_grad_reg<1>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
+    launch(k_softmax_grad, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
   else if (npl <= 2)
     launch(k_softmax_grad_reg<2>, grid, 256, 0, s, part, KS, bias, w_pitch, labels, idx, G, P, M, Mp, C, Cp);
   else if (npl <= 4)
