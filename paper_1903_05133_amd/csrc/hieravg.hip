@@ -55,7 +55,7 @@ const char* kClassNames[KC_COUNT] = {
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
     "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step",
     "fwd1_block_gemm_v", "scale_errors", "buffer_update_gemm", "update1_gemm_group_mean", "fwd1_group_gemm",
-    "update1_gemm_global_mean"};
+    "update1_gemm_global_mean", "head_fused"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -117,6 +117,10 @@ struct hieravg {
   // More than 32 classes, B <= 32, plain SGD: the hidden-error kernel also
   // steps W2 and b2 (no update GEMM for the second layer).
   bool w2_fused = false;
+  // At most 32 classes, eager steps: the loss side as k_head_fused and the
+  // second layer's step from its per-group gradient rows.
+  bool head_fused = false;
+  float* hgrad = nullptr;
   int ks_cur = 1;                // splits of the partials currently in `part`
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
@@ -196,7 +200,7 @@ void release(hieravg* h) {
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->Wm, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
-                  h->partv, h->Gu, h->Gt, h->Wc2, h->btab1,
+                  h->partv, h->Gu, h->Gt, h->Wc2, h->btab1, h->hgrad,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -339,6 +343,7 @@ int64_t plan(hieravg* h, int B) {
   h->upd_global = mlp && h->fused && step_w1_mean_supported(h->Bp, P);
   h->w2_fused = mlp && c.classes > kSmallC && bwd_hidden_update_supported(B) && c.momentum == 0.0f &&
                 c.weight_decay == 0.0f;
+  h->head_fused = mlp && c.classes <= kSmallC && head_fused_supported((int)h->Hp, (int)round_up(c.classes, 16));
   if (h->upd_mean) {
     plan_split_blk(P / c.S, c.S * h->Bp, (int)n1, (int)h->INp, &h->KS_g, &h->cps_g, HAV_FWD_BLOCK_TARGET);
     ks_max = std::max<int64_t>(ks_max, h->KS_g);
@@ -471,6 +476,11 @@ int build(hieravg* h) {
     if (mlp) {
       if ((rc = alloc_zero(h, (void**)&h->Z1, sizeof(float) * P * h->Bp * h->Hp, "hidden activations"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
+      if (h->head_fused &&
+          (rc = alloc_zero(h, (void**)&h->hgrad,
+                           sizeof(float) * head_fused_scratch_floats(P, h->Bp, h->C, (int)h->Hp),
+                           "head gradient rows")))
+        return rc;
     }
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
     if (any_delayed) {
@@ -824,6 +834,37 @@ bool launch_class(hieravg* h, int kc, int tt) {
                     C, Cp, Hp, h->hyper, mom);
       return true;
     }
+    case KC_HEAD_FUSED: {  // eager schedule
+      if (!small || h->in_delayed || !h->head_fused) return false;
+      HeadFusedArgs a;
+      a.part = h->part;
+      a.KS = h->ks_cur;
+      a.split = (int64_t)P * Bp * Hp;
+      a.b1 = W + h->off_b1;
+      a.W2 = W + h->off_W2;
+      a.b2 = W + h->off_b2;
+      a.w_pitch = h->Dp;
+      a.G1 = h->G1;
+      a.labels = h->y;
+      a.idx = ix;
+      a.P = P;
+      a.M = B;
+      a.Mp = Bp;
+      a.C = C;
+      a.Cp = Cp;
+      a.Hp = Hp;
+      a.lr = h->hyper;
+      a.mom.mu = c.momentum;
+      a.mom.wd = c.weight_decay;
+      if (h->V) {
+        a.mom.vw2 = h->V + h->off_W2;
+        a.mom.vb1 = h->V + h->off_b1;
+        a.mom.vb2 = h->V + h->off_b2;
+      }
+      a.scratch = h->hgrad;
+      launch_head_fused(s, a);
+      return true;
+    }
     case KC_HEAD_STEP:
     case KC_HEAD_END: {
       if (!h->in_delayed) return false;
@@ -945,6 +986,7 @@ bool launch_class(hieravg* h, int kc, int tt) {
 void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   static const int kSoftmax[] = {KC_SOFTMAX};
   static const int kSmall[] = {KC_HEAD_A, KC_HEAD_B};
+  static const int kSmallFused[] = {KC_HEAD_FUSED};
   static const int kLarge[] = {KC_REDUCE1, KC_FWD2, KC_SOFTMAX, KC_BWD_HIDDEN, KC_UPDATE2};
   const hieravg_config& c = h->cfg;
   const int* seq;
@@ -953,8 +995,8 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
     seq = kSoftmax;
     n = 1;
   } else if (h->C <= kSmallC) {
-    seq = kSmall;
-    n = 2;
+    seq = h->head_fused ? kSmallFused : kSmall;
+    n = h->head_fused ? 1 : 2;
   } else {
     seq = kLarge;
     n = h->w2_fused ? 4 : 5;  // KC_UPDATE2 last: the hidden-error kernel steps W2 and b2

@@ -671,6 +671,266 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
     step(b2 + po + tid, mom.vb2 ? mom.vb2 + po + tid : nullptr, b2[po + tid], db2);
 }
 
+// The loss side of an eager step in one launch (C <= 32).  Workgroup =
+// learner p and the 16 samples [16q, 16q + 16) with every hidden unit:
+//  * Z1 = (split-K partials added in split order) + b1 and the learner's W2
+//    (rows C..KC-1 zero) are staged in LDS;
+//  * logits = b2 + ReLU(Z1) W2^T as 16x16x4 MFMAs, the units split over the
+//    four waves and the waves' partial logits added in wave order; then the
+//    softmax cross-entropy gradient G2 = (softmax - onehot) / M, four lanes
+//    per sample;
+//  * G1 = (G2 W2) * [Z1 > 0] (stored) and the group's dW2 = G2^T ReLU(Z1),
+//    db1 = sum of G1 and db2 = sum of G2 over its samples, all per 16-unit
+//    tile as 16x16x4 MFMAs.
+// The group's dW2, db1, db2 go to its scratch row; k_head_w2_step adds the
+// rows and takes the step (a cross-workgroup sum inside this kernel would
+// need device-scope fences, each of which writes back and invalidates the
+// L2 of its XCD).  Samples M..Mp-1 have Z1 = 0 and G2 = 0 (their G1 rows
+// are written as zeros).
+// Scratch row of (p, q), HS = (C + 1) Hp + 32 floats: [db1 (Hp) | dW2 (C x Hp) | db2 (C)],
+// the order of b1 and W2 in the parameter vector.
+constexpr int kHfWaves = 8;  // waves of k_head_fused
+template <int KC, int HPM, int KSN>
+__global__ __launch_bounds__(64 * kHfWaves) void k_head_fused(HeadFusedArgs a) {
+  constexpr int NT = 64 * kHfWaves;
+  constexpr int kZL = HPM + 4;  // LDS row length (rows 4 banks apart: conflict-free 16-byte reads of 16 rows)
+  constexpr int kNB = 4 * HPM / NT;  // Z1 pieces per thread (at Hp = HPM: one batch of loads)
+  constexpr int kNW = (KC * HPM / 4 + NT - 1) / NT;  // most W2 pieces per thread
+  constexpr int kCT = KC / 16;                        // 16-class tiles
+  __shared__ __attribute__((aligned(16))) float zs[16 * kZL];
+  __shared__ __attribute__((aligned(16))) float ws[KC * kZL];
+  __shared__ float ls[kHfWaves][16][KC + 1];
+  __shared__ float g2s[16][KC + 1];
+  __shared__ int ys[16];
+  const int NS = a.Mp / 16;
+  const int p = blockIdx.x / NS, q = blockIdx.x % NS;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 15, lg = lane >> 4;
+  const int Hp = a.Hp, C = a.C, M = a.M, H4 = Hp / 4, runs = Hp / 16;
+  const int64_t po = (int64_t)p * a.w_pitch;
+  const float* W2 = a.W2 + po;
+
+  // Sample 16q + (tid & 15)'s row index now, its label once the loads
+  // below are in flight (clamped to an in-range sample, no branch).
+  const int sy = 16 * q + (tid & 15);
+  const int ixv = a.idx[(int64_t)p * M + (sy < M ? sy : M - 1)];
+  int yv = 0;
+  // W2 rows c < KC (KC Hp / 4 pieces) and Z1 of the group's 16 rows (4 Hp
+  // pieces, in batches) into LDS.  Every load is issued unconditionally:
+  // piece indices past the count repeat the last piece (the same value to
+  // the same LDS address), since a load behind a branch is waited for before
+  // the next one is issued.
+  {
+    const int lw = KC * H4 - 1, lz = 4 * Hp - 1;
+    f32x4 wr[kNW];
+#pragma unroll
+    for (int i = 0; i < kNW; ++i) {
+      const int e = min(tid + NT * i, lw), c = e / H4, c4 = e % H4;
+      const f32x4 v = *(const f32x4*)(W2 + (int64_t)(c < C ? c : 0) * Hp + 4 * c4);
+      const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
+      wr[i] = c < C ? v : z4;
+    }
+    const float* pbase = a.part + ((int64_t)p * a.Mp + 16 * q) * Hp;
+    const float* b1 = a.b1 + po;
+    const int nz = (4 * Hp + NT - 1) / NT;
+    for (int i0 = 0; i0 < nz; i0 += kNB) {
+      f32x4 zr[kNB][KSN > 0 ? KSN : 1], br[kNB];
+#pragma unroll
+      for (int i = 0; i < kNB; ++i) {
+        const int e = min(tid + NT * min(i0 + i, nz - 1), lz), s = e / H4, c4 = e % H4;
+        const float* src = pbase + (int64_t)s * Hp + 4 * c4;
+        br[i] = *(const f32x4*)(b1 + 4 * c4);
+        if (KSN > 0) {
+#pragma unroll
+          for (int k = 0; k < (KSN > 0 ? KSN : 1); ++k) zr[i][k] = *(const f32x4*)(src + k * a.split);
+        } else {
+          f32x4 z = {0.f, 0.f, 0.f, 0.f};
+          for (int k = 0; k < a.KS; ++k) z += *(const f32x4*)(src + k * a.split);
+          zr[i][0] = z;
+        }
+      }
+      if (i0 == 0) yv = a.labels[ixv];
+#pragma unroll
+      for (int i = 0; i < kNB; ++i) {
+        const int e = min(tid + NT * min(i0 + i, nz - 1), lz), s = e / H4, c4 = e % H4;
+        f32x4 z = zr[i][0];
+#pragma unroll
+        for (int k = 1; k < KSN; ++k) z += zr[i][k];
+        z += br[i];
+        const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
+        *(f32x4*)&zs[s * kZL + 4 * c4] = 16 * q + s < M ? z : z4;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kNW; ++i) {
+      const int e = min(tid + NT * i, lw), c = e / H4, c4 = e % H4;
+      *(f32x4*)&ws[c * kZL + 4 * c4] = wr[i];
+    }
+  }
+  if (tid < 16) ys[tid] = sy < M ? yv : 0;
+  float b2v[KC / 4];  // b2 of the classes lane & 3 + 4k (softmax lanes of wave 0)
+#pragma unroll
+  for (int k = 0; k < KC / 4; ++k) {
+    const int c = (lane & 3) + 4 * k;
+    const float v = a.b2[po + (c < C ? c : 0)];
+    b2v[k] = c < C ? v : 0.0f;
+  }
+  __syncthreads();
+
+  // Partial logits over this wave's 16-unit runs (runs wave, wave + 8, ...):
+  // lane group lg takes units 16 run + 4lg .. + 3 in the four k slots of four
+  // MFMAs (the same units for both operands).
+  {
+    f32x4 acc[kCT];
+#pragma unroll
+    for (int ct = 0; ct < kCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int run = wave; run < runs; run += kHfWaves) {
+      const int col = 16 * run + 4 * lg;
+      const f32x4 z = *(const f32x4*)&zs[li * kZL + col];
+      const f32x4 av = {fmaxf(z.x, 0.0f), fmaxf(z.y, 0.0f), fmaxf(z.z, 0.0f), fmaxf(z.w, 0.0f)};
+#pragma unroll
+      for (int ct = 0; ct < kCT; ++ct) {
+        const f32x4 bv = *(const f32x4*)&ws[(16 * ct + li) * kZL + col];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bv[e], acc[ct], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int ct = 0; ct < kCT; ++ct)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ls[wave][4 * lg + r][16 * ct + li] = acc[ct][r];
+  }
+  __syncthreads();
+
+  // Softmax gradient: wave 0, lanes 4s .. 4s + 3 for sample s, classes
+  // (lane & 3) + 4k; the waves' partial logits added in wave order.
+  if (wave == 0) {
+    const int s = lane >> 2;
+    float lv[KC / 4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < KC / 4; ++k) {
+      const int c = (lane & 3) + 4 * k;
+      float v = b2v[k];
+#pragma unroll
+      for (int w = 0; w < kHfWaves; ++w) v += ls[w][s][c];
+      lv[k] = v;
+      if (c < C) mx = fmaxf(mx, v);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+    float sum = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KC / 4; ++k) {
+      const int c = (lane & 3) + 4 * k;
+      const float e = c < C ? expf(lv[k] - mx) : 0.0f;
+      lv[k] = e;
+      sum += e;
+    }
+    sum += __shfl_xor(sum, 1, 64);
+    sum += __shfl_xor(sum, 2, 64);
+    const bool valid = 16 * q + s < M;
+    const int y = ys[s];
+    const float invM = 1.0f / (float)M;
+#pragma unroll
+    for (int k = 0; k < KC / 4; ++k) {
+      const int c = (lane & 3) + 4 * k;
+      g2s[s][c] = valid && c < C ? (lv[k] / sum - (c == y ? 1.0f : 0.0f)) * invM : 0.0f;
+    }
+  }
+  __syncthreads();
+
+  // Per 16-unit run of this wave: G1 (samples 4lg + r, unit u) and dW2
+  // (classes 16ct + 4lg + r, unit u), u = 16 run + li.
+  float* hrow = a.scratch + ((int64_t)p * NS + q) * ((int64_t)(C + 1) * Hp + 32);
+  float* g1 = a.G1 + ((int64_t)p * a.Mp + 16 * q) * Hp;
+  for (int run = wave; run < runs; run += kHfWaves) {
+    const int u = 16 * run + li;
+    f32x4 d1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < KC / 4; ++t)
+      d1 = __builtin_amdgcn_mfma_f32_16x16x4f32(g2s[li][4 * t + lg], ws[(4 * t + lg) * kZL + u], d1, 0, 0, 0);
+    f32x4 d2[kCT];
+#pragma unroll
+    for (int ct = 0; ct < kCT; ++ct) {
+      d2[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        d2[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(g2s[4 * t + lg][16 * ct + li],
+                                                      fmaxf(zs[(4 * t + lg) * kZL + u], 0.0f), d2[ct], 0, 0, 0);
+    }
+    float db1 = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float g = zs[(4 * lg + r) * kZL + u] > 0.0f ? d1[r] : 0.0f;
+      g1[(int64_t)(4 * lg + r) * Hp + u] = g;
+      db1 += g;
+    }
+    db1 += __shfl_xor(db1, 16, 64);
+    db1 += __shfl_xor(db1, 32, 64);
+    if (lg == 0) hrow[u] = db1;
+#pragma unroll
+    for (int ct = 0; ct < kCT; ++ct)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = 16 * ct + 4 * lg + r;
+        if (c < C) hrow[Hp + (int64_t)c * Hp + u] = d2[ct][r];
+      }
+  }
+  if (tid < C) {
+    float s2 = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 16; ++s) s2 += g2s[s][tid];
+    hrow[(int64_t)(C + 1) * Hp + tid] = s2;
+  }
+}
+
+// The step of b1, W2 and b2 after k_head_fused: per learner the groups'
+// gradient rows added in group order, then the SGD step (heavy-ball and
+// decay as in k_head_b).  Workgroup = learner p and 1024 consecutive floats
+// of [b1 | W2] (contiguous in the parameters, the buffers and the rows);
+// block 0 of a learner also steps b2.
+__global__ __launch_bounds__(256) void k_head_w2_step(HeadFusedArgs a, int nblk) {
+  const int p = blockIdx.x / nblk, blk = blockIdx.x % nblk;
+  const int tid = threadIdx.x;
+  const int NS = a.Mp / 16, C = a.C, Hp = a.Hp;
+  const int64_t HS = (int64_t)(C + 1) * Hp + 32;
+  const int64_t po = (int64_t)p * a.w_pitch;
+  const float* h0 = a.scratch + (int64_t)p * NS * HS;
+  const float lr = *a.lr;
+  const HeadMom& mom = a.mom;
+  const int e = blk * 256 + tid;
+  if (e < (C + 1) * (Hp / 4)) {
+    f32x4 g = *(const f32x4*)(h0 + 4 * e);
+    for (int k = 1; k < NS; ++k) g += *(const f32x4*)(h0 + k * HS + 4 * e);
+    const bool isb = 4 * e < Hp;
+    const int64_t o = isb ? 4 * e : 4 * e - Hp;
+    f32x4* w = (f32x4*)((isb ? a.b1 : a.W2) + po + o);
+    float* vbase = isb ? mom.vb1 : mom.vw2;
+    const f32x4 wo = *w;
+    f32x4 d = g + mom.wd * wo;
+    if (vbase) {
+      f32x4* v = (f32x4*)(vbase + po + o);
+      d = mom.mu * *v + d;
+      *v = d;
+    }
+    *w = wo - lr * d;
+  }
+  if (blk == 0 && tid < C) {
+    float g = h0[(int64_t)(C + 1) * Hp + tid];
+    for (int k = 1; k < NS; ++k) g += h0[k * HS + (int64_t)(C + 1) * Hp + tid];
+    float* w = a.b2 + po + tid;
+    const float wo = *w;
+    float d = g + mom.wd * wo;
+    if (mom.vb2) {
+      float* v = mom.vb2 + po + tid;
+      d = mom.mu * *v + d;
+      *v = d;
+    }
+    *w = wo - lr * d;
+  }
+}
+
 // Value of another lane in the same group of eight by a DPP move: control
 // 0xB1 (quad_perm 1,0,3,2) takes lane i^1, 0x4E (quad_perm 2,3,0,1) lane
 // i^2, 0x141 (row_half_mirror) lane 7-i of the eight.
@@ -1226,6 +1486,33 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, float* W2, int64_t w_pitc
 }
 
 bool bwd_hidden_update_supported(int M) { return M <= kBhM; }
+
+bool head_fused_supported(int Hp, int Cp) { return Cp <= 16 ? Hp <= 1024 : Cp <= 32 && Hp <= 512; }
+
+int64_t head_fused_scratch_floats(int P, int Mp, int C, int Hp) {
+  return (int64_t)P * (Mp / 16) * ((int64_t)(C + 1) * Hp + 32);
+}
+
+void launch_head_fused(hipStream_t s, const HeadFusedArgs& a) {
+  const int grid = a.P * (a.Mp / 16), nt = 64 * kHfWaves;
+  const int ks = a.KS >= 1 && a.KS <= 3 ? a.KS : 0;
+#define HAV_HEAD_FUSED(KC_, HPM_)                                                 \
+  do {                                                                           \
+    if (ks == 1) launch(k_head_fused<KC_, HPM_, 1>, grid, nt, 0, s, a);          \
+    else if (ks == 2) launch(k_head_fused<KC_, HPM_, 2>, grid, nt, 0, s, a);     \
+    else if (ks == 3) launch(k_head_fused<KC_, HPM_, 3>, grid, nt, 0, s, a);     \
+    else launch(k_head_fused<KC_, HPM_, 0>, grid, nt, 0, s, a);                  \
+  } while (0)
+  if (a.Cp <= 16 && a.Hp <= 512)
+    HAV_HEAD_FUSED(16, 512);
+  else if (a.Cp <= 16)
+    HAV_HEAD_FUSED(16, 1024);
+  else
+    HAV_HEAD_FUSED(32, 512);
+#undef HAV_HEAD_FUSED
+  const int nblk = ((a.C + 1) * (a.Hp / 4) + 255) / 256;
+  launch(k_head_w2_step, a.P * nblk, 256, 0, s, a, nblk);
+}
 
 void launch_head_a(hipStream_t s, const float* part, int KS, const float* b1, const float* W2, const float* b2,
                    int64_t w_pitch, float* Z1, float* PL, int P, int M, int Mp, int C, int Cp, int Hp,

@@ -126,6 +126,39 @@ def test_update_mean_block_end_kernels(name, gpu_lib):
     assert "step1_gemm_group_mean" not in stats and "group_mean" not in stats, stats
 
 
+# Eager loss side at most 32 classes: the one-workgroup-per-16-samples head
+# (16 or 32 class slots, hidden widths up to its LDS limit) and, past that
+# limit, the two-kernel head over 32-unit slices.
+EAGER_HEADS = {
+    # 16 class slots, Hp = 1024, B = 20: two sample groups, the second ragged
+    "fused16_h1000": (cases.case("mlp", 4, 2, 2, 2, B=20, IN=130, H=1000, C=7, N=300, sigma=0.5, lr=0.05, seed=61),
+                      "head_fused"),
+    # 32 class slots, Hp = 320, B = 40: three sample groups
+    "fused32_h300": (cases.case("mlp", 4, 2, 2, 2, B=40, IN=100, H=300, C=20, N=300, sigma=0.5, lr=0.05, seed=62),
+                     "head_fused"),
+    # 32 class slots with Hp = 640: past the fused head's LDS
+    "slices_c20_h600": (cases.case("mlp", 4, 2, 2, 2, B=12, IN=100, H=600, C=20, N=300, sigma=0.5, lr=0.05,
+                                   seed=63), "head_b"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EAGER_HEADS))
+def test_eager_small_class_heads(name, gpu_lib):
+    from paper_1903_05133_amd import HierAvg
+    c, head = EAGER_HEADS[name]
+    with HierAvg(config=cases.native_config(c, "eager")) as h:
+        h.profile(True)
+        h.round()
+        stats = h.profile_read()
+        h.profile(False)
+        h.round()
+        got = h.params()
+        idx = h.last_indices()
+    assert head in stats, stats
+    assert ("head_a" in stats) == (head == "head_b") and ("head_fused" in stats) == (head == "head_fused"), stats
+    _check(c, got, idx, *_oracle(c, 2), mode="eager")
+
+
 # MLP cases within the delayed-update limits (at most 32 classes, B <= 32, K1 <= 8)
 DELAYED = sorted(n for n, c in SMALL.items() if c["kind"] == "mlp" and c["C"] <= 32 and c["B"] <= 32)
 
@@ -648,9 +681,12 @@ def test_global_interval_not_multiple_of_k1(name, gpu_lib):
 
 # ---------------------------------------------------- momentum and weight decay
 MOMENTUM_CASES = {
-    # small-class head (k_head_a/k_head_b) and the update GEMM of the first layer
+    # small-class head and the update GEMM of the first layer
     "mlp_head_mom_wd": cases.case("mlp", 4, 2, 2, 2, B=12, IN=150, H=70, C=6, N=200, sigma=0.5, lr=0.05,
                                   momentum=0.9, weight_decay=0.01, seed=31),
+    # 32 class slots of the small-class head, three sample groups
+    "mlp_head32_mom_wd": cases.case("mlp", 4, 2, 2, 2, B=40, IN=100, H=300, C=20, N=300, sigma=0.5, lr=0.05,
+                                    momentum=0.9, weight_decay=0.01, seed=64),
     # more than 32 classes: layer-2 forward GEMM and the update GEMM with bias
     "mlp_large_c_mom": cases.case("mlp", 4, 4, 2, 2, B=20, IN=130, H=80, C=40, N=300, sigma=0.5, lr=0.05,
                                   momentum=0.8, seed=32),
