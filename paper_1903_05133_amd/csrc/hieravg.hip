@@ -121,6 +121,17 @@ struct hieravg {
   // second layer's step from its per-group gradient rows.
   bool head_fused = false;
   float* hgrad = nullptr;
+  // Eager rounds whose steps take the full-tile kernels: the round-end global
+  // mean of W1 goes once to Wg (once_global) and the block-end cluster means
+  // once to the cluster copies Wc (once_block); the next step reads its old
+  // W1 there, and the next round's first forward is one GEMM from Wg.  With
+  // rows_stale, w1_wg says that every learner's W1 is Wg (not replica 0's).
+  bool once_cond = false, once_alloc = false, once_global = false, once_block = false;
+  float* Wg = nullptr;
+  bool w1_wg = false;
+  bool in_wg = false;         // the round being enqueued starts from Wg
+  int KS_g0 = 1, cps_g0 = 1;  // splits of that first forward
+  bool launch_failed = false; // a launch the plan promised was refused
   int ks_cur = 1;                // splits of the partials currently in `part`
   // Delayed first-layer updates (see hieravg.h, HIERAVG_UPDATE_DELAYED).
   bool delayed = false;    // the handle uses them for rounds that start with equal W1
@@ -158,7 +169,7 @@ struct hieravg {
   int T = 1;  // SGD steps per round
   // One round's kernels, captured on first use and replayed for every round
   // that is not profiled (every launch argument is the same in every round).
-  hipGraphExec_t round_exec[2] = {nullptr, nullptr};  // [eager, delayed]
+  hipGraphExec_t round_exec[3] = {nullptr, nullptr, nullptr};  // [eager, delayed, eager from Wg]
 
   bool profiling = false;
   std::vector<ProfRec> recs;
@@ -200,7 +211,7 @@ void release(hieravg* h) {
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   void* bufs[] = {h->W,  h->V,  h->Gr, h->Wm, h->X,  h->y,  h->idx, h->part, h->Z1, h->hyper, h->btab,
                   h->PL, h->G2, h->G1, h->ctr, h->Wc, h->Gs, h->gram, h->ylab, h->part2, h->flag, h->eval_iota,
-                  h->partv, h->Gu, h->Gt, h->Wc2, h->btab1, h->hgrad,
+                  h->partv, h->Gu, h->Gt, h->Wc2, h->btab1, h->hgrad, h->Wg,
                   h->eval_part, h->eval_part2, h->eval_Z1, h->eval_loss, h->eval_hit, h->Xtest, h->ytest};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
@@ -352,6 +363,16 @@ int64_t plan(hieravg* h, int B) {
     h->KS_mean = step_w1_splits(P, c.S, h->Bp, (int)n1, (int)h->INp);
     ks_max = std::max<int64_t>(ks_max, h->KS_mean);
   }
+  // Step 0 must be a kernel that reads a redirected old W1: a full-tile step
+  // or update with the mean (not the fused mean step or the update GEMM).
+  h->once_cond = mlp && h->fused && h->upd_global && (c.K1 > 1 || c.S == 1 || h->upd_mean) &&
+                 step_full_shape(B, h->Bp, (int)h->Hp, (int)h->INp, h->N, h->INp, h->Hp, h->INp);
+  h->once_global = h->once_cond && h->once_alloc;
+  h->once_block = h->once_global && h->upd_mean && c.S > 1;
+  if (h->once_cond) {
+    plan_split_blk(1, P * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_g0, &h->cps_g0, HAV_FWD_BLOCK_TARGET);
+    ks_max = std::max<int64_t>(ks_max, h->KS_g0);
+  }
   h->delayed = false;
   hieravg_config cb = c;
   cb.B = B;
@@ -445,11 +466,12 @@ int build(hieravg* h) {
     // create-time B (hieravg_set_batch may lower it).
     h->Bmax = c.B;
     int64_t part_floats = 0, part2_floats = 0, partv_floats = 0;
-    bool any_delayed = false, any_hb = false;
+    bool any_delayed = false, any_hb = false, any_once = false;
     int Bp_del = 0;
     for (int b = 16; b <= round_up(c.B, 16); b += 16) {
       const int64_t pf = plan(h, std::min(b, c.B));
       part_floats = std::max(part_floats, pf);
+      any_once = any_once || h->once_cond;
       if (h->delayed) {
         any_delayed = true;
         any_hb = any_hb || h->hb;
@@ -476,6 +498,13 @@ int build(hieravg* h) {
     if (mlp) {
       if ((rc = alloc_zero(h, (void**)&h->Z1, sizeof(float) * P * h->Bp * h->Hp, "hidden activations"))) return rc;
       if ((rc = alloc_zero(h, (void**)&h->G1, sizeof(float) * P * h->Bp * h->Hp, "hidden error"))) return rc;
+      if (any_once) {
+        const size_t w1 = sizeof(float) * h->Hp * h->INp;
+        if ((rc = alloc_zero(h, (void**)&h->Wg, w1, "common first layer")) ||
+            (c.S > 1 && (rc = alloc_zero(h, (void**)&h->Wc, w1 * (P / c.S), "cluster copies of W1"))))
+          return rc;
+        h->once_alloc = true;
+      }
       if (h->head_fused &&
           (rc = alloc_zero(h, (void**)&h->hgrad,
                            sizeof(float) * head_fused_scratch_floats(P, h->Bp, h->C, (int)h->Hp),
@@ -485,7 +514,8 @@ int build(hieravg* h) {
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
     if (any_delayed) {
       const int64_t w1 = h->Hp * h->INp;
-      if ((rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1"))) return rc;
+      if (!h->Wc && (rc = alloc_zero(h, (void**)&h->Wc, sizeof(float) * (P / c.S) * w1, "cluster copies of W1")))
+        return rc;
       if ((rc = alloc_zero(h, (void**)&h->Gs, sizeof(float) * c.K1 * P * Bp_del * h->Hp, "block errors"))) return rc;
       if (any_hb) {
         if ((rc = alloc_zero(h, (void**)&h->Wc2, sizeof(float) * (P / c.S) * w1, "second cluster copies of W1")) ||
@@ -515,6 +545,7 @@ int build(hieravg* h) {
                                        sizeof(float) * h->KSG * c.K2 * P * c.K1 * c.K1 * Bp_del * Bp_del, "Gram blocks")))
         return rc;
     }
+    plan(h, c.B);  // again, now that the buffers of the once-written means exist
     h->key_index = hash64(seed, kTagIndex);
     launch_gen_labels(h->stream, h->y, h->N, hash64(seed, kTagLabel), (uint64_t)h->C);
     launch_gen_data(h->stream, h->X, h->y, h->N, h->IN, h->INp, hash64(seed, kTagMean), hash64(seed, kTagNoise),
@@ -599,6 +630,24 @@ bool launch_class(hieravg* h, int kc, int tt) {
   const int32_t* ix = h->idx + (int64_t)tt * P * B;
   const int Bp = h->Bp, C = (int)h->C, Cp = (int)h->Cp, Hp = (int)h->Hp, INp = (int)h->INp;
   const bool mlp = c.kind == HIERAVG_KIND_MLP, small = mlp && C <= kSmallC;
+  const int64_t w1 = (int64_t)h->Hp * h->INp;
+  // Where step tt reads its old W1: Wg for a round's first step after a
+  // round that wrote it, a cluster copy for the step after a block end
+  // (once_block), else the learner's row.
+  auto old_w1 = [&](StepArgs& a) {
+    if (tt == 0 && h->in_wg) {
+      a.w_src = h->Wg;
+      a.src_pitch = 0;
+      a.src_group = P;
+    } else if (h->once_block && tt > 0 && tt % c.K1 == 0) {
+      a.w_src = h->Wc;
+      a.src_pitch = w1;
+      a.src_group = S;
+    }
+  };
+  auto step = [&](const StepArgs& a) {
+    if (!launch_step_w1(s, a)) h->launch_failed = true;
+  };
   switch (kc) {
     case KC_DRAW: {
       BlkTables tb;
@@ -624,6 +673,13 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     }
     case KC_FWD1: {
+      if (tt == 0 && h->in_wg) {  // every learner's W1 is Wg: one GEMM over all P minibatches
+        FwdArgs f{h->X, ix, h->INp, h->Wg, 0, h->INp, h->part, P, B, Bp, Hp, INp, h->KS_g0, h->cps_g0};
+        f.SG = P;
+        launch_fwd_blk(s, f);
+        h->ks_cur = h->KS_g0;
+        return true;
+      }
       FwdArgs f{h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp, h->part, P, B, Bp, mlp ? Hp : Cp, INp, h->KS1,
                 h->cps1};
       launch_fwd(s, f, A_GATHER);
@@ -666,7 +722,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.part = h->part;
       a.SG = mean ? S : 1;
       a.x_rows = h->N;
-      launch_step_w1(s, a);
+      if (!mean) old_w1(a);
+      step(a);
       h->ks_cur = mean ? h->KS_mean : h->KS_step;
       return true;
     }
@@ -680,15 +737,20 @@ bool launch_class(hieravg* h, int kc, int tt) {
       a.SG = global ? P : S;
       a.no_fwd = true;
       a.x_rows = h->N;
-      launch_step_w1(s, a);
+      old_w1(a);
+      if (global ? h->once_global : h->once_block) {
+        a.w_dst = global ? h->Wg : h->Wc;
+        a.dst_pitch = global ? 0 : w1;
+      }
+      step(a);
       return true;
     }
     case KC_FWD1_GROUP: {
       // Step tt's forward from each cluster's common first layer (every row of
       // the cluster holds it; row g*S is read): SG = S learners per GEMM.
       if (!h->upd_mean) return false;
-      FwdArgs f{h->X, ix, h->INp, W + h->off_W1, (int64_t)S * h->Dp, h->INp, h->part, P, B, Bp, Hp, INp,
-                h->KS_g, h->cps_g};
+      FwdArgs f{h->X, ix, h->INp, h->once_block ? h->Wc : W + h->off_W1, h->once_block ? w1 : (int64_t)S * h->Dp,
+                h->INp, h->part, P, B, Bp, Hp, INp, h->KS_g, h->cps_g};
       f.SG = S;
       launch_fwd_blk(s, f);
       h->ks_cur = h->KS_g;
@@ -741,7 +803,6 @@ bool launch_class(hieravg* h, int kc, int tt) {
       // v = r_K W_b + s_K v + sum_k t_{K-1-k} G_k^T X_k (its own rows).
       if (!h->delayed || !h->hb || !h->V) return false;
       const int b = tt / c.K1;
-      const int64_t w1 = h->Hp * h->INp;
       const int64_t rp1 = round_up((int64_t)c.K1 * B, 32), blk1 = (int64_t)P * rp1;
       BlkArgs a{h->Gt, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp,
                 b == 0 ? W + h->off_W1 : wc_buf(h, b - 1), b == 0 ? 0 : w1, h->V + h->off_W1, h->Dp, h->INp, P, 1,
@@ -759,7 +820,6 @@ bool launch_class(hieravg* h, int kc, int tt) {
     case KC_BLOCK_UPDATE: {
       if (!h->delayed) return false;
       const int b = tt / c.K1;
-      const int64_t w1 = h->Hp * h->INp;
       const int64_t rp = round_up((int64_t)c.K1 * S * B, 32), blk = (int64_t)(P / S) * rp;
       BlkArgs a{h->hb ? h->Gu : h->Gs, h->Hp, h->X, h->idx + (int64_t)b * c.K1 * P * B, h->INp,
                 b == 0 ? W + h->off_W1 : wc_buf(h, b - 1), b == 0 ? 0 : w1, wc_buf(h, b), w1, h->INp, P, S, c.K1, B,
@@ -1252,7 +1312,7 @@ int eval_chunks(hieravg* h, const EvalBufs& b, int replica, int split, int64_t n
   // Replica `replica`; its first weight block lives in replica 0 while the
   // learners share it under delayed updates.
   const float* Wr = h->W + (int64_t)replica * h->Dp;
-  const float* W1r = (h->rows_stale ? h->W : Wr) + h->off_W1;
+  const float* W1r = h->rows_stale ? (h->w1_wg ? h->Wg : h->W + h->off_W1) : Wr + h->off_W1;
   double total = 0.0;
   int64_t hits = 0;
   float lh[kEvalMaxChunk];
@@ -1382,7 +1442,18 @@ int hieravg_round(hieravg_t h) {
   // W1; the averaging kind starts from Wm when the learners share it.
   h->in_delayed = h->delayed && h->w1_shared;
   h->in_shared = avg && h->w1_shared;
-  if (!avg && !h->in_delayed && h->rows_stale) {
+  h->in_wg = !avg && !h->in_delayed && h->once_global && h->rows_stale && h->w1_wg;
+  if (!avg && h->rows_stale && h->w1_wg && !h->in_wg) {
+    // Every learner's W1 is Wg: a delayed round reads it in replica 0, any
+    // other eager round in every row.
+    const size_t w1 = sizeof(float) * h->Hp * h->INp;
+    for (int p = 0; p < (h->in_delayed ? 1 : h->cfg.P); ++p)
+      HAV_CHECK(hipMemcpyAsync(h->W + (int64_t)p * h->Dp + h->off_W1, h->Wg, w1, hipMemcpyDeviceToDevice,
+                               h->stream));
+    h->w1_wg = false;
+    h->rows_stale = h->in_delayed;
+  }
+  if (!avg && !h->in_delayed && h->rows_stale && !h->in_wg) {
     // An eager round reads every replica's W1: copy replica 0's to the others.
     const size_t w1 = sizeof(float) * h->Hp * h->INp;
     for (int p = 1; p < h->cfg.P; ++p)
@@ -1390,15 +1461,22 @@ int hieravg_round(hieravg_t h) {
                                hipMemcpyDeviceToDevice, h->stream));
     h->rows_stale = false;
   }
+  h->launch_failed = false;
+  const char* refused = "a step launch of the round's plan was refused (internal error)";
   if (h->profiling) {
     enqueue_round(h);
   } else {
-    hipGraphExec_t& exec = h->round_exec[h->in_delayed || h->in_shared ? 1 : 0];
+    hipGraphExec_t& exec = h->round_exec[h->in_delayed || h->in_shared ? 1 : h->in_wg ? 2 : 0];
     if (!exec) {
       HAV_CHECK(hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
       enqueue_round(h);
       hipGraph_t graph = nullptr;
       HAV_CHECK(hipStreamEndCapture(h->stream, &graph));
+      if (h->launch_failed) {
+        (void)hipGraphDestroy(graph);
+        set_error(refused);
+        return HIERAVG_EINVAL;
+      }
       const hipError_t e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
       (void)hipGraphDestroy(graph);
       if (e != hipSuccess) {
@@ -1410,6 +1488,10 @@ int hieravg_round(hieravg_t h) {
     HAV_CHECK(hipGraphLaunch(exec, h->stream));
   }
   HAV_CHECK(hipGetLastError());
+  if (h->launch_failed) {
+    set_error(refused);
+    return HIERAVG_EINVAL;
+  }
   // After the global mean every learner holds replica 0's W1 (under delayed
   // updates only replica 0's copy is written); averaging kind: Wm holds every
   // learner's parameters (with P = 1 the round's last step writes row 0).
@@ -1420,6 +1502,10 @@ int hieravg_round(hieravg_t h) {
   }
   h->w1_shared = true;
   if (h->in_delayed) h->rows_stale = true;
+  if (!avg && !h->in_delayed && h->once_global) {  // the global mean of W1 went to Wg only
+    h->rows_stale = true;
+    h->w1_wg = true;
+  }
   h->steps += h->T;
   return HIERAVG_OK;
 }
@@ -1587,7 +1673,7 @@ int hieravg_params(hieravg_t h, float* dst, size_t n_floats) {
       // After delayed updates only replica 0 holds the (common) W1; after an
       // averaging-kind round Wm holds every learner's parameters.
       const float* src = h->W + (int64_t)p * h->Dp;
-      if (i == 0 && h->rows_stale) src = h->cfg.kind == HIERAVG_KIND_AVERAGING ? h->Wm : h->W;
+      if (i == 0 && h->rows_stale) src = h->cfg.kind == HIERAVG_KIND_AVERAGING ? h->Wm : h->w1_wg ? h->Wg : h->W;
       HAV_CHECK(hipMemcpy2DAsync(dst + (int64_t)p * h->D + g.dst_off, sizeof(float) * g.cols, src + g.src_off,
                                  sizeof(float) * g.src_ld, sizeof(float) * g.cols, g.rows, hipMemcpyDefault,
                                  h->stream));
@@ -1614,6 +1700,7 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
                                  sizeof(float) * g.cols, g.rows, hipMemcpyDefault, h->stream));
   h->w1_shared = false;  // unless every row's W1 equals row 0's (a round-boundary checkpoint)
   h->rows_stale = false;
+  h->w1_wg = false;
   const bool avg = h->cfg.kind == HIERAVG_KIND_AVERAGING;
   if (h->cfg.kind == HIERAVG_KIND_MLP || avg) {
     // MLP: equal W1 rows allow delayed updates; averaging kind: equal rows
@@ -1700,7 +1787,10 @@ int hieravg_check_finite(hieravg_t h) {
   HAV_CHECK(hipMemsetAsync(h->flag, 0, sizeof(int), h->stream));
   // After a round every learner's parameters are replica 0's (Wm for the
   // averaging kind); the other rows may hold older values.
-  if (h->rows_stale)
+  if (h->rows_stale && h->w1_wg) {
+    launch_any_nonfinite(h->stream, h->Wg, h->Hp * h->INp, h->flag);
+    launch_any_nonfinite(h->stream, h->W + h->off_b1, h->Dp - h->off_b1, h->flag);
+  } else if (h->rows_stale)
     launch_any_nonfinite(h->stream, h->cfg.kind == HIERAVG_KIND_AVERAGING ? h->Wm : h->W, h->Dp, h->flag);
   else
     launch_any_nonfinite(h->stream, h->W, (int64_t)h->cfg.P * h->Dp, h->flag);

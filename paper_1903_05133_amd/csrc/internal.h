@@ -321,7 +321,20 @@ struct StepArgs {
   int NT;                   // set by the launcher: 128-column tiles per workgroup
   int64_t x_rows = 0;       // rows of the dataset u.Bsrc (0: unknown)
   bool no_fwd = false;      // SG > 1: the update and the group mean only (no partials)
+  // Full tiles only (step_full_shape): learner p reads its old block from
+  // w_src + (p / src_group) * src_pitch (a mean written once) instead of its
+  // own row; the update with the group mean writes group g's mean once, to
+  // w_dst + g * dst_pitch, instead of to every learner's row.  Both blocks
+  // are [Mrows][ldw] like W.
+  const float* w_src = nullptr;
+  int64_t src_pitch = 0;
+  int src_group = 1;
+  float* w_dst = nullptr;
+  int64_t dst_pitch = 0;
 };
+// Whether the full-tile step kernels take a launch of this shape (the only
+// ones that read w_src or write w_dst).
+bool step_full_shape(int Kb, int Mp, int Mrows, int Ncols, int64_t x_rows, int64_t ldb, int64_t ldg, int64_t ldw);
 // Whether the fused kernel handles this shape (Mp a multiple of 16 up to 64,
 // SG in {1, 2, 4, 8}, SG * Mp / 16 <= 16).
 bool step_w1_supported(int Mp, int SG);
@@ -330,7 +343,8 @@ bool step_w1_supported(int Mp, int SG);
 bool step_w1_mean_supported(int Mp, int SG);
 // Number of forward splits KS the fused kernel writes for this shape.
 int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols);
-void launch_step_w1(hipStream_t s, StepArgs a);
+// False (nothing launched) for a w_src / w_dst launch the full-tile kernels do not take.
+bool launch_step_w1(hipStream_t s, StepArgs a);
 
 // Head of the network (k_head.hip).
 void launch_reduce_bias(hipStream_t s, const float* part, int KS, const float* bias, int64_t w_pitch, float* Z,

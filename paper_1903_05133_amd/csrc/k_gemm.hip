@@ -805,6 +805,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
       buf_rsrc(u.G + (int64_t)p * u.Mp * u.ldg + mrow0, (uint64_t)u.Mp * u.ldg * 4);
   const __amdgpu_buffer_rsrc_t rW =
       buf_rsrc(u.W + (int64_t)p * u.w_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
+  const __amdgpu_buffer_rsrc_t rWi =
+      a.w_src ? buf_rsrc(a.w_src + (int64_t)(p / a.src_group) * a.src_pitch + (int64_t)mrow0 * u.ldw,
+                         (uint64_t)kUM * u.ldw * 4)
+              : rW;
   const __amdgpu_buffer_rsrc_t rX = buf_rsrc(u.Bsrc, (uint64_t)a.x_rows * u.ldb * 4);
   {
     // G[s][mrow0 + 4pc4], s = pr0 + 16i, once for the whole workgroup.
@@ -832,7 +836,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
   };
   auto load_w = [&](int n) {
 #pragma unroll
-    for (int i = 0; i < kWL; ++i) wv[i] = buf_ld16(rW, vo_w, n * kSN * 4 + i * w16);
+    for (int i = 0; i < kWL; ++i) wv[i] = buf_ld16(rWi, vo_w, n * kSN * 4 + i * w16);
   };
   auto load_next = [&](int n) {
 #pragma unroll
@@ -930,7 +934,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3
 // Full-tile update with the group mean (no forward) for groups of SG
 // learners: per 64-column tile, each learner's new tile W_j - lr * G_j^T X_j
 // (the update of k_step_w1_full), added in learner order and scaled by 1/SG
-// (SG a power of two: exact), the mean written to every learner's row.  Per
+// (SG a power of two: exact), the mean written to every learner's row (or
+// once, to w_dst).  Per
 // learner the errors and input rows of the tile are staged through LDS while
 // the next learner's are loaded; every global access is a buffer access with
 // a fixed per-lane offset (the gathered rows' byte offsets from LDS) and a
@@ -970,6 +975,12 @@ __global__ __launch_bounds__(256) void k_step_mean_full(StepArgs a, int mtiles, 
   auto rW = [&](int j) {
     return buf_rsrc(u.W + (int64_t)(pg * SG + j) * u.w_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
   };
+  auto rWi = [&](int j) {  // learner j's old block
+    return a.w_src ? buf_rsrc(a.w_src + (int64_t)((pg * SG + j) / a.src_group) * a.src_pitch +
+                                  (int64_t)mrow0 * u.ldw,
+                              (uint64_t)kUM * u.ldw * 4)
+                   : rW(j);
+  };
   const int nst = Kb / kRP;  // 16-row passes of the minibatch (2 or 4)
 
   f32x4 ga[kXL], xb[kXL], wv[kWL], msum[kWL];
@@ -983,7 +994,7 @@ __global__ __launch_bounds__(256) void k_step_mean_full(StepArgs a, int mtiles, 
     }
   };
   auto load_w = [&](int n, int j) {
-    const __amdgpu_buffer_rsrc_t r = rW(j);
+    const __amdgpu_buffer_rsrc_t r = rWi(j);
 #pragma unroll
     for (int i = 0; i < kWL; ++i) wv[i] = buf_ld16(r, vo_w, n * kSN * 4 + i * w16);
   };
@@ -1043,10 +1054,17 @@ __global__ __launch_bounds__(256) void k_step_mean_full(StepArgs a, int mtiles, 
     }
 #pragma unroll
     for (int i = 0; i < kWL; ++i) msum[i] = msum[i] * (1.0f / (float)SG);
-    for (int j = 0; j < SG; ++j) {
-      const __amdgpu_buffer_rsrc_t r = rW(j);
+    if (a.w_dst) {  // the group's mean once (a tile's loads above all precede its store)
+      const __amdgpu_buffer_rsrc_t r =
+          buf_rsrc(a.w_dst + (int64_t)pg * a.dst_pitch + (int64_t)mrow0 * u.ldw, (uint64_t)kUM * u.ldw * 4);
 #pragma unroll
       for (int i = 0; i < kWL; ++i) buf_st16(r, vo_w, n * kSN * 4 + i * w16, msum[i]);
+    } else {
+      for (int j = 0; j < SG; ++j) {
+        const __amdgpu_buffer_rsrc_t r = rW(j);
+#pragma unroll
+        for (int i = 0; i < kWL; ++i) buf_st16(r, vo_w, n * kSN * 4 + i * w16, msum[i]);
+      }
     }
   }
   // Bias step (more than 32 classes), once per learner and row tile.
@@ -1090,20 +1108,25 @@ static void step_plan(int P, int SG, int Mp, int Mrows, int Ncols, int* mtiles, 
   *nchunks = (*ntiles + *NT - 1) / *NT;
 }
 
+bool step_full_shape(int Kb, int Mp, int Mrows, int Ncols, int64_t x_rows, int64_t ldb, int64_t ldg, int64_t ldw) {
+  const uint64_t lim = 0xffffffffull;
+  return Kb == Mp && Mp % kSC == 0 && Mp <= kStepMaxB && Mrows % kUM == 0 && Ncols % kSN == 0 && x_rows > 0 &&
+         (uint64_t)x_rows * ldb * 4 < lim && (uint64_t)Mp * ldg * 4 < lim && (uint64_t)kUM * ldw * 4 < lim;
+}
+
 int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols) {
   int mt, ntl, nc, NT;
   step_plan(P, SG, Mp, Mrows, Ncols, &mt, &ntl, &nc, &NT);
   return nc;
 }
 
-void launch_step_w1(hipStream_t s, StepArgs a) {
+bool launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
   step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
-  const uint64_t lim = 0xffffffffull;
-  const bool full = a.u.Kb == a.u.Mp && a.u.Mp % kSC == 0 && a.u.Mp <= kStepMaxB && a.u.Mrows % kUM == 0 &&
-                    a.u.Ncols % kSN == 0 && a.x_rows > 0 && (uint64_t)a.x_rows * a.u.ldb * 4 < lim &&
-                    (uint64_t)a.u.Mp * a.u.ldg * 4 < lim && (uint64_t)kUM * a.u.ldw * 4 < lim;
+  const bool full =
+      step_full_shape(a.u.Kb, a.u.Mp, a.u.Mrows, a.u.Ncols, a.x_rows, a.u.ldb, a.u.ldg, a.u.ldw);
+  if ((a.w_src || a.w_dst) && !(full && (a.no_fwd || a.SG == 1))) return false;  // only the full-tile kernels redirect
   if (a.no_fwd && full) {
     switch (a.SG) {
       case 2: launch(k_step_mean_full<2>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
@@ -1113,7 +1136,7 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
       case 32: launch(k_step_mean_full<32>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
       default: launch(k_step_mean_full<64>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
     }
-    return;
+    return true;
   }
   if (a.no_fwd) {
     switch (a.SG) {
@@ -1124,14 +1147,14 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
       case 32: launch(k_step_w1<32, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
       default: launch(k_step_w1<64, 1, false>, grid, 256, 0, s, a, mtiles, ntiles, nchunks); break;
     }
-    return;
+    return true;
   }
   if (full && a.SG == 1) {
     if (a.u.Mp == 32)
       launch(k_step_w1_full<2>, grid, 256, 0, s, a, mtiles, ntiles, nchunks);
     else
       launch(k_step_w1_full<4>, grid, 256, 0, s, a, mtiles, ntiles, nchunks);
-    return;
+    return true;
   }
 #define HAV_STEP(SG_, MBF_) launch(k_step_w1<SG_, MBF_>, grid, 256, 0, s, a, mtiles, ntiles, nchunks)
 #define HAV_STEP_MBF(SG_)           \
@@ -1154,6 +1177,7 @@ void launch_step_w1(hipStream_t s, StepArgs a) {
   }
 #undef HAV_STEP_MBF
 #undef HAV_STEP
+  return true;
 }
 
 }  // namespace hav

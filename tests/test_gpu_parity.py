@@ -532,6 +532,10 @@ EVAL_CASES = {
     "mlp_ragged_delayed": (SMALL["mlp_ragged"], "delayed"),
     "mlp_multi_tile_large_C": (SMALL["mlp_multi_tile"], "eager"),
     "mlp_3072_512_10": (cases.named("mlp_3072_512_10", 16, 4, 4, 4, 32, 0.05, seed=0), "auto"),
+    # full-tile eager steps: after the round every learner's first layer is the
+    # once-written global mean, not a replica row
+    "mlp_eager_common_w1": (cases.case("mlp", 8, 4, 2, 2, B=32, IN=192, H=128, C=6, N=400, sigma=0.5, lr=0.05,
+                                       seed=71), "eager"),
 }
 
 
@@ -634,6 +638,36 @@ def _schedule_run(c, schedule, mode="auto"):
             print(f"[gpu case] lr={lr} B={B} worst {det['worst']} flipped {det.get('flipped')}", flush=True)
             assert ok, det
         assert h.steps == len(schedule) * prob.T
+
+
+# Eager rounds of full-tile steps (B = 32 or 64) write the round-end global
+# mean of the first layer once, to a common copy, and (S * B too large for the
+# fused mean step) the block-end cluster means once, to cluster copies; the
+# step after a mean reads its old first layer there.  Delayed rounds in
+# between (AUTO, B <= 32 with K1 = 3, H = 128) start from that copy too.
+ONCE_CASES = {
+    "global_copy_schedule": (cases.case("mlp", 8, 4, 3, 2, B=64, IN=192, H=128, C=6, N=500, sigma=0.5, lr=0.05,
+                                        seed=73), [(0.05, 64), (0.05, 64), (0.05, 32), (0.05, 64), (0.05, 64),
+                                                   (0.05, 16)]),
+    "cluster_copies_schedule": (cases.case("mlp", 16, 8, 3, 2, B=64, IN=192, H=128, C=6, N=600, sigma=0.5,
+                                           lr=0.05, seed=74), [(0.05, 64), (0.05, 64), (0.05, 32), (0.05, 64)]),
+    # every step ends a block: each update with the mean reads the copy the
+    # previous one wrote (the first from the common copy)
+    "cluster_copies_K1_1": (cases.case("mlp", 16, 8, 1, 3, B=64, IN=192, H=128, C=6, N=600, sigma=0.5, lr=0.05,
+                                       seed=75), None),
+    "global_copy_B32": (cases.case("mlp", 4, 2, 2, 3, B=32, IN=128, H=64, C=4, N=300, sigma=0.5, lr=0.05, seed=76),
+                        None),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ONCE_CASES))
+def test_eager_means_written_once(name, gpu_lib):
+    c, schedule = ONCE_CASES[name]
+    if schedule is None:
+        got, idx, steps = _run_gpu(c, rounds=2, mode="eager")
+        _check(c, got, idx, *_oracle(c, 2), mode="eager")
+    else:
+        _schedule_run(c, schedule, "auto")
 
 
 @pytest.mark.parametrize("mode", ["auto", "eager"])
@@ -878,12 +912,17 @@ def test_edge_shapes_match_oracle(name, gpu_lib):
     _check(c, got, idx, *_oracle(c, 1))
 
 
-def test_divergence_check(gpu_lib):
+@pytest.mark.parametrize("kind", ["softmax", "mlp_common_w1"])
+def test_divergence_check(kind, gpu_lib):
     """hieravg_check_finite: finite replicas pass; a step size far too large
-    for the data drives them to inf/NaN, which the check reports."""
+    for the data drives them to inf/NaN, which the check reports (MLP: with
+    the first layer in the once-written common copy)."""
     from paper_1903_05133_amd import HierAvg
-    ok = cases.case("softmax", 4, 2, 2, 1, B=8, IN=20, C=3, N=40, lr=0.1, seed=61)
-    with HierAvg(config=cases.native_config(ok)) as h:
+    if kind == "softmax":
+        ok, mode = cases.case("softmax", 4, 2, 2, 1, B=8, IN=20, C=3, N=40, lr=0.1, seed=61), "auto"
+    else:
+        ok, mode = cases.case("mlp", 4, 2, 2, 2, B=32, IN=64, H=64, C=3, N=100, sigma=0.5, lr=0.1, seed=72), "eager"
+    with HierAvg(config=cases.native_config(ok, mode)) as h:
         h.round()
         assert h.finite()
         h.set_lr(3.0e38)
