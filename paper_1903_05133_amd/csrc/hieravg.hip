@@ -352,7 +352,7 @@ int64_t plan(hieravg* h, int B) {
   }
   h->upd_mean = mlp && h->fused && c.S > 1 && !h->fused_mean && step_w1_mean_supported(h->Bp, c.S);
   h->upd_global = mlp && h->fused && step_w1_mean_supported(h->Bp, P);
-  h->w2_fused = mlp && c.classes > kSmallC && bwd_hidden_update_supported(B) && c.momentum == 0.0f &&
+  h->w2_fused = mlp && c.classes > kSmallC && bwd_hidden_update_supported(B, (int)round_up(c.classes, 16)) && c.momentum == 0.0f &&
                 c.weight_decay == 0.0f;
   h->head_fused = mlp && c.classes <= kSmallC && head_fused_supported((int)h->Hp, (int)round_up(c.classes, 16));
   if (h->upd_mean) {

@@ -75,6 +75,25 @@ __device__ inline int qdiv_small(int n, int d, float inv) {
 // Workgroup index -> logical tile index such that consecutive logical tiles
 // run on the same XCD (the hardware deals workgroups to the 8 XCDs round
 // robin).  Tiles that share operands then share an L2.
+// Buffer accesses: a resource of (base, size in bytes), a per-lane 32-bit
+// byte offset and a wave-uniform one; reads past the size return zero.
+// The base address and size pass through readfirstlane: the resource then
+// sits in scalar registers (the caller's values are uniform), and no access
+// turns into a per-lane loop over resource values.
+__device__ inline __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint64_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b), hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)(bytes < 0xffffffffull ? bytes : 0xffffffffull));
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n, 0x00020000);
+}
+__device__ inline f32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ inline void buf_st16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff, f32x4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
+}
+
 __device__ inline int xcd_remap(int bid, int nblocks) {
   constexpr int kXcd = 8;
   int q = nblocks / kXcd, r = nblocks % kXcd;
@@ -362,7 +381,7 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, float* W2, int64_t w_pitc
                        int M, int Mp, int C, int Cp, int Hp, float* b1 = nullptr, const float* lr = nullptr,
                        float* vb1 = nullptr, float mu = 0.0f, float wd = 0.0f, float* b2 = nullptr);
 // Whether launch_bwd_hidden takes the second layer's step for M samples.
-bool bwd_hidden_update_supported(int M);
+bool bwd_hidden_update_supported(int M, int Cp);
 // Heavy-ball delayed updates, after a block's last step: Gu[k] = u_{K1-1-k}
 // Gs[k] and (Gt set) Gt[k] = t_{K1-1-k} Gs[k] for k < K1, n floats per step
 // (n a multiple of 4).

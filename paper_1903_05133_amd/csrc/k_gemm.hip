@@ -748,23 +748,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(!FWD || SG 
 // the waves raise their priority over the MFMA loops so that the SIMD keeps
 // issuing MFMAs while other workgroups stage data.  Same tiles, operand
 // layouts, k order and outputs as k_step_w1.
-// The base address and size pass through readfirstlane: the resource then
-// sits in scalar registers (the caller's values are uniform), and no access
-// turns into a per-lane loop over resource values.
-__device__ inline __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint64_t bytes) {
-  const uint64_t b = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b), hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
-  const int n = __builtin_amdgcn_readfirstlane((int)(bytes < 0xffffffffull ? bytes : 0xffffffffull));
-  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n, 0x00020000);
-}
-__device__ inline f32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
-  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-__device__ inline void buf_st16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff, f32x4 v) {
-  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
-}
-
 template <int MBF>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MBF > 2 ? 3 : 4))) void k_step_w1_full(
     StepArgs a, int mtiles, int ntiles, int nchunks) {

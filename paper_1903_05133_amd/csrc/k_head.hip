@@ -226,6 +226,7 @@ __global__ __launch_bounds__(256) void k_bwd_hidden(const float* __restrict__ G2
 // other workgroup reads or writes these columns of W2, so the update-GEMM's
 // separate pass over W2 is not needed.
 constexpr int kBhM = 32, kBhN = 32, kBhC = 64;
+constexpr int kBhMaxC = 1024;  // most class slots Cp of the second-layer step (UPD): b2 sums in registers
 constexpr int kBhLG = kBhM + 1, kBhLW = kBhN + 4;  // odd G2 stride: the transposing stores spread over the banks
 constexpr int kBhLds = 2 * kBhC * (kBhLG + kBhLW);
 template <bool UPD>
@@ -262,58 +263,48 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
 
   // G2 pieces: q = tid + 256*i, sample q >> 4, classes 4*(q & 15) .. +3.
   // W2 pieces: q = tid + 256*i, class q >> 3, units 4*(q & 7) .. +3.
-  f32x4 ga[2][2], wa[2][2];
+  // Loads are unconditional from clamped in-range addresses (a load whose
+  // value is used in its own branch is waited for at once); rows past M and
+  // classes past Cp become zero when stored to LDS.
+  f32x4 ga0[2], wa0[2], ga1[2], wa1[2];
   auto load = [&](int c0, f32x4 (&g)[2], f32x4 (&w)[2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i, r = q >> 4, c = c0 + 4 * (q & 15);
-      const bool ok = m0 + r < M && c < Cp;
-      const f32x4 v = *(const f32x4*)(g2 + (ok ? (int64_t)(m0 + r) * Cp + c : 0));
-      g[i] = ok ? v : zero4;
+      g[i] = *(const f32x4*)(g2 + (int64_t)min(m0 + r, M - 1) * Cp + min(c, Cp - 4));
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i, c = c0 + (q >> 3);
-      const bool ok = c < Cp;
-      const f32x4 v = *(const f32x4*)(w2 + (ok ? (int64_t)c * Hp + h0 + 4 * (q & 7) : 0));
-      w[i] = ok ? v : zero4;
+      w[i] = *(const f32x4*)(w2 + (int64_t)min(c, Cp - 1) * Hp + h0 + 4 * (q & 7));
     }
   };
-  auto store = [&](int buf, const f32x4 (&g)[2], const f32x4 (&w)[2]) {
+  auto store = [&](int buf, int c0, const f32x4 (&g)[2], const f32x4 (&w)[2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i, r = q >> 4, c4 = 4 * (q & 15);
+      const bool ok = m0 + r < M && c0 + c4 < Cp;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) gsb(buf)[(c4 + j) * kBhLG + r] = g[i][j];
+      for (int j = 0; j < 4; ++j) gsb(buf)[(c4 + j) * kBhLG + r] = ok ? g[i][j] : 0.0f;
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i;
-      *(f32x4*)&wsb(buf)[(q >> 3) * kBhLW + 4 * (q & 7)] = w[i];
+      *(f32x4*)&wsb(buf)[(q >> 3) * kBhLW + 4 * (q & 7)] = c0 + (q >> 3) < Cp ? w[i] : zero4;
     }
   };
 
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-  load(0, ga[0], wa[0]);
-  if (nch > 1) load(kBhC, ga[1], wa[1]);
-  store(0, ga[0], wa[0]);
-  __syncthreads();
-  // Chunk ch sits in LDS buffer ch & 1; chunk ch + 1 is in register set
-  // (ch + 1) & 1 (loaded one iteration earlier); chunk ch + 2 goes into the
-  // register set that chunk ch used.
-  for (int ch = 0; ch < nch; ++ch) {
-    const int buf = ch & 1;
-    if (ch + 2 < nch) {
-      if (buf == 0)
-        load((ch + 2) * kBhC, ga[0], wa[0]);
-      else
-        load((ch + 2) * kBhC, ga[1], wa[1]);
-    }
-    __builtin_amdgcn_sched_barrier(0);  // those loads go out before the MFMAs
-    const float* gb = gsb(buf);
-    const float* wb = wsb(buf);
+  // b2 (slice 0, UPD): thread t < 64 sums class 64 ch + t of every chunk;
+  // the step is taken once at the end.
+  float sb2[UPD ? (kBhMaxC + kBhC - 1) / kBhC : 1];
+#pragma unroll
+  for (int k = 0; k < (UPD ? (kBhMaxC + kBhC - 1) / kBhC : 1); ++k) sb2[k] = 0.0f;
+  auto chunk = [&](int ch) {  // the products of chunk ch, which sits in LDS buffer ch & 1
+    const float* gb = gsb(ch & 1);
+    const float* wb = wsb(ch & 1);
 #pragma unroll
     for (int ss = 0; ss < kBhC / 4; ss += 2) {
       const int k = wave * (kBhC / 4) + ss + lhi;
@@ -339,20 +330,46 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
           w2[(int64_t)c * Hp + h0 + 16 + i16] = wb[cl * kBhLW + 16 + i16] - lr * d1[r];
         }
       }
-      if (ht == 0 && tid < kBhC && ch * kBhC + tid < Cp) {  // b2: column sums of G2 over the samples
+      if (ht == 0 && tid < kBhC) {  // b2: column sums of G2 over the samples
         float sb = 0.0f;
 #pragma unroll 8
         for (int m = 0; m < kBhM; ++m) sb += gb[tid * kBhLG + m];
-        b2[(int64_t)p * w_pitch + ch * kBhC + tid] -= lr * sb;
+#pragma unroll
+        for (int k = 0; k < (kBhMaxC + kBhC - 1) / kBhC; ++k)
+          if (k == ch) sb2[k] = sb;
       }
     }
-    if (ch + 1 < nch) {
-      if (buf == 0)
-        store(1, ga[1], wa[1]);
-      else
-        store(0, ga[0], wa[0]);
-    }
+  };
+  // Chunks alternate between register sets 0 / 1 and LDS buffers 0 / 1; the
+  // loads of chunk ch + 2 are in flight while chunk ch is multiplied (past
+  // the last chunk they read an in-range chunk again, not stored).
+  load(0, ga0, wa0);
+  load(kBhC, ga1, wa1);
+  store(0, 0, ga0, wa0);
+  __syncthreads();
+  for (int ch = 0; ch < nch; ch += 2) {
+    load((ch + 2) * kBhC, ga0, wa0);
+    __builtin_amdgcn_sched_barrier(0);  // those loads go out before the MFMAs
+    chunk(ch);
+    if (ch + 1 < nch) store(1, (ch + 1) * kBhC, ga1, wa1);
     __syncthreads();
+    if (ch + 1 >= nch) break;
+    load((ch + 3) * kBhC, ga1, wa1);
+    __builtin_amdgcn_sched_barrier(0);
+    chunk(ch + 1);
+    if (ch + 2 < nch) store(0, (ch + 2) * kBhC, ga0, wa0);
+    __syncthreads();
+  }
+  if constexpr (UPD) {
+    if (ht == 0 && tid < kBhC) {
+      float bo[(kBhMaxC + kBhC - 1) / kBhC];
+#pragma unroll
+      for (int k = 0; k < (kBhMaxC + kBhC - 1) / kBhC; ++k)
+        bo[k] = b2[(int64_t)p * w_pitch + min(k * kBhC + tid, Cp - 1)];
+#pragma unroll
+      for (int k = 0; k < (kBhMaxC + kBhC - 1) / kBhC; ++k)
+        if (k < nch && k * kBhC + tid < Cp) b2[(int64_t)p * w_pitch + k * kBhC + tid] = bo[k] - lr * sb2[k];
+    }
   }
   // Waves 1-3 hand their blocks to wave 0 through LDS ([3][32][33]).
   if (wave > 0) {
@@ -363,15 +380,21 @@ __global__ __launch_bounds__(256) void k_bwd_hidden_mfma(const float* __restrict
   __syncthreads();
   if (wave == 0) {
     const int h = h0 + l32;
+    // the ReLU masks of the 16 rows in one batch of loads (rows past M: clamped, unused)
+    float zv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+      zv[r] = Z1[((int64_t)p * Mp + min(m, M - 1)) * Hp + h];
+    }
     float db = 0.0f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 8 * (r >> 2) + 4 * lhi + (r & 3), m = m0 + row;
       const float g = ((acc[r] + lds[row * 33 + l32]) + lds[(32 + row) * 33 + l32]) + lds[(64 + row) * 33 + l32];
       if (m < M) {
-        const int64_t o = ((int64_t)p * Mp + m) * Hp + h;
-        const float g1 = Z1[o] > 0.0f ? g : 0.0f;
-        G1[o] = g1;
+        const float g1 = zv[r] > 0.0f ? g : 0.0f;
+        G1[((int64_t)p * Mp + m) * Hp + h] = g1;
         db += g1;
       }
     }
@@ -1485,7 +1508,7 @@ void launch_bwd_hidden(hipStream_t s, const float* G2, float* W2, int64_t w_pitc
            vb1, mu, wd, (float*)nullptr);
 }
 
-bool bwd_hidden_update_supported(int M) { return M <= kBhM; }
+bool bwd_hidden_update_supported(int M, int Cp) { return M <= kBhM && Cp <= kBhMaxC; }
 
 bool head_fused_supported(int Hp, int Cp) { return Cp <= 16 ? Hp <= 1024 : Cp <= 32 && Hp <= 512; }
 
