@@ -55,7 +55,7 @@ const char* kClassNames[KC_COUNT] = {
     "w1_global_mean", "tail_global_mean", "gram_reduce", "head_step", "head_step_end",
     "z1_delayed", "momentum_buffer_group_mean", "momentum_buffer_global_mean", "momentum_first_step",
     "fwd1_block_gemm_v", "scale_errors", "buffer_update_gemm", "update1_gemm_group_mean", "fwd1_group_gemm",
-    "update1_gemm_global_mean", "head_fused"};
+    "update1_gemm_global_mean", "head_fused", "head_w2_step"};
 
 struct ProfRec {
   hipEvent_t a, b;
@@ -223,6 +223,7 @@ void release(hieravg* h) {
   for (auto e : h->round_exec)
     if (e) (void)hipGraphExecDestroy(e);
   if (h->own_stream) (void)hipStreamDestroy(h->own_stream);
+
   delete h;
 }
 
@@ -505,11 +506,12 @@ int build(hieravg* h) {
           return rc;
         h->once_alloc = true;
       }
-      if (h->head_fused &&
-          (rc = alloc_zero(h, (void**)&h->hgrad,
-                           sizeof(float) * head_fused_scratch_floats(P, h->Bp, h->C, (int)h->Hp),
-                           "head gradient rows")))
-        return rc;
+      if (h->head_fused) {
+        if ((rc = alloc_zero(h, (void**)&h->hgrad,
+                             sizeof(float) * head_fused_scratch_floats(P, h->Bp, h->C, (int)h->Hp),
+                             "head gradient rows")))
+          return rc;
+      }
     }
     if ((rc = alloc_zero(h, (void**)&h->ctr, 2 * sizeof(uint64_t), "counters"))) return rc;
     if (any_delayed) {
@@ -894,7 +896,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
                     C, Cp, Hp, h->hyper, mom);
       return true;
     }
-    case KC_HEAD_FUSED: {  // eager schedule
+    case KC_HEAD_FUSED:
+    case KC_HEAD_W2: {  // eager schedule
       if (!small || h->in_delayed || !h->head_fused) return false;
       HeadFusedArgs a;
       a.part = h->part;
@@ -922,7 +925,10 @@ bool launch_class(hieravg* h, int kc, int tt) {
         a.mom.vb2 = h->V + h->off_b2;
       }
       a.scratch = h->hgrad;
-      launch_head_fused(s, a);
+      if (kc == KC_HEAD_FUSED)
+        launch_head_fused(s, a);
+      else
+        launch_head_w2_step(s, a);
       return true;
     }
     case KC_HEAD_STEP:
@@ -1064,6 +1070,10 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   auto go = [&](int kc) { run(h, kc, [&] { launch_class(h, kc, tt); }); };
   if (!have_fwd) go(KC_FWD1);
   for (int i = 0; i < n; ++i) go(seq[i]);
+  // Small-C head: then the step of W2, b1, b2 from its gradient rows (on a
+  // second stream beside the first-layer kernel below, which reads none of
+  // them, the captured round was 0.13 ms slower on the 64-learner MLP).
+  if (seq == kSmallFused) go(KC_HEAD_W2);
   const int T = h->T;
   const bool last = tt == T - 1;
   const bool mean = !last && (tt + 1) % c.K1 == 0 && c.S > 1;

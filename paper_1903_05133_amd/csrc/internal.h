@@ -139,7 +139,8 @@ enum KernelClass {
   KC_UPD1_MEAN,      // layer-1 update of every learner with the local mean, no forward
   KC_FWD1_GROUP,     // layer-1 forward of a step from each cluster's common first layer (one GEMM per cluster)
   KC_UPD1_GLOBAL,    // layer-1 update of every learner with the global mean (a round's last step)
-  KC_HEAD_FUSED,     // small C, eager: the loss side of a step in one launch
+  KC_HEAD_FUSED,     // small C, eager: the loss side of a step (G1, gradient rows of W2, b1, b2)
+  KC_HEAD_W2,        // small C, eager: the step of W2, b1, b2 from those rows
   KC_COUNT
 };
 
@@ -424,8 +425,9 @@ void launch_head_b(hipStream_t s, const float* PL, float* W2, float* b1, float* 
                    const float* Z1, float* G1, const int32_t* labels, const int32_t* idx, int P, int M, int Mp, int C,
                    int Cp, int Hp, const float* lr, HeadMom mom = HeadMom());
 // The eager loss side (C <= 32) in two launches: one workgroup per learner
-// and 16 samples (G1 and the group's gradient rows of b1, W2, b2), then the
-// step of b1, W2, b2 from the rows.  Supported when head_fused_supported(Hp, Cp).
+// and 16 samples (G1 and the group's gradient rows of b1, W2, b2:
+// launch_head_fused), then the step of b1, W2, b2 from the rows
+// (launch_head_w2_step).  Supported when head_fused_supported(Hp, Cp).
 struct HeadFusedArgs {
   const float* part = nullptr;  // [KS][P][Mp][Hp] split-K partials of the layer-1 product, `split` floats apart
   int KS = 1;
@@ -445,6 +447,7 @@ struct HeadFusedArgs {
 bool head_fused_supported(int Hp, int Cp);
 int64_t head_fused_scratch_floats(int P, int Mp, int C, int Hp);
 void launch_head_fused(hipStream_t s, const HeadFusedArgs& a);
+void launch_head_w2_step(hipStream_t s, const HeadFusedArgs& a);
 
 // Head of the delayed schedule (C <= 32, M <= 32, K1 <= 8), step k of a
 // block: workgroup (p, slice of 32 hidden units) finishes step k-1's backward

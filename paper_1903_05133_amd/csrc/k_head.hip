@@ -923,14 +923,24 @@ __global__ __launch_bounds__(256) void k_head_w2_step(HeadFusedArgs a, int nblk)
   const float lr = *a.lr;
   const HeadMom& mom = a.mom;
   const int e = blk * 256 + tid;
+  // The groups' rows in batches of eight loads issued together (indices past
+  // NS repeat the last row and are not added).
+  constexpr int kB = 8;
   if (e < (C + 1) * (Hp / 4)) {
-    f32x4 g = *(const f32x4*)(h0 + 4 * e);
-    for (int k = 1; k < NS; ++k) g += *(const f32x4*)(h0 + k * HS + 4 * e);
     const bool isb = 4 * e < Hp;
     const int64_t o = isb ? 4 * e : 4 * e - Hp;
     f32x4* w = (f32x4*)((isb ? a.b1 : a.W2) + po + o);
     float* vbase = isb ? mom.vb1 : mom.vw2;
-    const f32x4 wo = *w;
+    const f32x4 wo = *w;  // issued with the rows below
+    f32x4 g = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < NS; k0 += kB) {
+      f32x4 v[kB];
+#pragma unroll
+      for (int k = 0; k < kB; ++k) v[k] = *(const f32x4*)(h0 + min(k0 + k, NS - 1) * HS + 4 * e);
+#pragma unroll
+      for (int k = 0; k < kB; ++k)
+        if (k0 + k < NS) g = k0 + k == 0 ? v[k] : g + v[k];
+    }
     f32x4 d = g + mom.wd * wo;
     if (vbase) {
       f32x4* v = (f32x4*)(vbase + po + o);
@@ -940,10 +950,17 @@ __global__ __launch_bounds__(256) void k_head_w2_step(HeadFusedArgs a, int nblk)
     *w = wo - lr * d;
   }
   if (blk == 0 && tid < C) {
-    float g = h0[(int64_t)(C + 1) * Hp + tid];
-    for (int k = 1; k < NS; ++k) g += h0[k * HS + (int64_t)(C + 1) * Hp + tid];
     float* w = a.b2 + po + tid;
     const float wo = *w;
+    float g = 0.0f;
+    for (int k0 = 0; k0 < NS; k0 += kB) {
+      float v[kB];
+#pragma unroll
+      for (int k = 0; k < kB; ++k) v[k] = h0[min(k0 + k, NS - 1) * HS + (int64_t)(C + 1) * Hp + tid];
+#pragma unroll
+      for (int k = 0; k < kB; ++k)
+        if (k0 + k < NS) g = k0 + k == 0 ? v[k] : g + v[k];
+    }
     float d = g + mom.wd * wo;
     if (mom.vb2) {
       float* v = mom.vb2 + po + tid;
@@ -1533,6 +1550,9 @@ void launch_head_fused(hipStream_t s, const HeadFusedArgs& a) {
   else
     HAV_HEAD_FUSED(32, 512);
 #undef HAV_HEAD_FUSED
+}
+
+void launch_head_w2_step(hipStream_t s, const HeadFusedArgs& a) {
   const int nblk = ((a.C + 1) * (a.Hp / 4) + 255) / 256;
   launch(k_head_w2_step, a.P * nblk, 256, 0, s, a, nblk);
 }
