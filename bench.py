@@ -73,7 +73,21 @@ def step_work(c):
     return 4 * B * IN * H + 6 * B * H * C, 8 * D + 4 * B * IN + 4 * B
 
 
-def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
+def eager_means_once(c):
+    """Whether an eager MLP round writes the first layer's global mean once
+    (full-tile steps: B of 32 or 64, plain SGD, P a power of two up to 64)
+    and its block-end cluster means once (S * B / 16 > 16: past the fused
+    mean step), as the library plans it."""
+    P, S, B = c["P"], c["S"], c["B"]
+    pow2 = lambda n: 2 <= n <= 64 and n & (n - 1) == 0
+    plain = c.get("momentum", 0.0) == 0.0 and c.get("weight_decay", 0.0) == 0.0
+    upd_mean = S > 1 and pow2(S) and S * B // 16 > 16
+    once_global = (c["kind"] == "mlp" and plain and B in (32, 64) and pow2(P) and c["K1"] * c["K2"] >= 2
+                   and (c["K1"] > 1 or S == 1 or upd_mean))
+    return once_global, once_global and upd_mean
+
+
+def mlp_kernel_work(P, S, K1, K2, B, IN, H, C, once=(False, False)):
     """Algorithmic (bytes, flops) per launch of each kernel class of an MLP
     round: every operand a launch needs read once and every result written
     once, at its logical (unpadded) size.  Split-K partial sums are an
@@ -107,7 +121,8 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
         # pre-activations of one step with the Gram correction of the earlier
         # steps (more than 32 classes)
         "z1_delayed": (F * P * (B * H + H + k_avg * (B * H + B * B) + B * H), P * 2 * B * B * H * k_avg),
-        "fwd1_gemm": (P * F * (H * IN + B * IN + B * H), P * 2 * B * H * IN),
+        # (a round's first forward from the once-written global mean: W1 read once)
+        "fwd1_gemm": (F * ((1 if once[0] else P) * H * IN + P * B * IN + P * B * H), P * 2 * B * H * IN),
         "reduce1": (P * F * (H + B * H), P * B * H),
         "fwd2_gemm": (P * F * (C * H + B * H + B * C), P * 2 * B * C * H),
         "softmax_grad": (P * F * (C + 2 * B * C) + P * B * 8, P * B * C * 4),
@@ -119,11 +134,13 @@ def mlp_kernel_work(P, S, K1, K2, B, IN, H, C):
         # written once; the cluster-mean variant moves the same bytes
         "step1_gemm": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
         "step1_gemm_group_mean": (P * F * (2 * H * IN + 2 * B * H + 2 * B * IN), P * 4 * B * H * IN),
-        # update of every learner's W1 with the cluster (or global) mean
-        # written to every row: W1 read and written once per learner, G1 and
-        # the minibatch read
-        "update1_gemm_group_mean": (P * F * (2 * H * IN + B * H + B * IN), P * 2 * B * H * IN),
-        "update1_gemm_global_mean": (P * F * (2 * H * IN + B * H + B * IN), P * 2 * B * H * IN),
+        # update of every learner's W1 with the cluster (or global) mean: W1
+        # read once per learner, the mean written to every row or once per
+        # cluster (once), G1 and the minibatch read
+        "update1_gemm_group_mean": (F * (P * H * IN + (G if once[1] else P) * H * IN + P * B * H + P * B * IN),
+                                    P * 2 * B * H * IN),
+        "update1_gemm_global_mean": (F * (P * H * IN + (1 if once[0] else P) * H * IN + P * B * H + P * B * IN),
+                                     P * 2 * B * H * IN),
         # next step's forward from each cluster's common W1: one copy per
         # cluster, the minibatches, the pre-activations
         "fwd1_group_gemm": (F * (G * H * IN + P * B * IN + P * B * H), P * 2 * B * H * IN),
@@ -153,7 +170,7 @@ def kernel_work(c, classes=None):
                 "step1_gemm": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
                 "step1_gemm_group_mean": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
                 "global_mean": (2 * F * P * D, P * D)}
-    w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"])
+    w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"], eager_means_once(c))
     if classes is not None and "bwd_hidden" in classes and "update2_gemm" not in classes:
         # hidden error and the W2 step in one pass: G2, W2, Z1 read, G1 and W2 written
         B, H, C = c["B"], c["H"], c["C"]
