@@ -73,20 +73,6 @@ def step_work(c):
     return 4 * B * IN * H + 6 * B * H * C, 8 * D + 4 * B * IN + 4 * B
 
 
-def eager_means_once(c):
-    """Whether an eager MLP round writes the first layer's global mean once
-    (full-tile steps: B of 32 or 64, plain SGD, P a power of two up to 64)
-    and its block-end cluster means once (S * B / 16 > 16: past the fused
-    mean step), as the library plans it."""
-    P, S, B = c["P"], c["S"], c["B"]
-    pow2 = lambda n: 2 <= n <= 64 and n & (n - 1) == 0
-    plain = c.get("momentum", 0.0) == 0.0 and c.get("weight_decay", 0.0) == 0.0
-    upd_mean = S > 1 and pow2(S) and S * B // 16 > 16
-    once_global = (c["kind"] == "mlp" and plain and B in (32, 64) and pow2(P) and c["K1"] * c["K2"] >= 2
-                   and (c["K1"] > 1 or S == 1 or upd_mean))
-    return once_global, once_global and upd_mean
-
-
 def mlp_kernel_work(P, S, K1, K2, B, IN, H, C, once=(False, False)):
     """Algorithmic (bytes, flops) per launch of each kernel class of an MLP
     round: every operand a launch needs read once and every result written
@@ -170,7 +156,8 @@ def kernel_work(c, classes=None):
                 "step1_gemm": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
                 "step1_gemm_group_mean": (P * F * (2 * D + 2 * B * C + 2 * B * IN), P * 4 * B * C * IN),
                 "global_mean": (2 * F * P * D, P * D)}
-    w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"], eager_means_once(c))
+    import cases
+    w = mlp_kernel_work(P, S, K1, K2, c["B"], c["IN"], c["H"], c["C"], cases.eager_means_once(c))
     if classes is not None and "bwd_hidden" in classes and "update2_gemm" not in classes:
         # hidden error and the W2 step in one pass: G2, W2, Z1 read, G1 and W2 written
         B, H, C = c["B"], c["H"], c["C"]

@@ -132,3 +132,18 @@ def branch_parity(prob, got, want, monitor, rerun, max_runs=MAX_BRANCH_RUNS):
                 det2["unflipped_worst"] = det["worst"]
                 return True, det2
     return False, det
+
+
+def eager_means_once(c):
+    """Whether an eager MLP round writes the first layer's global mean once
+    (full-tile steps: B of 32 or 64, plain SGD, P a power of two up to 64)
+    and its block-end cluster means once (S * B / 16 > 16: past the fused
+    mean step), as the library plans it."""
+    P, S, B = c["P"], c["S"], c["B"]
+    pow2 = lambda n: 2 <= n <= 64 and n & (n - 1) == 0
+    plain = c.get("momentum", 0.0) == 0.0 and c.get("weight_decay", 0.0) == 0.0
+    upd_mean = S > 1 and pow2(S) and S * B // 16 > 16
+    T = c.get("k_global", 0) or c["K1"] * c["K2"]  # steps per round
+    once_global = (c["kind"] == "mlp" and plain and B in (32, 64) and pow2(P) and T >= 2
+                   and (c["K1"] > 1 or S == 1 or upd_mean))
+    return once_global, once_global and upd_mean
