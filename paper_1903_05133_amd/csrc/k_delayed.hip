@@ -938,9 +938,12 @@ __global__ __launch_bounds__(256) void k_gram_reduce(float* __restrict__ gram, i
   }
 }
 
+#ifndef HAV_GRAM_TARGET
+#define HAV_GRAM_TARGET 512
+#endif
 int gram_splits(int P, int K2, int K) {
   // about two workgroups per CU, at least two 64-wide chunks per split
-  const int target = 512;
+  const int target = HAV_GRAM_TARGET;
   int ksg = (target + P * K2 - 1) / (P * K2);
   return std::max(1, std::min(ksg, K / kKC / 2));
 }
