@@ -732,7 +732,8 @@ bool launch_class(hieravg* h, int kc, int tt) {
     case KC_UPD1_MEAN:
     case KC_UPD1_GLOBAL: {
       const bool global = kc == KC_UPD1_GLOBAL;
-      if (global ? !h->upd_global : !h->upd_mean || tt + 1 >= h->T) return false;
+      // (the cluster form also ends an eager round whose means go to the copies)
+      if (global ? !h->upd_global : !h->upd_mean || (tt + 1 >= h->T && !h->once_block)) return false;
       StepArgs a{};
       a.u = UpdArgs{h->G1, h->Hp, Bp, h->X, ix, h->INp, W + h->off_W1, h->Dp, h->INp,
                     small ? nullptr : W + h->off_b1, P, B, Hp, INp, h->hyper};
@@ -861,7 +862,11 @@ bool launch_class(hieravg* h, int kc, int tt) {
       return true;
     }
     case KC_W1_MEAN:  // with the global mean of b1, W2, b2 in the same launch
-      if (!h->delayed) return false;
+      if (!h->in_delayed) {  // eager, cluster copies: their mean into the common copy
+        if (!h->once_block) return false;
+        launch_mean_rows(s, h->Wg, h->Wc, w1, w1, P / S, W + h->off_b1, h->Dp, h->Dp - h->off_b1, P);
+        return true;
+      }
       launch_mean_rows(s, W + h->off_W1, wc_buf(h, c.K2 - 1), h->Hp * h->INp, h->Hp * h->INp, P / S,
                        P > 1 ? W + h->off_b1 : nullptr,
                        h->Dp, h->Dp - h->off_b1, P);
@@ -1078,7 +1083,13 @@ void enqueue_step(hieravg* h, int tt, bool& have_fwd) {
   const bool last = tt == T - 1;
   const bool mean = !last && (tt + 1) % c.K1 == 0 && c.S > 1;
   have_fwd = false;
-  if (last && h->upd_global) {  // with the global mean of every block
+  if (last && h->upd_global && h->once_block) {
+    // the cluster means, once, to the copies, then their mean into the
+    // common copy with the global mean of b1, W2, b2 (one group of P
+    // learners per tile would leave the GPU half idle)
+    go(KC_UPD1_MEAN);
+    go(KC_W1_MEAN);
+  } else if (last && h->upd_global) {  // with the global mean of every block
     go(KC_UPD1_GLOBAL);
     go(KC_TAIL_GLOBAL);
   } else if (last || !h->fused || (mean && !h->fused_mean && !h->upd_mean)) {

@@ -1079,13 +1079,19 @@ bool step_w1_mean_supported(int Mp, int SG) {
 // Workgroups a step launch aims for: about four per CU, or two waves of three
 // per CU for 64-sample steps of one learner (the full-tile kernel's LDS
 // allows three workgroups per CU there).
+#ifndef HAV_STEP_TARGET_MEAN
+#define HAV_STEP_TARGET_MEAN 1536
+#endif
 static int step_target(int SG, int Mp) { return SG == 1 && Mp == 64 ? HAV_STEP_TARGET_WG64 : kStepTargetWG; }
 
-static void step_plan(int P, int SG, int Mp, int Mrows, int Ncols, int* mtiles, int* ntiles, int* nchunks, int* NT) {
+// no_fwd: the update with the group mean alone (its column chunks write no
+// forward partials), with a grid target of its own.
+static void step_plan(int P, int SG, int Mp, int Mrows, int Ncols, int* mtiles, int* ntiles, int* nchunks, int* NT,
+                      bool no_fwd = false) {
   *mtiles = (Mrows + kUM - 1) / kUM;
   *ntiles = (Ncols + kSN - 1) / kSN;
   const int64_t base = (int64_t)(P / SG) * *mtiles;
-  const int target = step_target(SG, Mp);
+  const int target = no_fwd ? HAV_STEP_TARGET_MEAN : step_target(SG, Mp);
   int nc = (int)std::min<int64_t>(*ntiles, std::max<int64_t>(1, (target + base - 1) / base));
   *NT = (*ntiles + nc - 1) / nc;
   *nchunks = (*ntiles + *NT - 1) / *NT;
@@ -1105,7 +1111,7 @@ int step_w1_splits(int P, int SG, int Mp, int Mrows, int Ncols) {
 
 bool launch_step_w1(hipStream_t s, StepArgs a) {
   int mtiles, ntiles, nchunks;
-  step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT);
+  step_plan(a.u.P, a.SG, a.u.Mp, a.u.Mrows, a.u.Ncols, &mtiles, &ntiles, &nchunks, &a.NT, a.no_fwd);
   const unsigned grid = (unsigned)((int64_t)(a.u.P / a.SG) * mtiles * nchunks);
   const bool full =
       step_full_shape(a.u.Kb, a.u.Mp, a.u.Mrows, a.u.Ncols, a.x_rows, a.u.ldb, a.u.ldg, a.u.ldw);
