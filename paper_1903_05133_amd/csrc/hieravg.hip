@@ -1736,6 +1736,16 @@ int hieravg_set_params(hieravg_t h, const float* src, size_t n_floats) {
     h->w1_shared = differ == 0;
     if (avg && h->w1_shared)
       HAV_CHECK(hipMemcpyAsync(h->Wm, h->W, sizeof(float) * h->Dp, hipMemcpyDeviceToDevice, h->stream));
+    // Equal rows where eager rounds write the global mean of W1 once: the
+    // state such a round leaves, so the next round starts from the common
+    // copy as it would have (the same launches and rounding: checkpoints at
+    // a round boundary resume exactly).
+    if (!avg && h->w1_shared && h->once_global) {
+      HAV_CHECK(hipMemcpyAsync(h->Wg, h->W + h->off_W1, sizeof(float) * h->Hp * h->INp, hipMemcpyDeviceToDevice,
+                               h->stream));
+      h->rows_stale = true;
+      h->w1_wg = true;
+    }
   }
   HAV_CHECK(hipStreamSynchronize(h->stream));
   return HIERAVG_OK;

@@ -397,6 +397,42 @@ def test_resume_from_params_continues_the_trajectory(gpu_lib):
     assert ok, det
 
 
+@pytest.mark.parametrize("name", ["global_copy_B32", "cluster_copies_K1_1"])
+def test_resume_after_common_copy_round(name, gpu_lib):
+    """After an eager round that left the first layer in the common copy
+    (the learner rows stale): params() expands it, and set_params of those
+    values, in the same handle and in a fresh one, continues the oracle's
+    trajectory (the next round reads the rows again, not the copy)."""
+    from paper_1903_05133_amd import HierAvg
+    c, _ = ONCE_CASES[name]
+    prob = cases.oracle_problem(c)
+    st = M.create(prob)
+    M.hieravg_round(prob, st)
+    with HierAvg(config=cases.native_config(c, "eager")) as h:
+        h.round()
+        w1 = h.params()
+        ok, det = cases.parity_report(prob, w1, st.W)
+        assert ok, det
+        h.set_params(w1)
+        assert h.finite()
+        h.round()
+        got_same = h.params()
+    with HierAvg(config=cases.native_config(c, "eager")) as h2:
+        h2.set_params(w1)
+        h2.round()
+        got_fresh = h2.params()
+    # the same handle continues at global step T: the oracle's second round;
+    # the fresh one draws from step 0: one oracle round started from w1
+    M.hieravg_round(prob, st)
+    ok, det = cases.parity_report(prob, got_same, st.W)
+    assert ok, det
+    st2 = M.create(prob)
+    st2.W = w1.astype(np.float64)
+    M.hieravg_round(prob, st2)
+    ok, det = cases.parity_report(prob, got_fresh, st2.W)
+    assert ok, det
+
+
 def test_torch_stream_and_profile(gpu_lib):
     import torch
     from paper_1903_05133_amd import HierAvg
@@ -859,15 +895,16 @@ def test_no_buffers_without_momentum(gpu_lib):
             h.momentum()
 
 
-@pytest.mark.parametrize("name", ["delayed_mlp", "momentum_softmax", "eager_unequal_rows"])
+@pytest.mark.parametrize("name", ["delayed_mlp", "momentum_softmax", "eager_unequal_rows", "eager_common_copy"])
 def test_checkpoint_resume_is_exact(name, gpu_lib, tmp_path):
     """save() after one round, load() into a fresh handle, one more round:
     bit for bit the second round of the uninterrupted run (same step counter,
     parameters, buffers and, for equal first-layer rows, the same schedule)."""
     from paper_1903_05133_amd import HierAvg
     c = {"delayed_mlp": SMALL["mlp_ragged"], "momentum_softmax": MOMENTUM_CASES["softmax_mom_wd"],
-         "eager_unequal_rows": SMALL["mlp_ragged"]}[name]
-    cfg = cases.native_config(c)
+         "eager_unequal_rows": SMALL["mlp_ragged"], "eager_common_copy": ONCE_CASES["cluster_copies_schedule"][0]}[name]
+    # eager_common_copy: eager rounds that leave the first layer in the common copy
+    cfg = cases.native_config(c, "eager" if name == "eager_common_copy" else "auto")
     with HierAvg(config=cfg) as h:
         h.round()
         if name == "eager_unequal_rows":  # rows that differ: the resumed round must run eager
