@@ -694,17 +694,18 @@ __global__ __launch_bounds__(256) void k_head_b(const float* __restrict__ PL, fl
     step(b2 + po + tid, mom.vb2 ? mom.vb2 + po + tid : nullptr, b2[po + tid], db2);
 }
 
-// The loss side of an eager step in one launch (C <= 32).  Workgroup =
-// learner p and the 16 samples [16q, 16q + 16) with every hidden unit:
+// The loss side of an eager step (C <= 32), before the second layer's
+// step.  Workgroup = learner p and the 16 samples [16q, 16q + 16) with every
+// hidden unit, eight waves:
 //  * Z1 = (split-K partials added in split order) + b1 and the learner's W2
 //    (rows C..KC-1 zero) are staged in LDS;
-//  * logits = b2 + ReLU(Z1) W2^T as 16x16x4 MFMAs, the units split over the
-//    four waves and the waves' partial logits added in wave order; then the
-//    softmax cross-entropy gradient G2 = (softmax - onehot) / M, four lanes
-//    per sample;
+//  * logits = b2 + ReLU(Z1) W2^T as 16x16x4 MFMAs, the 16-unit runs dealt
+//    to the waves in turn and the waves' partial logits added in wave order;
+//    then the softmax cross-entropy gradient G2 = (softmax - onehot) / M,
+//    four lanes per sample;
 //  * G1 = (G2 W2) * [Z1 > 0] (stored) and the group's dW2 = G2^T ReLU(Z1),
-//    db1 = sum of G1 and db2 = sum of G2 over its samples, all per 16-unit
-//    tile as 16x16x4 MFMAs.
+//    db1 = sum of G1 and db2 = sum of G2 over its samples, per 16-unit run
+//    as 16x16x4 MFMAs.
 // The group's dW2, db1, db2 go to its scratch row; k_head_w2_step adds the
 // rows and takes the step (a cross-workgroup sum inside this kernel would
 // need device-scope fences, each of which writes back and invalidates the
