@@ -357,7 +357,7 @@ int64_t plan(hieravg* h, int B) {
                 c.weight_decay == 0.0f;
   h->head_fused = mlp && c.classes <= kSmallC && head_fused_supported((int)h->Hp, (int)round_up(c.classes, 16));
   if (h->upd_mean) {
-    plan_split_blk(P / c.S, c.S * h->Bp, (int)n1, (int)h->INp, &h->KS_g, &h->cps_g, HAV_FWD_BLOCK_TARGET);
+    plan_split_blk(P / c.S, c.S * h->Bp, (int)n1, (int)h->INp, &h->KS_g, &h->cps_g);
     ks_max = std::max<int64_t>(ks_max, h->KS_g);
   }
   if (h->fused_mean) {
@@ -371,7 +371,7 @@ int64_t plan(hieravg* h, int B) {
   h->once_global = h->once_cond && h->once_alloc;
   h->once_block = h->once_global && h->upd_mean && c.S > 1;
   if (h->once_cond) {
-    plan_split_blk(1, P * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_g0, &h->cps_g0, HAV_FWD_BLOCK_TARGET);
+    plan_split_blk(1, P * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_g0, &h->cps_g0);
     ks_max = std::max<int64_t>(ks_max, h->KS_g0);
   }
   h->delayed = false;
@@ -391,13 +391,12 @@ int64_t plan(hieravg* h, int B) {
                    !(h->hb && c.K2 < 2);
   if (h->delayed) {
     // One GEMM per cluster and block: the K1*S minibatches against the copy.
-    plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b,
-                   HAV_FWD_BLOCK_TARGET);
+    plan_split_blk(P / c.S, c.K1 * c.S * h->Bp, (int)h->Hp, (int)h->INp, &h->KS_b, &h->cps_b);
     ks_max = std::max<int64_t>(ks_max, (int64_t)h->KS_b * c.K1);
     // Heavy-ball with momentum: one more per learner, its K1 minibatches
     // against its own buffer.
     if (h->hb && c.momentum > 0.0f)
-      plan_split_blk(P, c.K1 * h->Bp, (int)h->Hp, (int)h->INp, &h->KSv, &h->cpsv, HAV_FWD_BLOCK_TARGET);
+      plan_split_blk(P, c.K1 * h->Bp, (int)h->Hp, (int)h->INp, &h->KSv, &h->cpsv);
   }
   h->ks_cur = h->KS1;
   return std::max<int64_t>(ks_max * P * h->Bp * n1, mlp ? (int64_t)h->KS2 * P * h->Bp * h->Cp : 0);

@@ -245,7 +245,7 @@ void plan_split(int P, int Mp, int N, int K, int* KS, int* cps, int target_wg = 
 // Large-tile forward (128 x 128 tiles, 1024 threads) for many rows per weight
 // copy, and its split count.
 void launch_fwd_blk(hipStream_t s, const FwdArgs& a);
-void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg);
+void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps);
 // Workgroup target of the block-wide forward from the cluster copies.
 #ifndef HAV_FWD_BLOCK_TARGET
 #define HAV_FWD_BLOCK_TARGET 256

@@ -329,11 +329,19 @@ __global__ __launch_bounds__(1024) void k_fwd_blk256(FwdArgs a, int ntiles, int 
   }
 }
 
-// The large tile where it applies: every tile full, M = Mp, and at least
-// 64 32-wide chunks per split (the pipeline start is then a small share).
-static bool fwd_blk256_applies(const FwdArgs& a) {
-  const int GM = a.SG * a.Mp;
-  return GM % kBT2 == 0 && a.N % kBT2 == 0 && a.M == a.Mp && 2 * a.cps >= 64 && a.Mp % 8 == 0;
+// Whether a block forward over `groups` row groups of `rows` rows takes the
+// 256 x 256 tile: every tile full, and with the split count that brings the
+// grid to about HAV_FWD_BLOCK_TARGET workgroups each split still at least 64
+// 32-wide chunks long (the pipeline start is then a small share).  The split
+// planner and the launcher both decide by this, so a launch runs the tile its
+// split count was planned for (a split count planned for 128 x 128 tiles
+// fills a quarter as many 256 x 256 workgroups).
+static bool blk256_planned(int64_t groups, int rows, int N, int K) {
+  if (rows % kBT2 != 0 || N % kBT2 != 0) return false;
+  const int nch = K / kKC;
+  const int64_t t2 = groups * (rows / kBT2) * (N / kBT2);
+  const int64_t ks2 = std::min<int64_t>(nch, std::max<int64_t>(1, (HAV_FWD_BLOCK_TARGET + t2 - 1) / t2));
+  return 2 * ((nch + ks2 - 1) / ks2) >= 64;
 }
 
 void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
@@ -342,7 +350,7 @@ void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
   const int ntiles = (a.N + kBT - 1) / kBT;
   const int groups = a.vS > 0 ? a.P / a.vS : a.P / a.SG;
   const unsigned grid = (unsigned)((int64_t)groups * a.KS * mtiles * ntiles);
-  if (fwd_blk256_applies(a)) {
+  if (a.M == a.Mp && a.Mp % 8 == 0 && blk256_planned(groups, GM, a.N, a.K)) {
     const int mt2 = GM / kBT2, nt2 = a.N / kBT2;
     launch(k_fwd_blk256, (unsigned)((int64_t)groups * a.KS * mt2 * nt2), 1024, 0, s, a, nt2, mt2);
     return;
@@ -350,16 +358,14 @@ void launch_fwd_blk(hipStream_t s, const FwdArgs& a) {
   launch(k_fwd_blk, grid, 1024, 0, s, a, ntiles, mtiles);
 }
 
-// Split count of k_fwd_blk: about target_wg workgroups, no empty split.
-void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps, int target_wg) {
-  int64_t tiles = (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
+// Split count of k_fwd_blk: about HAV_FWD_BLOCK_TARGET workgroups of the
+// tile blk256_planned picks, no empty split.
+void plan_split_blk(int groups, int rows, int N, int K, int* KS, int* cps) {
+  const int64_t tiles = blk256_planned(groups, rows, N, K)
+                            ? (int64_t)groups * (rows / kBT2) * (N / kBT2)
+                            : (int64_t)groups * ((rows + kBT - 1) / kBT) * ((N + kBT - 1) / kBT);
   const int nch = K / kKC;
-  if (rows % kBT2 == 0 && N % kBT2 == 0) {  // the 256 x 256 tile if its splits stay long
-    const int64_t t2 = (int64_t)groups * (rows / kBT2) * (N / kBT2);
-    const int64_t ks2 = std::min<int64_t>(nch, std::max<int64_t>(1, (target_wg + t2 - 1) / t2));
-    if (2 * ((nch + ks2 - 1) / ks2) >= 64) tiles = t2;
-  }
-  int ks = (int)std::max<int64_t>(1, (target_wg + tiles - 1) / tiles);
+  int ks = (int)std::max<int64_t>(1, (HAV_FWD_BLOCK_TARGET + tiles - 1) / tiles);
   ks = std::min(ks, nch);
   const int c = (nch + ks - 1) / ks;
   *KS = (nch + c - 1) / c;

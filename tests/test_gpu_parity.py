@@ -525,6 +525,17 @@ def test_delayed_block_update_large_grid(gpu_lib):
     _check(c, got, idx, *_oracle(c, 2), mode="delayed")
 
 
+def test_delayed_block_forward_many_clusters(gpu_lib):
+    """Block forwards of 8 clusters x 4 steps x 32 samples (1024 rows per
+    cluster, 2048 inputs, 512 hidden units): with the split count that fills
+    the GPU, 256 x 256 tiles would keep splits under 64 chunks, so the launch
+    takes the 128 x 128 tile with one split over all 2048 inputs, the plan made
+    for that tile.  P=64 S=8 K1=4 K2=1 B=32, one round against the oracle."""
+    c = cases.case("mlp", 64, 8, 4, 1, B=32, IN=2048, H=512, C=10, N=2000, sigma=0.5, lr=0.05, seed=45)
+    got, idx, _ = _run_gpu(c, rounds=1, mode="delayed")
+    _check(c, got, idx, *_oracle(c, 1), mode="delayed")
+
+
 @pytest.mark.parametrize("name", ["fused_wide", "fused_one_block", "separate_many_rows"])
 def test_delayed_last_block_global_mean(name, gpu_lib):
     """The last block's update over all P learners from the mean of the
