@@ -764,13 +764,28 @@ __global__ __launch_bounds__(64 * kHfWaves) void k_head_fused(HeadFusedArgs a) {
         const int e = min(tid + NT * min(i0 + i, nz - 1), lz), s = e / H4, c4 = e % H4;
         const float* src = pbase + (int64_t)s * Hp + 4 * c4;
         br[i] = *(const f32x4*)(b1 + 4 * c4);
-        if (KSN > 0) {
 #pragma unroll
-          for (int k = 0; k < (KSN > 0 ? KSN : 1); ++k) zr[i][k] = *(const f32x4*)(src + k * a.split);
-        } else {
-          f32x4 z = {0.f, 0.f, 0.f, 0.f};
-          for (int k = 0; k < a.KS; ++k) z += *(const f32x4*)(src + k * a.split);
-          zr[i][0] = z;
+        for (int k = 0; k < (KSN > 0 ? KSN : 1); ++k)
+          zr[i][k] = KSN > 0 ? *(const f32x4*)(src + k * a.split) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      if (KSN == 0) {
+        // Any split count: kKG splits of every piece per batch of loads, all
+        // issued before the first add (split indices past the count load the
+        // last split again and add zero), the splits added in order.
+        constexpr int kKG = kNB > 4 ? 2 : 4;
+        for (int k0 = 0; k0 < a.KS; k0 += kKG) {
+          f32x4 zk[kNB][kKG];
+#pragma unroll
+          for (int i = 0; i < kNB; ++i) {
+            const int e = min(tid + NT * min(i0 + i, nz - 1), lz), s = e / H4, c4 = e % H4;
+            const float* src = pbase + (int64_t)s * Hp + 4 * c4;
+#pragma unroll
+            for (int k = 0; k < kKG; ++k) zk[i][k] = *(const f32x4*)(src + (int64_t)min(k0 + k, a.KS - 1) * a.split);
+          }
+#pragma unroll
+          for (int i = 0; i < kNB; ++i)
+#pragma unroll
+            for (int k = 0; k < kKG; ++k) zr[i][0] += k0 + k < a.KS ? zk[i][k] : f32x4{0.f, 0.f, 0.f, 0.f};
         }
       }
       if (i0 == 0) yv = a.labels[ixv];

@@ -141,6 +141,13 @@ EAGER_HEADS = {
     # 32 class slots, Hp = 320, B = 40: three sample groups
     "fused32_h300": (cases.case("mlp", 4, 2, 2, 2, B=40, IN=100, H=300, C=20, N=300, sigma=0.5, lr=0.05, seed=62),
                      "head_fused"),
+    # more than three K splits of the step's forward (the head's batched loads
+    # for any split count): 32 class slots, 384 inputs in six splits; 16 class
+    # slots, Hp = 1024, 320 inputs in five splits
+    "fused32_h300_ks6": (cases.case("mlp", 4, 2, 2, 2, B=20, IN=384, H=300, C=20, N=300, sigma=0.5, lr=0.05,
+                                    seed=64), "head_fused"),
+    "fused16_h1000_ks5": (cases.case("mlp", 4, 2, 2, 2, B=20, IN=320, H=1000, C=7, N=300, sigma=0.5, lr=0.05,
+                                     seed=65), "head_fused"),
     # 32 class slots with Hp = 640: past the fused head's LDS
     "slices_c20_h600": (cases.case("mlp", 4, 2, 2, 2, B=12, IN=100, H=600, C=20, N=300, sigma=0.5, lr=0.05,
                                    seed=63), "head_b"),
