@@ -21,7 +21,6 @@ constexpr int kLdsStride = 68;  // LDS row stride in floats (64 + 4: conflict-fr
 constexpr int kUM = 64;         // W rows per block-update workgroup
 constexpr int kUN = 128;        // W columns per block-update workgroup
 constexpr int kSC = 32;         // contraction rows per LDS stage
-constexpr int kLA = kUM + 4;    // LDS row length of the error stage
 constexpr int kLB = kUN + 4;    // LDS row length of the input stage and of the gradient tile
 
 // Large-tile variant for the block-wide forward of delayed updates (many rows
