@@ -17,8 +17,10 @@ special cases Sec. 3.1 names (synchronous SGD, K-AVG), a plain minibatch-SGD
 and momentum-SGD run through ``torch.autograd``/``torch.optim`` on the CPU in
 float64, finite differences, the worker-average dynamics of the proof of
 Thm 3.1, and the pure-noise variance that follows from the decomposition in
-Lemma 1.  Absolute parameter values after a round of the named workloads have
-no printed example in the paper: beyond those pins they are parity unpinned.
+Lemma 1.  Every function here is pinned by one or more of these.  The paper
+prints no parameter values after a round of the named workloads, so those
+absolute values are checked only through the pinned functions that compute
+them.
 
 Modules:
   rng      -- SplitMix64 hash, the minibatch index draw, the exact normal
