@@ -340,7 +340,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Hier-AVG learners are rows of one replica array on a single "
-              "MI355X; multi-GPU sharding is not part of this build", file=sys.stderr)
+              "MI355X; the library has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs the GPU"
